@@ -1,0 +1,31 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+
+
+def read_golden(name):
+    """Parse a tests/golden fixture: '# ...' comment lines, then 'key v1 v2 ...' rows
+    (or a bare row of numbers)."""
+    path = os.path.join(ROOT, "tests", "golden", name)
+    rows = {}
+    bare = []
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            parts = line.split()
+            try:
+                bare.append([float(p) for p in parts])
+            except ValueError:
+                rows[parts[0]] = [float(p) for p in parts[1:]]
+    return rows, bare
