@@ -1,0 +1,209 @@
+/*
+ * scaleqlora.h -- C ABI of the Scale-QLoRA frozen-code FP4 linear layer for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The layer stores a weight as a frozen plane of 4-bit E2M1 codes and a plane
+ * of per-block scale bytes (paper, Section 2, "Native FP4 microscaling
+ * storage"):
+ *
+ *     W[o,i] = code[o,i] * eff[o, i / B]
+ *
+ *   MXFP4 (SQ_MXFP4): B = 32, one E8M0 byte per block, eff = 2^(byte-127).
+ *   NVFP4 (SQ_NVFP4): B = 16, one E4M3 byte per block times one fp32
+ *                     per-tensor scalar ws2, eff = e4m3(byte) * ws2.
+ *
+ * The only trainable field is the block scale (Section 3, "Scale-QLoRA
+ * forward" and "QAST makes merge exact by construction").  This library
+ * provides the layer's forward, its two backward products (dX and the
+ * per-block scale gradient dS), the scale-plane merge / swap, and the
+ * round-to-nearest re-quantiser that the naive weight-space merge uses.
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * Shapes    T tokens, O output features, I input features, G = I / B blocks.
+ * Layouts   all row-major, densely packed, no strides:
+ *             X   bf16  [T, I]        dY  bf16  [T, O]
+ *             Y         [T, O]        dX        [T, I]
+ *             codes uint8 [O, I/2]    two codes per byte, the LOW nibble holds
+ *                                     the even column i, the high nibble i+1;
+ *                                     nibble = sign(bit 3) | exponent(2) |
+ *                                     mantissa(1), values +-{0,.5,1,1.5,2,3,4,6}
+ *             scales uint8 [O, G]     E8M0 (MX) or E4M3 "fn" (NV) bytes
+ *             dS  fp32  [O, G]
+ * Pointers  every data pointer is a DEVICE pointer (memory of the current HIP
+ *           device); the caller allocates and owns every buffer.  No entry point
+ *           allocates device memory.  Inputs are never written.
+ * Streams   `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *           Every call only enqueues work on it and returns; nothing is
+ *           synchronised.  Calls are reentrant and thread-safe.
+ * Shapes    T >= 0; O >= 1, O % 8 == 0; I >= 1, I % B == 0.  T == 0 is legal:
+ *           Y and dX are empty and dS is written as zeros.  Every dimension and
+ *           every buffer size must stay below 2^31 elements.
+ * Alignment X, dY, Y, dX: 16 bytes.  codes: 4 bytes.  dS: 4 bytes.
+ *           Merge scale planes, deltas and sources: 16 bytes.
+ * Errors    arguments are checked on the host before anything is enqueued; a
+ *           violation returns a negative sq_status and enqueues nothing.  A
+ *           failed launch returns SQ_ERR_HIP.  Data values are never checked:
+ *           NaN inputs and NaN scale bytes (E8M0 0xFF, E4M3 0x7F/0xFF)
+ *           propagate to the outputs.
+ */
+#ifndef SCALEQLORA_H
+#define SCALEQLORA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SQ_ABI_VERSION 1
+
+/* Status codes returned by every int-valued entry point. */
+typedef enum {
+  SQ_OK = 0,
+  SQ_ERR_ARG = -1,           /* NULL pointer, unknown enum value, bad scalar */
+  SQ_ERR_SHAPE = -2,         /* dimension out of range or not a multiple */
+  SQ_ERR_ALIGN = -3,         /* pointer misaligned for the layout above */
+  SQ_ERR_FORMAT = -4,        /* unknown sq_format */
+  SQ_ERR_WORKSPACE = -5,     /* workspace missing or too small */
+  SQ_ERR_HIP = -6,           /* the HIP runtime reported an error */
+  SQ_ERR_UNIMPLEMENTED = -7
+} sq_status;
+
+typedef enum { SQ_MXFP4 = 0, SQ_NVFP4 = 1 } sq_format;
+typedef enum { SQ_OUT_F32 = 0, SQ_OUT_BF16 = 1 } sq_out_dtype;
+typedef enum { SQ_TIE_EVEN = 0, SQ_TIE_AWAY = 1 } sq_tie;
+typedef enum { SQ_MERGE_DELTA = 0, SQ_MERGE_COPY = 1 } sq_merge_mode;
+
+/*
+ * Forward, Y = X W^T (paper Section 2 storage equation; Section 3,
+ * "Scale-QLoRA forward": y = x W'^T).
+ *
+ * X bf16 [T, I]; codes [O, I/2]; scales [O, G]; ws2 the NVFP4 per-tensor
+ * scalar (ignored for MXFP4; for NVFP4 it must be finite and > 0).
+ * Y [T, O] is written in y_dtype (SQ_OUT_F32 or SQ_OUT_BF16, round to nearest
+ * even).  The dequantised weight code * scale is formed exactly in bf16 on
+ * chip and the contraction accumulates in fp32 on the bf16 matrix cores; for
+ * NVFP4 ws2 is applied once to the fp32 accumulator.
+ */
+int sq_fwd(int fmt, int64_t T, int64_t O, int64_t I,
+           const void* X, const uint8_t* codes, const uint8_t* scales, float ws2,
+           void* Y, int y_dtype, void* stream);
+
+/*
+ * Input gradient, dX = dY W.  With the codes frozen, the gradient reaching the
+ * layer input passes through the same on-grid weight the forward used
+ * (Section 3, QAST forward with the straight-through estimator: the forward
+ * runs on the on-grid scale).
+ *
+ * dY bf16 [T, O]; codes, scales, ws2 as for sq_fwd; dX [T, I] in dx_dtype.
+ */
+int sq_bwd_dx(int fmt, int64_t T, int64_t O, int64_t I,
+              const void* dY, const uint8_t* codes, const uint8_t* scales, float ws2,
+              void* dX, int dx_dtype, void* stream);
+
+/*
+ * Per-block scale gradient (the gradient Section 3's scale adapter receives
+ * through eff_scale', by the chain rule through W = code * eff):
+ *
+ *     dS[o,b] = sum_{j in block b} code[o,j] * sum_t dY[t,o] * X[t,j]
+ *
+ * X bf16 [T, I]; dY bf16 [T, O]; codes [O, I/2]; dS fp32 [O, G], fully
+ * overwritten.  dS is the gradient with respect to the effective fp32 scale
+ * eff (for NVFP4 the gradient with respect to the E4M3 value is dS * ws2), so
+ * this call takes no scale plane.  The dW tile is produced on the matrix cores
+ * and reduced against the codes on chip; no [O, I] tensor is written.
+ * Deterministic: the same inputs give bitwise identical dS.
+ * workspace / workspace_bytes: scratch of at least
+ * sq_bwd_dscale_workspace(fmt, T, O, I) bytes (NULL / 0 when that is 0).
+ */
+int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I,
+                  const void* X, const void* dY, const uint8_t* codes, float* dS,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes sq_bwd_dscale needs for this shape (0 = none).  Returns 0 for
+ * invalid arguments as well; sq_bwd_dscale then reports the error. */
+size_t sq_bwd_dscale_workspace(int fmt, int64_t T, int64_t O, int64_t I);
+
+/*
+ * Scale-plane merge or swap, in place, over n scale bytes (Section 3, "QAST
+ * makes merge exact by construction": the merge writes the on-grid scale byte
+ * training used and copies the codes; stability recipe items (ii)-(iii): the
+ * NVFP4 ceiling clamp min(eff, 448*ws2) runs on the same path; Appendix B,
+ * "Payoff 2": a hot swap overwrites the scale bytes and leaves codes
+ * untouched).  No code plane is taken, so no code byte can change.
+ *
+ * mode SQ_MERGE_DELTA: delta fp32 [n] is an update of the effective scale.
+ *   NVFP4: e = fp32(e4m3(b) * ws2); e2 = fp32(e + delta); e2 = min(e2,
+ *          fp32(448 * ws2)); q = fp32(e2 / ws2); b' = E4M3 nearest-even,
+ *          saturating at 448.
+ *   MXFP4: e2 = fp32(2^(b-127) + delta); b' = E8M0 of 2^round(log2 e2),
+ *          nearest in the log domain (exponent clamped to [-127, 127];
+ *          e2 <= 0 gives 0x00; NaN gives 0xFF).
+ *   Every step is one correctly rounded fp32 operation (no fused multiply-add).
+ *   src is ignored.
+ * mode SQ_MERGE_COPY: scales[k] = src[k] (delta and ws2 ignored).
+ * scales, delta, src: device, 16-byte aligned; n >= 0.
+ */
+int sq_merge_scales(int fmt, int64_t n, uint8_t* scales, const float* delta,
+                    const uint8_t* src, float ws2, int mode, void* stream);
+
+/* One scale plane of a grouped merge. */
+typedef struct sq_merge_desc {
+  int64_t n;                /* scale bytes in this plane */
+  uint8_t* scales;          /* device, in place, 16-byte aligned */
+  const float* delta;       /* device, SQ_MERGE_DELTA */
+  const uint8_t* src;       /* device, SQ_MERGE_COPY */
+  float ws2;                /* NVFP4 per-tensor scalar */
+  int32_t fmt;              /* sq_format */
+  int32_t mode;             /* sq_merge_mode */
+  int32_t reserved;         /* must be 0 */
+} sq_merge_desc;
+
+/*
+ * sq_merge_scales over many planes in as few launches as possible (a whole
+ * model's scale planes, Appendix B "Payoff 2": swapping the served task writes
+ * only the scale plane of every target linear).  descs is a HOST array of
+ * n_desc descriptors, each validated like a sq_merge_scales call; planes must
+ * not overlap.  The descriptors are read during the call only.
+ */
+int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream);
+
+/*
+ * Round-to-nearest re-quantisation of a bf16 weight [O, I] into codes and
+ * scales, the naive merge W' = requant(dequant(W) + (alpha/r) BA) (Section 2,
+ * "The naive re-quantized merge is the failure mode").
+ *
+ *   MXFP4: per block k = ceil(log2(fp32(amax / 6))) (the shipping rule, with
+ *          the mantissa masked off; Appendix "Calibrated PTQ on a Sparse MoE"),
+ *          clamped to [-127, 127], all-zero block -> k = -127; byte k + 127;
+ *          q = w / 2^k.
+ *   NVFP4: per-tensor ws2 = ws2_in when ws2_in > 0, else recomputed as
+ *          fp32(fp32(amax_tensor / 6) / 448) (1 for an all-zero tensor); per
+ *          block byte = E4M3 nearest-even of fp32(fp32(amax / 6) / ws2) (the
+ *          amax/6 nearest rule; Appendix "Why the Naive Merge Returns the
+ *          Base"); se = fp32(e4m3(byte) * ws2); q = fp32(w / se) (0 if se = 0).
+ *   Codes: |q| to the nearest E2M1 magnitude with ties per `tie` (SQ_TIE_EVEN:
+ *          even mantissa; SQ_TIE_AWAY: away from zero), saturating at 6; the
+ *          sign bit is the sign of w, also for a zero magnitude; a NaN q codes
+ *          as magnitude 0.
+ *
+ * W bf16 [O, I]; codes_out [O, I/2]; scales_out [O, G]; ws2_out: device fp32
+ * scalar receiving the ws2 used (NVFP4; may be NULL for MXFP4 or when ws2_in
+ * > 0).  Recomputing ws2 needs ws2_out (it holds the tensor amax in between).
+ */
+int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int tie,
+                 uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream);
+
+/* Human-readable name of a status code (static storage). */
+const char* sq_status_str(int status);
+
+/* SQ_ABI_VERSION of the built library. */
+int sq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCALEQLORA_H */

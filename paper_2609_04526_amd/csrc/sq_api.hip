@@ -1,0 +1,177 @@
+// C ABI of libscaleqlora (declared in include/scaleqlora.h): host-side
+// argument validation, then one or a few launches on the caller's stream.
+// Nothing here allocates device memory or synchronises.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/scaleqlora.h"
+#include "sq_launch.h"
+
+#define SQ_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+constexpr int64_t kDimMax = (int64_t(1) << 31) - 1;
+
+int block_of(int fmt) { return fmt == SQ_MXFP4 ? 32 : 16; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int check_layer(int fmt, int64_t T, int64_t O, int64_t I) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  if (T < 0 || O < 1 || I < 1 || T > kDimMax || O > kDimMax || I > kDimMax) return SQ_ERR_SHAPE;
+  if (O % 8 != 0 || I % block_of(fmt) != 0) return SQ_ERR_SHAPE;
+  return SQ_OK;
+}
+
+bool ws2_ok(float ws2) { return isfinite(ws2) && ws2 > 0.0f; }
+
+int check_gemm(int fmt, int64_t T, int64_t O, int64_t I, const void* act, const uint8_t* codes,
+               const uint8_t* scales, float ws2, const void* out, int out_dtype) {
+  int st = check_layer(fmt, T, O, I);
+  if (st != SQ_OK) return st;
+  if (out_dtype != SQ_OUT_F32 && out_dtype != SQ_OUT_BF16) return SQ_ERR_ARG;
+  if (!codes || !scales) return SQ_ERR_ARG;
+  if (T > 0 && (!act || !out)) return SQ_ERR_ARG;
+  if (fmt == SQ_NVFP4 && !ws2_ok(ws2)) return SQ_ERR_ARG;
+  if (!aligned(act, 16) || !aligned(out, 16) || !aligned(codes, 4)) return SQ_ERR_ALIGN;
+  return SQ_OK;
+}
+
+int hip_status(int rc) { return rc == 0 ? SQ_OK : SQ_ERR_HIP; }
+
+int check_merge_plane(int fmt, int64_t n, const uint8_t* scales, const float* delta, const uint8_t* src,
+                      float ws2, int mode) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  if (mode != SQ_MERGE_DELTA && mode != SQ_MERGE_COPY) return SQ_ERR_ARG;
+  if (n < 0) return SQ_ERR_SHAPE;
+  if (n == 0) return SQ_OK;
+  if (!scales) return SQ_ERR_ARG;
+  if (mode == SQ_MERGE_DELTA) {
+    if (!delta) return SQ_ERR_ARG;
+    if (fmt == SQ_NVFP4 && !ws2_ok(ws2)) return SQ_ERR_ARG;
+    if (!aligned(delta, 16)) return SQ_ERR_ALIGN;
+  } else {
+    if (!src) return SQ_ERR_ARG;
+    if (!aligned(src, 16)) return SQ_ERR_ALIGN;
+  }
+  if (!aligned(scales, 16)) return SQ_ERR_ALIGN;
+  return SQ_OK;
+}
+
+int run_merge(int n_desc, const sq_merge_desc* d, hipStream_t s) {
+  sq::MergeBatch batch{};
+  int64_t chunks = 0;
+  for (int k = 0; k < n_desc; ++k) {
+    if (d[k].n == 0) continue;
+    if (batch.count == sq::kMergePlanesPerLaunch) {
+      if (sq::merge_launch(batch, chunks, s) != 0) return SQ_ERR_HIP;
+      batch = sq::MergeBatch{};
+      chunks = 0;
+    }
+    sq::MergePlane& p = batch.p[batch.count++];
+    p.scales = d[k].scales;
+    p.delta = d[k].delta;
+    p.src = d[k].src;
+    p.n = d[k].n;
+    p.chunk_begin = chunks;
+    p.ws2 = d[k].ws2;
+    p.fmt = d[k].fmt;
+    p.mode = d[k].mode;
+    chunks += (d[k].n + sq::kMergeChunk - 1) / sq::kMergeChunk;
+  }
+  if (batch.count > 0 && sq::merge_launch(batch, chunks, s) != 0) return SQ_ERR_HIP;
+  return SQ_OK;
+}
+
+}  // namespace
+
+SQ_EXPORT int sq_fwd(int fmt, int64_t T, int64_t O, int64_t I, const void* X, const uint8_t* codes,
+                     const uint8_t* scales, float ws2, void* Y, int y_dtype, void* stream) {
+  int st = check_gemm(fmt, T, O, I, X, codes, scales, ws2, Y, y_dtype);
+  if (st != SQ_OK) return st;
+  if (T == 0) return SQ_OK;
+  return hip_status(sq::gemm_fwd(fmt, (int)T, (int)O, (int)I, X, codes, scales, ws2, Y,
+                                 y_dtype == SQ_OUT_BF16, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int sq_bwd_dx(int fmt, int64_t T, int64_t O, int64_t I, const void* dY, const uint8_t* codes,
+                        const uint8_t* scales, float ws2, void* dX, int dx_dtype, void* stream) {
+  int st = check_gemm(fmt, T, O, I, dY, codes, scales, ws2, dX, dx_dtype);
+  if (st != SQ_OK) return st;
+  if (T == 0) return SQ_OK;
+  return hip_status(sq::gemm_dx(fmt, (int)T, (int)O, (int)I, dY, codes, scales, ws2, dX,
+                                dx_dtype == SQ_OUT_BF16, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT size_t sq_bwd_dscale_workspace(int fmt, int64_t T, int64_t O, int64_t I) {
+  (void)fmt; (void)T; (void)O; (void)I;
+  return 0;
+}
+
+SQ_EXPORT int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I, const void* X, const void* dY,
+                            const uint8_t* codes, float* dS, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  int st = check_layer(fmt, T, O, I);
+  if (st != SQ_OK) return st;
+  if (!codes || !dS) return SQ_ERR_ARG;
+  if (T > 0 && (!X || !dY)) return SQ_ERR_ARG;
+  if (!aligned(X, 16) || !aligned(dY, 16) || !aligned(codes, 4) || !aligned(dS, 4)) return SQ_ERR_ALIGN;
+  if (workspace_bytes < sq_bwd_dscale_workspace(fmt, T, O, I)) return SQ_ERR_WORKSPACE;
+  (void)workspace;
+  return hip_status(sq::gemm_dscale(fmt, (int)T, (int)O, (int)I, X, dY, codes, dS,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int sq_merge_scales(int fmt, int64_t n, uint8_t* scales, const float* delta, const uint8_t* src,
+                              float ws2, int mode, void* stream) {
+  int st = check_merge_plane(fmt, n, scales, delta, src, ws2, mode);
+  if (st != SQ_OK) return st;
+  sq_merge_desc d{};
+  d.n = n; d.scales = scales; d.delta = delta; d.src = src; d.ws2 = ws2; d.fmt = fmt; d.mode = mode;
+  return run_merge(1, &d, static_cast<hipStream_t>(stream));
+}
+
+SQ_EXPORT int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream) {
+  if (n_desc < 0 || (n_desc > 0 && !descs)) return SQ_ERR_ARG;
+  for (int k = 0; k < n_desc; ++k) {
+    const sq_merge_desc& d = descs[k];
+    if (d.reserved != 0) return SQ_ERR_ARG;
+    int st = check_merge_plane(d.fmt, d.n, d.scales, d.delta, d.src, d.ws2, d.mode);
+    if (st != SQ_OK) return st;
+  }
+  return run_merge(n_desc, descs, static_cast<hipStream_t>(stream));
+}
+
+SQ_EXPORT int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int tie,
+                           uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream) {
+  int st = check_layer(fmt, 0, O, I);
+  if (st != SQ_OK) return st;
+  if (tie != SQ_TIE_EVEN && tie != SQ_TIE_AWAY) return SQ_ERR_ARG;
+  if (!W || !codes_out || !scales_out) return SQ_ERR_ARG;
+  if (fmt == SQ_NVFP4) {
+    if (!(ws2_in > 0.0f) && !ws2_out) return SQ_ERR_ARG;     // recomputing needs the slot
+    if (ws2_in > 0.0f && !isfinite(ws2_in)) return SQ_ERR_ARG;
+    if (ws2_out && !aligned(ws2_out, 4)) return SQ_ERR_ALIGN;
+  }
+  if (!aligned(W, 16) || !aligned(codes_out, 4)) return SQ_ERR_ALIGN;
+  return hip_status(sq::rtn_launch(fmt, (int)O, (int)I, W, ws2_in, tie, codes_out, scales_out,
+                                   fmt == SQ_NVFP4 ? ws2_out : nullptr, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT const char* sq_status_str(int status) {
+  switch (status) {
+    case SQ_OK: return "SQ_OK";
+    case SQ_ERR_ARG: return "SQ_ERR_ARG: invalid argument";
+    case SQ_ERR_SHAPE: return "SQ_ERR_SHAPE: invalid shape";
+    case SQ_ERR_ALIGN: return "SQ_ERR_ALIGN: misaligned pointer";
+    case SQ_ERR_FORMAT: return "SQ_ERR_FORMAT: unknown format";
+    case SQ_ERR_WORKSPACE: return "SQ_ERR_WORKSPACE: workspace too small";
+    case SQ_ERR_HIP: return "SQ_ERR_HIP: HIP runtime error";
+    case SQ_ERR_UNIMPLEMENTED: return "SQ_ERR_UNIMPLEMENTED";
+    default: return "unknown status";
+  }
+}
+
+SQ_EXPORT int sq_abi_version(void) { return SQ_ABI_VERSION; }

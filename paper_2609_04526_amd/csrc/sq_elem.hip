@@ -1,0 +1,270 @@
+// Bandwidth-bound kernels of the frozen-code FP4 layer on gfx950:
+//   * the scale-plane merge / swap (paper Section 3, "QAST makes merge exact
+//     by construction" and stability recipe items (ii)-(iii); Appendix B
+//     "Payoff 2" hot swap), which reads and writes scale bytes only;
+//   * round-to-nearest re-quantisation of a bf16 weight (Section 2, "The naive
+//     re-quantized merge is the failure mode"), the baseline that rewrites
+//     every code.
+// Every fp32 step is an explicitly correctly rounded operation (__fmul_rn,
+// __fadd_rn, __fdiv_rn); fp32 subnormals are kept (E8M0 2^-127 is one).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sq_device.h"
+#include "sq_launch.h"
+
+namespace sq {
+
+// ------------------------------------------------------------------ encoders
+// fp32 -> E8M0 byte of 2^round(log2 x), nearest in the log domain: with
+// x = m * 2^k, m in [1, 2), round up iff m > sqrt(2), i.e. iff the 23-bit
+// fraction field is >= 0x3504F4 (fp32(sqrt 2) = 0x3FB504F3 lies below sqrt 2).
+// Exponent clamped to [-127, 127]; x <= 0 -> 0x00, +inf -> 0xFE, NaN -> 0xFF.
+__device__ __forceinline__ uint32_t e8m0_encode_log(float x) {
+  if (x != x) return 0xFFu;
+  if (!(x > 0.0f)) return 0x00u;
+  uint32_t u = __float_as_uint(x);
+  if (u >= 0x7F800000u) return 0xFEu;
+  int e = (int)(u >> 23);
+  uint32_t frac = u & 0x7FFFFFu;
+  int k;
+  if (e == 0) {                             // subnormal: x = frac * 2^-149
+    const int p = 31 - __clz(frac);         // top set bit
+    k = p - 149;
+    frac = (frac << (23 - p)) & 0x7FFFFFu;
+  } else {
+    k = e - 127;
+  }
+  if (frac >= 0x3504F4u) k += 1;
+  k = k < -127 ? -127 : (k > 127 ? 127 : k);
+  return (uint32_t)(k + 127);
+}
+
+// fp32 -> E4M3 "fn" byte, round to nearest, ties to even mantissa, saturating
+// at +-448; NaN -> 0x7F.
+__device__ __forceinline__ uint32_t e4m3_encode_rne_sat(float x) {
+  if (x != x) return 0x7Fu;
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const uint32_t ua = u & 0x7FFFFFFFu;
+  if (ua >= 0x43E00000u) return sign | 0x7Eu;                  // |x| >= 448
+  const uint32_t e = ua >> 23;
+  uint32_t code;
+  if (e < 121u) {
+    // |x| < 2^-6: E4M3 subnormal spacing 2^-9; |x| * 512 is exact, round to
+    // nearest even integer (8 is the smallest normal, byte 0x08).
+    code = (uint32_t)__builtin_rintf(__uint_as_float(ua) * 512.0f);
+  } else {
+    const uint32_t frac = ua & 0x7FFFFFu;
+    code = ((e - 120u) << 3) | (frac >> 20);
+    const uint32_t rem = frac & 0xFFFFFu;
+    if (rem > 0x80000u || (rem == 0x80000u && (code & 1u))) code += 1u;
+  }
+  return sign | code;
+}
+
+// E2M1 magnitude index (0..7 for 0,.5,1,1.5,2,3,4,6) of |q| with ties to the
+// even mantissa or away from zero; >= 6 saturates, NaN gives 0.
+template <bool AWAY>
+__device__ __forceinline__ uint32_t e2m1_round_index(float a) {
+  uint32_t i = 0;
+  if (AWAY) {
+    i += (a >= 0.25f); i += (a >= 0.75f); i += (a >= 1.25f); i += (a >= 1.75f);
+    i += (a >= 2.5f);  i += (a >= 3.5f);  i += (a >= 5.0f);
+  } else {
+    // a tie goes to whichever neighbour has an even index: 0.25->0, 0.75->1.0,
+    // 1.25->1.0, 1.75->2.0, 2.5->2.0, 3.5->4.0, 5->4.0
+    i += (a > 0.25f); i += (a >= 0.75f); i += (a > 1.25f); i += (a >= 1.75f);
+    i += (a > 2.5f);  i += (a >= 3.5f);  i += (a > 5.0f);
+  }
+  return i;
+}
+
+// ------------------------------------------------------------------ merge
+__device__ __forceinline__ uint32_t merge_one(int fmt, uint32_t b, float d, float ws2) {
+  if (fmt == kNV) {
+    const float e = __fmul_rn(e4m3_to_f32(b), ws2);
+    float e2 = __fadd_rn(e, d);
+    const float cap = __fmul_rn(448.0f, ws2);
+    e2 = (e2 > cap) ? cap : e2;                 // NaN compares false and is kept
+    return e4m3_encode_rne_sat(__fdiv_rn(e2, ws2));
+  }
+  return e8m0_encode_log(__fadd_rn(e8m0_to_f32(b), d));
+}
+
+__global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch) {
+  const int64_t chunk = blockIdx.x;
+  int pi = 0;
+  for (int p = 1; p < batch.count; ++p)
+    if (batch.p[p].chunk_begin <= chunk) pi = p;
+  const MergePlane P = batch.p[pi];
+  const int64_t base = (chunk - P.chunk_begin) * kMergeChunk;
+  const int tid = threadIdx.x;
+  if (P.mode == 1) {                                    // copy: 16 bytes per thread
+    const int64_t i = base + (int64_t)tid * 16;
+    if (i + 16 <= P.n) {
+      *reinterpret_cast<uint4*>(P.scales + i) = *reinterpret_cast<const uint4*>(P.src + i);
+    } else {
+      for (int64_t k = i; k < P.n && k < i + 16; ++k) P.scales[k] = P.src[k];
+    }
+    return;
+  }
+#pragma unroll
+  for (int g = 0; g < kMergeChunk / 1024; ++g) {        // 4 scales per thread per step
+    const int64_t i = base + g * 1024 + (int64_t)tid * 4;
+    if (i + 4 <= P.n) {
+      const uint32_t s = *reinterpret_cast<const uint32_t*>(P.scales + i);
+      const float4 d = *reinterpret_cast<const float4*>(P.delta + i);
+      const uint32_t r = merge_one(P.fmt, s & 0xFFu, d.x, P.ws2) |
+                         (merge_one(P.fmt, (s >> 8) & 0xFFu, d.y, P.ws2) << 8) |
+                         (merge_one(P.fmt, (s >> 16) & 0xFFu, d.z, P.ws2) << 16) |
+                         (merge_one(P.fmt, s >> 24, d.w, P.ws2) << 24);
+      *reinterpret_cast<uint32_t*>(P.scales + i) = r;
+    } else {
+      for (int64_t k = i; k < P.n && k < i + 4; ++k)
+        P.scales[k] = (uint8_t)merge_one(P.fmt, P.scales[k], P.delta[k], P.ws2);
+    }
+  }
+}
+
+int merge_launch(const MergeBatch& b, int64_t total_chunks, hipStream_t s) {
+  if (total_chunks <= 0) return 0;
+  hipLaunchKernelGGL(merge_kernel, dim3((unsigned)total_chunks), dim3(256), 0, s, b);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// ------------------------------------------------------------------ RTN
+// ceil(log2 x) for positive finite fp32 x (subnormals included).
+__device__ __forceinline__ int ceil_log2_pos(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t e = u >> 23, frac = u & 0x7FFFFFu;
+  if (e == 0u) {
+    const int p = 31 - __clz(frac);
+    return p - 149 + ((frac & (frac - 1u)) != 0u);
+  }
+  return (int)e - 127 + (frac != 0u);
+}
+
+// One thread per 8 consecutive weights of a row (16 bytes of bf16); the
+// B/8 threads of a block are adjacent lanes and share the block amax.
+template <int FMT, bool AWAY>
+__global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W, int64_t n_chunks,
+                                                  const float* ws2_ptr, float ws2_val,
+                                                  uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
+  constexpr int B = ScaleOperand<FMT>::kBlock;
+  constexpr int LPB = B / 8;
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool valid = c < n_chunks;
+  uint4 v = valid ? *reinterpret_cast<const uint4*>(W + 8 * c) : make_uint4(0, 0, 0, 0);
+  const uint32_t h[4] = {v.x, v.y, v.z, v.w};
+  // amax as a bit pattern: for |x| the integer order of the bits is the
+  // numeric order, with NaN above +inf, so NaN propagates like a max.
+  uint32_t am = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    am = max(am, h[k] & 0x7FFFu);
+    am = max(am, (h[k] >> 16) & 0x7FFFu);
+  }
+  am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+  if (LPB == 4) am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+  const float amax = __uint_as_float(am << 16);
+  const float sixth = __fdiv_rn(amax, 6.0f);
+
+  uint32_t sbyte;
+  float eff;            // effective block scale (what q divides by)
+  if (FMT == kMX) {
+    int k;
+    if (sixth != sixth) {
+      sbyte = 0xFFu;
+      k = 0;
+    } else {
+      if (sixth == 0.0f) k = -127;
+      else if (sixth > 3.4028234e38f) k = 127;
+      else k = ceil_log2_pos(sixth);
+      k = k < -127 ? -127 : (k > 127 ? 127 : k);
+      sbyte = (uint32_t)(k + 127);
+    }
+    // 2^-k as fp32 (2^-127 is subnormal, 2^127 normal): exact
+    const float inv = (k == 127) ? __uint_as_float(0x00400000u) : __uint_as_float((uint32_t)(127 - k) << 23);
+    eff = (sbyte == 0xFFu) ? __uint_as_float(0x7FC00000u) : inv;   // used as a multiplier below
+  } else {
+    const float ws2 = ws2_ptr ? *ws2_ptr : ws2_val;
+    sbyte = e4m3_encode_rne_sat(__fdiv_rn(sixth, ws2));
+    eff = __fmul_rn(e4m3_to_f32(sbyte), ws2);
+  }
+
+  uint32_t packed = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t hb = (h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+    const float w = __uint_as_float(hb << 16);
+    float q;
+    if (FMT == kMX) q = __fmul_rn(w, eff);                  // w / 2^k, one rounding
+    else q = (eff == 0.0f) ? 0.0f : __fdiv_rn(w, eff);
+    const uint32_t mag = e2m1_round_index<AWAY>(fabsf(q));
+    packed |= (mag | ((hb >> 12) & 8u)) << (4 * k);
+  }
+  if (valid) {
+    reinterpret_cast<uint32_t*>(codes)[c] = packed;
+    if ((c % LPB) == 0) scales[c / LPB] = (uint8_t)sbyte;
+  }
+}
+
+__global__ void rtn_amax_init(float* slot) { *reinterpret_cast<uint32_t*>(slot) = 0u; }
+
+__global__ __launch_bounds__(256) void rtn_amax(const uint16_t* __restrict__ W, int64_t n_chunks, float* slot) {
+  uint32_t am = 0;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * 256) {
+    const uint4 v = *reinterpret_cast<const uint4*>(W + 8 * c);
+    const uint32_t h[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      am = max(am, h[k] & 0x7FFFu);
+      am = max(am, (h[k] >> 16) & 0x7FFFu);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) am = max(am, (uint32_t)__shfl_xor((int)am, off));
+  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(slot), am << 16);
+}
+
+__global__ void rtn_ws2_store(float* slot, float v) { *slot = v; }
+
+__global__ void rtn_ws2_finalize(float* slot) {
+  const float amax = *slot;
+  float ws2 = __fdiv_rn(__fdiv_rn(amax, 6.0f), 448.0f);
+  if (ws2 == 0.0f) ws2 = 1.0f;
+  *slot = ws2;
+}
+
+int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
+               uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s) {
+  const int64_t n_chunks = (int64_t)O * I / 8;
+  const uint16_t* w = static_cast<const uint16_t*>(W);
+  const float* ws2_ptr = nullptr;
+  if (fmt == kNV) {
+    if (ws2_in > 0.0f) {
+      if (ws2_out) hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, ws2_out, ws2_in);
+    } else {
+      hipLaunchKernelGGL(rtn_amax_init, dim3(1), dim3(1), 0, s, ws2_out);
+      const int64_t want = (n_chunks + 255) / 256;
+      const unsigned grid = (unsigned)(want < 4096 ? (want > 0 ? want : 1) : 4096);
+      hipLaunchKernelGGL(rtn_amax, dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_out);
+      hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, ws2_out);
+      ws2_ptr = ws2_out;
+    }
+  }
+  if (n_chunks > 0) {
+    const unsigned grid = (unsigned)((n_chunks + 255) / 256);
+    if (fmt == kMX) {
+      if (tie == 1) hipLaunchKernelGGL((rtn_kernel<kMX, true>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, 1.0f, codes, scales);
+      else hipLaunchKernelGGL((rtn_kernel<kMX, false>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, 1.0f, codes, scales);
+    } else {
+      if (tie == 1) hipLaunchKernelGGL((rtn_kernel<kNV, true>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, ws2_in, codes, scales);
+      else hipLaunchKernelGGL((rtn_kernel<kNV, false>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, ws2_in, codes, scales);
+    }
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace sq

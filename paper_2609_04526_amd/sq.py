@@ -1,0 +1,210 @@
+"""ctypes binding of libscaleqlora (C ABI in include/scaleqlora.h).
+
+Argument marshalling only: each function takes torch tensors that already live
+on the current HIP device, passes their data pointers, sizes and the current
+torch stream to the entry point of the same name, and raises on a non-zero
+status.  All compute happens in the library's HIP kernels.  The library must
+have been built (``python -m paper_2609_04526_amd.build``); there is no
+fallback path.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libscaleqlora.so")
+
+MXFP4, NVFP4 = 0, 1
+OUT_F32, OUT_BF16 = 0, 1
+TIE_EVEN, TIE_AWAY = 0, 1
+MERGE_DELTA, MERGE_COPY = 0, 1
+FORMATS = {"mx": MXFP4, "nv": NVFP4}
+BLOCK = {MXFP4: 32, NVFP4: 16}
+
+_c_i64 = ctypes.c_int64
+_c_p = ctypes.c_void_p
+
+
+class SqError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+        self.status = status
+
+
+class MergeDesc(ctypes.Structure):
+    """Mirror of sq_merge_desc."""
+    _fields_ = [
+        ("n", ctypes.c_int64),
+        ("scales", ctypes.c_void_p),
+        ("delta", ctypes.c_void_p),
+        ("src", ctypes.c_void_p),
+        ("ws2", ctypes.c_float),
+        ("fmt", ctypes.c_int32),
+        ("mode", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load():
+    """Load the library (once).  Raises if it was not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2609_04526_amd.build` first")
+    lib = ctypes.CDLL(LIB_PATH)
+    sigs = {
+        "sq_fwd": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, ctypes.c_float,
+                                  _c_p, ctypes.c_int, _c_p]),
+        "sq_bwd_dx": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, ctypes.c_float,
+                                     _c_p, ctypes.c_int, _c_p]),
+        "sq_bwd_dscale": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p,
+                                         _c_p, ctypes.c_size_t, _c_p]),
+        "sq_bwd_dscale_workspace": (ctypes.c_size_t, [ctypes.c_int, _c_i64, _c_i64, _c_i64]),
+        "sq_merge_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_p, _c_p, _c_p, ctypes.c_float,
+                                           ctypes.c_int, _c_p]),
+        "sq_merge_scales_grouped": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(MergeDesc), _c_p]),
+        "rtn_quantize": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
+                                        _c_p, _c_p, _c_p, _c_p]),
+        "sq_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+        "sq_abi_version": (ctypes.c_int, []),
+    }
+    for name, (res, args) in sigs.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(fn, status):
+    if status != 0:
+        raise SqError(fn, status, load().sq_status_str(status).decode())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _fmt(fmt):
+    return FORMATS.get(fmt, fmt)
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libscaleqlora takes device tensors")
+
+
+# ---------------------------------------------------------------- entry points
+def sq_fwd(fmt, X, codes, scales, ws2=1.0, out_dtype=torch.float32, Y=None):
+    """Y = X W^T.  X bf16 [T, I], codes uint8 [O, I/2], scales uint8 [O, G]."""
+    fmt = _fmt(fmt)
+    T, I = X.shape
+    O = codes.shape[0]
+    if Y is None:
+        Y = torch.empty((T, O), dtype=out_dtype, device=X.device)
+    _dev(X, codes, scales, Y)
+    _check("sq_fwd", load().sq_fwd(fmt, T, O, I, _ptr(X), _ptr(codes), _ptr(scales), float(ws2), _ptr(Y),
+                                   OUT_BF16 if Y.dtype == torch.bfloat16 else OUT_F32, _stream()))
+    return Y
+
+
+def sq_bwd_dx(fmt, dY, codes, scales, ws2=1.0, out_dtype=torch.float32, dX=None):
+    """dX = dY W.  dY bf16 [T, O] -> dX [T, I]."""
+    fmt = _fmt(fmt)
+    T, O = dY.shape
+    I = codes.shape[1] * 2
+    if dX is None:
+        dX = torch.empty((T, I), dtype=out_dtype, device=dY.device)
+    _dev(dY, codes, scales, dX)
+    _check("sq_bwd_dx", load().sq_bwd_dx(fmt, T, O, I, _ptr(dY), _ptr(codes), _ptr(scales), float(ws2),
+                                         _ptr(dX), OUT_BF16 if dX.dtype == torch.bfloat16 else OUT_F32,
+                                         _stream()))
+    return dX
+
+
+def sq_bwd_dscale_workspace(fmt, T, O, I):
+    return int(load().sq_bwd_dscale_workspace(_fmt(fmt), T, O, I))
+
+
+def sq_bwd_dscale(fmt, X, dY, codes, dS=None, workspace=None):
+    """dS[o,b] = sum_{j in b} code[o,j] (dY^T X)[o,j], fp32 [O, G]."""
+    fmt = _fmt(fmt)
+    T, I = X.shape
+    O = dY.shape[1]
+    if dS is None:
+        dS = torch.empty((O, I // BLOCK[fmt]), dtype=torch.float32, device=X.device)
+    _dev(X, dY, codes, dS)
+    ws_bytes = sq_bwd_dscale_workspace(fmt, T, O, I)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=X.device)
+    wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check("sq_bwd_dscale", load().sq_bwd_dscale(fmt, T, O, I, _ptr(X), _ptr(dY), _ptr(codes), _ptr(dS),
+                                                 _ptr(workspace), wsz, _stream()))
+    return dS
+
+
+def sq_merge_scales(fmt, scales, delta=None, src=None, ws2=1.0, mode=None):
+    """In-place merge (delta given) or swap (src given) of one scale plane."""
+    fmt = _fmt(fmt)
+    if mode is None:
+        mode = MERGE_COPY if src is not None else MERGE_DELTA
+    _dev(scales, delta, src)
+    _check("sq_merge_scales", load().sq_merge_scales(fmt, scales.numel(), _ptr(scales), _ptr(delta),
+                                                     _ptr(src), float(ws2), mode, _stream()))
+    return scales
+
+
+class MergeGroup:
+    """A prepared descriptor table for sq_merge_scales_grouped (built once,
+    reused across calls; the tensors it names must stay alive)."""
+
+    def __init__(self, planes):
+        self.planes = planes
+        self.arr = (MergeDesc * max(len(planes), 1))()
+        for k, p in enumerate(planes):
+            mode = p.get("mode", MERGE_COPY if p.get("src") is not None else MERGE_DELTA)
+            _dev(p["scales"], p.get("delta"), p.get("src"))
+            self.arr[k] = MergeDesc(p["scales"].numel(), p["scales"].data_ptr(),
+                                    p["delta"].data_ptr() if p.get("delta") is not None else 0,
+                                    p["src"].data_ptr() if p.get("src") is not None else 0,
+                                    float(p.get("ws2", 1.0)), _fmt(p["fmt"]), mode, 0)
+
+
+def sq_merge_scales_grouped(planes):
+    """planes: a MergeGroup, or a list of dicts with keys fmt, scales,
+    delta / src, ws2, mode."""
+    group = planes if isinstance(planes, MergeGroup) else MergeGroup(planes)
+    _check("sq_merge_scales_grouped",
+           load().sq_merge_scales_grouped(len(group.planes), group.arr, _stream()))
+
+
+def rtn_quantize(fmt, W, tie=TIE_EVEN, ws2_in=0.0, codes=None, scales=None, ws2_out=None):
+    """Round-to-nearest re-quantisation of bf16 W [O, I] -> (codes, scales, ws2_out)."""
+    fmt = _fmt(fmt)
+    O, I = W.shape
+    dev = W.device
+    if codes is None:
+        codes = torch.empty((O, I // 2), dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty((O, I // BLOCK[fmt]), dtype=torch.uint8, device=dev)
+    if fmt == NVFP4 and ws2_out is None:
+        ws2_out = torch.empty(1, dtype=torch.float32, device=dev)
+    _dev(W, codes, scales, ws2_out)
+    _check("rtn_quantize", load().rtn_quantize(fmt, O, I, _ptr(W), float(ws2_in), int(tie), _ptr(codes),
+                                               _ptr(scales), _ptr(ws2_out), _stream()))
+    return codes, scales, ws2_out
+
+
+def abi_version():
+    return int(load().sq_abi_version())

@@ -29,3 +29,19 @@ def read_golden(name):
             except ValueError:
                 rows[parts[0]] = [float(p) for p in parts[1:]]
     return rows, bare
+
+
+def ensure_library():
+    """Build libscaleqlora.so if it is not there yet (hipcc cross-compiles without a GPU)."""
+    from paper_2609_04526_amd import build as _build, sq as _sq
+    if not os.path.exists(_sq.LIB_PATH):
+        _build.build()
+    return _sq.load()
+
+
+def gpu_ready():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False

@@ -1,0 +1,121 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+the header declares, and rejects bad arguments on the host before any launch."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT, ensure_library
+
+HEADER = os.path.join(ROOT, "include", "scaleqlora.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^(?:int|size_t|const char\s*\*)\s*(\w+)\s*\(", text, flags=re.M)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ensure_library()
+
+
+def test_header_declares_the_boundary():
+    names = set(declared_functions())
+    assert {"sq_fwd", "sq_bwd_dx", "sq_bwd_dscale", "sq_merge_scales", "rtn_quantize"} <= names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version(lib):
+    from paper_2609_04526_amd import sq
+    assert lib.sq_status_str(0) == b"SQ_OK"
+    assert lib.sq_status_str(-2).startswith(b"SQ_ERR_SHAPE")
+    assert sq.abi_version() == 1
+
+
+def test_merge_desc_layout_matches_header():
+    from paper_2609_04526_amd import sq
+    assert ctypes.sizeof(sq.MergeDesc) == 48
+    assert sq.MergeDesc.ws2.offset == 32 and sq.MergeDesc.reserved.offset == 44
+
+
+FAKE = 0x10000            # a 16-byte-aligned address that is never dereferenced
+MISALIGNED = 0x10008
+
+
+def _fwd(lib, fmt=0, T=64, O=256, I=512, X=FAKE, codes=FAKE, scales=FAKE, ws2=1.0, Y=FAKE, dt=0):
+    return lib.sq_fwd(fmt, T, O, I, X, codes, scales, ws2, Y, dt, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(fmt=2), -4),
+    (dict(O=0), -2),
+    (dict(O=12), -2),                      # O % 8
+    (dict(I=48), -2),                      # MX needs I % 32
+    (dict(fmt=1, I=40), -2),               # NV needs I % 16
+    (dict(T=-1), -2),
+    (dict(I=1 << 31), -2),
+    (dict(dt=7), -1),
+    (dict(codes=None), -1),
+    (dict(X=None), -1),
+    (dict(fmt=1, ws2=0.0), -1),
+    (dict(fmt=1, ws2=float("nan")), -1),
+    (dict(X=MISALIGNED), -3),
+    (dict(Y=MISALIGNED), -3),
+    (dict(codes=FAKE + 2), -3),
+])
+def test_fwd_validation(lib, kw, status):
+    assert _fwd(lib, **kw) == status
+
+
+def test_empty_token_batch_is_a_noop(lib):
+    # T = 0: nothing to compute for Y / dX, and nothing is launched
+    assert _fwd(lib, T=0, X=None, Y=None) == 0
+    assert lib.sq_bwd_dx(0, 0, 256, 512, None, FAKE, FAKE, 1.0, None, 0, None) == 0
+
+
+def test_dx_and_dscale_validation(lib):
+    assert lib.sq_bwd_dx(0, 8, 250, 512, FAKE, FAKE, FAKE, 1.0, FAKE, 0, None) == -2
+    assert lib.sq_bwd_dscale(0, 8, 256, 500, FAKE, FAKE, FAKE, FAKE, None, 0, None) == -2
+    assert lib.sq_bwd_dscale(0, 8, 256, 512, FAKE, FAKE, FAKE, None, None, 0, None) == -1
+    assert lib.sq_bwd_dscale(0, 8, 256, 512, MISALIGNED, FAKE, FAKE, FAKE, None, 0, None) == -3
+    assert lib.sq_bwd_dscale(0, 8, 256, 512, FAKE, FAKE, FAKE, FAKE + 2, None, 0, None) == -3
+    assert lib.sq_bwd_dscale_workspace(0, 4096, 4096, 4096) == 0
+
+
+def test_merge_validation(lib):
+    from paper_2609_04526_amd import sq
+    assert lib.sq_merge_scales(0, 0, None, None, None, 1.0, 0, None) == 0          # empty plane
+    assert lib.sq_merge_scales(3, 16, FAKE, FAKE, None, 1.0, 0, None) == -4
+    assert lib.sq_merge_scales(0, -1, FAKE, FAKE, None, 1.0, 0, None) == -2
+    assert lib.sq_merge_scales(0, 16, FAKE, None, None, 1.0, 0, None) == -1         # delta missing
+    assert lib.sq_merge_scales(0, 16, FAKE, None, None, 1.0, 1, None) == -1         # src missing
+    assert lib.sq_merge_scales(0, 16, FAKE, FAKE, None, 1.0, 2, None) == -1         # bad mode
+    assert lib.sq_merge_scales(1, 16, FAKE, FAKE, None, -1.0, 0, None) == -1        # NV ws2
+    assert lib.sq_merge_scales(0, 16, FAKE + 1, FAKE, None, 1.0, 0, None) == -3
+    assert lib.sq_merge_scales(0, 16, FAKE, MISALIGNED, None, 1.0, 0, None) == -3
+    # grouped: one bad descriptor rejects the whole call before anything runs
+    arr = (sq.MergeDesc * 2)()
+    arr[0] = sq.MergeDesc(16, FAKE, FAKE, 0, 1.0, 0, 0, 0)
+    arr[1] = sq.MergeDesc(16, FAKE, 0, 0, 1.0, 0, 0, 0)
+    assert lib.sq_merge_scales_grouped(2, arr, None) == -1
+    arr[1] = sq.MergeDesc(16, FAKE, FAKE, 0, 1.0, 0, 0, 5)
+    assert lib.sq_merge_scales_grouped(2, arr, None) == -1                           # reserved != 0
+    assert lib.sq_merge_scales_grouped(-1, arr, None) == -1
+    assert lib.sq_merge_scales_grouped(0, None, None) == 0
+
+
+def test_rtn_validation(lib):
+    assert lib.rtn_quantize(0, 256, 500, FAKE, 0.0, 0, FAKE, FAKE, None, None) == -2
+    assert lib.rtn_quantize(0, 256, 512, FAKE, 0.0, 3, FAKE, FAKE, None, None) == -1
+    assert lib.rtn_quantize(1, 256, 512, FAKE, 0.0, 0, FAKE, FAKE, None, None) == -1   # NV recompute needs ws2_out
+    assert lib.rtn_quantize(1, 256, 512, FAKE, float("inf"), 0, FAKE, FAKE, None, None) == -1
+    assert lib.rtn_quantize(0, 256, 512, MISALIGNED, 0.0, 0, FAKE, FAKE, None, None) == -3
+    assert lib.rtn_quantize(0, 256, 512, None, 0.0, 0, FAKE, FAKE, None, None) == -1

@@ -1,0 +1,169 @@
+"""GPU parity of sq_fwd / sq_bwd_dx / sq_bwd_dscale against the oracle.
+
+Small and ragged shapes are compared element by element on full outputs
+(normwise relative error <= 2e-3, the bound the target sets for bf16 inputs
+with fp32 accumulation; the measured error is printed).  Full-size 8B shapes
+are compared on seeded sampled rows that the oracle computes one by one, plus
+the exact identity sum(eff * dS) = <dY, Y> = <X, dX> over the full outputs."""
+
+import numpy as np
+import pytest
+import torch
+
+from conftest import ensure_library, gpu_ready
+from oracle import codec, linear
+from paper_2609_04526_amd import inputs
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not gpu_ready(), reason="needs a GPU")]
+
+TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def sq():
+    ensure_library()
+    from paper_2609_04526_amd import sq as _sq
+    return _sq
+
+
+def normwise(got, ref):
+    ref = np.asarray(ref, np.float64)
+    got = np.asarray(got, np.float64)
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
+
+
+def make_layer(fmt, T, O, I, seed, mx_exp=(-8, -3)):
+    G = I // codec.BLOCK[fmt]
+    X = inputs.bf16_normal(seed, (T, I))
+    dY = inputs.bf16_normal(seed + 1, (T, O))
+    codes = inputs.codes_uniform(seed + 2, O, I)
+    if fmt == "mx":
+        sb = inputs.e8m0_uniform_exponents(seed + 3, O, G, *mx_exp)
+        ws2 = 1.0
+    else:
+        sb = inputs.e4m3_abs_normal(seed + 3, O, G)
+        ws2 = float(np.float32(1.0 / 448.0))
+    return X, dY, codes, sb, ws2
+
+
+def to_dev(X, dY, codes, sb):
+    return (X.cuda(), dY.cuda(), torch.from_numpy(codes).cuda(), torch.from_numpy(sb).cuda())
+
+
+def run_all(sq, fmt, X, dY, codes, sb, ws2, out_dtype=torch.float32):
+    print(f"[gemm] fmt={fmt} T={X.shape[0]} O={codes.shape[0]} I={X.shape[1]} out={out_dtype}", flush=True)
+    dX_, dY_, c_, s_ = to_dev(X, dY, codes, sb)
+    Y = sq.sq_fwd(fmt, dX_, c_, s_, ws2, out_dtype)
+    dXo = sq.sq_bwd_dx(fmt, dY_, c_, s_, ws2, out_dtype)
+    dS = sq.sq_bwd_dscale(fmt, dX_, dY_, c_)
+    torch.cuda.synchronize()
+    return Y.float().cpu().numpy(), dXo.float().cpu().numpy(), dS.cpu().numpy()
+
+
+SHAPES = [
+    ("mx", 64, 256, 512),       # the tiny MXFP4 workload
+    ("nv", 64, 256, 512),
+    ("mx", 300, 264, 416),      # several tiles and a ragged tail in every dimension
+    ("nv", 300, 264, 208),
+    ("mx", 1, 8, 32),           # smallest legal layer
+    ("nv", 5, 8, 16),
+    ("mx", 129, 136, 160),
+    ("nv", 257, 520, 1040),
+]
+
+
+@pytest.mark.parametrize("fmt,T,O,I", SHAPES)
+def test_parity_full_outputs(sq, fmt, T, O, I):
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed=1000 + T + O + I)
+    Y, dX, dS = run_all(sq, fmt, X, dY, codes, sb, ws2)
+    Xd, dYd = X.double().numpy(), dY.double().numpy()
+    W = linear.dequant(fmt, codes, sb, ws2)
+    eY = normwise(Y, linear.forward(Xd, W))
+    eX = normwise(dX, linear.backward_dx(dYd, W))
+    eS = normwise(dS, linear.backward_dscale(fmt, Xd, dYd, codes))
+    print(f"  normwise errors Y {eY:.2e} dX {eX:.2e} dS {eS:.2e}")
+    assert eY <= TOL and eX <= TOL and eS <= TOL
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+def test_bf16_outputs_within_one_ulp(sq, fmt):
+    T, O, I = 192, 264, 416 if fmt == "mx" else 400
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed=2000)
+    Y, dX, _ = run_all(sq, fmt, X, dY, codes, sb, ws2, torch.bfloat16)
+    W = linear.dequant(fmt, codes, sb, ws2)
+    for got, ref in ((Y, linear.forward(X.double().numpy(), W)), (dX, linear.backward_dx(dY.double().numpy(), W))):
+        ref32 = ref.astype(np.float32)
+        ref_bf = torch.from_numpy(ref32).to(torch.bfloat16).float().numpy()
+        ulp = np.abs(np.spacing(ref_bf.astype(np.float32)) * 65536.0)       # bf16 ulp = 2^16 fp32 ulps
+        assert np.all(np.abs(got - ref_bf) <= ulp + 1e-30)
+        assert normwise(got, ref) <= 4e-3
+
+
+def test_zero_tokens_gives_zero_dscale(sq):
+    O, I = 64, 128
+    codes = torch.from_numpy(inputs.codes_uniform(5, O, I)).cuda()
+    X = torch.empty((0, I), dtype=torch.bfloat16, device="cuda")
+    dY = torch.empty((0, O), dtype=torch.bfloat16, device="cuda")
+    dS = torch.full((O, I // 32), 7.0, device="cuda")
+    sq.sq_bwd_dscale("mx", X, dY, codes, dS=dS)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dS).item() == 0
+
+
+def test_dscale_deterministic_and_scale_independent(sq):
+    fmt, T, O, I = "mx", 333, 136, 320
+    X, dY, codes, _, _ = make_layer(fmt, T, O, I, seed=3000)
+    Xc, dYc, cc = X.cuda(), dY.cuda(), torch.from_numpy(codes).cuda()
+    a = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
+    b = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_nan_scale_propagates(sq):
+    fmt, T, O, I = "mx", 32, 64, 128
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed=3100)
+    sb = sb.copy()
+    sb[3, 1] = 0xFF                                          # NaN scale in row 3, block 1
+    codes = codes.copy()
+    codes[3, 16:32] = 0x11                                   # nonzero codes in that block
+    Y, _, _ = run_all(sq, fmt, X, dY, codes, sb, ws2)
+    assert np.all(np.isnan(Y[:, 3]))
+    assert np.all(np.isfinite(np.delete(Y, 3, axis=1)))
+
+
+def _sampled_check(sq, fmt, T, O, I, seed, mx_exp=None, n_rows=6):
+    kw = {} if mx_exp is None else {"mx_exp": mx_exp}
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed, **kw)
+    if mx_exp is None and fmt == "mx":
+        sb = inputs.e8m0_normal_exponents(seed + 3, O, I // 32, -6.0, 1.5)
+    Y, dX, dS = run_all(sq, fmt, X, dY, codes, sb, ws2)
+    g = inputs.rng(seed + 99)
+    rows_t = g.choice(T, n_rows, replace=False)
+    rows_o = g.choice(O, n_rows, replace=False)
+    W = linear.dequant(fmt, codes, sb, ws2)
+    Xd = X.double().numpy()
+    dYd = dY.double().numpy()
+    eY = normwise(Y[rows_t], linear.forward(Xd[rows_t], W))
+    eX = normwise(dX[rows_t], linear.backward_dx(dYd[rows_t], W))
+    eS = normwise(dS[rows_o], linear.backward_dscale(fmt, Xd, dYd[:, rows_o], codes[rows_o]))
+    eff = codec.effective_scales(fmt, sb, ws2)
+    a = float(np.sum(eff * dS.astype(np.float64)))
+    b = float(np.sum(dYd * Y.astype(np.float64)))
+    c = float(np.sum(Xd * dX.astype(np.float64)))
+    scale = float(np.sqrt(np.sum(dYd ** 2) * np.sum(Y.astype(np.float64) ** 2)))
+    print(f"  sampled normwise Y {eY:.2e} dX {eX:.2e} dS {eS:.2e}; identity {a:.6e} {b:.6e} {c:.6e}")
+    assert eY <= TOL and eX <= TOL and eS <= TOL
+    assert abs(a - b) <= TOL * scale and abs(c - b) <= TOL * scale
+
+
+def test_parity_8b_attention_projection_mx(sq):
+    """4096 x 4096 MXFP4 projection, 4096 tokens, exponents rint(N(-6, 1.5))."""
+    _sampled_check(sq, "mx", 4096, 4096, 4096, seed=2000)
+
+
+@pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336)])
+def test_parity_8b_mlp_nv(sq, O, I):
+    """NVFP4 gate/up (14336 x 4096) and down (4096 x 14336), 8192 tokens."""
+    _sampled_check(sq, "nv", 8192, O, I, seed=3000 + O)

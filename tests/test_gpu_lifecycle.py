@@ -1,0 +1,217 @@
+"""GPU parity of sq_merge_scales(_grouped) and rtn_quantize against the oracle:
+bit-exact bytes, with guard bytes around every written plane, and the code
+plane untouched by merges."""
+
+import numpy as np
+import pytest
+import torch
+
+from conftest import ensure_library, gpu_ready
+from oracle import codec, linear, merge, rtn
+from paper_2609_04526_amd import inputs
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not gpu_ready(), reason="needs a GPU")]
+
+GUARD = 256          # bytes of canary on each side (keeps 16-byte alignment)
+
+
+@pytest.fixture(scope="module")
+def sq():
+    ensure_library()
+    from paper_2609_04526_amd import sq as _sq
+    return _sq
+
+
+def guarded(host_bytes):
+    """Device buffer = canary | plane | canary; returns (buffer, plane view)."""
+    n = host_bytes.size
+    buf = torch.full((n + 2 * GUARD,), 0xA5, dtype=torch.uint8, device="cuda")
+    buf[GUARD:GUARD + n] = torch.from_numpy(np.ascontiguousarray(host_bytes).reshape(-1)).cuda()
+    return buf, buf[GUARD:GUARD + n]
+
+
+def guards_intact(buf):
+    b = buf.cpu().numpy()
+    return bool(np.all(b[:GUARD] == 0xA5) and np.all(b[-GUARD:] == 0xA5))
+
+
+def test_merge_tiny_mx_perturbed_plane(sq):
+    """The tiny MXFP4 workload: 256 x 16 scale plane, +-1 exponent step on 10% of blocks."""
+    sb = inputs.e8m0_uniform_exponents(1003, 256, 16, -8, -3)
+    d = inputs.e8m0_step_delta(1009, sb, 0.10)
+    buf, plane = guarded(sb)
+    sq.sq_merge_scales("mx", plane, delta=torch.from_numpy(d.reshape(-1)).cuda())
+    torch.cuda.synchronize()
+    ref = merge.merge_delta("mx", sb, d)
+    assert np.array_equal(plane.cpu().numpy().reshape(sb.shape), ref)
+    assert guards_intact(buf)
+    assert (ref != sb).sum() == round(0.1 * sb.size)
+
+
+@pytest.mark.parametrize("fmt,n", [("mx", 4096 * 3 + 20), ("nv", 4096 * 3 + 20), ("nv", 7), ("mx", 1000003)])
+def test_merge_delta_random_matches_oracle(sq, fmt, n):
+    g = inputs.rng(77 + n)
+    if fmt == "mx":
+        sb = g.integers(90, 150, size=n).astype(np.uint8)
+        eff = np.ldexp(1.0, sb.astype(int) - 127)
+        ws2 = 1.0
+    else:
+        sb = g.integers(0, 0x7F, size=n).astype(np.uint8)
+        ws2 = float(np.float32(1 / 448))
+        eff = codec.E4M3_TABLE[sb] * ws2
+    d = (g.standard_normal(n) * 0.7 * eff).astype(np.float32)
+    d[::97] = 0.0
+    if fmt == "nv":
+        d[5::101] = np.float32(1000 * ws2)        # past the ceiling: clamp, never NaN
+    buf, plane = guarded(sb)
+    sq.sq_merge_scales(fmt, plane, delta=torch.from_numpy(d).cuda(), ws2=ws2)
+    torch.cuda.synchronize()
+    got = plane.cpu().numpy()
+    ref = merge.merge_delta(fmt, sb, d, ws2)
+    assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
+    assert guards_intact(buf)
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+def test_merge_all_bytes_delta_zero_identity(sq, fmt):
+    sb = np.arange(0, 255 if fmt == "mx" else 0x7F, dtype=np.uint8)
+    sb = np.tile(sb, 33)
+    buf, plane = guarded(sb)
+    sq.sq_merge_scales(fmt, plane, delta=torch.zeros(sb.size, device="cuda"), ws2=float(np.float32(1 / 448)))
+    torch.cuda.synchronize()
+    assert np.array_equal(plane.cpu().numpy(), sb)
+    assert guards_intact(buf)
+
+
+def test_merge_special_values(sq):
+    sb = np.array([0, 1, 127, 254, 255, 200, 50, 3] * 4, dtype=np.uint8)
+    d = np.array([0.0, -1.0, np.inf, np.nan, 0.0, -np.inf, 1e-40, 3e38] * 4, dtype=np.float32)
+    buf, plane = guarded(sb)
+    sq.sq_merge_scales("mx", plane, delta=torch.from_numpy(d).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(plane.cpu().numpy(), merge.merge_delta("mx", sb, d))
+
+
+def test_swap_and_grouped_merge_leave_codes_untouched(sq):
+    """A model-like set of planes: swap some, merge others, in one grouped call;
+    the code planes (held next to them) keep their bytes."""
+    planes = []
+    refs = []
+    code_planes = []
+    shapes = [("mx", 64, 4096), ("nv", 96, 4096), ("mx", 32, 14336), ("nv", 40, 14336), ("mx", 8, 1024)]
+    for k, (fmt, O, I) in enumerate(shapes):
+        B = codec.BLOCK[fmt]
+        if fmt == "mx":
+            sb = inputs.e8m0_normal_exponents(500 + k, O, I // B, -6, 1.5)
+            eff = np.ldexp(1.0, sb.astype(int) - 127)
+            ws2 = 1.0
+        else:
+            sb = inputs.e4m3_abs_normal(500 + k, O, I // B)
+            ws2 = float(np.float32(1 / 448))
+            eff = codec.E4M3_TABLE[sb] * ws2
+        codes = inputs.codes_uniform(600 + k, O, I)
+        cbuf, cplane = guarded(codes)
+        code_planes.append((cbuf, cplane, codes))
+        buf, plane = guarded(sb)
+        if k % 2 == 0:
+            d = inputs.relative_jitter(700 + k, eff, 0.3)
+            planes.append(dict(fmt=fmt, scales=plane, delta=torch.from_numpy(d.reshape(-1)).cuda(), ws2=ws2))
+            refs.append((buf, plane, merge.merge_delta(fmt, sb, d, ws2).reshape(-1)))
+        else:
+            src = inputs.e4m3_abs_normal(800 + k, O, I // B) if fmt == "nv" else \
+                inputs.e8m0_normal_exponents(800 + k, O, I // B, -6, 1.5)
+            planes.append(dict(fmt=fmt, scales=plane, src=torch.from_numpy(src.reshape(-1)).cuda()))
+            refs.append((buf, plane, merge.merge_copy(sb, src).reshape(-1)))
+    sq.sq_merge_scales_grouped(planes)
+    torch.cuda.synchronize()
+    for buf, plane, ref in refs:
+        assert np.array_equal(plane.cpu().numpy(), ref)
+        assert guards_intact(buf)
+    for cbuf, cplane, codes in code_planes:
+        assert np.array_equal(cplane.cpu().numpy().reshape(codes.shape), codes)
+        assert guards_intact(cbuf)
+
+
+def test_grouped_merge_many_planes(sq):
+    """More planes than one launch takes, with sizes that leave ragged tails."""
+    planes, refs = [], []
+    for k in range(97):
+        n = 16 * (1 + (k * 37) % 700)
+        sb = inputs.rng(k).integers(100, 140, size=n).astype(np.uint8)
+        d = inputs.relative_jitter(k + 1000, np.ldexp(1.0, sb.astype(int) - 127), 0.8)
+        buf, plane = guarded(sb)
+        planes.append(dict(fmt="mx", scales=plane, delta=torch.from_numpy(d).cuda()))
+        refs.append((buf, plane, merge.merge_delta("mx", sb, d)))
+    sq.sq_merge_scales_grouped(planes)
+    torch.cuda.synchronize()
+    for buf, plane, ref in refs:
+        assert np.array_equal(plane.cpu().numpy(), ref)
+        assert guards_intact(buf)
+
+
+def _merged_weight(fmt, O, I, seed):
+    """bf16(dequant(W) + B A) with a rank-16 update, the naive merge's input."""
+    codes = inputs.codes_uniform(seed, O, I)
+    if fmt == "mx":
+        sb = inputs.e8m0_normal_exponents(seed + 1, O, I // 32, -6, 1.5)
+        ws2 = 1.0
+    else:
+        sb = inputs.e4m3_abs_normal(seed + 1, O, I // 16)
+        ws2 = float(np.float32(1 / 448))
+    B, A = inputs.lora_factors(seed + 2, O, I, 16, 0.02)
+    W = linear.dequant(fmt, codes, sb, ws2).astype(np.float32) + (B @ A).astype(np.float32)
+    Wb = torch.from_numpy(W.astype(np.float32)).to(torch.bfloat16)
+    return Wb, codes, sb, ws2
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+@pytest.mark.parametrize("tie", ["even", "away"])
+@pytest.mark.parametrize("ws2_mode", ["fixed", "recompute"])
+def test_rtn_matches_oracle(sq, fmt, tie, ws2_mode):
+    if fmt == "mx" and ws2_mode == "recompute":
+        pytest.skip("MXFP4 has no per-tensor scalar")
+    O, I = 264, 1024
+    Wb, codes, sb, ws2 = _merged_weight(fmt, O, I, seed=4000)
+    Wf = Wb.float().numpy()
+    tie_c = sq.TIE_EVEN if tie == "even" else sq.TIE_AWAY
+    ws2_in = ws2 if ws2_mode == "fixed" else 0.0
+    c, s, w2 = sq.rtn_quantize(fmt, Wb.cuda(), tie_c, ws2_in)
+    torch.cuda.synchronize()
+    rc, rs, rw = rtn.quantize(fmt, Wf, tie, ws2 if ws2_mode == "fixed" else None)
+    assert np.array_equal(s.cpu().numpy(), rs)
+    assert np.array_equal(c.cpu().numpy(), rc)
+    if fmt == "nv":
+        assert w2.cpu().numpy()[0] == rw
+    # codes moved relative to the base plane (the naive merge rewrites codes)
+    print(f"  {fmt} {tie} {ws2_mode}: code bytes changed vs base {np.mean(rc != codes):.3f}")
+
+
+def test_rtn_ties_and_specials(sq):
+    """Exact midpoints of the E2M1 grid and zero / negative-zero weights."""
+    O, I = 8, 64
+    W = np.zeros((O, I), np.float32)
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0], np.float32)
+    for o in range(O):
+        W[o, :8] = mids
+        W[o, 8:16] = -mids
+        W[o, 32] = -0.0
+        W[o, 33] = 1e-30
+    Wb = torch.from_numpy(W).to(torch.bfloat16)
+    for tie, tc in (("even", 0), ("away", 1)):
+        c, s, _ = sq.rtn_quantize("mx", Wb.cuda(), tc)
+        torch.cuda.synchronize()
+        rc, rs, _ = rtn.quantize("mx", Wb.float().numpy(), tie)
+        assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(c.cpu().numpy(), rc)
+
+
+def test_rtn_delta_zero_fixed_point(sq):
+    O, I = 64, 256
+    codes = inputs.codes_uniform(4100, O, I)
+    nib = codec.unpack_nibbles(codes)
+    nib[:, ::32] = 7
+    codes = codec.pack_nibbles(nib)
+    sb = inputs.e8m0_uniform_exponents(4101, O, I // 32, -8, -3)
+    W = torch.from_numpy(linear.dequant("mx", codes, sb).astype(np.float32)).to(torch.bfloat16)
+    c, s, _ = sq.rtn_quantize("mx", W.cuda(), sq.TIE_EVEN)
+    torch.cuda.synchronize()
+    assert np.array_equal(s.cpu().numpy(), sb) and np.array_equal(c.cpu().numpy(), codes)
