@@ -38,8 +38,8 @@ namespace sq {
 
 enum Mode { kFwd = 0, kDx = 1, kDs = 2 };
 
-constexpr int kThreads = 256;     // 4 waves
 constexpr int kBK = 64;           // K per LDS stage (one 128-byte row)
+constexpr int kXcds = 8;          // MI355X: workgroups are dealt round-robin to 8 XCDs
 
 struct GemmArgs {
   const uint16_t* a;      // FWD: X [T,I]   DX: dY [T,O]   DS: X [T,I]
@@ -68,14 +68,15 @@ __device__ __forceinline__ uint4 ld_global16(const uint16_t* p) {
 // ------------------------------------------------------------------ loaders
 // K-contiguous bf16 tile: rows [r0, r0+R) of a [rows_total, ld] matrix,
 // columns [k0, k0+64).  Out-of-range rows or 8-element chunks read as zero.
-template <int R>
+template <int R, int NT>
 struct LoadKContig {
-  static constexpr int kPer = R * 8 / kThreads;   // 16-byte chunks per thread
+  static constexpr int kPer = R * 8 / NT;         // 16-byte chunks per thread
+  static_assert(kPer * NT == R * 8, "tile rows must split evenly");
   uint4 v[kPer];
   __device__ __forceinline__ void fetch(const uint16_t* src, int ld, int rows_total, int kdim, int r0, int k0, int tid) {
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * kThreads;
+      const int idx = tid + p * NT;
       const int row = idx >> 3, chunk = idx & 7;
       const int gr = r0 + row, gk = k0 + chunk * 8;
       if (gr < rows_total && gk < kdim)
@@ -87,23 +88,24 @@ struct LoadKContig {
   __device__ __forceinline__ void commit(uint16_t* s, int tid) const {
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * kThreads;
+      const int idx = tid + p * NT;
       st_lds16(s, idx >> 3, idx & 7, v[p]);
     }
   }
 };
 
 // W tile for FWD: rows o in [n0, n0+R), K = i in [k0, k0+64), from packed codes.
-template <int R, int FMT>
+template <int R, int FMT, int NT>
 struct LoadWKContig {
-  static constexpr int kPer = R * 8 / kThreads;
+  static constexpr int kPer = R * 8 / NT;
+  static_assert(kPer * NT == R * 8, "tile rows must split evenly");
   uint32_t w[kPer];
   uint32_t sb[kPer];
   __device__ __forceinline__ void fetch(const GemmArgs& g, int n0, int k0, int tid) {
     constexpr int B = ScaleOperand<FMT>::kBlock;
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * kThreads;
+      const int idx = tid + p * NT;
       const int row = idx >> 3, chunk = idx & 7;
       const int o = n0 + row, i = k0 + chunk * 8;
       if (o < g.O && i < g.I) {
@@ -118,7 +120,7 @@ struct LoadWKContig {
   __device__ __forceinline__ void commit(uint16_t* s, int tid) const {
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * kThreads;
+      const int idx = tid + p * NT;
       const float so = ScaleOperand<FMT>::of(sb[p]);
       st_lds16(s, idx >> 3, idx & 7, ScaleOperand<FMT>::dequant8(w[p], so));
     }
@@ -126,87 +128,134 @@ struct LoadWKContig {
 };
 
 // W^T tile for DX: LDS rows are i in [n0, n0+R), K = o in [k0, k0+64).
-// Thread t (< R) takes the 8x8 block (i-block t % (R/8), o-block t / (R/8)).
-template <int R, int FMT>
+// The tile holds R 8x8 blocks (R/8 along i, 8 along o); block q is taken by
+// thread q % NT, item q / NT.
+template <int R, int FMT, int NT>
 struct LoadWTrans {
-  static constexpr int kBlocks = (R / 8) * 8;     // 8x8 blocks in the tile
-  static_assert(kBlocks <= kThreads, "one block per thread");
-  uint32_t w[8];
-  uint32_t sb[8];
+  static constexpr int kBlocks = R;
+  static constexpr int kPer = (kBlocks + NT - 1) / NT;
+  uint32_t w[kPer][8];
+  uint32_t sb[kPer][8];
   __device__ __forceinline__ void fetch(const GemmArgs& g, int n0, int k0, int tid) {
     constexpr int B = ScaleOperand<FMT>::kBlock;
-    if (tid >= kBlocks) return;
-    const int ib = tid % (R / 8), ob = tid / (R / 8);
-    const int i = n0 + ib * 8;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int o = k0 + ob * 8 + r;
-      if (o < g.O && i < g.I) {
-        w[r] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
-        sb[r] = g.scales[(size_t)o * g.G + i / B];
-      } else {
-        w[r] = 0u;
-        sb[r] = 0x38u;
+    for (int p = 0; p < kPer; ++p) {
+      const int q = tid + p * NT;
+      if (q >= kBlocks) break;
+      const int ib = q % (R / 8), ob = q / (R / 8);
+      const int i = n0 + ib * 8;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const int o = k0 + ob * 8 + r;
+        if (o < g.O && i < g.I) {
+          w[p][r] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
+          sb[p][r] = g.scales[(size_t)o * g.G + i / B];
+        } else {
+          w[p][r] = 0u;
+          sb[p][r] = 0x38u;
+        }
       }
     }
   }
   __device__ __forceinline__ void commit(uint16_t* s, int tid) const {
-    if (tid >= kBlocks) return;
-    const int ib = tid % (R / 8), ob = tid / (R / 8);
-    uint32_t rows[8][4], cols[8][4];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const uint4 d = ScaleOperand<FMT>::dequant8(w[r], ScaleOperand<FMT>::of(sb[r]));
-      rows[r][0] = d.x; rows[r][1] = d.y; rows[r][2] = d.z; rows[r][3] = d.w;
+    for (int p = 0; p < kPer; ++p) {
+      const int q = tid + p * NT;
+      if (q >= kBlocks) break;
+      const int ib = q % (R / 8), ob = q / (R / 8);
+      uint32_t rows[8][4], cols[8][4];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const uint4 d = ScaleOperand<FMT>::dequant8(w[p][r], ScaleOperand<FMT>::of(sb[p][r]));
+        rows[r][0] = d.x; rows[r][1] = d.y; rows[r][2] = d.z; rows[r][3] = d.w;
+      }
+      transpose8x8_b16(rows, cols);
+#pragma unroll
+      for (int c = 0; c < 8; ++c)
+        st_lds16(s, ib * 8 + c, ob, make_uint4(cols[c][0], cols[c][1], cols[c][2], cols[c][3]));
     }
-    transpose8x8_b16(rows, cols);
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-      st_lds16(s, ib * 8 + c, ob, make_uint4(cols[c][0], cols[c][1], cols[c][2], cols[c][3]));
   }
 };
 
-// Transposed bf16 tile for DS: source [K_total, ld] (K = tokens) contiguous
-// along the tile's rows.  LDS rows are m in [m0, m0+R), K = t in [k0, k0+64).
-// Threads [first, first + R) each take one 8x8 block.
-template <int R>
-struct LoadTrans {
-  static constexpr int kBlocks = (R / 8) * 8;
-  uint4 v[8];
-  __device__ __forceinline__ void fetch(const uint16_t* src, int ld, int mdim, int kdim, int m0, int k0, int lt) {
-    if (lt < 0 || lt >= kBlocks) return;
-    const int mb = lt % (R / 8), kb = lt / (R / 8);
-    const int m = m0 + mb * 8;
+// Both DS tiles (X^T rows j in [m0, m0+BM), dY^T rows o in [n0, n0+BN), K = t
+// in [k0, k0+64)) from sources [T, ld] that are contiguous along the tile
+// rows.  The BM + BN 8x8 blocks (A blocks first) are dealt to the threads.
+template <int BM, int BN, int NT>
+struct LoadTransDS {
+  static constexpr int kBlocks = BM + BN;
+  static constexpr int kPer = (kBlocks + NT - 1) / NT;
+  uint4 v[kPer][8];
+  __device__ __forceinline__ void fetch(const GemmArgs& g, int m0, int n0, int k0, int tid) {
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const int k = k0 + kb * 8 + r;
-      if (k < kdim && m < mdim)
-        v[r] = ld_global16(src + (size_t)k * ld + m);
-      else
-        v[r] = make_uint4(0, 0, 0, 0);
+    for (int p = 0; p < kPer; ++p) {
+      const int q = tid + p * NT;
+      if (q >= kBlocks) break;
+      const bool isA = q < BM;
+      const int lq = isA ? q : q - BM;
+      const int rows8 = (isA ? BM : BN) / 8;
+      const int mb = lq % rows8, kb = lq / rows8;
+      const int m = (isA ? m0 : n0) + mb * 8;
+      const int mdim = isA ? g.I : g.O;
+      const uint16_t* src = isA ? g.a : g.b;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const int k = k0 + kb * 8 + r;
+        if (k < g.T && m < mdim)
+          v[p][r] = ld_global16(src + (size_t)k * mdim + m);
+        else
+          v[p][r] = make_uint4(0, 0, 0, 0);
+      }
     }
   }
-  __device__ __forceinline__ void commit(uint16_t* s, int lt) const {
-    if (lt < 0 || lt >= kBlocks) return;
-    const int mb = lt % (R / 8), kb = lt / (R / 8);
-    uint32_t rows[8][4], cols[8][4];
+  __device__ __forceinline__ void commit(uint16_t* sa, uint16_t* sb, int tid) const {
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      rows[r][0] = v[r].x; rows[r][1] = v[r].y; rows[r][2] = v[r].z; rows[r][3] = v[r].w;
+    for (int p = 0; p < kPer; ++p) {
+      const int q = tid + p * NT;
+      if (q >= kBlocks) break;
+      const bool isA = q < BM;
+      const int lq = isA ? q : q - BM;
+      const int rows8 = (isA ? BM : BN) / 8;
+      const int mb = lq % rows8, kb = lq / rows8;
+      uint32_t rows[8][4], cols[8][4];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        rows[r][0] = v[p][r].x; rows[r][1] = v[p][r].y; rows[r][2] = v[p][r].z; rows[r][3] = v[p][r].w;
+      }
+      transpose8x8_b16(rows, cols);
+      uint16_t* s = isA ? sa : sb;
+#pragma unroll
+      for (int c = 0; c < 8; ++c)
+        st_lds16(s, mb * 8 + c, kb, make_uint4(cols[c][0], cols[c][1], cols[c][2], cols[c][3]));
     }
-    transpose8x8_b16(rows, cols);
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-      st_lds16(s, mb * 8 + c, kb, make_uint4(cols[c][0], cols[c][1], cols[c][2], cols[c][3]));
   }
 };
+
+// ------------------------------------------------------------------ tile order
+// Workgroup w runs on XCD w % 8, and each XCD has its own L2.  Tiles are
+// enumerated in groups of kGroupM tile-rows (column by column inside a group)
+// and each XCD is given one contiguous stretch of that order, so the
+// workgroups that share an L2 also share operand panels.
+constexpr int kGroupM = 8;
+
+__device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int x = bid % kXcds, q = nb / kXcds, r = nb % kXcds;
+  const int idx = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + bid / kXcds;
+  const int per_group = kGroupM * tiles_n;
+  const int group = idx / per_group;
+  const int first_m = group * kGroupM;
+  const int gm = min(kGroupM, tiles_m - first_m);
+  const int in = idx - group * per_group;
+  tm = first_m + in % gm;
+  tn = in / gm;
+}
 
 // ------------------------------------------------------------------ kernel
-// Block tile BM x BN, 4 waves in a 2x2 grid, each wave (BM/2) x (BN/2) built
+// Block tile BM x BN, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN) built
 // from 32x32 MFMA tiles.
-template <int MODE, int FMT, int BM, int BN>
-__global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs g) {
-  constexpr int WM = BM / 2, WN = BN / 2;
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   uint16_t* sA = smem;                       // [2][BM][64]
@@ -214,8 +263,11 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs g) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * WM, wn0 = (wave & 1) * WN;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  int tm, tn;
+  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -225,12 +277,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // operand loaders for this mode
-  LoadKContig<BM> la_k;       // FWD: X, DX: dY
-  LoadWKContig<BN, FMT> lb_w; // FWD
-  LoadWTrans<BN, FMT> lb_wt;  // DX
-  LoadTrans<BM> la_t;         // DS: X^T
-  LoadTrans<BN> lb_t;         // DS: dY^T
+  LoadKContig<BM, NT> la_k;          // FWD: X, DX: dY
+  LoadWKContig<BN, FMT, NT> lb_w;    // FWD
+  LoadWTrans<BN, FMT, NT> lb_wt;     // DX
+  LoadTransDS<BM, BN, NT> l_ds;      // DS
 
   auto fetch = [&](int k0) {
     if constexpr (MODE == kFwd) {
@@ -240,8 +290,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs g) {
       la_k.fetch(g.a, g.O, g.T, g.O, m0, k0, tid);
       lb_wt.fetch(g, n0, k0, tid);
     } else {
-      la_t.fetch(g.a, g.I, g.I, g.T, m0, k0, tid);
-      lb_t.fetch(g.b, g.O, g.O, g.T, n0, k0, tid - LoadTrans<BM>::kBlocks);
+      l_ds.fetch(g, m0, n0, k0, tid);
     }
   };
   auto commit = [&](int buf) {
@@ -254,8 +303,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs g) {
       la_k.commit(a, tid);
       lb_wt.commit(b, tid);
     } else {
-      la_t.commit(a, tid);
-      lb_t.commit(b, tid - LoadTrans<BM>::kBlocks);
+      l_ds.commit(a, b, tid);
     }
   };
 
@@ -354,16 +402,32 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs g) {
   }
 }
 
-template <int MODE, int FMT, int BM, int BN>
+// Tile configurations (compile-time; SQ_CFG_* selects one per product for
+// tuning builds).  Each entry: BM, BN, waves along M, waves along N.
+#ifndef SQ_CFG_FWD
+#define SQ_CFG_FWD 256, 256, 4, 2
+#endif
+#ifndef SQ_CFG_DX
+#define SQ_CFG_DX 256, 256, 2, 2
+#endif
+#ifndef SQ_CFG_DS
+#define SQ_CFG_DS 256, 256, 4, 2
+#endif
+
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN>
 static int launch_gemm(const GemmArgs& g, hipStream_t s) {
   const size_t lds = (size_t)2 * (BM + BN) * kBK * sizeof(uint16_t);
-  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM);
-  if (grid.x == 0 || grid.y == 0) return 0;
-  auto kern = gemm_kernel<MODE, FMT, BM, BN>;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return -1;
-  hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, g);
+  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  if (tiles == 0) return 0;
+  auto kern = gemm_kernel<MODE, FMT, BM, BN, WGM, WGN>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds) != hipSuccess)
+      return -1;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * WGM * WGN), lds, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -377,7 +441,7 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
   g.M = T; g.N = O; g.K = I;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = y_bf16;
-  return fmt == kMX ? launch_gemm<kFwd, kMX, 128, 128>(g, s) : launch_gemm<kFwd, kNV, 128, 128>(g, s);
+  return fmt == kMX ? launch_gemm<kFwd, kMX, SQ_CFG_FWD>(g, s) : launch_gemm<kFwd, kNV, SQ_CFG_FWD>(g, s);
 }
 
 int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
@@ -389,7 +453,7 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
   g.M = T; g.N = I; g.K = O;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = dx_bf16;
-  return fmt == kMX ? launch_gemm<kDx, kMX, 128, 128>(g, s) : launch_gemm<kDx, kNV, 128, 128>(g, s);
+  return fmt == kMX ? launch_gemm<kDx, kMX, SQ_CFG_DX>(g, s) : launch_gemm<kDx, kNV, SQ_CFG_DX>(g, s);
 }
 
 int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
@@ -402,7 +466,7 @@ int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
   g.M = I; g.N = O; g.K = T;
   g.ws2 = 1.0f;
   g.out_bf16 = 0;
-  return fmt == kMX ? launch_gemm<kDs, kMX, 128, 128>(g, s) : launch_gemm<kDs, kNV, 128, 128>(g, s);
+  return fmt == kMX ? launch_gemm<kDs, kMX, SQ_CFG_DS>(g, s) : launch_gemm<kDs, kNV, SQ_CFG_DS>(g, s);
 }
 
 }  // namespace sq
