@@ -9,20 +9,27 @@
 //   DS   dS[o,b] = sum_{j in b} code[o,j] sum_t dY[t,o] X[t,j]
 //                                                M=I  N=O  K=T
 //
-// Every operand tile is staged in LDS as bf16 rows that are contiguous along
-// K, so all three products feed v_mfma_f32_32x32x16_bf16 from the same
-// fragment reads.  What differs is how a tile reaches LDS:
-//   * X (FWD) and dY (DX) are already K-contiguous: 16-byte copies;
-//   * W (FWD) is K-contiguous in its packed code plane: each 4-byte word of 8
-//     codes is dequantised in registers (exact, see sq_device.h) and written
-//     as 16 bytes of bf16;
-//   * W^T (DX) and X^T, dY^T (DS) are contiguous along N/M: a thread loads an
-//     8x8 block (8 rows of 16 bytes, or 8 rows of one code word that it
-//     dequantises first), transposes it in registers with byte permutes and
-//     writes 8 K-contiguous 16-byte rows.
-// LDS rows are 64 bf16 (128 bytes) with the 16-byte chunk index XOR-swizzled
-// by (row ^ row/8) & 7, which keeps the fragment reads and both write
-// patterns free of bank conflicts within each group of 8 lanes.
+// All three feed v_mfma_f32_32x32x16_bf16 (fp32 accumulation) from LDS, in
+// K stages of 64.  How each operand reaches the matrix cores:
+//   * bf16 activations are copied global -> LDS by buffer loads that write LDS
+//     directly (no registers), in a ring of LDS stages, with reads past the
+//     operand's end returning zeros (ragged tiles need no branches);
+//   * K-contiguous tiles (X in FWD, dY in DX) are stored as 128-byte rows and
+//     read with ds_read_b128;
+//   * tiles that are contiguous along M or N (X and dY in DS, W in DX) are
+//     stored in their natural [k][m] layout and read with the gfx950 LDS
+//     transpose read ds_read_b64_tr_b16: within each 16-lane group, lane i
+//     receives column i of the 4x16 block whose rows the group's lanes supply,
+//     so two reads give a lane the 8 consecutive k of its MFMA operand;
+//   * W in FWD stays packed in LDS; each lane reads the 32 codes of one block
+//     (16 bytes) and dequantises them in registers (exact, see sq_device.h).
+//     The K order inside a stage is permuted to make that possible: MFMA step
+//     kk, lane half h, element e covers k = 32h + 8kk + e, and X is read with
+//     the same permutation;
+//   * W in DX is dequantised in registers from its packed codes and written to
+//     LDS as bf16 rows.
+// Stages are synchronised with explicit vmcnt waits and raw s_barrier, so the
+// loads of later stages stay in flight across the barrier.
 //
 // The DS epilogue multiplies each accumulator dW[o,j] by its E2M1 code and
 // sums over the block in registers (the 32x32 MFMA output puts 8 of a
@@ -31,6 +38,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "sq_device.h"
 #include "sq_launch.h"
 
@@ -38,8 +47,13 @@ namespace sq {
 
 enum Mode { kFwd = 0, kDx = 1, kDs = 2 };
 
-constexpr int kBK = 64;           // K per LDS stage (one 128-byte row)
-constexpr int kXcds = 8;          // MI355X: workgroups are dealt round-robin to 8 XCDs
+constexpr int kBK = 64;                 // K per LDS stage
+constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
+constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: reads zero
+
+#define SQ_LDS __attribute__((address_space(3)))
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct GemmArgs {
   const uint16_t* a;      // FWD: X [T,I]   DX: dY [T,O]   DS: X [T,I]
@@ -53,181 +67,120 @@ struct GemmArgs {
   int out_bf16;
 };
 
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * kBK + (((chunk ^ row ^ (row >> 3)) & 7) << 3);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-__device__ __forceinline__ void st_lds16(uint16_t* s, int row, int chunk, uint4 v) {
-  *reinterpret_cast<uint4*>(s + lds_off(row, chunk)) = v;
+// 16 bytes per lane, global -> LDS; lane l writes dst + 16 l.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, SQ_LDS void* dst, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, (int)voff, 0, 0, 0);
 }
 
-__device__ __forceinline__ uint4 ld_global16(const uint16_t* p) {
-  return *reinterpret_cast<const uint4*>(p);
+// Wait until at most n vector-memory loads of this wave are outstanding and
+// all of its LDS operations are done (raw s_barrier has no memory semantics).
+template <int n>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0070 | (n & 15) | ((n >> 4) << 14));
 }
 
-// ------------------------------------------------------------------ loaders
-// K-contiguous bf16 tile: rows [r0, r0+R) of a [rows_total, ld] matrix,
-// columns [k0, k0+64).  Out-of-range rows or 8-element chunks read as zero.
+// ------------------------------------------------------------------ layouts
+// KC: K-contiguous [rows][64] bf16; 16-byte chunk c of row r lives at chunk
+// c ^ swz_kc(r), so 8 consecutive rows read at one logical chunk hit 8
+// different bank groups.
+__device__ __forceinline__ int swz_kc(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int kc_off(int r, int c) { return r * kBK + ((c ^ swz_kc(r)) << 3); }
+
+// NAT: [64][R] bf16 with R elements per k-row; 16-byte chunk c of row k lives
+// at chunk c ^ swz_nat(k): each of the 4 rows a 16-lane transpose read spans
+// lands in its own 64-byte slot.
+template <int R>
+__device__ __forceinline__ int swz_nat(int k) { return (4 * (k & 7)) & (R / 8 - 1); }
+template <int R>
+__device__ __forceinline__ int nat_off(int k, int col) {
+  return k * R + ((((col >> 3) ^ swz_nat<R>(k))) << 3) + (col & 7);
+}
+
+// MFMA operand (8 consecutive k at one m) from a NAT tile: rows
+// 16*kk + 8*(lane/32) + 0..7 of column mbase + lane%32.
+template <int R>
+__device__ __forceinline__ bf16x8 nat_frag(const SQ_LDS uint16_t* s, int kk, int mbase, int lane) {
+  const int i = lane & 15, g = lane >> 4;
+  const int col = mbase + 16 * (g & 1) + 4 * (i & 3);
+  const int row0 = 16 * kk + 8 * (g >> 1) + (i >> 2);
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SQ_LDS v4i16*)(s + nat_off<R>(row0, col)));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SQ_LDS v4i16*)(s + nat_off<R>(row0 + 4, col)));
+  bf16x8 r;
+  __builtin_memcpy(&r, &lo, 8);
+  __builtin_memcpy(reinterpret_cast<char*>(&r) + 8, &hi, 8);
+  return r;
+}
+
+// ------------------------------------------------------------------ DMA issue
+// KC tile: rows [r0, r0+R) of a [rows_total, ld] bf16 matrix, k in [k0, k0+64).
+// One wave instruction fills 8 consecutive LDS rows (1 KiB).
 template <int R, int NT>
-struct LoadKContig {
-  static constexpr int kPer = R * 8 / NT;         // 16-byte chunks per thread
-  static_assert(kPer * NT == R * 8, "tile rows must split evenly");
-  uint4 v[kPer];
-  __device__ __forceinline__ void fetch(const uint16_t* src, int ld, int rows_total, int kdim, int r0, int k0, int tid) {
+__device__ __forceinline__ void dma_kc(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int ld, int rows_total,
+                                       int kdim, int r0, int k0, int tid) {
+  constexpr int kInst = R / 8 / (NT / 64);
+  static_assert(kInst * (NT / 64) * 8 == R, "tile rows must split over the waves");
+  const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * NT;
-      const int row = idx >> 3, chunk = idx & 7;
-      const int gr = r0 + row, gk = k0 + chunk * 8;
-      if (gr < rows_total && gk < kdim)
-        v[p] = ld_global16(src + (size_t)gr * ld + gk);
-      else
-        v[p] = make_uint4(0, 0, 0, 0);
-    }
+  for (int q = 0; q < kInst; ++q) {
+    const int blk = q * (NT / 64) + wave;
+    const int r = blk * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ swz_kc(r);
+    const int gr = r0 + r, gk = k0 + c * 8;
+    const uint32_t off = (gr < rows_total && gk < kdim) ? (uint32_t)((size_t)gr * ld + gk) * 2u : kOOB;
+    dma16(rs, s + blk * 8 * kBK, off);
   }
-  __device__ __forceinline__ void commit(uint16_t* s, int tid) const {
-#pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * NT;
-      st_lds16(s, idx >> 3, idx & 7, v[p]);
-    }
-  }
-};
+}
 
-// W tile for FWD: rows o in [n0, n0+R), K = i in [k0, k0+64), from packed codes.
-template <int R, int FMT, int NT>
-struct LoadWKContig {
-  static constexpr int kPer = R * 8 / NT;
-  static_assert(kPer * NT == R * 8, "tile rows must split evenly");
-  uint32_t w[kPer];
-  uint32_t sb[kPer];
-  __device__ __forceinline__ void fetch(const GemmArgs& g, int n0, int k0, int tid) {
-    constexpr int B = ScaleOperand<FMT>::kBlock;
+// NAT tile: k-rows [k0, k0+64) of a [kdim, ld] bf16 matrix, columns [m0, m0+R).
+template <int R, int NT>
+__device__ __forceinline__ void dma_nat(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int ld, int mdim,
+                                        int kdim, int m0, int k0, int tid) {
+  constexpr int kCpr = R / 8;                       // chunks per row
+  constexpr int kInst = kBK * kCpr / 64 / (NT / 64);
+  static_assert(kInst * (NT / 64) * 64 == kBK * kCpr, "tile must split over the waves");
+  const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * NT;
-      const int row = idx >> 3, chunk = idx & 7;
-      const int o = n0 + row, i = k0 + chunk * 8;
-      if (o < g.O && i < g.I) {
-        w[p] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
-        sb[p] = g.scales[(size_t)o * g.G + i / B];
-      } else {
-        w[p] = 0u;
-        sb[p] = 0x38u;   // any finite scale: the codes are zero
-      }
-    }
+  for (int q = 0; q < kInst; ++q) {
+    const int blk = q * (NT / 64) + wave;
+    const int p = blk * 64 + lane;
+    const int k = p / kCpr, pc = p % kCpr;
+    const int c = pc ^ swz_nat<R>(k);
+    const int gk = k0 + k, gm = m0 + c * 8;
+    const uint32_t off = (gk < kdim && gm < mdim) ? (uint32_t)((size_t)gk * ld + gm) * 2u : kOOB;
+    dma16(rs, s + blk * 64 * 8, off);
   }
-  __device__ __forceinline__ void commit(uint16_t* s, int tid) const {
-#pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int idx = tid + p * NT;
-      const float so = ScaleOperand<FMT>::of(sb[p]);
-      st_lds16(s, idx >> 3, idx & 7, ScaleOperand<FMT>::dequant8(w[p], so));
-    }
-  }
-};
+}
 
-// W^T tile for DX: LDS rows are i in [n0, n0+R), K = o in [k0, k0+64).
-// The tile holds R 8x8 blocks (R/8 along i, 8 along o); block q is taken by
-// thread q % NT, item q / NT.
-template <int R, int FMT, int NT>
-struct LoadWTrans {
-  static constexpr int kBlocks = R;
-  static constexpr int kPer = (kBlocks + NT - 1) / NT;
-  uint32_t w[kPer][8];
-  uint32_t sb[kPer][8];
-  __device__ __forceinline__ void fetch(const GemmArgs& g, int n0, int k0, int tid) {
-    constexpr int B = ScaleOperand<FMT>::kBlock;
+// Packed W tile for FWD: LDS [2][R][16 bytes]; entry (h, n) holds the 32 codes
+// of row n0+n at k0+32h .. k0+32h+31.
+template <int R, int NT>
+__device__ __forceinline__ void dma_wpack(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint8_t* s, int O, int I,
+                                          int n0, int k0, int tid) {
+  constexpr int kInst = 2 * R / 64 / (NT / 64);
+  static_assert(kInst * (NT / 64) * 64 == 2 * R, "tile must split over the waves");
+  const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int q = tid + p * NT;
-      if (q >= kBlocks) break;
-      const int ib = q % (R / 8), ob = q / (R / 8);
-      const int i = n0 + ib * 8;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int o = k0 + ob * 8 + r;
-        if (o < g.O && i < g.I) {
-          w[p][r] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
-          sb[p][r] = g.scales[(size_t)o * g.G + i / B];
-        } else {
-          w[p][r] = 0u;
-          sb[p][r] = 0x38u;
-        }
-      }
-    }
+  for (int q = 0; q < kInst; ++q) {
+    const int blk = q * (NT / 64) + wave;
+    const int p = blk * 64 + lane;
+    const int h = p / R, n = p % R;
+    const int o = n0 + n, k = k0 + 32 * h;
+    const uint32_t off = (o < O && k < I) ? (uint32_t)((size_t)o * (I >> 1) + (k >> 1)) : kOOB;
+    dma16(rs, s + blk * 64 * 16, off);
   }
-  __device__ __forceinline__ void commit(uint16_t* s, int tid) const {
-#pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int q = tid + p * NT;
-      if (q >= kBlocks) break;
-      const int ib = q % (R / 8), ob = q / (R / 8);
-      uint32_t rows[8][4], cols[8][4];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const uint4 d = ScaleOperand<FMT>::dequant8(w[p][r], ScaleOperand<FMT>::of(sb[p][r]));
-        rows[r][0] = d.x; rows[r][1] = d.y; rows[r][2] = d.z; rows[r][3] = d.w;
-      }
-      transpose8x8_b16(rows, cols);
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        st_lds16(s, ib * 8 + c, ob, make_uint4(cols[c][0], cols[c][1], cols[c][2], cols[c][3]));
-    }
-  }
-};
+}
 
-// Both DS tiles (X^T rows j in [m0, m0+BM), dY^T rows o in [n0, n0+BN), K = t
-// in [k0, k0+64)) from sources [T, ld] that are contiguous along the tile
-// rows.  The BM + BN 8x8 blocks (A blocks first) are dealt to the threads.
-template <int BM, int BN, int NT>
-struct LoadTransDS {
-  static constexpr int kBlocks = BM + BN;
-  static constexpr int kPer = (kBlocks + NT - 1) / NT;
-  uint4 v[kPer][8];
-  __device__ __forceinline__ void fetch(const GemmArgs& g, int m0, int n0, int k0, int tid) {
-#pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int q = tid + p * NT;
-      if (q >= kBlocks) break;
-      const bool isA = q < BM;
-      const int lq = isA ? q : q - BM;
-      const int rows8 = (isA ? BM : BN) / 8;
-      const int mb = lq % rows8, kb = lq / rows8;
-      const int m = (isA ? m0 : n0) + mb * 8;
-      const int mdim = isA ? g.I : g.O;
-      const uint16_t* src = isA ? g.a : g.b;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int k = k0 + kb * 8 + r;
-        if (k < g.T && m < mdim)
-          v[p][r] = ld_global16(src + (size_t)k * mdim + m);
-        else
-          v[p][r] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  }
-  __device__ __forceinline__ void commit(uint16_t* sa, uint16_t* sb, int tid) const {
-#pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int q = tid + p * NT;
-      if (q >= kBlocks) break;
-      const bool isA = q < BM;
-      const int lq = isA ? q : q - BM;
-      const int rows8 = (isA ? BM : BN) / 8;
-      const int mb = lq % rows8, kb = lq / rows8;
-      uint32_t rows[8][4], cols[8][4];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        rows[r][0] = v[p][r].x; rows[r][1] = v[p][r].y; rows[r][2] = v[p][r].z; rows[r][3] = v[p][r].w;
-      }
-      transpose8x8_b16(rows, cols);
-      uint16_t* s = isA ? sa : sb;
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        st_lds16(s, mb * 8 + c, kb, make_uint4(cols[c][0], cols[c][1], cols[c][2], cols[c][3]));
-    }
-  }
+template <int MODE, int BM, int BN, int NT>
+struct DmaCount {
+  static constexpr int value =
+      MODE == kFwd ? BM / 8 / (NT / 64) + 2 * BN / 64 / (NT / 64)
+    : MODE == kDx  ? BM / 8 / (NT / 64)
+                   : kBK * (BM / 8) / 64 / (NT / 64) + kBK * (BN / 8) / 64 / (NT / 64);
 };
 
 // ------------------------------------------------------------------ tile order
@@ -249,17 +202,33 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
   tn = in / gm;
 }
 
+template <int MODE, int BM, int BN, int STAGES>
+struct SmemLayout {
+  static constexpr int kA = MODE == kDs ? kBK * BM * 2 : BM * kBK * 2;       // bytes per A stage
+  static constexpr int kB = MODE == kFwd ? BN * 32 : kBK * BN * 2;            // bytes per B stage
+  static constexpr int kStage = kA + (MODE == kDx ? 0 : kB);                  // DMA bytes per stage
+  static constexpr int kWBytes = MODE == kDx ? 2 * kB : 0;                    // DX: bf16 W double buffer
+  static constexpr int kBytes = STAGES * kStage + kWBytes;
+};
+
 // ------------------------------------------------------------------ kernel
 // Block tile BM x BN, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN) built
-// from 32x32 MFMA tiles.
-template <int MODE, int FMT, int BM, int BN, int WGM, int WGN>
+// from 32x32 MFMA tiles; STAGES LDS stages for the DMA operands.
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
-  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  uint16_t* sA = smem;                       // [2][BM][64]
-  uint16_t* sB = smem + 2 * BM * kBK;        // [2][BN][64]
+  constexpr int B = ScaleOperand<FMT>::kBlock;
+  using L = SmemLayout<MODE, BM, BN, STAGES>;
+  constexpr int kDma = DmaCount<MODE, BM, BN, NT>::value;   // DMA loads per thread per stage
+  // One static array per DMA stage (distinct objects, so the compiler can see
+  // that a stage being filled does not alias the stage being read).
+  __shared__ __attribute__((aligned(16))) uint8_t lds0[L::kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t lds1[L::kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t lds2[STAGES > 2 ? L::kStage : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t ldsw[MODE == kDx ? L::kWBytes : 16];
+  static_assert(STAGES == 2 || STAGES == 3, "2 or 3 stages");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -269,6 +238,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
+  auto stage = [&](auto SC) -> SQ_LDS uint8_t* {
+    constexpr int S = decltype(SC)::value;
+    if constexpr (S == 0) return (SQ_LDS uint8_t*)lds0;
+    else if constexpr (S == 1) return (SQ_LDS uint8_t*)lds1;
+    else return (SQ_LDS uint8_t*)lds2;
+  };
+
+  __amdgpu_buffer_rsrc_t ra, rb;
+  if constexpr (MODE == kFwd) {
+    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+    rb = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
+  } else if constexpr (MODE == kDx) {
+    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.O * 2));
+  } else {
+    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+    rb = make_rsrc(g.b, (uint32_t)((size_t)g.T * g.O * 2));
+  }
+
   f32x16 acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -277,65 +264,184 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  LoadKContig<BM, NT> la_k;          // FWD: X, DX: dY
-  LoadWKContig<BN, FMT, NT> lb_w;    // FWD
-  LoadWTrans<BN, FMT, NT> lb_wt;     // DX
-  LoadTransDS<BM, BN, NT> l_ds;      // DS
-
-  auto fetch = [&](int k0) {
-    if constexpr (MODE == kFwd) {
-      la_k.fetch(g.a, g.I, g.T, g.I, m0, k0, tid);
-      lb_w.fetch(g, n0, k0, tid);
-    } else if constexpr (MODE == kDx) {
-      la_k.fetch(g.a, g.O, g.T, g.O, m0, k0, tid);
-      lb_wt.fetch(g, n0, k0, tid);
-    } else {
-      l_ds.fetch(g, m0, n0, k0, tid);
-    }
-  };
-  auto commit = [&](int buf) {
-    uint16_t* a = sA + buf * BM * kBK;
-    uint16_t* b = sB + buf * BN * kBK;
-    if constexpr (MODE == kFwd) {
-      la_k.commit(a, tid);
-      lb_w.commit(b, tid);
-    } else if constexpr (MODE == kDx) {
-      la_k.commit(a, tid);
-      lb_wt.commit(b, tid);
-    } else {
-      l_ds.commit(a, b, tid);
-    }
-  };
-
   const int nk = (g.K + kBK - 1) / kBK;
-  if (nk > 0) {
-    fetch(0);
-    commit(0);
-    __syncthreads();
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) fetch((kt + 1) * kBK);
-    const uint16_t* a = sA + buf * BM * kBK;
-    const uint16_t* b = sB + buf * BN * kBK;
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int chunk = kk * 2 + (lane >> 5);
-      bf16x8 fa[TM], fb[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        fa[i] = *reinterpret_cast<const bf16x8*>(a + lds_off(wm0 + i * 32 + (lane & 31), chunk));
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        fb[j] = *reinterpret_cast<const bf16x8*>(b + lds_off(wn0 + j * 32 + (lane & 31), chunk));
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+
+  // ---- DMA of one K stage into stage buffer SC
+  auto issue_dma = [&](auto SC, int kt) {
+    SQ_LDS uint8_t* st = stage(SC);
+    const int k0 = kt * kBK;
+    if constexpr (MODE == kFwd) {
+      dma_kc<BM, NT>(ra, (SQ_LDS uint16_t*)st, g.I, g.T, g.I, m0, k0, tid);
+      dma_wpack<BN, NT>(rb, st + L::kA, g.O, g.I, n0, k0, tid);
+    } else if constexpr (MODE == kDx) {
+      dma_kc<BM, NT>(ra, (SQ_LDS uint16_t*)st, g.O, g.T, g.O, m0, k0, tid);
+    } else {
+      dma_nat<BM, NT>(ra, (SQ_LDS uint16_t*)st, g.I, g.I, g.T, m0, k0, tid);
+      dma_nat<BN, NT>(rb, (SQ_LDS uint16_t*)(st + L::kA), g.O, g.O, g.T, n0, k0, tid);
     }
-    if (kt + 1 < nk) commit(buf ^ 1);
-    __syncthreads();
+  };
+
+  // ---- FWD: block scales of this lane's W fragments, one k-stage ahead
+  constexpr int kSB = (MODE == kFwd) ? TN * (B == 16 ? 2 : 1) : 1;
+  uint32_t sb_next[kSB], sb_cur[kSB];
+  auto load_scales = [&](int kt) {
+    if constexpr (MODE == kFwd) {
+      const int h = lane >> 5;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int o = n0 + wn0 + j * 32 + (lane & 31);
+#pragma unroll
+        for (int u = 0; u < kSB / TN; ++u) {
+          const int k = kt * kBK + 32 * h + 16 * u;
+          sb_next[j * (kSB / TN) + u] = (o < g.O && k < g.I) ? g.scales[(size_t)o * g.G + k / B] : 0x38u;
+        }
+      }
+    }
+  };
+
+  // ---- DX: W^T stage through registers: dwords of 8 codes along i, per o-row
+  constexpr int kWPer = (MODE == kDx) ? kBK * (BN / 8) / NT : 1;
+  static_assert(MODE != kDx || kWPer * NT == kBK * (BN / 8), "W tile must split over the threads");
+  uint32_t w_reg[kWPer], w_sb[kWPer];
+  auto load_w = [&](int kt) {
+    if constexpr (MODE == kDx) {
+#pragma unroll
+      for (int p = 0; p < kWPer; ++p) {
+        const int idx = tid + p * NT;
+        const int kr = idx / (BN / 8), ic = idx % (BN / 8);
+        const int o = kt * kBK + kr, i = n0 + ic * 8;
+        if (o < g.O && i < g.I) {
+          w_reg[p] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
+          w_sb[p] = g.scales[(size_t)o * g.G + i / B];
+        } else {
+          w_reg[p] = 0u;
+          w_sb[p] = 0x38u;
+        }
+      }
+    }
+  };
+  auto wbuf = [&](int kt) { return (SQ_LDS uint16_t*)((SQ_LDS uint8_t*)ldsw + (kt & 1) * L::kB); };
+  auto commit_w = [&](int kt) {
+    if constexpr (MODE == kDx) {
+      SQ_LDS uint16_t* s = wbuf(kt);
+#pragma unroll
+      for (int p = 0; p < kWPer; ++p) {
+        const int idx = tid + p * NT;
+        const int kr = idx / (BN / 8), ic = idx % (BN / 8);
+        const uint4 d = ScaleOperand<FMT>::dequant8(w_reg[p], ScaleOperand<FMT>::of(w_sb[p]));
+        u32x4 v;
+        __builtin_memcpy(&v, &d, 16);
+        *(SQ_LDS u32x4*)(s + nat_off<BN>(kr, ic * 8)) = v;
+      }
+    }
+  };
+
+  // ---- one K stage: wait for its data, refill the oldest stage, multiply
+  auto step = [&](auto SC, int kt) {
+    constexpr int S = decltype(SC)::value;
+    constexpr int SNEXT = (S + STAGES - 1) % STAGES;          // stage that receives kt + STAGES - 1
+    // stage kt is complete once only the DMA of later stages is outstanding
+    const int later = min(STAGES - 2, nk - 1 - kt);
+    if (later >= 1) wait_vm_lgkm0<kDma>();
+    else wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (MODE == kFwd) {
+#pragma unroll
+      for (int u = 0; u < kSB; ++u) sb_cur[u] = sb_next[u];
+      if (kt + 1 < nk) load_scales(kt + 1);
+    }
+    if constexpr (MODE == kDx) {
+      if (kt + 1 < nk) load_w(kt + 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + STAGES - 1 < nk) issue_dma(std::integral_constant<int, SNEXT>{}, kt + STAGES - 1);
+    __builtin_amdgcn_sched_barrier(0);
+
+    SQ_LDS uint8_t* st = stage(SC);
+    if constexpr (MODE == kFwd) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS u32x4* wb = (const SQ_LDS u32x4*)(st + L::kA);
+      const int h = lane >> 5;
+      u32x4 wv[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wv[j] = wb[h * BN + wn0 + j * 32 + (lane & 31)];
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        bf16x8 fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 4 * h + kk));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const uint32_t w = wv[j][kk];
+          const uint32_t sbyte = (B == 16) ? sb_cur[2 * j + (kk >> 1)] : sb_cur[j];
+          const uint4 d = ScaleOperand<FMT>::dequant8(w, ScaleOperand<FMT>::of(sbyte));
+          __builtin_memcpy(&fb[j], &d, 16);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+    } else if constexpr (MODE == kDx) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = wbuf(kt);
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        bf16x8 fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 2 * kk + (lane >> 5)));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fb[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+      if (kt + 1 < nk) commit_w(kt + 1);
+    } else {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        bf16x8 fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) fa[i] = nat_frag<BM>(a, kk, wm0 + i * 32, lane);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fb[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+
+  // ---- prologue: the first STAGES-1 stages in flight
+  if constexpr (MODE == kDx) {
+    if (nk > 0) { load_w(0); commit_w(0); }
+  }
+  if constexpr (MODE == kFwd) {
+    if (nk > 0) load_scales(0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (0 < nk) issue_dma(std::integral_constant<int, 0>{}, 0);
+  if constexpr (STAGES > 2) {
+    if (1 < nk) issue_dma(std::integral_constant<int, 1>{}, 1);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  for (int kt0 = 0; kt0 < nk; kt0 += STAGES) {
+    step(std::integral_constant<int, 0>{}, kt0);
+    if (kt0 + 1 < nk) step(std::integral_constant<int, 1>{}, kt0 + 1);
+    if constexpr (STAGES > 2) {
+      if (kt0 + 2 < nk) step(std::integral_constant<int, 2>{}, kt0 + 2);
+    }
   }
 
   // ---------------------------------------------------------------- epilogue
@@ -403,31 +509,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 }
 
 // Tile configurations (compile-time; SQ_CFG_* selects one per product for
-// tuning builds).  Each entry: BM, BN, waves along M, waves along N.
+// tuning builds).  Each entry: BM, BN, waves along M, waves along N, stages.
 #ifndef SQ_CFG_FWD
-#define SQ_CFG_FWD 256, 256, 4, 2
+#define SQ_CFG_FWD 256, 256, 2, 2, 3
 #endif
 #ifndef SQ_CFG_DX
-#define SQ_CFG_DX 256, 256, 2, 2
+#define SQ_CFG_DX 128, 256, 2, 4, 3
 #endif
 #ifndef SQ_CFG_DS
-#define SQ_CFG_DS 256, 256, 4, 2
+#define SQ_CFG_DS 256, 256, 4, 2, 2
 #endif
 
-template <int MODE, int FMT, int BM, int BN, int WGM, int WGN>
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES>
 static int launch_gemm(const GemmArgs& g, hipStream_t s) {
-  const size_t lds = (size_t)2 * (BM + BN) * kBK * sizeof(uint16_t);
+  using L = SmemLayout<MODE, BM, BN, STAGES>;
+  static_assert(L::kBytes <= 160 * 1024, "LDS budget");
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return 0;
-  auto kern = gemm_kernel<MODE, FMT, BM, BN, WGM, WGN>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
-      return -1;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL(kern, dim3(tiles), dim3(64 * WGM * WGN), lds, s, g);
+  hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES>), dim3(tiles), dim3(64 * WGM * WGN), 0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
