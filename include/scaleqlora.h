@@ -37,8 +37,9 @@
  *           Every call only enqueues work on it and returns; nothing is
  *           synchronised.  Calls are reentrant and thread-safe.
  * Shapes    T >= 0; O >= 1, O % 8 == 0; I >= 1, I % B == 0.  T == 0 is legal:
- *           Y and dX are empty and dS is written as zeros.  Every dimension and
- *           every buffer size must stay below 2^31 elements.
+ *           Y and dX are empty and dS is written as zeros.  Every dimension
+ *           stays below 2^31, and X, dY and the code plane each stay below
+ *           2 GiB (T*I*2, T*O*2 and O*I/2 bytes).
  * Alignment X, dY, Y, dX: 16 bytes.  codes: 4 bytes.  dS: 4 bytes.
  *           Merge scale planes, deltas and sources: 16 bytes.
  * Errors    arguments are checked on the host before anything is enqueued; a

@@ -18,10 +18,17 @@ int block_of(int fmt) { return fmt == SQ_MXFP4 ? 32 : 16; }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
+// The GEMM kernels address each operand through one buffer resource with a
+// 32-bit byte range (offsets from 2^31 up read as zeros), so every operand
+// must stay below 2 GiB.
+constexpr int64_t kOperandBytesMax = (int64_t(1) << 31) - 16;
+
 int check_layer(int fmt, int64_t T, int64_t O, int64_t I) {
   if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
   if (T < 0 || O < 1 || I < 1 || T > kDimMax || O > kDimMax || I > kDimMax) return SQ_ERR_SHAPE;
   if (O % 8 != 0 || I % block_of(fmt) != 0) return SQ_ERR_SHAPE;
+  if (T * I * 2 > kOperandBytesMax || T * O * 2 > kOperandBytesMax || O * I / 2 > kOperandBytesMax)
+    return SQ_ERR_SHAPE;
   return SQ_OK;
 }
 

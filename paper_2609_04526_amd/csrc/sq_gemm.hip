@@ -45,7 +45,9 @@
 
 namespace sq {
 
-enum Mode { kFwd = 0, kDx = 1, kDs = 2 };
+// kFwdR is the forward with W dequantised once per workgroup into a bf16
+// K-contiguous LDS tile (instead of per wave from packed codes in LDS).
+enum Mode { kFwd = 0, kDx = 1, kDs = 2, kFwdR = 3 };
 
 constexpr int kBK = 64;                 // K per LDS stage
 constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
@@ -91,7 +93,7 @@ __device__ __forceinline__ void wait_vm_lgkm0() {
 __device__ __forceinline__ int swz_kc(int r) { return (r ^ (r >> 3)) & 7; }
 __device__ __forceinline__ int kc_off(int r, int c) { return r * kBK + ((c ^ swz_kc(r)) << 3); }
 
-// NAT: [64][R] bf16 with R elements per k-row; 16-byte chunk c of row k lives
+// NAT: [BK][R] bf16 with R elements per k-row; 16-byte chunk c of row k lives
 // at chunk c ^ swz_nat(k): each of the 4 rows a 16-lane transpose read spans
 // lands in its own 64-byte slot.
 template <int R>
@@ -117,71 +119,116 @@ __device__ __forceinline__ bf16x8 nat_frag(const SQ_LDS uint16_t* s, int kk, int
 }
 
 // ------------------------------------------------------------------ DMA issue
-// KC tile: rows [r0, r0+R) of a [rows_total, ld] bf16 matrix, k in [k0, k0+64).
-// One wave instruction fills 8 consecutive LDS rows (1 KiB).
+// Each thread issues the same set of 16-byte buffer->LDS loads every stage,
+// at byte offsets that advance by a fixed step per stage.  The offsets, their
+// per-stage step and the K limit of each load are computed once.
+//
+// KC tile: rows [r0, r0+R) of a [rows_total, ld] bf16 matrix, k in
+// [k0, k0+64); one wave instruction fills 8 consecutive LDS rows (1 KiB).
+// Rows past the matrix read zeros from the buffer bound; k past kdim is
+// masked explicitly on a ragged last stage.
 template <int R, int NT>
-__device__ __forceinline__ void dma_kc(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int ld, int rows_total,
-                                       int kdim, int r0, int k0, int tid) {
-  constexpr int kInst = R / 8 / (NT / 64);
+struct DmaKC {
+  static constexpr int kInst = R / 8 / (NT / 64);
   static_assert(kInst * (NT / 64) * 8 == R, "tile rows must split over the waves");
-  const int wave = tid >> 6, lane = tid & 63;
+  uint32_t off[kInst];      // byte offset at k0 = 0 (kOOB if the row is outside)
+  int klim[kInst];          // the load is valid while k0 < klim
+  __device__ __forceinline__ void init(int ld, int rows_total, int kdim, int r0, int tid) {
+    const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
-  for (int q = 0; q < kInst; ++q) {
-    const int blk = q * (NT / 64) + wave;
-    const int r = blk * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ swz_kc(r);
-    const int gr = r0 + r, gk = k0 + c * 8;
-    const uint32_t off = (gr < rows_total && gk < kdim) ? (uint32_t)((size_t)gr * ld + gk) * 2u : kOOB;
-    dma16(rs, s + blk * 8 * kBK, off);
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      const int r = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ swz_kc(r);
+      const int gr = r0 + r;
+      off[q] = gr < rows_total ? (uint32_t)((size_t)gr * ld + c * 8) * 2u : kOOB;
+      klim[q] = kdim - c * 8;
+    }
   }
-}
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int k0, bool full,
+                                        int wave) const {
+#pragma unroll
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      uint32_t o = off[q] + (uint32_t)k0 * 2u;
+      if (!full && k0 >= klim[q]) o = kOOB;
+      dma16(rs, s + blk * 8 * kBK, o);
+    }
+  }
+};
 
-// NAT tile: k-rows [k0, k0+64) of a [kdim, ld] bf16 matrix, columns [m0, m0+R).
-template <int R, int NT>
-__device__ __forceinline__ void dma_nat(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int ld, int mdim,
-                                        int kdim, int m0, int k0, int tid) {
-  constexpr int kCpr = R / 8;                       // chunks per row
-  constexpr int kInst = kBK * kCpr / 64 / (NT / 64);
-  static_assert(kInst * (NT / 64) * 64 == kBK * kCpr, "tile must split over the waves");
-  const int wave = tid >> 6, lane = tid & 63;
+// NAT tile: k-rows [k0, k0+BK) of a [kdim, ld] bf16 matrix, columns [m0, m0+R).
+// Rows past kdim fall past the buffer's end and read zeros; columns past mdim
+// only feed accumulators of rows/columns that are never stored.
+template <int R, int NT, int BK>
+struct DmaNat {
+  static constexpr int kCpr = R / 8;                       // chunks per row
+  static constexpr int kInst = BK * kCpr / 64 / (NT / 64);
+  static_assert(kInst * (NT / 64) * 64 == BK * kCpr, "tile must split over the waves");
+  uint32_t off[kInst];
+  __device__ __forceinline__ void init(int ld, int mdim, int m0, int tid) {
+    const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
-  for (int q = 0; q < kInst; ++q) {
-    const int blk = q * (NT / 64) + wave;
-    const int p = blk * 64 + lane;
-    const int k = p / kCpr, pc = p % kCpr;
-    const int c = pc ^ swz_nat<R>(k);
-    const int gk = k0 + k, gm = m0 + c * 8;
-    const uint32_t off = (gk < kdim && gm < mdim) ? (uint32_t)((size_t)gk * ld + gm) * 2u : kOOB;
-    dma16(rs, s + blk * 64 * 8, off);
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      const int p = blk * 64 + lane;
+      const int k = p / kCpr, pc = p % kCpr;
+      const int c = pc ^ swz_nat<R>(k);
+      const int gm = m0 + c * 8;
+      off[q] = gm < mdim ? (uint32_t)((size_t)k * ld + gm) * 2u : kOOB;
+    }
   }
-}
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
+                                        int wave) const {
+#pragma unroll
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      const uint32_t o = off[q] == kOOB ? kOOB : off[q] + kstep_bytes;
+      dma16(rs, s + blk * 64 * 8, o);
+    }
+  }
+};
 
 // Packed W tile for FWD: LDS [2][R][16 bytes]; entry (h, n) holds the 32 codes
 // of row n0+n at k0+32h .. k0+32h+31.
 template <int R, int NT>
-__device__ __forceinline__ void dma_wpack(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint8_t* s, int O, int I,
-                                          int n0, int k0, int tid) {
-  constexpr int kInst = 2 * R / 64 / (NT / 64);
+struct DmaWPack {
+  static constexpr int kInst = 2 * R / 64 / (NT / 64);
   static_assert(kInst * (NT / 64) * 64 == 2 * R, "tile must split over the waves");
-  const int wave = tid >> 6, lane = tid & 63;
+  uint32_t off[kInst];
+  int klim[kInst];
+  __device__ __forceinline__ void init(int O, int I, int n0, int tid) {
+    const int wave = tid >> 6, lane = tid & 63;
 #pragma unroll
-  for (int q = 0; q < kInst; ++q) {
-    const int blk = q * (NT / 64) + wave;
-    const int p = blk * 64 + lane;
-    const int h = p / R, n = p % R;
-    const int o = n0 + n, k = k0 + 32 * h;
-    const uint32_t off = (o < O && k < I) ? (uint32_t)((size_t)o * (I >> 1) + (k >> 1)) : kOOB;
-    dma16(rs, s + blk * 64 * 16, off);
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      const int p = blk * 64 + lane;
+      const int h = p / R, n = p % R;
+      const int o = n0 + n;
+      off[q] = o < O ? (uint32_t)((size_t)o * (I >> 1) + 16 * h) : kOOB;
+      klim[q] = I - 32 * h;
+    }
   }
-}
-
-template <int MODE, int BM, int BN, int NT>
-struct DmaCount {
-  static constexpr int value =
-      MODE == kFwd ? BM / 8 / (NT / 64) + 2 * BN / 64 / (NT / 64)
-    : MODE == kDx  ? BM / 8 / (NT / 64)
-                   : kBK * (BM / 8) / 64 / (NT / 64) + kBK * (BN / 8) / 64 / (NT / 64);
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint8_t* s, int k0, bool full,
+                                        int wave) const {
+#pragma unroll
+    for (int q = 0; q < kInst; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      uint32_t o = off[q] == kOOB ? kOOB : off[q] + (uint32_t)(k0 >> 1);
+      if (!full && k0 >= klim[q]) o = kOOB;
+      dma16(rs, s + blk * 64 * 16, o);
+    }
+  }
 };
+
+// 16-byte DMA loads each thread issues per stage (only the mode's own
+// operand layouts are instantiated)
+template <int MODE, int BM, int BN, int NT, int BK>
+__host__ __device__ constexpr int dma_count() {
+  if constexpr (MODE == kFwd) return DmaKC<BM, NT>::kInst + DmaWPack<BN, NT>::kInst;
+  else if constexpr (MODE == kDx || MODE == kFwdR) return DmaKC<BM, NT>::kInst;
+  else return DmaNat<BM, NT, BK>::kInst + DmaNat<BN, NT, BK>::kInst;
+}
 
 // ------------------------------------------------------------------ tile order
 // Workgroup w runs on XCD w % 8, and each XCD has its own L2.  Tiles are
@@ -202,33 +249,38 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
   tn = in / gm;
 }
 
-template <int MODE, int BM, int BN, int STAGES>
+template <int MODE, int BM, int BN, int STAGES, int BK>
 struct SmemLayout {
-  static constexpr int kA = MODE == kDs ? kBK * BM * 2 : BM * kBK * 2;       // bytes per A stage
-  static constexpr int kB = MODE == kFwd ? BN * 32 : kBK * BN * 2;            // bytes per B stage
-  static constexpr int kStage = kA + (MODE == kDx ? 0 : kB);                  // DMA bytes per stage
-  static constexpr int kWBytes = MODE == kDx ? 2 * kB : 0;                    // DX: bf16 W double buffer
+  static constexpr int kA = BM * BK * 2;                                      // bytes per A stage
+  static constexpr int kB = MODE == kFwd ? BN * 32 : BK * BN * 2;             // bytes per B stage
+  static constexpr bool kWReg = MODE == kDx || MODE == kFwdR;                 // W staged through registers
+  static constexpr int kStage = kA + (kWReg ? 0 : kB);                        // DMA bytes per stage
+  static constexpr int kWBytes = kWReg ? 2 * kB : 0;                          // bf16 W double buffer
   static constexpr int kBytes = STAGES * kStage + kWBytes;
 };
 
 // ------------------------------------------------------------------ kernel
 // Block tile BM x BN, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN) built
 // from 32x32 MFMA tiles; STAGES LDS stages for the DMA operands.
-template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES>
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int B = ScaleOperand<FMT>::kBlock;
-  using L = SmemLayout<MODE, BM, BN, STAGES>;
-  constexpr int kDma = DmaCount<MODE, BM, BN, NT>::value;   // DMA loads per thread per stage
+  static_assert(MODE == kDs || BK == kBK, "K-contiguous tiles use 64-wide stages");
+  static_assert(BK == 32 || BK == 64, "stage depth");
+  using L = SmemLayout<MODE, BM, BN, STAGES, BK>;
+  constexpr bool kWReg = L::kWReg;
+  constexpr int kDma = dma_count<MODE, BM, BN, NT, BK>();   // DMA loads per thread per stage
   // One static array per DMA stage (distinct objects, so the compiler can see
   // that a stage being filled does not alias the stage being read).
   __shared__ __attribute__((aligned(16))) uint8_t lds0[L::kStage];
   __shared__ __attribute__((aligned(16))) uint8_t lds1[L::kStage];
   __shared__ __attribute__((aligned(16))) uint8_t lds2[STAGES > 2 ? L::kStage : 16];
-  __shared__ __attribute__((aligned(16))) uint8_t ldsw[MODE == kDx ? L::kWBytes : 16];
-  static_assert(STAGES == 2 || STAGES == 3, "2 or 3 stages");
+  __shared__ __attribute__((aligned(16))) uint8_t lds3[STAGES > 3 ? L::kStage : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t ldsw[kWReg ? L::kWBytes : 16];
+  static_assert(STAGES >= 2 && STAGES <= 4, "2 to 4 stages");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -242,13 +294,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     constexpr int S = decltype(SC)::value;
     if constexpr (S == 0) return (SQ_LDS uint8_t*)lds0;
     else if constexpr (S == 1) return (SQ_LDS uint8_t*)lds1;
-    else return (SQ_LDS uint8_t*)lds2;
+    else if constexpr (S == 2) return (SQ_LDS uint8_t*)lds2;
+    else return (SQ_LDS uint8_t*)lds3;
   };
 
   __amdgpu_buffer_rsrc_t ra, rb;
   if constexpr (MODE == kFwd) {
     ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
     rb = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
+  } else if constexpr (MODE == kFwdR) {
+    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
   } else if constexpr (MODE == kDx) {
     ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.O * 2));
   } else {
@@ -264,20 +319,41 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = (g.K + kBK - 1) / kBK;
+  const int nk = (g.K + BK - 1) / BK;
 
   // ---- DMA of one K stage into stage buffer SC
+  using DA_kc = std::conditional_t<MODE != kDs, DmaKC<BM, NT>, DmaKC<8 * NT / 64, NT>>;  // unused in DS
+  using DB_w = std::conditional_t<MODE == kFwd, DmaWPack<BN, NT>, DmaWPack<NT / 2, NT>>;
+  using DA_nat = std::conditional_t<MODE == kDs, DmaNat<BM, NT, BK>, DmaNat<512, NT, 64>>;
+  using DB_nat = std::conditional_t<MODE == kDs, DmaNat<BN, NT, BK>, DmaNat<512, NT, 64>>;
+  DA_kc dA_kc;
+  DB_w dB_w;
+  DA_nat dA_nat;
+  DB_nat dB_nat;
+  if constexpr (MODE == kFwd) {
+    dA_kc.init(g.I, g.T, g.I, m0, tid);
+    dB_w.init(g.O, g.I, n0, tid);
+  } else if constexpr (MODE == kFwdR) {
+    dA_kc.init(g.I, g.T, g.I, m0, tid);
+  } else if constexpr (MODE == kDx) {
+    dA_kc.init(g.O, g.T, g.O, m0, tid);
+  } else {
+    dA_nat.init(g.I, g.I, m0, tid);
+    dB_nat.init(g.O, g.O, n0, tid);
+  }
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto issue_dma = [&](auto SC, int kt) {
     SQ_LDS uint8_t* st = stage(SC);
-    const int k0 = kt * kBK;
+    const int k0 = kt * BK;
+    const bool full = k0 + BK <= g.K;
     if constexpr (MODE == kFwd) {
-      dma_kc<BM, NT>(ra, (SQ_LDS uint16_t*)st, g.I, g.T, g.I, m0, k0, tid);
-      dma_wpack<BN, NT>(rb, st + L::kA, g.O, g.I, n0, k0, tid);
-    } else if constexpr (MODE == kDx) {
-      dma_kc<BM, NT>(ra, (SQ_LDS uint16_t*)st, g.O, g.T, g.O, m0, k0, tid);
+      dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
+      dB_w.issue(rb, st + L::kA, k0, full, wave_u);
+    } else if constexpr (MODE == kFwdR || MODE == kDx) {
+      dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
     } else {
-      dma_nat<BM, NT>(ra, (SQ_LDS uint16_t*)st, g.I, g.I, g.T, m0, k0, tid);
-      dma_nat<BN, NT>(rb, (SQ_LDS uint16_t*)(st + L::kA), g.O, g.O, g.T, n0, k0, tid);
+      dA_nat.issue(ra, (SQ_LDS uint16_t*)st, (uint32_t)k0 * (uint32_t)g.I * 2u, wave_u);
+      dB_nat.issue(rb, (SQ_LDS uint16_t*)(st + L::kA), (uint32_t)k0 * (uint32_t)g.O * 2u, wave_u);
     }
   };
 
@@ -299,17 +375,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     }
   };
 
-  // ---- DX: W^T stage through registers: dwords of 8 codes along i, per o-row
-  constexpr int kWPer = (MODE == kDx) ? kBK * (BN / 8) / NT : 1;
-  static_assert(MODE != kDx || kWPer * NT == kBK * (BN / 8), "W tile must split over the threads");
+  // ---- W through registers (DX: W^T tile [64 o][BN i]; FWDR: W tile
+  // [BN o][64 i]), one dword of 8 codes along i per item, dequantised and
+  // written to LDS as bf16
+  constexpr int kWPer = kWReg ? kBK * (BN / 8) / NT : 1;
+  static_assert(!kWReg || kWPer * NT == kBK * (BN / 8), "W tile must split over the threads");
   uint32_t w_reg[kWPer], w_sb[kWPer];
-  auto load_w = [&](int kt) {
+  auto w_item = [&](int p, int kt, int& o, int& i) {
+    const int idx = tid + p * NT;
     if constexpr (MODE == kDx) {
+      o = kt * kBK + idx / (BN / 8);
+      i = n0 + (idx % (BN / 8)) * 8;
+    } else {
+      o = n0 + idx / 8;
+      i = kt * kBK + (idx % 8) * 8;
+    }
+  };
+  auto load_w = [&](int kt) {
+    if constexpr (kWReg) {
 #pragma unroll
       for (int p = 0; p < kWPer; ++p) {
-        const int idx = tid + p * NT;
-        const int kr = idx / (BN / 8), ic = idx % (BN / 8);
-        const int o = kt * kBK + kr, i = n0 + ic * 8;
+        int o, i;
+        w_item(p, kt, o, i);
         if (o < g.O && i < g.I) {
           w_reg[p] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
           w_sb[p] = g.scales[(size_t)o * g.G + i / B];
@@ -322,16 +409,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   };
   auto wbuf = [&](int kt) { return (SQ_LDS uint16_t*)((SQ_LDS uint8_t*)ldsw + (kt & 1) * L::kB); };
   auto commit_w = [&](int kt) {
-    if constexpr (MODE == kDx) {
+    if constexpr (kWReg) {
       SQ_LDS uint16_t* s = wbuf(kt);
 #pragma unroll
       for (int p = 0; p < kWPer; ++p) {
         const int idx = tid + p * NT;
-        const int kr = idx / (BN / 8), ic = idx % (BN / 8);
         const uint4 d = ScaleOperand<FMT>::dequant8(w_reg[p], ScaleOperand<FMT>::of(w_sb[p]));
         u32x4 v;
         __builtin_memcpy(&v, &d, 16);
-        *(SQ_LDS u32x4*)(s + nat_off<BN>(kr, ic * 8)) = v;
+        if constexpr (MODE == kDx)
+          *(SQ_LDS u32x4*)(s + nat_off<BN>(idx / (BN / 8), (idx % (BN / 8)) * 8)) = v;
+        else
+          *(SQ_LDS u32x4*)(s + kc_off(idx / 8, idx % 8)) = v;
       }
     }
   };
@@ -342,7 +431,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     constexpr int SNEXT = (S + STAGES - 1) % STAGES;          // stage that receives kt + STAGES - 1
     // stage kt is complete once only the DMA of later stages is outstanding
     const int later = min(STAGES - 2, nk - 1 - kt);
-    if (later >= 1) wait_vm_lgkm0<kDma>();
+    if (later >= 2) wait_vm_lgkm0<(2 * kDma < 63 ? 2 * kDma : 63)>();
+    else if (later == 1) wait_vm_lgkm0<kDma>();
     else wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
@@ -351,7 +441,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
       for (int u = 0; u < kSB; ++u) sb_cur[u] = sb_next[u];
       if (kt + 1 < nk) load_scales(kt + 1);
     }
-    if constexpr (MODE == kDx) {
+    if constexpr (kWReg) {
       if (kt + 1 < nk) load_w(kt + 1);
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -385,6 +475,26 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
+    } else if constexpr (MODE == kFwdR) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = wbuf(kt);
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        const int chunk = 2 * kk + (lane >> 5);
+        bf16x8 fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), chunk));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          fb[j] = *(const SQ_LDS bf16x8*)(b + kc_off(wn0 + j * 32 + (lane & 31), chunk));
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+      if (kt + 1 < nk) commit_w(kt + 1);
     } else if constexpr (MODE == kDx) {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = wbuf(kt);
@@ -407,7 +517,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
 #pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
+      for (int kk = 0; kk < BK / 16; ++kk) {
         bf16x8 fa[TM], fb[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i) fa[i] = nat_frag<BM>(a, kk, wm0 + i * 32, lane);
@@ -423,7 +533,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   };
 
   // ---- prologue: the first STAGES-1 stages in flight
-  if constexpr (MODE == kDx) {
+  if constexpr (kWReg) {
     if (nk > 0) { load_w(0); commit_w(0); }
   }
   if constexpr (MODE == kFwd) {
@@ -434,6 +544,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   if constexpr (STAGES > 2) {
     if (1 < nk) issue_dma(std::integral_constant<int, 1>{}, 1);
   }
+  if constexpr (STAGES > 3) {
+    if (2 < nk) issue_dma(std::integral_constant<int, 2>{}, 2);
+  }
   __builtin_amdgcn_sched_barrier(0);
 
   for (int kt0 = 0; kt0 < nk; kt0 += STAGES) {
@@ -442,13 +555,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     if constexpr (STAGES > 2) {
       if (kt0 + 2 < nk) step(std::integral_constant<int, 2>{}, kt0 + 2);
     }
+    if constexpr (STAGES > 3) {
+      if (kt0 + 3 < nk) step(std::integral_constant<int, 3>{}, kt0 + 3);
+    }
   }
 
   // ---------------------------------------------------------------- epilogue
   // 32x32 output tile: lane l, register r holds row 8*(r/4) + 4*(l/32) + r%4,
   // column l%32.
   const int lrow = 4 * (lane >> 5), lcol = lane & 31;
-  if constexpr (MODE == kFwd || MODE == kDx) {
+  if constexpr (MODE != kDs) {
     const float f = g.ws2;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -509,24 +625,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 }
 
 // Tile configurations (compile-time; SQ_CFG_* selects one per product for
-// tuning builds).  Each entry: BM, BN, waves along M, waves along N, stages.
+// tuning builds).  Each entry: BM, BN, waves along M, waves along N, stages,
+// K per stage.
+#ifndef SQ_FWD_MODE
+#define SQ_FWD_MODE kFwdR
+#endif
 #ifndef SQ_CFG_FWD
-#define SQ_CFG_FWD 256, 256, 2, 2, 3
+#define SQ_CFG_FWD 256, 256, 4, 2, 2, 64
 #endif
 #ifndef SQ_CFG_DX
-#define SQ_CFG_DX 128, 256, 2, 4, 3
+#define SQ_CFG_DX 256, 256, 4, 2, 2, 64
 #endif
 #ifndef SQ_CFG_DS
-#define SQ_CFG_DS 256, 256, 4, 2, 2
+#define SQ_CFG_DS 256, 256, 4, 2, 2, 64
 #endif
 
-template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES>
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 static int launch_gemm(const GemmArgs& g, hipStream_t s) {
-  using L = SmemLayout<MODE, BM, BN, STAGES>;
+  using L = SmemLayout<MODE, BM, BN, STAGES, BK>;
   static_assert(L::kBytes <= 160 * 1024, "LDS budget");
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return 0;
-  hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES>), dim3(tiles), dim3(64 * WGM * WGN), 0, s, g);
+  hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(tiles), dim3(64 * WGM * WGN), 0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -540,7 +660,7 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
   g.M = T; g.N = O; g.K = I;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = y_bf16;
-  return fmt == kMX ? launch_gemm<kFwd, kMX, SQ_CFG_FWD>(g, s) : launch_gemm<kFwd, kNV, SQ_CFG_FWD>(g, s);
+  return fmt == kMX ? launch_gemm<SQ_FWD_MODE, kMX, SQ_CFG_FWD>(g, s) : launch_gemm<SQ_FWD_MODE, kNV, SQ_CFG_FWD>(g, s);
 }
 
 int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,

@@ -62,6 +62,7 @@ def _fwd(lib, fmt=0, T=64, O=256, I=512, X=FAKE, codes=FAKE, scales=FAKE, ws2=1.
     (dict(fmt=1, I=40), -2),               # NV needs I % 16
     (dict(T=-1), -2),
     (dict(I=1 << 31), -2),
+    (dict(T=1 << 17, I=1 << 13), -2),      # X would reach 2 GiB
     (dict(dt=7), -1),
     (dict(codes=None), -1),
     (dict(X=None), -1),
