@@ -105,37 +105,44 @@ def merged_weight_bf16(codes_d, sb_d, sq):
 
 
 def model_merge(sq, steps):
-    """Grouped delta merge over every MXFP4 scale plane of the 8B model
-    (32 layers x 7 linears, 218,103,808 scale bytes); 6 bytes per scale."""
-    planes = []
-    total = 0
-    for layer in range(inputs.LLAMA8B_LAYERS):
-        for k, (_, o, i) in enumerate(inputs.LLAMA8B_LAYER):
-            n = o * (i // 32)
-            total += n
-            planes.append(n)
-    scales = torch.randint(100, 140, (total,), dtype=torch.uint8, device="cuda")
-    delta = (torch.randn(total, device="cuda") * 1e-3).float()
-    descs = []
-    off = 0
-    for n in planes:
-        descs.append(dict(fmt="mx", scales=scales[off:off + n], delta=delta[off:off + n]))
-        off += n
-    group = sq.MergeGroup(descs)
-    for _ in range(3):
-        sq.sq_merge_scales_grouped(group)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        sq.sq_merge_scales_grouped(group)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
-    nbytes = 6 * total
-    gbs = nbytes / (ms * 1e-3) / 1e9
-    return {"scales": total, "planes": len(planes), "bytes_per_scale": 6, "ms": round(ms, 4),
-            "GB/s": round(gbs, 1), "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    """Grouped merges over every scale plane of the 8B model (32 layers x 7
+    linears): MXFP4 delta merge (218,103,808 scales, 6 bytes per scale moved),
+    NVFP4 delta merge (436,207,616 scales, 6 bytes) and the MXFP4 hot swap
+    (copy mode, 2 bytes per scale)."""
+    out = {}
+    for name, fmt, block, mode in (("mx_delta", "mx", 32, "delta"), ("nv_delta", "nv", 16, "delta"),
+                                   ("mx_swap", "mx", 32, "copy")):
+        sizes = [o * (i // block) for _ in range(inputs.LLAMA8B_LAYERS) for (_, o, i) in inputs.LLAMA8B_LAYER]
+        total = sum(sizes)
+        if fmt == "mx":
+            scales = torch.randint(100, 140, (total,), dtype=torch.uint8, device="cuda")
+        else:
+            scales = torch.randint(0x20, 0x70, (total,), dtype=torch.uint8, device="cuda")
+        aux = (torch.randn(total, device="cuda") * 1e-3).float() if mode == "delta" else \
+            torch.randint(100, 140, (total,), dtype=torch.uint8, device="cuda")
+        descs, off = [], 0
+        for n in sizes:
+            d = dict(fmt=fmt, scales=scales[off:off + n], ws2=1.0 / 448.0)
+            d["delta" if mode == "delta" else "src"] = aux[off:off + n]
+            descs.append(d)
+            off += n
+        group = sq.MergeGroup(descs)
+        for _ in range(3):
+            sq.sq_merge_scales_grouped(group)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            sq.sq_merge_scales_grouped(group)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        bps = 6 if mode == "delta" else 2
+        gbs = bps * total / (ms * 1e-3) / 1e9
+        out[name] = {"scales": total, "planes": len(sizes), "bytes_per_scale": bps, "ms": round(ms, 4),
+                     "GB/s": round(gbs, 1), "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        del scales, aux, descs, group
+    return out
 
 
 def cpu_baseline(X, dY, codes, sb, delta, src, Wm_host):

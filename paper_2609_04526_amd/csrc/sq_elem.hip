@@ -81,6 +81,18 @@ __device__ __forceinline__ uint32_t e2m1_round_index(float a) {
 }
 
 // ------------------------------------------------------------------ merge
+template <int FMT>
+__device__ __forceinline__ uint32_t merge_one_t(uint32_t b, float d, float ws2) {
+  if (FMT == kNV) {
+    const float e = __fmul_rn(e4m3_to_f32(b), ws2);
+    float e2 = __fadd_rn(e, d);
+    const float cap = __fmul_rn(448.0f, ws2);
+    e2 = (e2 > cap) ? cap : e2;                 // NaN compares false and is kept
+    return e4m3_encode_rne_sat(__fdiv_rn(e2, ws2));
+  }
+  return e8m0_encode_log(__fadd_rn(e8m0_to_f32(b), d));
+}
+
 __device__ __forceinline__ uint32_t merge_one(int fmt, uint32_t b, float d, float ws2) {
   if (fmt == kNV) {
     const float e = __fmul_rn(e4m3_to_f32(b), ws2);
@@ -92,39 +104,107 @@ __device__ __forceinline__ uint32_t merge_one(int fmt, uint32_t b, float d, floa
   return e8m0_encode_log(__fadd_rn(e8m0_to_f32(b), d));
 }
 
-__global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch) {
-  const int64_t chunk = blockIdx.x;
-  int pi = 0;
-  for (int p = 1; p < batch.count; ++p)
-    if (batch.p[p].chunk_begin <= chunk) pi = p;
-  const MergePlane P = batch.p[pi];
-  const int64_t base = (chunk - P.chunk_begin) * kMergeChunk;
-  const int tid = threadIdx.x;
-  if (P.mode == 1) {                                    // copy: 16 bytes per thread
-    const int64_t i = base + (int64_t)tid * 16;
-    if (i + 16 <= P.n) {
-      *reinterpret_cast<uint4*>(P.scales + i) = *reinterpret_cast<const uint4*>(P.src + i);
+// One workgroup per batch.chunk scale bytes of one plane (a multiple of
+// kMergeUnit, chosen per launch so the grid fills the chip).  In each pass a
+// lane issues all of its loads before computing (the plane pointers are
+// restrict: a scale store cannot alias a later load); consecutive lanes touch
+// consecutive 4-byte scale words and 16-byte delta words; delta and copy
+// sources are read once, with streaming (non-temporal) loads.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+#ifndef SQ_MERGE_PASS
+#define SQ_MERGE_PASS 8
+#endif
+// Delta merge of the scale bytes [base, end) of one plane, in
+// passes of SQ_MERGE_PASS steps of 4 scales per lane: all loads of a pass are issued before
+// any compute.
+template <int FMT>
+__device__ __forceinline__ void merge_delta_chunk(uint8_t* __restrict__ sc, const float* __restrict__ dl,
+                                                  int64_t n, int64_t base, int64_t end, float ws2, int tid) {
+  constexpr int kPass = SQ_MERGE_PASS;
+  constexpr int kPassBytes = kPass * 1024;
+  for (int64_t b = base; b < end && b < n; b += kPassBytes) {
+    if (b + kPassBytes <= n) {
+      uint32_t sv[kPass];
+      f32x4_t dv[kPass];
+#pragma unroll
+      for (int g = 0; g < kPass; ++g) {
+        const int64_t i = b + g * 1024 + tid * 4;
+        sv[g] = *reinterpret_cast<const uint32_t*>(sc + i);
+        dv[g] = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(dl + i));
+      }
+#pragma unroll
+      for (int g = 0; g < kPass; ++g) {
+        const uint32_t s = sv[g];
+        sv[g] = merge_one_t<FMT>(s & 0xFFu, dv[g][0], ws2) |
+                (merge_one_t<FMT>((s >> 8) & 0xFFu, dv[g][1], ws2) << 8) |
+                (merge_one_t<FMT>((s >> 16) & 0xFFu, dv[g][2], ws2) << 16) |
+                (merge_one_t<FMT>(s >> 24, dv[g][3], ws2) << 24);
+      }
+#pragma unroll
+      for (int g = 0; g < kPass; ++g)
+        *reinterpret_cast<uint32_t*>(sc + b + g * 1024 + tid * 4) = sv[g];
     } else {
-      for (int64_t k = i; k < P.n && k < i + 16; ++k) P.scales[k] = P.src[k];
+      for (int64_t k = b + tid; k < n && k < b + kPassBytes; k += 256)
+        sc[k] = (uint8_t)merge_one_t<FMT>(sc[k], dl[k], ws2);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
+  (void)batch_arg;
+  // The batch is the kernel's only explicit argument, so it sits at offset 0
+  // of the kernarg segment; reading it there (constant address space) turns a
+  // workgroup-uniform plane index into scalar loads instead of a private copy.
+  const __attribute__((address_space(4))) MergeBatch& batch =
+      *(const __attribute__((address_space(4))) MergeBatch*)__builtin_amdgcn_kernarg_segment_ptr();
+  const int chunk = blockIdx.x;
+  // plane of this workgroup: the last plane whose first chunk is <= chunk
+  // (binary search over the workgroup-uniform chunk_begin array)
+  int lo = 0, hi = batch.count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (batch.chunk_begin[mid] <= chunk) lo = mid;
+    else hi = mid - 1;
+  }
+  const int pi = lo;
+  uint8_t* __restrict__ sc = batch.scales[pi];
+  const int64_t n = batch.n[pi];
+  const int fmt = batch.fmt[pi];
+  const float ws2 = batch.ws2[pi];
+  const int64_t base = (int64_t)(chunk - batch.chunk_begin[pi]) * batch.chunk;
+  const int64_t end = base + batch.chunk;
+  const int tid = threadIdx.x;
+  if (batch.mode[pi] == 1) {                                  // copy: 16 bytes per lane per step
+    constexpr int kCopyPass = kMergeUnit / 4096;
+    const uint8_t* __restrict__ sr = static_cast<const uint8_t*>(batch.aux[pi]);
+    for (int64_t b = base; b < end && b < n; b += kMergeUnit) {
+      if (b + kMergeUnit <= n) {
+        u32x4_t v[kCopyPass];
+#pragma unroll
+        for (int g = 0; g < kCopyPass; ++g)
+          v[g] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(sr + b + g * 4096 + tid * 16));
+#pragma unroll
+        for (int g = 0; g < kCopyPass; ++g) *reinterpret_cast<u32x4_t*>(sc + b + g * 4096 + tid * 16) = v[g];
+      } else {
+        for (int64_t k = b + tid; k < n && k < b + kMergeUnit; k += 256) sc[k] = sr[k];
+      }
     }
     return;
   }
-#pragma unroll
-  for (int g = 0; g < kMergeChunk / 1024; ++g) {        // 4 scales per thread per step
-    const int64_t i = base + g * 1024 + (int64_t)tid * 4;
-    if (i + 4 <= P.n) {
-      const uint32_t s = *reinterpret_cast<const uint32_t*>(P.scales + i);
-      const float4 d = *reinterpret_cast<const float4*>(P.delta + i);
-      const uint32_t r = merge_one(P.fmt, s & 0xFFu, d.x, P.ws2) |
-                         (merge_one(P.fmt, (s >> 8) & 0xFFu, d.y, P.ws2) << 8) |
-                         (merge_one(P.fmt, (s >> 16) & 0xFFu, d.z, P.ws2) << 16) |
-                         (merge_one(P.fmt, s >> 24, d.w, P.ws2) << 24);
-      *reinterpret_cast<uint32_t*>(P.scales + i) = r;
-    } else {
-      for (int64_t k = i; k < P.n && k < i + 4; ++k)
-        P.scales[k] = (uint8_t)merge_one(P.fmt, P.scales[k], P.delta[k], P.ws2);
-    }
-  }
+  const float* __restrict__ dl = static_cast<const float*>(batch.aux[pi]);
+  if (fmt == kNV)
+    merge_delta_chunk<kNV>(sc, dl, n, base, end, ws2, tid);
+  else
+    merge_delta_chunk<kMX>(sc, dl, n, base, end, ws2, tid);
+}
+
+int64_t merge_chunk_for(int64_t total) {
+  // about 8 workgroups per CU on 256 CUs, between 1 and 8 units each
+  int64_t units = (total + 2048 * (int64_t)kMergeUnit - 1) / (2048 * (int64_t)kMergeUnit);
+  units = units < 1 ? 1 : (units > 8 ? 8 : units);
+  return units * kMergeUnit;
 }
 
 int merge_launch(const MergeBatch& b, int64_t total_chunks, hipStream_t s) {

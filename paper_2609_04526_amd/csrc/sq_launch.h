@@ -14,24 +14,27 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
 int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
                 const uint8_t* codes, float* dS, hipStream_t s);
 
-// One plane of a merge launch.
-struct MergePlane {
-  uint8_t* scales;
-  const float* delta;
-  const uint8_t* src;
-  int64_t n;
-  int64_t chunk_begin;   // first global chunk index of this plane
-  float ws2;
-  int32_t fmt;
-  int32_t mode;
-};
-constexpr int kMergePlanesPerLaunch = 40;
-constexpr int kMergeChunk = 4096;     // scale bytes per workgroup
+// Planes of one merge launch, as arrays (kernel arguments are limited to
+// 4 KiB; this layout fits 112 planes).  Plane p covers workgroups
+// [chunk_begin[p], chunk_begin[p+1]).
+constexpr int kMergePlanesPerLaunch = 112;
+constexpr int kMergeUnit = 8192;      // workgroup chunks are multiples of this many scale bytes
 struct MergeBatch {
-  MergePlane p[kMergePlanesPerLaunch];
+  uint8_t* scales[kMergePlanesPerLaunch];
+  const void* aux[kMergePlanesPerLaunch];     // fp32 delta (delta mode) or source bytes (copy mode)
+  int64_t n[kMergePlanesPerLaunch];
+  int32_t chunk_begin[kMergePlanesPerLaunch];
+  float ws2[kMergePlanesPerLaunch];
+  uint8_t fmt[kMergePlanesPerLaunch];
+  uint8_t mode[kMergePlanesPerLaunch];
   int32_t count;
+  int32_t chunk;                      // scale bytes per workgroup (a multiple of kMergeUnit)
 };
+static_assert(sizeof(MergeBatch) <= 4096, "kernel argument budget");
 int merge_launch(const MergeBatch& b, int64_t total_chunks, hipStream_t s);
+// Workgroup chunk for a launch over `total` scale bytes: enough workgroups to
+// fill the chip, each large enough to amortise its set-up.
+int64_t merge_chunk_for(int64_t total);
 
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
