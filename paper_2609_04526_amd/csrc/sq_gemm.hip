@@ -259,6 +259,91 @@ struct SmemLayout {
   static constexpr int kBytes = STAGES * kStage + kWBytes;
 };
 
+// ------------------------------------------------------------------ output
+// Output element offsets stay below 2^31: every output holds fewer than 2^31
+// elements, since each of T, O and I times the other operand dimension does.
+template <bool CHECK, int FMT, int TM, int TN>
+__device__ __forceinline__ void epi_store_direct(const f32x16 (&acc)[TM][TN], const GemmArgs& g, int r0, int c0,
+                                                 int lane) {
+  const int lrow = 4 * (lane >> 5), lcol = lane & 31;
+  const float f = g.ws2;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int col = c0 + j * 32 + lcol;
+      if (CHECK && col >= g.N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = r0 + i * 32 + 8 * (r >> 2) + lrow + (r & 3);
+        if (CHECK && row >= g.M) continue;
+        const float v = (FMT == kNV) ? acc[i][j][r] * f : acc[i][j][r];
+        const uint32_t at = (uint32_t)row * (uint32_t)g.N + (uint32_t)col;
+        if (g.out_bf16)
+          reinterpret_cast<uint16_t*>(g.out)[at] = (uint16_t)f32_to_bf16_rne(v);
+        else
+          reinterpret_cast<float*>(g.out)[at] = v;
+      }
+    }
+}
+
+// Staged bf16 store of one wave's (32*TM) x (32*TN) block, fully inside the
+// output.  LDS holds the block column-major in 8-byte units of 4 rows; unit
+// (col, q) sits at col * (WM/4) + (q ^ (4*(col%4) + (col/4)%4) % (WM/4)), so
+// the 4-row writes of 16 consecutive columns and the transposing reads of a
+// 4-column x 16-row patch each touch 16 distinct 8-byte bank slots.  A
+// transposing read gives lane i of a 16-lane group row i of 4 consecutive
+// columns; two of them make one 16-byte store.
+template <int WM>
+__device__ __forceinline__ int epi_unit(int col, int q) {
+  const int f = 4 * (col & 3) + ((col >> 2) & 3);
+  return col * (WM / 4) + ((q ^ f) & (WM / 4 - 1));
+}
+template <int FMT, int TM, int TN>
+__device__ __forceinline__ void epi_store_bf16(const f32x16 (&acc)[TM][TN], SQ_LDS uint16_t* s, const GemmArgs& g,
+                                               int r0, int c0, int lane) {
+  constexpr int WM = 32 * TM, WN = 32 * TN;
+  const float f = g.ws2;
+  const int lq = lane >> 5, lcol = lane & 31;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        typedef float f2 __attribute__((ext_vector_type(2)));
+        typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+        f2 lo = {acc[i][j][4 * q], acc[i][j][4 * q + 1]};
+        f2 hi = {acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if constexpr (FMT == kNV) { lo = lo * f; hi = hi * f; }
+        const b2 blo = __builtin_convertvector(lo, b2), bhi = __builtin_convertvector(hi, b2);
+        v4i16 v;
+        __builtin_memcpy(&v, &blo, 4);
+        __builtin_memcpy(reinterpret_cast<char*>(&v) + 4, &bhi, 4);
+        // rows i*32 + 8q + 4*lq .. +3 of column j*32 + lcol
+        *(SQ_LDS v4i16*)(s + 4 * epi_unit<WM>(j * 32 + lcol, i * 8 + 2 * q + lq)) = v;
+      }
+  // lane i of group gq: row 16p + i, columns cb*32 + 8gq .. +7
+  const int li = lane & 15, gq = lane >> 4;
+  uint16_t* out = reinterpret_cast<uint16_t*>(g.out);
+#pragma unroll
+  for (int p = 0; p < WM / 16; ++p)
+#pragma unroll
+    for (int cb = 0; cb < WN / 32; ++cb) {
+      v4i16 h[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int col = cb * 32 + 8 * gq + 4 * e + (li >> 2);
+        const int q = 4 * p + (li & 3);
+        h[e] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SQ_LDS v4i16*)(s + 4 * epi_unit<WM>(col, q)));
+      }
+      u32x4 w;
+      __builtin_memcpy(&w, h, 16);
+      const uint32_t at = (uint32_t)(r0 + 16 * p + li) * (uint32_t)g.N + (uint32_t)(c0 + cb * 32 + 8 * gq);
+      *reinterpret_cast<u32x4*>(out + at) = w;
+    }
+}
+
 // ------------------------------------------------------------------ kernel
 // Block tile BM x BN, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN) built
 // from 32x32 MFMA tiles; STAGES LDS stages for the DMA operands.
@@ -281,6 +366,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) uint8_t lds3[STAGES > 3 ? L::kStage : 16];
   __shared__ __attribute__((aligned(16))) uint8_t ldsw[kWReg ? L::kWBytes : 16];
   static_assert(STAGES >= 2 && STAGES <= 4, "2 to 4 stages");
+  // The bf16 output staging reuses the operand LDS: one WM x WN bf16 region
+  // per wave, taken from the stage arrays and the W buffer in turn.
+  constexpr int kEpiRegion = WM * WN * 2;
+  constexpr int kEpiPerStage = L::kStage / kEpiRegion, kEpiPerW = (kWReg ? L::kWBytes : 0) / kEpiRegion;
+  constexpr bool kEpiStaged =
+      MODE != kDs && WM >= 16 && (WM & (WM - 1)) == 0 && WN % 32 == 0 && STAGES * kEpiPerStage + kEpiPerW >= WGM * WGN;
+  auto epi_region = [&](int w) -> SQ_LDS uint16_t* {
+    SQ_LDS uint8_t* base;
+    if (w < kEpiPerStage) base = (SQ_LDS uint8_t*)lds0 + w * kEpiRegion;
+    else if (w < 2 * kEpiPerStage) base = (SQ_LDS uint8_t*)lds1 + (w - kEpiPerStage) * kEpiRegion;
+    else if (STAGES > 2 && w < 3 * kEpiPerStage) base = (SQ_LDS uint8_t*)lds2 + (w - 2 * kEpiPerStage) * kEpiRegion;
+    else if (STAGES > 3 && w < 4 * kEpiPerStage) base = (SQ_LDS uint8_t*)lds3 + (w - 3 * kEpiPerStage) * kEpiRegion;
+    else base = (SQ_LDS uint8_t*)ldsw + (w - STAGES * kEpiPerStage) * kEpiRegion;
+    return (SQ_LDS uint16_t*)base;
+  };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -563,28 +663,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   // ---------------------------------------------------------------- epilogue
   // 32x32 output tile: lane l, register r holds row 8*(r/4) + 4*(l/32) + r%4,
   // column l%32.
-  const int lrow = 4 * (lane >> 5), lcol = lane & 31;
   if constexpr (MODE != kDs) {
-    const float f = g.ws2;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = n0 + wn0 + j * 32 + lcol;
-        if (col >= g.N) continue;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm0 + i * 32 + 8 * (r >> 2) + lrow + (r & 3);
-          if (row >= g.M) continue;
-          const float v = (FMT == kNV) ? acc[i][j][r] * f : acc[i][j][r];
-          if (g.out_bf16)
-            reinterpret_cast<uint16_t*>(g.out)[(size_t)row * g.N + col] = (uint16_t)f32_to_bf16_rne(v);
-          else
-            reinterpret_cast<float*>(g.out)[(size_t)row * g.N + col] = v;
-        }
+    const bool interior = m0 + BM <= g.M && n0 + BN <= g.N;
+    if constexpr (kEpiStaged) {
+      if (g.out_bf16 && interior) {
+        // Every wave is done with the operand tiles; each stages its own
+        // WM x WN bf16 block in LDS and leaves it as 16-byte row pieces.
+        __syncthreads();
+        epi_store_bf16<FMT, TM, TN>(acc, epi_region(wave), g, m0 + wm0, n0 + wn0, lane);
+        return;
       }
+    }
+    if (interior)
+      epi_store_direct<false, FMT, TM, TN>(acc, g, m0 + wm0, n0 + wn0, lane);
+    else
+      epi_store_direct<true, FMT, TM, TN>(acc, g, m0 + wm0, n0 + wn0, lane);
   } else {
     // rows are input features j, columns output features o
+    const int lrow = 4 * (lane >> 5), lcol = lane & 31;
     float* dS = reinterpret_cast<float*>(g.out);
 #pragma unroll
     for (int j = 0; j < TN; ++j) {

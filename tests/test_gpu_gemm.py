@@ -100,6 +100,19 @@ def test_bf16_outputs_within_one_ulp(sq, fmt):
         assert normwise(got, ref) <= 4e-3
 
 
+@pytest.mark.parametrize("fmt,T,O,I", [("mx", 600, 520, 544), ("nv", 520, 776, 528), ("mx", 4096, 4096, 4096)])
+def test_bf16_outputs_are_rounded_f32_outputs(sq, fmt, T, O, I):
+    """Full 256 x 256 output tiles leave through the staged 16-byte store path,
+    ragged ones through per-element stores; both must equal the fp32 result of
+    the same contraction rounded to nearest even."""
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed=2100 + T)
+    Y32, dX32, _ = run_all(sq, fmt, X, dY, codes, sb, ws2, torch.float32)
+    Y16, dX16, _ = run_all(sq, fmt, X, dY, codes, sb, ws2, torch.bfloat16)
+    for got, f32 in ((Y16, Y32), (dX16, dX32)):
+        want = torch.from_numpy(f32).to(torch.bfloat16).float().numpy()
+        assert np.array_equal(got, want)
+
+
 def test_zero_tokens_gives_zero_dscale(sq):
     O, I = 64, 128
     codes = torch.from_numpy(inputs.codes_uniform(5, O, I)).cuda()
