@@ -722,7 +722,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 
 // Tile configurations (compile-time; SQ_CFG_* selects one per product for
 // tuning builds).  Each entry: BM, BN, waves along M, waves along N, stages,
-// K per stage.
+// K per stage.  The large tile is used when its grid still gives every CU a
+// workgroup; smaller grids (the 1024-wide key/value projections) take the
+// 128 x 128 tile, with four times as many workgroups.
 #ifndef SQ_FWD_MODE
 #define SQ_FWD_MODE kFwdR
 #endif
@@ -735,6 +737,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 #ifndef SQ_CFG_DS
 #define SQ_CFG_DS 256, 256, 4, 2, 2, 64
 #endif
+#ifndef SQ_CFG_SMALL
+#define SQ_CFG_SMALL 128, 128, 2, 2, 2, 64
+#endif
+constexpr int kCUs = 256;   // MI355X compute units
 
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 static int launch_gemm(const GemmArgs& g, hipStream_t s) {
@@ -744,6 +750,13 @@ static int launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (tiles == 0) return 0;
   hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(tiles), dim3(64 * WGM * WGN), 0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+template <int MODE, int FMT, int BM, int BN, int... REST>
+static int launch_sized(const GemmArgs& g, hipStream_t s) {
+  const int64_t big = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  if (big >= kCUs) return launch_gemm<MODE, FMT, BM, BN, REST...>(g, s);
+  return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
 }
 
 // ------------------------------------------------------------------ entry
@@ -756,7 +769,7 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
   g.M = T; g.N = O; g.K = I;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = y_bf16;
-  return fmt == kMX ? launch_gemm<SQ_FWD_MODE, kMX, SQ_CFG_FWD>(g, s) : launch_gemm<SQ_FWD_MODE, kNV, SQ_CFG_FWD>(g, s);
+  return fmt == kMX ? launch_sized<SQ_FWD_MODE, kMX, SQ_CFG_FWD>(g, s) : launch_sized<SQ_FWD_MODE, kNV, SQ_CFG_FWD>(g, s);
 }
 
 int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
@@ -768,7 +781,7 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
   g.M = T; g.N = I; g.K = O;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = dx_bf16;
-  return fmt == kMX ? launch_gemm<kDx, kMX, SQ_CFG_DX>(g, s) : launch_gemm<kDx, kNV, SQ_CFG_DX>(g, s);
+  return fmt == kMX ? launch_sized<kDx, kMX, SQ_CFG_DX>(g, s) : launch_sized<kDx, kNV, SQ_CFG_DX>(g, s);
 }
 
 int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
@@ -781,7 +794,7 @@ int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
   g.M = I; g.N = O; g.K = T;
   g.ws2 = 1.0f;
   g.out_bf16 = 0;
-  return fmt == kMX ? launch_gemm<kDs, kMX, SQ_CFG_DS>(g, s) : launch_gemm<kDs, kNV, SQ_CFG_DS>(g, s);
+  return fmt == kMX ? launch_sized<kDs, kMX, SQ_CFG_DS>(g, s) : launch_sized<kDs, kNV, SQ_CFG_DS>(g, s);
 }
 
 }  // namespace sq

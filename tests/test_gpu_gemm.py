@@ -70,6 +70,12 @@ SHAPES = [
     ("nv", 5, 8, 16),
     ("mx", 129, 136, 160),
     ("nv", 257, 520, 1040),
+    # at least 256 workgroups of 256 x 256, so the large tile runs, with
+    # ragged edges: forward, dX and dS in turn
+    ("mx", 4100, 4104, 64),
+    ("nv", 4100, 64, 4112),
+    ("mx", 96, 4104, 4128),
+    ("nv", 80, 4104, 4112),
 ]
 
 
@@ -174,6 +180,12 @@ def _sampled_check(sq, fmt, T, O, I, seed, mx_exp=None, n_rows=6):
 def test_parity_8b_attention_projection_mx(sq):
     """4096 x 4096 MXFP4 projection, 4096 tokens, exponents rint(N(-6, 1.5))."""
     _sampled_check(sq, "mx", 4096, 4096, 4096, seed=2000)
+
+
+def test_parity_8b_key_value_projection_mx(sq):
+    """1024 x 4096 MXFP4 key/value projection, 4096 tokens: the forward and
+    dS grids are too small for the large tile and take the small one."""
+    _sampled_check(sq, "mx", 4096, 1024, 4096, seed=2500)
 
 
 @pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336)])
