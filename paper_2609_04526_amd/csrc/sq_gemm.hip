@@ -10,10 +10,12 @@
 //                                                M=I  N=O  K=T
 //
 // All three feed v_mfma_f32_32x32x16_bf16 (fp32 accumulation) from LDS, in
-// K stages of 64.  How each operand reaches the matrix cores:
+// K stages of 64, on 256 x 256 tiles of 8 waves (each 64 x 128) with two LDS
+// stages; grids that would leave CUs idle use 128 x 128 tiles of 4 waves.
+// How each operand reaches the matrix cores:
 //   * bf16 activations are copied global -> LDS by buffer loads that write LDS
-//     directly (no registers), in a ring of LDS stages, with reads past the
-//     operand's end returning zeros (ragged tiles need no branches);
+//     directly (no registers), with reads past the operand's end returning
+//     zeros (ragged tiles need no branches);
 //   * K-contiguous tiles (X in FWD, dY in DX) are stored as 128-byte rows and
 //     read with ds_read_b128;
 //   * tiles that are contiguous along M or N (X and dY in DS, W in DX) are
@@ -21,15 +23,14 @@
 //     transpose read ds_read_b64_tr_b16: within each 16-lane group, lane i
 //     receives column i of the 4x16 block whose rows the group's lanes supply,
 //     so two reads give a lane the 8 consecutive k of its MFMA operand;
-//   * W in FWD stays packed in LDS; each lane reads the 32 codes of one block
-//     (16 bytes) and dequantises them in registers (exact, see sq_device.h).
-//     The K order inside a stage is permuted to make that possible: MFMA step
-//     kk, lane half h, element e covers k = 32h + 8kk + e, and X is read with
-//     the same permutation;
-//   * W in DX is dequantised in registers from its packed codes and written to
-//     LDS as bf16 rows.
-// Stages are synchronised with explicit vmcnt waits and raw s_barrier, so the
-// loads of later stages stay in flight across the barrier.
+//   * W (FWD and DX) is loaded as packed codes and scale bytes into registers
+//     one or two stages ahead, dequantised exactly to bf16 (sq_device.h) and
+//     written to a double-buffered LDS tile once per workgroup.
+// Each stage: wait for its DMA, one s_barrier, issue the W loads, then four
+// 16-deep MFMA slices; the next stage's DMA is issued in quarters between the
+// operand reads and the MFMAs of the first slices, so the address unit is
+// not flooded at the barrier.  Waits are explicit vmcnt counts and the
+// barrier is the raw s_barrier, so later loads stay in flight across it.
 //
 // The DS epilogue multiplies each accumulator dW[o,j] by its E2M1 code and
 // sums over the block in registers (the 32x32 MFMA output puts 8 of a
@@ -45,15 +46,24 @@
 
 namespace sq {
 
-// kFwdR is the forward with W dequantised once per workgroup into a bf16
-// K-contiguous LDS tile (instead of per wave from packed codes in LDS).
-enum Mode { kFwd = 0, kDx = 1, kDs = 2, kFwdR = 3 };
+// The three products (kFwdR: the forward, with W dequantised once per
+// workgroup into a bf16 K-contiguous LDS tile).
+enum Mode { kDx = 1, kDs = 2, kFwdR = 3 };
 
 constexpr int kBK = 64;                 // K per LDS stage
 constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
 constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: reads zero
 
 #define SQ_LDS __attribute__((address_space(3)))
+// Schedule knobs for tuning builds: SQ_DMA_SPREAD 0 issues a stage's DMA at
+// the barrier, 1 one quarter per MFMA slice, 2 two quarters in each of the
+// first two slices; SQ_FWD_W_AHEAD2 1 fetches the forward's W two stages ahead.
+#ifndef SQ_DMA_SPREAD
+#define SQ_DMA_SPREAD 2
+#endif
+#ifndef SQ_FWD_W_AHEAD2
+#define SQ_FWD_W_AHEAD2 1
+#endif
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -147,8 +157,13 @@ struct DmaKC {
   }
   __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int k0, bool full,
                                         int wave) const {
+    issue_part<0, kInst>(rs, s, k0, full, wave);
+  }
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_part(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int k0, bool full,
+                                             int wave) const {
 #pragma unroll
-    for (int q = 0; q < kInst; ++q) {
+    for (int q = Q0; q < Q1; ++q) {
       const int blk = q * (NT / 64) + wave;
       uint32_t o = off[q] + (uint32_t)k0 * 2u;
       if (!full && k0 >= klim[q]) o = kOOB;
@@ -180,43 +195,16 @@ struct DmaNat {
   }
   __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
                                         int wave) const {
+    issue_part<0, kInst>(rs, s, kstep_bytes, wave);
+  }
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_part(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
+                                             int wave) const {
 #pragma unroll
-    for (int q = 0; q < kInst; ++q) {
+    for (int q = Q0; q < Q1; ++q) {
       const int blk = q * (NT / 64) + wave;
       const uint32_t o = off[q] == kOOB ? kOOB : off[q] + kstep_bytes;
       dma16(rs, s + blk * 64 * 8, o);
-    }
-  }
-};
-
-// Packed W tile for FWD: LDS [2][R][16 bytes]; entry (h, n) holds the 32 codes
-// of row n0+n at k0+32h .. k0+32h+31.
-template <int R, int NT>
-struct DmaWPack {
-  static constexpr int kInst = 2 * R / 64 / (NT / 64);
-  static_assert(kInst * (NT / 64) * 64 == 2 * R, "tile must split over the waves");
-  uint32_t off[kInst];
-  int klim[kInst];
-  __device__ __forceinline__ void init(int O, int I, int n0, int tid) {
-    const int wave = tid >> 6, lane = tid & 63;
-#pragma unroll
-    for (int q = 0; q < kInst; ++q) {
-      const int blk = q * (NT / 64) + wave;
-      const int p = blk * 64 + lane;
-      const int h = p / R, n = p % R;
-      const int o = n0 + n;
-      off[q] = o < O ? (uint32_t)((size_t)o * (I >> 1) + 16 * h) : kOOB;
-      klim[q] = I - 32 * h;
-    }
-  }
-  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint8_t* s, int k0, bool full,
-                                        int wave) const {
-#pragma unroll
-    for (int q = 0; q < kInst; ++q) {
-      const int blk = q * (NT / 64) + wave;
-      uint32_t o = off[q] == kOOB ? kOOB : off[q] + (uint32_t)(k0 >> 1);
-      if (!full && k0 >= klim[q]) o = kOOB;
-      dma16(rs, s + blk * 64 * 16, o);
     }
   }
 };
@@ -225,8 +213,7 @@ struct DmaWPack {
 // operand layouts are instantiated)
 template <int MODE, int BM, int BN, int NT, int BK>
 __host__ __device__ constexpr int dma_count() {
-  if constexpr (MODE == kFwd) return DmaKC<BM, NT>::kInst + DmaWPack<BN, NT>::kInst;
-  else if constexpr (MODE == kDx || MODE == kFwdR) return DmaKC<BM, NT>::kInst;
+  if constexpr (MODE == kDx || MODE == kFwdR) return DmaKC<BM, NT>::kInst;
   else return DmaNat<BM, NT, BK>::kInst + DmaNat<BN, NT, BK>::kInst;
 }
 
@@ -252,7 +239,7 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
 template <int MODE, int BM, int BN, int STAGES, int BK>
 struct SmemLayout {
   static constexpr int kA = BM * BK * 2;                                      // bytes per A stage
-  static constexpr int kB = MODE == kFwd ? BN * 32 : BK * BN * 2;             // bytes per B stage
+  static constexpr int kB = BK * BN * 2;                                      // bytes per B stage
   static constexpr bool kWReg = MODE == kDx || MODE == kFwdR;                 // W staged through registers
   static constexpr int kStage = kA + (kWReg ? 0 : kB);                        // DMA bytes per stage
   static constexpr int kWBytes = kWReg ? 2 * kB : 0;                          // bf16 W double buffer
@@ -399,10 +386,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   };
 
   __amdgpu_buffer_rsrc_t ra, rb;
-  if constexpr (MODE == kFwd) {
-    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
-    rb = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
-  } else if constexpr (MODE == kFwdR) {
+  if constexpr (MODE == kFwdR) {
     ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
   } else if constexpr (MODE == kDx) {
     ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.O * 2));
@@ -423,17 +407,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 
   // ---- DMA of one K stage into stage buffer SC
   using DA_kc = std::conditional_t<MODE != kDs, DmaKC<BM, NT>, DmaKC<8 * NT / 64, NT>>;  // unused in DS
-  using DB_w = std::conditional_t<MODE == kFwd, DmaWPack<BN, NT>, DmaWPack<NT / 2, NT>>;
   using DA_nat = std::conditional_t<MODE == kDs, DmaNat<BM, NT, BK>, DmaNat<512, NT, 64>>;
   using DB_nat = std::conditional_t<MODE == kDs, DmaNat<BN, NT, BK>, DmaNat<512, NT, 64>>;
   DA_kc dA_kc;
-  DB_w dB_w;
   DA_nat dA_nat;
   DB_nat dB_nat;
-  if constexpr (MODE == kFwd) {
-    dA_kc.init(g.I, g.T, g.I, m0, tid);
-    dB_w.init(g.O, g.I, n0, tid);
-  } else if constexpr (MODE == kFwdR) {
+  if constexpr (MODE == kFwdR) {
     dA_kc.init(g.I, g.T, g.I, m0, tid);
   } else if constexpr (MODE == kDx) {
     dA_kc.init(g.O, g.T, g.O, m0, tid);
@@ -446,10 +425,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     SQ_LDS uint8_t* st = stage(SC);
     const int k0 = kt * BK;
     const bool full = k0 + BK <= g.K;
-    if constexpr (MODE == kFwd) {
-      dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
-      dB_w.issue(rb, st + L::kA, k0, full, wave_u);
-    } else if constexpr (MODE == kFwdR || MODE == kDx) {
+    if constexpr (MODE == kFwdR || MODE == kDx) {
       dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
     } else {
       dA_nat.issue(ra, (SQ_LDS uint16_t*)st, (uint32_t)k0 * (uint32_t)g.I * 2u, wave_u);
@@ -457,30 +433,37 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     }
   };
 
-  // ---- FWD: block scales of this lane's W fragments, one k-stage ahead
-  constexpr int kSB = (MODE == kFwd) ? TN * (B == 16 ? 2 : 1) : 1;
-  uint32_t sb_next[kSB], sb_cur[kSB];
-  auto load_scales = [&](int kt) {
-    if constexpr (MODE == kFwd) {
-      const int h = lane >> 5;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int o = n0 + wn0 + j * 32 + (lane & 31);
-#pragma unroll
-        for (int u = 0; u < kSB / TN; ++u) {
-          const int k = kt * kBK + 32 * h + 16 * u;
-          sb_next[j * (kSB / TN) + u] = (o < g.O && k < g.I) ? g.scales[(size_t)o * g.G + k / B] : 0x38u;
-        }
-      }
+  // Quarter PART of the DMA of stage kt (the spread schedule issues one
+  // quarter after each 16-deep slice of MFMAs instead of all at the start).
+  auto dma_part = [&](auto SC, int kt, auto PART) {
+    constexpr int P = decltype(PART)::value;
+    SQ_LDS uint8_t* st = stage(SC);
+    const int k0 = kt * BK;
+    const bool full = k0 + BK <= g.K;
+    if constexpr (MODE == kFwdR || MODE == kDx) {
+      constexpr int n = decltype(dA_kc)::kInst;
+      dA_kc.template issue_part<P * n / 4, (P + 1) * n / 4>(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
+    } else if constexpr (MODE == kDs) {
+      constexpr int na = decltype(dA_nat)::kInst, nb = decltype(dB_nat)::kInst;
+      dA_nat.template issue_part<P * na / 4, (P + 1) * na / 4>(ra, (SQ_LDS uint16_t*)st,
+                                                              (uint32_t)k0 * (uint32_t)g.I * 2u, wave_u);
+      dB_nat.template issue_part<P * nb / 4, (P + 1) * nb / 4>(rb, (SQ_LDS uint16_t*)(st + L::kA),
+                                                              (uint32_t)k0 * (uint32_t)g.O * 2u, wave_u);
     }
   };
+  constexpr bool kSpread = SQ_DMA_SPREAD && STAGES == 2;
 
   // ---- W through registers (DX: W^T tile [64 o][BN i]; FWDR: W tile
   // [BN o][64 i]), one dword of 8 codes along i per item, dequantised and
   // written to LDS as bf16
   constexpr int kWPer = kWReg ? kBK * (BN / 8) / NT : 1;
   static_assert(!kWReg || kWPer * NT == kBK * (BN / 8), "W tile must split over the threads");
-  uint32_t w_reg[kWPer], w_sb[kWPer];
+  // The forward fetches W two stages ahead through branch-free buffer loads
+  // (an item outside the layer reads at an offset past the operand: zeros),
+  // so the wait before a dequantisation leaves the newer loads in flight.
+  constexpr int kWAhead = (MODE == kFwdR && SQ_FWD_W_AHEAD2) ? 2 : 1;
+  static_assert(kWAhead == 1 || STAGES == 2, "two W register sets alternate with the stage parity");
+  uint32_t w_reg[kWAhead][kWPer], w_sb[kWAhead][kWPer];
   auto w_item = [&](int p, int kt, int& o, int& i) {
     const int idx = tid + p * NT;
     if constexpr (MODE == kDx) {
@@ -491,30 +474,58 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
       i = kt * kBK + (idx % 8) * 8;
     }
   };
-  auto load_w = [&](int kt) {
+  // Forward W items: row o = n0 + idx/8 is fixed, the 8 columns start at
+  // kt*64 + (idx%8)*8, so each item keeps byte offsets at kt = 0 (past the
+  // operand for rows outside the layer) and a column limit.
+  __amdgpu_buffer_rsrc_t rw_codes, rw_scales;
+  uint32_t wc0[kWAhead == 2 ? kWPer : 1], ws0[kWAhead == 2 ? kWPer : 1];
+  int wklim = 0;
+  if constexpr (kWAhead == 2) {
+    rw_codes = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
+    rw_scales = make_rsrc(g.scales, (uint32_t)((size_t)g.O * g.G));
+    const int c8 = (tid % 8) * 8;
+    wklim = g.I - c8;                       // the item is inside while kt*64 < wklim
+#pragma unroll
+    for (int p = 0; p < kWPer; ++p) {
+      const int o = n0 + (tid + p * NT) / 8;
+      wc0[p] = o < g.O ? (uint32_t)o * (uint32_t)(g.I >> 1) + (uint32_t)(c8 >> 1) : kOOB;
+      ws0[p] = o < g.O ? (uint32_t)o * (uint32_t)g.G + (uint32_t)(c8 / B) : kOOB;
+    }
+  }
+  auto load_w = [&](int kt, auto BUF) {
+    constexpr int u = decltype(BUF)::value;
     if constexpr (kWReg) {
 #pragma unroll
       for (int p = 0; p < kWPer; ++p) {
+        if constexpr (kWAhead == 2) {
+          const bool in = kt * kBK < wklim;
+          const uint32_t oc = in ? wc0[p] + (uint32_t)kt * (kBK / 2) : kOOB;
+          const uint32_t os = in ? ws0[p] + (uint32_t)kt * (kBK / B) : kOOB;
+          w_reg[u][p] = __builtin_amdgcn_raw_buffer_load_b32(rw_codes, (int)oc, 0, 0);
+          w_sb[u][p] = __builtin_amdgcn_raw_buffer_load_b8(rw_scales, (int)os, 0, 0);
+          continue;
+        }
         int o, i;
         w_item(p, kt, o, i);
         if (o < g.O && i < g.I) {
-          w_reg[p] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
-          w_sb[p] = g.scales[(size_t)o * g.G + i / B];
+          w_reg[u][p] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
+          w_sb[u][p] = g.scales[(size_t)o * g.G + i / B];
         } else {
-          w_reg[p] = 0u;
-          w_sb[p] = 0x38u;
+          w_reg[u][p] = 0u;
+          w_sb[u][p] = 0x38u;
         }
       }
     }
   };
   auto wbuf = [&](int kt) { return (SQ_LDS uint16_t*)((SQ_LDS uint8_t*)ldsw + (kt & 1) * L::kB); };
-  auto commit_w = [&](int kt) {
+  auto commit_w = [&](int kt, auto BUF) {
+    constexpr int u = decltype(BUF)::value;
     if constexpr (kWReg) {
       SQ_LDS uint16_t* s = wbuf(kt);
 #pragma unroll
       for (int p = 0; p < kWPer; ++p) {
         const int idx = tid + p * NT;
-        const uint4 d = ScaleOperand<FMT>::dequant8(w_reg[p], ScaleOperand<FMT>::of(w_sb[p]));
+        const uint4 d = ScaleOperand<FMT>::dequant8(w_reg[u][p], ScaleOperand<FMT>::of(w_sb[u][p]));
         u32x4 v;
         __builtin_memcpy(&v, &d, 16);
         if constexpr (MODE == kDx)
@@ -530,52 +541,54 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
     constexpr int S = decltype(SC)::value;
     constexpr int SNEXT = (S + STAGES - 1) % STAGES;          // stage that receives kt + STAGES - 1
     // stage kt is complete once only the DMA of later stages is outstanding
-    const int later = min(STAGES - 2, nk - 1 - kt);
-    if (later >= 2) wait_vm_lgkm0<(2 * kDma < 63 ? 2 * kDma : 63)>();
-    else if (later == 1) wait_vm_lgkm0<kDma>();
-    else wait_vm_lgkm0<0>();
+    if constexpr (kSpread) {
+      wait_vm_lgkm0<0>();           // the last DMA quarter was issued at the end of the previous step
+    } else if constexpr (kWAhead == 2) {
+      wait_vm_lgkm0<2 * kWPer>();   // the W loads of stage kt+1 may still be out
+    } else {
+      const int later = min(STAGES - 2, nk - 1 - kt);
+      if (later >= 2) wait_vm_lgkm0<(2 * kDma < 63 ? 2 * kDma : 63)>();
+      else if (later == 1) wait_vm_lgkm0<kDma>();
+      else wait_vm_lgkm0<0>();
+    }
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (MODE == kFwd) {
-#pragma unroll
-      for (int u = 0; u < kSB; ++u) sb_cur[u] = sb_next[u];
-      if (kt + 1 < nk) load_scales(kt + 1);
+    if constexpr (kSpread) {
+      if constexpr (kWAhead == 2) load_w(kt + 2, std::integral_constant<int, S % 2>{});
+      else if constexpr (kWReg) {
+        if (kt + 1 < nk) load_w(kt + 1, std::integral_constant<int, 0>{});
+      }
+    } else if constexpr (kWAhead == 2) {
+      // issued every step, past the end too, so every step has the same
+      // loads; the DMA goes first, so the wait for it at the next step start
+      // leaves these W loads in flight
+      issue_dma(std::integral_constant<int, SNEXT>{}, kt + STAGES - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      load_w(kt + 2, std::integral_constant<int, S % 2>{});
+    } else {
+      if constexpr (kWReg) {
+        if (kt + 1 < nk) load_w(kt + 1, std::integral_constant<int, 0>{});
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (kt + STAGES - 1 < nk) issue_dma(std::integral_constant<int, SNEXT>{}, kt + STAGES - 1);
     }
-    if constexpr (kWReg) {
-      if (kt + 1 < nk) load_w(kt + 1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    if (kt + STAGES - 1 < nk) issue_dma(std::integral_constant<int, SNEXT>{}, kt + STAGES - 1);
     __builtin_amdgcn_sched_barrier(0);
 
-    SQ_LDS uint8_t* st = stage(SC);
-    if constexpr (MODE == kFwd) {
-      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
-      const SQ_LDS u32x4* wb = (const SQ_LDS u32x4*)(st + L::kA);
-      const int h = lane >> 5;
-      u32x4 wv[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) wv[j] = wb[h * BN + wn0 + j * 32 + (lane & 31)];
-#pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        bf16x8 fa[TM], fb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 4 * h + kk));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const uint32_t w = wv[j][kk];
-          const uint32_t sbyte = (B == 16) ? sb_cur[2 * j + (kk >> 1)] : sb_cur[j];
-          const uint4 d = ScaleOperand<FMT>::dequant8(w, ScaleOperand<FMT>::of(sbyte));
-          __builtin_memcpy(&fb[j], &d, 16);
+    // quarter q of the next stage's DMA is issued between the operand reads
+    // and the MFMAs of slice slot_of(q)
+    auto slot_of = [](int q) { return SQ_DMA_SPREAD == 1 ? q : q / 2; };
+    auto before_mfma = [&](int kk) {
+      if constexpr (kSpread) {
+        if (kWAhead == 2 || kt + STAGES - 1 < nk) {
+          if (slot_of(0) == kk) dma_part(std::integral_constant<int, SNEXT>{}, kt + 1, std::integral_constant<int, 0>{});
+          if (slot_of(1) == kk) dma_part(std::integral_constant<int, SNEXT>{}, kt + 1, std::integral_constant<int, 1>{});
+          if (slot_of(2) == kk) dma_part(std::integral_constant<int, SNEXT>{}, kt + 1, std::integral_constant<int, 2>{});
+          if (slot_of(3) == kk) dma_part(std::integral_constant<int, SNEXT>{}, kt + 1, std::integral_constant<int, 3>{});
         }
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
-    } else if constexpr (MODE == kFwdR) {
+    };
+    SQ_LDS uint8_t* st = stage(SC);
+    if constexpr (MODE == kFwdR) {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = wbuf(kt);
 #pragma unroll
@@ -588,13 +601,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           fb[j] = *(const SQ_LDS bf16x8*)(b + kc_off(wn0 + j * 32 + (lane & 31), chunk));
+        before_mfma(kk);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
-      if (kt + 1 < nk) commit_w(kt + 1);
+      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
     } else if constexpr (MODE == kDx) {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = wbuf(kt);
@@ -606,13 +620,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
           fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 2 * kk + (lane >> 5)));
 #pragma unroll
         for (int j = 0; j < TN; ++j) fb[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+        before_mfma(kk);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
-      if (kt + 1 < nk) commit_w(kt + 1);
+      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
     } else {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
@@ -623,6 +638,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
         for (int i = 0; i < TM; ++i) fa[i] = nat_frag<BM>(a, kk, wm0 + i * 32, lane);
 #pragma unroll
         for (int j = 0; j < TN; ++j) fb[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+        before_mfma(kk);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -634,13 +650,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 
   // ---- prologue: the first STAGES-1 stages in flight
   if constexpr (kWReg) {
-    if (nk > 0) { load_w(0); commit_w(0); }
-  }
-  if constexpr (MODE == kFwd) {
-    if (nk > 0) load_scales(0);
+    if (nk > 0) {
+      load_w(0, std::integral_constant<int, 0>{});
+      commit_w(0, std::integral_constant<int, 0>{});
+    }
   }
   __builtin_amdgcn_sched_barrier(0);
   if (0 < nk) issue_dma(std::integral_constant<int, 0>{}, 0);
+  if constexpr (kWAhead == 2) {
+    if (0 < nk) load_w(1, std::integral_constant<int, 1>{});
+  }
   if constexpr (STAGES > 2) {
     if (1 < nk) issue_dma(std::integral_constant<int, 1>{}, 1);
   }
@@ -659,6 +678,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
       if (kt0 + 3 < nk) step(std::integral_constant<int, 3>{}, kt0 + 3);
     }
   }
+
+  wait_vm_lgkm0<0>();   // loads issued past the last stage have landed before LDS is reused
 
   // ---------------------------------------------------------------- epilogue
   // 32x32 output tile: lane l, register r holds row 8*(r/4) + 4*(l/32) + r%4,
@@ -725,9 +746,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 // K per stage.  The large tile is used when its grid still gives every CU a
 // workgroup; smaller grids (the 1024-wide key/value projections) take the
 // 128 x 128 tile, with four times as many workgroups.
-#ifndef SQ_FWD_MODE
-#define SQ_FWD_MODE kFwdR
-#endif
 #ifndef SQ_CFG_FWD
 #define SQ_CFG_FWD 256, 256, 4, 2, 2, 64
 #endif
@@ -769,7 +787,7 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
   g.M = T; g.N = O; g.K = I;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = y_bf16;
-  return fmt == kMX ? launch_sized<SQ_FWD_MODE, kMX, SQ_CFG_FWD>(g, s) : launch_sized<SQ_FWD_MODE, kNV, SQ_CFG_FWD>(g, s);
+  return fmt == kMX ? launch_sized<kFwdR, kMX, SQ_CFG_FWD>(g, s) : launch_sized<kFwdR, kNV, SQ_CFG_FWD>(g, s);
 }
 
 int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,

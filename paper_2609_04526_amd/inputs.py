@@ -82,3 +82,30 @@ LLAMA8B_LAYER = (
     ("gate", 14336, 4096), ("up", 14336, 4096), ("down", 4096, 14336),
 )
 LLAMA8B_LAYERS = 32
+
+
+# ---------------------------------------------------------------- on device
+# Whole-model workloads (tens of GB of activations) are drawn on the GPU with
+# torch's seeded Philox generator instead of numpy; a test that checks such an
+# output reads the same device bytes back.
+
+def device_generator(seed: int) -> torch.Generator:
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    return g
+
+
+def device_bf16_normal(seed: int, shape) -> torch.Tensor:
+    """N(0, 1) samples in bf16, drawn on the current GPU."""
+    return torch.randn(shape, generator=device_generator(seed), device="cuda", dtype=torch.float32).to(torch.bfloat16)
+
+
+def device_codes_uniform(seed: int, O: int, I: int) -> torch.Tensor:
+    """Packed E2M1 code plane [O, I/2] on the GPU, every nibble uniform."""
+    return torch.randint(0, 256, (O, I // 2), generator=device_generator(seed), device="cuda", dtype=torch.uint8)
+
+
+def device_e8m0_normal_exponents(seed: int, O: int, G: int, mean: float, std: float) -> torch.Tensor:
+    """E8M0 bytes with exponents rint(N(mean, std)) clipped to [-127, 127], on the GPU."""
+    e = torch.randn((O, G), generator=device_generator(seed), device="cuda") * std + mean
+    return (torch.round(e).clamp_(-127, 127) + 127).to(torch.uint8)
