@@ -119,8 +119,8 @@ SQ_EXPORT int sq_bwd_dx(int fmt, int64_t T, int64_t O, int64_t I, const void* dY
 }
 
 SQ_EXPORT size_t sq_bwd_dscale_workspace(int fmt, int64_t T, int64_t O, int64_t I) {
-  (void)fmt; (void)T; (void)O; (void)I;
-  return 0;
+  if (check_layer(fmt, T, O, I) != SQ_OK) return 0;
+  return sq::gemm_dscale_workspace(fmt, (int)T, (int)O, (int)I);
 }
 
 SQ_EXPORT int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I, const void* X, const void* dY,
@@ -131,9 +131,10 @@ SQ_EXPORT int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I, const void
   if (!codes || !dS) return SQ_ERR_ARG;
   if (T > 0 && (!X || !dY)) return SQ_ERR_ARG;
   if (!aligned(X, 16) || !aligned(dY, 16) || !aligned(codes, 4) || !aligned(dS, 4)) return SQ_ERR_ALIGN;
-  if (workspace_bytes < sq_bwd_dscale_workspace(fmt, T, O, I)) return SQ_ERR_WORKSPACE;
-  (void)workspace;
-  return hip_status(sq::gemm_dscale(fmt, (int)T, (int)O, (int)I, X, dY, codes, dS,
+  const size_t need = sq_bwd_dscale_workspace(fmt, T, O, I);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return SQ_ERR_WORKSPACE;
+  if (need > 0 && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  return hip_status(sq::gemm_dscale(fmt, (int)T, (int)O, (int)I, X, dY, codes, dS, workspace,
                                     static_cast<hipStream_t>(stream)));
 }
 

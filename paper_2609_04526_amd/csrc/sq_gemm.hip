@@ -77,6 +77,8 @@ struct GemmArgs {
   int T, O, I, G;
   float ws2;              // NV epilogue factor (1 for MX)
   int out_bf16;
+  int ksplit;             // DS: K (token) ranges per tile; >1 writes partial planes to `out`
+  int ksteps_per;         // DS: K stages per range
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -373,8 +375,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  // a DS launch with split K runs ksplit workgroups per tile, each over its
+  // own range of K stages
+  const int tiles = tiles_m * tiles_n;
+  const int split = (MODE == kDs && g.ksplit > 1) ? (int)blockIdx.x / tiles : 0;
   int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_of((MODE == kDs && g.ksplit > 1) ? (int)blockIdx.x - split * tiles : (int)blockIdx.x,
+          (MODE == kDs && g.ksplit > 1) ? tiles : (int)gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
   auto stage = [&](auto SC) -> SQ_LDS uint8_t* {
@@ -403,7 +410,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = (g.K + BK - 1) / BK;
+  const int nk_all = (g.K + BK - 1) / BK;
+  const int kofs = (MODE == kDs && g.ksplit > 1) ? split * g.ksteps_per : 0;   // first K stage of this range
+  const int nk = (MODE == kDs && g.ksplit > 1) ? min(g.ksteps_per, nk_all - kofs) : nk_all;
 
   // ---- DMA of one K stage into stage buffer SC
   using DA_kc = std::conditional_t<MODE != kDs, DmaKC<BM, NT>, DmaKC<8 * NT / 64, NT>>;  // unused in DS
@@ -423,7 +432,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto issue_dma = [&](auto SC, int kt) {
     SQ_LDS uint8_t* st = stage(SC);
-    const int k0 = kt * BK;
+    const int k0 = (kofs + kt) * BK;
     const bool full = k0 + BK <= g.K;
     if constexpr (MODE == kFwdR || MODE == kDx) {
       dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
@@ -438,7 +447,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   auto dma_part = [&](auto SC, int kt, auto PART) {
     constexpr int P = decltype(PART)::value;
     SQ_LDS uint8_t* st = stage(SC);
-    const int k0 = kt * BK;
+    const int k0 = (kofs + kt) * BK;
     const bool full = k0 + BK <= g.K;
     if constexpr (MODE == kFwdR || MODE == kDx) {
       constexpr int n = decltype(dA_kc)::kInst;
@@ -702,7 +711,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   } else {
     // rows are input features j, columns output features o
     const int lrow = 4 * (lane >> 5), lcol = lane & 31;
-    float* dS = reinterpret_cast<float*>(g.out);
+    float* dS = reinterpret_cast<float*>(g.out) + (size_t)split * g.O * g.G;   // partial plane when split
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int o = n0 + wn0 + j * 32 + lcol;
@@ -766,7 +775,8 @@ static int launch_gemm(const GemmArgs& g, hipStream_t s) {
   static_assert(L::kBytes <= 160 * 1024, "LDS budget");
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return 0;
-  hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(tiles), dim3(64 * WGM * WGN), 0, s, g);
+  const int blocks = tiles * (MODE == kDs && g.ksplit > 1 ? g.ksplit : 1);
+  hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(blocks), dim3(64 * WGM * WGN), 0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -802,8 +812,48 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
   return fmt == kMX ? launch_sized<kDx, kMX, SQ_CFG_DX>(g, s) : launch_sized<kDx, kNV, SQ_CFG_DX>(g, s);
 }
 
+// Split of the token sum for dS when the large tile leaves CUs idle: each of
+// `splits` workgroups per tile reduces its own range of K stages into a
+// partial [O, G] plane, and a second pass adds the planes in order.
+struct DsPlan {
+  int splits, ksteps_per;
+};
+static DsPlan ds_plan(int fmt, int T, int O, int I) {
+  (void)fmt;
+  constexpr int BM = 256, BN = 256, BK = 64;     // the SQ_CFG_DS tile
+  const int64_t tiles = (int64_t)((I + BM - 1) / BM) * ((O + BN - 1) / BN);
+  const int nk = (T + BK - 1) / BK;
+  DsPlan p{1, nk};
+  if (tiles >= kCUs || tiles == 0) return p;
+  int splits = (int)(kCUs / tiles);
+  splits = min(splits, min(nk / 4, 8));
+  if (splits < 2) return p;
+  p.splits = splits;
+  p.ksteps_per = (nk + splits - 1) / splits;
+  return p;
+}
+
+size_t gemm_dscale_workspace(int fmt, int T, int O, int I) {
+  const DsPlan p = ds_plan(fmt, T, O, I);
+  if (p.splits < 2) return 0;
+  return (size_t)p.splits * O * (I / (fmt == kMX ? 32 : 16)) * sizeof(float);
+}
+
+// dS[i] = sum over s of part[s][i], s in increasing order.
+__global__ __launch_bounds__(256) void ds_reduce_kernel(const float* __restrict__ part, float* __restrict__ dS,
+                                                        int64_t n, int splits) {
+  const int64_t i4 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i4 >= n) return;
+  float4 acc = *reinterpret_cast<const float4*>(part + i4);
+  for (int sp = 1; sp < splits; ++sp) {
+    const float4 v = *reinterpret_cast<const float4*>(part + (size_t)sp * n + i4);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  dS[i4] = acc.x; dS[i4 + 1] = acc.y; dS[i4 + 2] = acc.z; dS[i4 + 3] = acc.w;
+}
+
 int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
-                const uint8_t* codes, float* dS, hipStream_t s) {
+                const uint8_t* codes, float* dS, void* workspace, hipStream_t s) {
   GemmArgs g{};
   g.a = static_cast<const uint16_t*>(X);
   g.b = static_cast<const uint16_t*>(dY);
@@ -812,7 +862,21 @@ int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
   g.M = I; g.N = O; g.K = T;
   g.ws2 = 1.0f;
   g.out_bf16 = 0;
-  return fmt == kMX ? launch_sized<kDs, kMX, SQ_CFG_DS>(g, s) : launch_sized<kDs, kNV, SQ_CFG_DS>(g, s);
+  const DsPlan p = ds_plan(fmt, T, O, I);
+  if (p.splits < 2) {
+    g.ksplit = 1;
+    return fmt == kMX ? launch_sized<kDs, kMX, SQ_CFG_DS>(g, s) : launch_sized<kDs, kNV, SQ_CFG_DS>(g, s);
+  }
+  g.ksplit = p.splits;
+  g.ksteps_per = p.ksteps_per;
+  g.out = workspace;
+  const int rc = fmt == kMX ? launch_gemm<kDs, kMX, SQ_CFG_DS>(g, s) : launch_gemm<kDs, kNV, SQ_CFG_DS>(g, s);
+  if (rc != 0) return rc;
+  const int64_t n = (int64_t)O * g.G;                 // a multiple of 8: O % 8 == 0
+  const int64_t blocks = (n / 4 + 255) / 256;
+  hipLaunchKernelGGL(ds_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     static_cast<const float*>(workspace), dS, n, p.splits);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 }  // namespace sq

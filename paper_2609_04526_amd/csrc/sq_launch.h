@@ -12,7 +12,9 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
 int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
             const uint8_t* scales, float ws2, void* dX, int dx_bf16, hipStream_t s);
 int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
-                const uint8_t* codes, float* dS, hipStream_t s);
+                const uint8_t* codes, float* dS, void* workspace, hipStream_t s);
+// Workspace bytes gemm_dscale needs (partial dS planes of a split token sum).
+size_t gemm_dscale_workspace(int fmt, int T, int O, int I);
 
 // Planes of one merge launch, as arrays (kernel arguments are limited to
 // 4 KiB; this layout fits 112 planes).  Plane p covers workgroups

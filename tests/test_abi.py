@@ -91,6 +91,20 @@ def test_dx_and_dscale_validation(lib):
     assert lib.sq_bwd_dscale_workspace(0, 4096, 4096, 4096) == 0
 
 
+def test_dscale_workspace_for_split_token_sum(lib):
+    # a 1024 x 4096 projection gives 64 tiles of 256 x 256: the token sum is
+    # split four ways into partial [O, G] planes held in the workspace
+    need = lib.sq_bwd_dscale_workspace(0, 4096, 1024, 4096)
+    assert need == 4 * 1024 * 128 * 4
+    assert lib.sq_bwd_dscale_workspace(1, 4096, 1024, 4096) == 4 * 1024 * 256 * 4
+    assert lib.sq_bwd_dscale_workspace(0, 0, 1024, 4096) == 0            # nothing to split
+    assert lib.sq_bwd_dscale_workspace(0, 64, 256, 512) == 0             # too few K stages
+    assert lib.sq_bwd_dscale_workspace(0, 64, 250, 512) == 0             # invalid shape
+    assert lib.sq_bwd_dscale(0, 4096, 1024, 4096, FAKE, FAKE, FAKE, FAKE, None, 0, None) == -5
+    assert lib.sq_bwd_dscale(0, 4096, 1024, 4096, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == -5
+    assert lib.sq_bwd_dscale(0, 4096, 1024, 4096, FAKE, FAKE, FAKE, FAKE, FAKE + 4, need, None) == -3
+
+
 def test_merge_validation(lib):
     from paper_2609_04526_amd import sq
     assert lib.sq_merge_scales(0, 0, None, None, None, 1.0, 0, None) == 0          # empty plane

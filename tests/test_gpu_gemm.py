@@ -76,6 +76,9 @@ SHAPES = [
     ("nv", 4100, 64, 4112),
     ("mx", 96, 4104, 4128),
     ("nv", 80, 4104, 4112),
+    # few tiles and many token stages: dS splits the token sum (workspace)
+    ("mx", 1000, 264, 512),
+    ("nv", 700, 520, 256),
 ]
 
 
@@ -133,6 +136,18 @@ def test_zero_tokens_gives_zero_dscale(sq):
 def test_dscale_deterministic_and_scale_independent(sq):
     fmt, T, O, I = "mx", 333, 136, 320
     X, dY, codes, _, _ = make_layer(fmt, T, O, I, seed=3000)
+    Xc, dYc, cc = X.cuda(), dY.cuda(), torch.from_numpy(codes).cuda()
+    a = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
+    b = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_split_dscale_deterministic(sq):
+    """The split token sum adds its partial planes in a fixed order."""
+    fmt, T, O, I = "mx", 1000, 264, 512
+    assert sq.sq_bwd_dscale_workspace(fmt, T, O, I) > 0
+    X, dY, codes, _, _ = make_layer(fmt, T, O, I, seed=3200)
     Xc, dYc, cc = X.cuda(), dY.cuda(), torch.from_numpy(codes).cuda()
     a = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
     b = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
