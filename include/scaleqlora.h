@@ -116,15 +116,21 @@ int sq_bwd_dx(int fmt, int64_t T, int64_t O, int64_t I,
  * this call takes no scale plane.  The dW tile is produced on the matrix cores
  * and reduced against the codes on chip; no [O, I] tensor is written.
  * Deterministic: the same inputs give bitwise identical dS.
- * workspace / workspace_bytes: scratch of at least
- * sq_bwd_dscale_workspace(fmt, T, O, I) bytes (NULL / 0 when that is 0).
+ * workspace / workspace_bytes: device scratch of at least
+ * sq_bwd_dscale_workspace(fmt, T, O, I) bytes, 16-byte aligned (NULL / 0
+ * when that is 0); its contents on entry do not matter and are overwritten.
+ * A missing or short workspace returns SQ_ERR_WORKSPACE.
  */
 int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I,
                   const void* X, const void* dY, const uint8_t* codes, float* dS,
                   void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes sq_bwd_dscale needs for this shape (0 = none).  Returns 0 for
- * invalid arguments as well; sq_bwd_dscale then reports the error. */
+/* Workspace bytes sq_bwd_dscale needs for this shape (0 = none).  It is
+ * nonzero when the layer has too few 256 x 256 output tiles to occupy every
+ * compute unit and enough tokens to split: the token sum then runs as S
+ * ranges (2 <= S <= 8) whose partial dS planes (S * O * G fp32) are added in
+ * a fixed order.  Returns 0 for invalid arguments as well; sq_bwd_dscale
+ * then reports the error. */
 size_t sq_bwd_dscale_workspace(int fmt, int64_t T, int64_t O, int64_t I);
 
 /*
