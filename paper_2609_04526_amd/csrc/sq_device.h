@@ -43,14 +43,9 @@ __device__ __forceinline__ float e8m0_to_f32(uint32_t b) {
 
 // E4M3 "fn" byte -> fp32 (bias 7, subnormals, 0x7F/0xFF NaN, no infinities).
 __device__ __forceinline__ float e4m3_to_f32(uint32_t b) {
-  const uint32_t e = (b >> 3) & 15u, m = b & 7u;
-  float mag;
-  if (e == 15u && m == 7u) return __uint_as_float(0x7FC00000u);
-  if (e == 0u)
-    mag = (float)m * 0.001953125f;                   // m * 2^-9, exact
-  else
-    mag = __uint_as_float(((e + 120u) << 23) | (m << 20));
-  return (b & 0x80u) ? -mag : mag;
+  // gfx950's fp8 convert reads the OCP E4M3 ("fn") format: exact for every
+  // byte, 0x7F / 0xFF decode to NaN.
+  return __builtin_amdgcn_cvt_f32_fp8((int)(b & 0xFFu), 0);
 }
 
 // E2M1 nibble -> fp32.  Magnitudes in half units: 0,1,2,3,4,6,8,12.

@@ -43,24 +43,12 @@ __device__ __forceinline__ uint32_t e8m0_encode_log(float x) {
 // fp32 -> E4M3 "fn" byte, round to nearest, ties to even mantissa, saturating
 // at +-448; NaN -> 0x7F.
 __device__ __forceinline__ uint32_t e4m3_encode_rne_sat(float x) {
+  // gfx950's fp8 convert rounds to the nearest OCP E4M3 value, ties to even;
+  // clamping to +-448 first makes it saturate (448 is the largest finite
+  // value, so the clamp changes no in-range rounding).  NaN -> 0x7F.
   if (x != x) return 0x7Fu;
-  const uint32_t u = __float_as_uint(x);
-  const uint32_t sign = (u >> 24) & 0x80u;
-  const uint32_t ua = u & 0x7FFFFFFFu;
-  if (ua >= 0x43E00000u) return sign | 0x7Eu;                  // |x| >= 448
-  const uint32_t e = ua >> 23;
-  uint32_t code;
-  if (e < 121u) {
-    // |x| < 2^-6: E4M3 subnormal spacing 2^-9; |x| * 512 is exact, round to
-    // nearest even integer (8 is the smallest normal, byte 0x08).
-    code = (uint32_t)__builtin_rintf(__uint_as_float(ua) * 512.0f);
-  } else {
-    const uint32_t frac = ua & 0x7FFFFFu;
-    code = ((e - 120u) << 3) | (frac >> 20);
-    const uint32_t rem = frac & 0xFFFFFu;
-    if (rem > 0x80000u || (rem == 0x80000u && (code & 1u))) code += 1u;
-  }
-  return sign | code;
+  const float c = __builtin_fminf(__builtin_fmaxf(x, -448.0f), 448.0f);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, c, 0, false) & 0xFFu;
 }
 
 // E2M1 magnitude index (0..7 for 0,.5,1,1.5,2,3,4,6) of |q| with ties to the
@@ -84,17 +72,6 @@ __device__ __forceinline__ uint32_t e2m1_round_index(float a) {
 template <int FMT>
 __device__ __forceinline__ uint32_t merge_one_t(uint32_t b, float d, float ws2) {
   if (FMT == kNV) {
-    const float e = __fmul_rn(e4m3_to_f32(b), ws2);
-    float e2 = __fadd_rn(e, d);
-    const float cap = __fmul_rn(448.0f, ws2);
-    e2 = (e2 > cap) ? cap : e2;                 // NaN compares false and is kept
-    return e4m3_encode_rne_sat(__fdiv_rn(e2, ws2));
-  }
-  return e8m0_encode_log(__fadd_rn(e8m0_to_f32(b), d));
-}
-
-__device__ __forceinline__ uint32_t merge_one(int fmt, uint32_t b, float d, float ws2) {
-  if (fmt == kNV) {
     const float e = __fmul_rn(e4m3_to_f32(b), ws2);
     float e2 = __fadd_rn(e, d);
     const float cap = __fmul_rn(448.0f, ws2);
