@@ -203,6 +203,45 @@ int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream
 int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int tie,
                  uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream);
 
+/*
+ * QAST low-rank scale step (Section 3, "Scale-QLoRA forward": Delta_S =
+ * (alpha/r) B A with A block-level, eff' = eff + Delta_S; "QAST makes merge
+ * exact by construction": the forward uses round_grid(eff'); stability recipe
+ * (ii)-(iii): the NVFP4 ceiling clamp, on the same grid-and-clamp path as the
+ * merge).
+ *
+ * sq_qast_scales writes the on-grid scale bytes the QAST forward computes with
+ * (pass them as `scales` to sq_fwd / sq_bwd_dx):
+ *   Delta_S[o,g] = fp32(alpha_over_r * S[o,g]), S[o,g] = sum over k = 0..r-1 in
+ *                  increasing order of B[o,k] A[k,g], fp32, each product exact;
+ *   scales_out   = the SQ_MERGE_DELTA update of base_scales by Delta_S (the
+ *                  same function the merge runs, bit for bit);
+ *   clamp_mask_out[o,g] = 0 where the NVFP4 ceiling min(eff', 448 ws2) bound,
+ *                  else 1 (always 1 for MXFP4); may be NULL.
+ * O, G >= 1 with O*G < 2^31; 1 <= r <= 64.  base_scales, scales_out,
+ * clamp_mask_out: device uint8 [O, G] (scales_out may equal base_scales);
+ * B: device bf16 [O, r]; A: device bf16 [r, G]; alpha_over_r finite; ws2 as
+ * for sq_fwd (ignored for MXFP4).
+ */
+int sq_qast_scales(int fmt, int64_t O, int64_t G, int r, const uint8_t* base_scales, const void* B,
+                   const void* A, float alpha_over_r, float ws2, uint8_t* scales_out,
+                   uint8_t* clamp_mask_out, void* stream);
+
+/*
+ * Gradients of the low-rank factors from the scale gradient dS (sq_bwd_dscale)
+ * through the straight-through estimator and the clamp:
+ *   dB = alpha_over_r (dS * m) A^T   fp32 [O, r]
+ *   dA = alpha_over_r B^T (dS * m)   fp32 [r, G]
+ * m = clamp_mask (NULL: all 1).  Accumulation is fp32 in a fixed order, so the
+ * results are deterministic.  workspace: device scratch of at least
+ * sq_qast_factor_grads_workspace(O, G, r) bytes (partial dA planes), 4-byte
+ * aligned, contents irrelevant.
+ */
+size_t sq_qast_factor_grads_workspace(int64_t O, int64_t G, int r);
+int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS, const uint8_t* clamp_mask,
+                         const void* B, const void* A, float alpha_over_r, float* dB, float* dA,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* sq_status_str(int status);
 

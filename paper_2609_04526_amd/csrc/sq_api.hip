@@ -174,6 +174,52 @@ SQ_EXPORT int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float w
                                    fmt == SQ_NVFP4 ? ws2_out : nullptr, static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+constexpr int kQastRankMax = 64;
+
+int check_qast_plane(int64_t O, int64_t G, int r) {
+  if (O < 1 || G < 1 || O > kDimMax || G > kDimMax || O * G > kDimMax) return SQ_ERR_SHAPE;
+  if (r < 1 || r > kQastRankMax) return SQ_ERR_SHAPE;
+  return SQ_OK;
+}
+}  // namespace
+
+SQ_EXPORT int sq_qast_scales(int fmt, int64_t O, int64_t G, int r, const uint8_t* base_scales, const void* B,
+                             const void* A, float alpha_over_r, float ws2, uint8_t* scales_out,
+                             uint8_t* clamp_mask_out, void* stream) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  int st = check_qast_plane(O, G, r);
+  if (st != SQ_OK) return st;
+  if (!base_scales || !B || !A || !scales_out) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (fmt == SQ_NVFP4 && !ws2_ok(ws2)) return SQ_ERR_ARG;
+  if (!aligned(B, 2) || !aligned(A, 2)) return SQ_ERR_ALIGN;
+  return hip_status(sq::qast_scales_launch(fmt, (int)O, (int)G, r, base_scales, B, A, alpha_over_r,
+                                           fmt == SQ_NVFP4 ? ws2 : 1.0f, scales_out, clamp_mask_out,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT size_t sq_qast_factor_grads_workspace(int64_t O, int64_t G, int r) {
+  if (check_qast_plane(O, G, r) != SQ_OK) return 0;
+  return sq::qast_grads_workspace((int)O, (int)G, r);
+}
+
+SQ_EXPORT int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS, const uint8_t* clamp_mask,
+                                   const void* B, const void* A, float alpha_over_r, float* dB, float* dA,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_qast_plane(O, G, r);
+  if (st != SQ_OK) return st;
+  if (!dS || !B || !A || !dB || !dA) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (!aligned(dS, 4) || !aligned(B, 2) || !aligned(A, 2) || !aligned(dB, 4) || !aligned(dA, 4))
+    return SQ_ERR_ALIGN;
+  const size_t need = sq::qast_grads_workspace((int)O, (int)G, r);
+  if (!workspace || workspace_bytes < need) return SQ_ERR_WORKSPACE;
+  if (!aligned(workspace, 4)) return SQ_ERR_ALIGN;
+  return hip_status(sq::qast_grads_launch((int)O, (int)G, r, dS, clamp_mask, B, A, alpha_over_r, dB, dA, workspace,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 SQ_EXPORT const char* sq_status_str(int status) {
   switch (status) {
     case SQ_OK: return "SQ_OK";

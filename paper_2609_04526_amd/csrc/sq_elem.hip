@@ -11,45 +11,10 @@
 #include <stdint.h>
 
 #include "sq_device.h"
+#include "sq_grid.h"
 #include "sq_launch.h"
 
 namespace sq {
-
-// ------------------------------------------------------------------ encoders
-// fp32 -> E8M0 byte of 2^round(log2 x), nearest in the log domain: with
-// x = m * 2^k, m in [1, 2), round up iff m > sqrt(2), i.e. iff the 23-bit
-// fraction field is >= 0x3504F4 (fp32(sqrt 2) = 0x3FB504F3 lies below sqrt 2).
-// Exponent clamped to [-127, 127]; x <= 0 -> 0x00, +inf -> 0xFE, NaN -> 0xFF.
-__device__ __forceinline__ uint32_t e8m0_encode_log(float x) {
-  if (x != x) return 0xFFu;
-  if (!(x > 0.0f)) return 0x00u;
-  uint32_t u = __float_as_uint(x);
-  if (u >= 0x7F800000u) return 0xFEu;
-  int e = (int)(u >> 23);
-  uint32_t frac = u & 0x7FFFFFu;
-  int k;
-  if (e == 0) {                             // subnormal: x = frac * 2^-149
-    const int p = 31 - __clz(frac);         // top set bit
-    k = p - 149;
-    frac = (frac << (23 - p)) & 0x7FFFFFu;
-  } else {
-    k = e - 127;
-  }
-  if (frac >= 0x3504F4u) k += 1;
-  k = k < -127 ? -127 : (k > 127 ? 127 : k);
-  return (uint32_t)(k + 127);
-}
-
-// fp32 -> E4M3 "fn" byte, round to nearest, ties to even mantissa, saturating
-// at +-448; NaN -> 0x7F.
-__device__ __forceinline__ uint32_t e4m3_encode_rne_sat(float x) {
-  // gfx950's fp8 convert rounds to the nearest OCP E4M3 value, ties to even;
-  // clamping to +-448 first makes it saturate (448 is the largest finite
-  // value, so the clamp changes no in-range rounding).  NaN -> 0x7F.
-  if (x != x) return 0x7Fu;
-  const float c = __builtin_fminf(__builtin_fmaxf(x, -448.0f), 448.0f);
-  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, c, 0, false) & 0xFFu;
-}
 
 // E2M1 magnitude index (0..7 for 0,.5,1,1.5,2,3,4,6) of |q| with ties to the
 // even mantissa or away from zero; >= 6 saturates, NaN gives 0.
@@ -69,18 +34,6 @@ __device__ __forceinline__ uint32_t e2m1_round_index(float a) {
 }
 
 // ------------------------------------------------------------------ merge
-template <int FMT>
-__device__ __forceinline__ uint32_t merge_one_t(uint32_t b, float d, float ws2) {
-  if (FMT == kNV) {
-    const float e = __fmul_rn(e4m3_to_f32(b), ws2);
-    float e2 = __fadd_rn(e, d);
-    const float cap = __fmul_rn(448.0f, ws2);
-    e2 = (e2 > cap) ? cap : e2;                 // NaN compares false and is kept
-    return e4m3_encode_rne_sat(__fdiv_rn(e2, ws2));
-  }
-  return e8m0_encode_log(__fadd_rn(e8m0_to_f32(b), d));
-}
-
 // One workgroup per batch.chunk scale bytes of one plane (a multiple of
 // kMergeUnit, chosen per launch so the grid fills the chip).  In each pass a
 // lane issues all of its loads before computing (the plane pointers are

@@ -41,4 +41,12 @@ int64_t merge_chunk_for(int64_t total);
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
 
+// QAST low-rank scale step: on-grid scale bytes (+ clamp mask) and the factor
+// gradients; qast_grads_workspace bytes of partial dA planes.
+int qast_scales_launch(int fmt, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
+                       float alpha_over_r, float ws2, uint8_t* out, uint8_t* mask, hipStream_t s);
+size_t qast_grads_workspace(int O, int G, int r);
+int qast_grads_launch(int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
+                      float alpha_over_r, float* dB, float* dA, void* workspace, hipStream_t s);
+
 }  // namespace sq

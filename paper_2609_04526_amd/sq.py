@@ -71,6 +71,11 @@ def load():
         "sq_merge_scales_grouped": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(MergeDesc), _c_p]),
         "rtn_quantize": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
                                         _c_p, _c_p, _c_p, _c_p]),
+        "sq_qast_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p,
+                                          ctypes.c_float, ctypes.c_float, _c_p, _c_p, _c_p]),
+        "sq_qast_factor_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, ctypes.c_int]),
+        "sq_qast_factor_grads": (ctypes.c_int, [_c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p, _c_p,
+                                                ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
         "sq_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "sq_abi_version": (ctypes.c_int, []),
     }
@@ -204,6 +209,44 @@ def rtn_quantize(fmt, W, tie=TIE_EVEN, ws2_in=0.0, codes=None, scales=None, ws2_
     _check("rtn_quantize", load().rtn_quantize(fmt, O, I, _ptr(W), float(ws2_in), int(tie), _ptr(codes),
                                                _ptr(scales), _ptr(ws2_out), _stream()))
     return codes, scales, ws2_out
+
+
+def sq_qast_scales(fmt, base_scales, B, A, alpha_over_r, ws2=1.0, scales_out=None, mask_out=None,
+                   want_mask=True):
+    """On-grid scale bytes of the QAST forward for Delta_S = alpha_over_r * B A, and the
+    clamp mask (1 where the gradient passes).  base_scales uint8 [O, G], B bf16 [O, r],
+    A bf16 [r, G].  Returns (scales_out, mask_out or None)."""
+    fmt = _fmt(fmt)
+    O, G = base_scales.shape
+    r = B.shape[1]
+    if scales_out is None:
+        scales_out = torch.empty_like(base_scales)
+    if want_mask and mask_out is None:
+        mask_out = torch.empty_like(base_scales)
+    _dev(base_scales, B, A, scales_out, mask_out)
+    _check("sq_qast_scales", load().sq_qast_scales(fmt, O, G, r, _ptr(base_scales), _ptr(B), _ptr(A),
+                                                   float(alpha_over_r), float(ws2), _ptr(scales_out),
+                                                   _ptr(mask_out), _stream()))
+    return scales_out, mask_out
+
+
+def sq_qast_factor_grads(dS, mask, B, A, alpha_over_r, dB=None, dA=None, workspace=None):
+    """dB [O, r] and dA [r, G] (fp32) from dS [O, G] through the clamp mask (None: all pass)."""
+    O, G = dS.shape
+    r = B.shape[1]
+    if dB is None:
+        dB = torch.empty((O, r), dtype=torch.float32, device=dS.device)
+    if dA is None:
+        dA = torch.empty((r, G), dtype=torch.float32, device=dS.device)
+    need = int(load().sq_qast_factor_grads_workspace(O, G, r))
+    if workspace is None:
+        workspace = torch.empty(max(need, 4), dtype=torch.uint8, device=dS.device)
+    _dev(dS, mask, B, A, dB, dA, workspace)
+    wsz = workspace.numel() * workspace.element_size()
+    _check("sq_qast_factor_grads", load().sq_qast_factor_grads(O, G, r, _ptr(dS), _ptr(mask), _ptr(B), _ptr(A),
+                                                               float(alpha_over_r), _ptr(dB), _ptr(dA),
+                                                               _ptr(workspace), wsz, _stream()))
+    return dB, dA
 
 
 def abi_version():

@@ -134,3 +134,27 @@ def test_rtn_validation(lib):
     assert lib.rtn_quantize(1, 256, 512, FAKE, float("inf"), 0, FAKE, FAKE, None, None) == -1
     assert lib.rtn_quantize(0, 256, 512, MISALIGNED, 0.0, 0, FAKE, FAKE, None, None) == -3
     assert lib.rtn_quantize(0, 256, 512, None, 0.0, 0, FAKE, FAKE, None, None) == -1
+
+
+def test_qast_validation(lib):
+    nan = float("nan")
+    q = lib.sq_qast_scales
+    assert q(3, 8, 4, 2, FAKE, FAKE, FAKE, 1.0, 1.0, FAKE, None, None) == -4        # format
+    assert q(0, 0, 4, 2, FAKE, FAKE, FAKE, 1.0, 1.0, FAKE, None, None) == -2        # O = 0
+    assert q(0, 8, 4, 0, FAKE, FAKE, FAKE, 1.0, 1.0, FAKE, None, None) == -2        # rank 0
+    assert q(0, 8, 4, 65, FAKE, FAKE, FAKE, 1.0, 1.0, FAKE, None, None) == -2       # rank above 64
+    assert q(0, 1 << 20, 1 << 12, 2, FAKE, FAKE, FAKE, 1.0, 1.0, FAKE, None, None) == -2   # O*G >= 2^31
+    assert q(0, 8, 4, 2, None, FAKE, FAKE, 1.0, 1.0, FAKE, None, None) == -1
+    assert q(0, 8, 4, 2, FAKE, FAKE, FAKE, nan, 1.0, FAKE, None, None) == -1        # alpha/r
+    assert q(1, 8, 4, 2, FAKE, FAKE, FAKE, 1.0, 0.0, FAKE, None, None) == -1        # NV ws2
+    assert q(0, 8, 4, 2, FAKE, FAKE + 1, FAKE, 1.0, 1.0, FAKE, None, None) == -3    # bf16 B
+    assert lib.sq_qast_factor_grads_workspace(64, 128, 32) == 1 * 32 * 128 * 4
+    assert lib.sq_qast_factor_grads_workspace(65, 128, 32) == 2 * 32 * 128 * 4
+    assert lib.sq_qast_factor_grads_workspace(64, 128, 0) == 0
+    need = lib.sq_qast_factor_grads_workspace(8, 4, 2)
+    g = lib.sq_qast_factor_grads
+    assert g(8, 4, 2, FAKE, None, FAKE, FAKE, 1.0, FAKE, FAKE, None, 0, None) == -5            # no workspace
+    assert g(8, 4, 2, FAKE, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, need - 1, None) == -5
+    assert g(8, 4, 2, FAKE + 2, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, need, None) == -3     # dS
+    assert g(8, 4, 2, FAKE, None, FAKE, FAKE, 1.0, None, FAKE, FAKE, need, None) == -1         # dB
+    assert g(8, 4, 65, FAKE, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, need, None) == -2
