@@ -226,12 +226,59 @@ def model_step(sq, steps, warmup, comparator=True):
             torch.cuda.synchronize()
             t = a.elapsed_time(b) / L
             per[f"{name}_{prod}"] = {"ms": round(t, 4), "TFLOP/s": round(2.0 * Tm * o * i / (t * 1e-3) / 1e12, 1)}
+    # The QAST step: every linear's scales come from its rank-32 adapter
+    # (on-grid bytes + clamp mask), the products run on those bytes, and dS
+    # turns into dB, dA.
+    r = 32
+    qa = []
+    for n, (name, o, i) in enumerate(shapes * L):
+        G = i // 32
+        g = inputs.device_generator(6000 + n)
+        qa.append(dict(B=(torch.randn((o, r), generator=g, device="cuda") * 0.02).to(torch.bfloat16),
+                       A=(torch.randn((r, G), generator=g, device="cuda") * 1e-3).to(torch.bfloat16),
+                       sc=torch.empty((o, G), dtype=torch.uint8, device="cuda"),
+                       m=torch.empty((o, G), dtype=torch.uint8, device="cuda"),
+                       dB=torch.empty((o, r), dtype=torch.float32, device="cuda"),
+                       dA=torch.empty((r, G), dtype=torch.float32, device="cuda")))
+    qws = torch.empty(max(sq.sq_qast_factor_grads_workspace(o, i // 32, r) for (_, o, i) in shapes),
+                      dtype=torch.uint8, device="cuda")
+
+    def run_qast():
+        for l in range(L):
+            for k, (name, o, i) in enumerate(shapes):
+                n = l * len(shapes) + k
+                q = qa[n]
+                sq.sq_qast_scales("mx", scales[n], q["B"], q["A"], 1.0, scales_out=q["sc"], mask_out=q["m"])
+                sq.sq_fwd("mx", xs[l][name], codes[n], q["sc"], 1.0, Y=ybuf[(o, i)])
+        for l in reversed(range(L)):
+            for k, (name, o, i) in reversed(list(enumerate(shapes))):
+                n = l * len(shapes) + k
+                q = qa[n]
+                sq.sq_bwd_dx("mx", dys[n], codes[n], q["sc"], 1.0, dX=dxbuf[(o, i)])
+                sq.sq_bwd_dscale("mx", xs[l][name], dys[n], codes[n], dS=dss[n])
+                sq.sq_qast_factor_grads(dss[n], q["m"], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"], workspace=qws)
+
+    for _ in range(warmup):
+        run_qast()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        run_qast()
+    e1.record()
+    torch.cuda.synchronize()
+    qast_ms = e0.elapsed_time(e1) / steps
+
     out = {"workload": "MXFP4 8B-shaped model, 32 layers x 7 linears, 4096 tokens: fwd + dX + dS of every linear",
            "ms": round(ms, 3), "TFLOP": round(flops / 1e12, 2),
            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-           "per_linear_one_layer": per}
-    del dys, xs
+           "per_linear_one_layer": per,
+           "qast_step": {"what": "the same step with every linear's scales from a rank-32 adapter: "
+                                 "sq_qast_scales before each forward, sq_qast_factor_grads after each dS",
+                         "ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
+                         "note": "the paper reports +49 ms per step for QAST on its own hardware and model "
+                                 "(context only)"}}
+    del dys, xs, qa
     if comparator:
         out["weight_space_ste"] = weight_space_ste(sq, codes[:len(shapes)], scales[:len(shapes)], Tm, ms, L)
     return out

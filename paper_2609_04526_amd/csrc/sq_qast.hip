@@ -11,8 +11,9 @@
 // Delta_S adds the r rank-one terms in increasing k in fp32; each product of
 // two bf16 values is exact in fp32, so the fused multiply-add below rounds
 // exactly like a separate multiply and add, and the scale bytes are fixed bit
-// for bit.  The factor gradients accumulate in fp32 in a fixed order (lanes,
-// then a butterfly; row chunks, then chunk index order): deterministic.
+// for bit.  The factor gradients accumulate in fp32 in a fixed order (dB: over
+// the blocks in order; dA: rows in order within 32-row chunks, then the chunk
+// partials through a fixed per-lane order and butterfly): deterministic.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -25,122 +26,144 @@ namespace sq {
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 // ------------------------------------------------------------------ scales
-// A wave per row o, 4 consecutive blocks per lane (256 per wave).
+// One thread per scale (o, g), consecutive threads along g: the A reads are
+// coalesced and a row's B entries are shared by its threads.
 template <int FMT>
 __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restrict__ base,
                                                           const uint16_t* __restrict__ B,
                                                           const uint16_t* __restrict__ A, int O, int G, int r,
                                                           float c, float ws2, uint8_t* out, uint8_t* mask) {
-  // 1-D grid: block = (row group of 4) * gchunks + chunk of 256 blocks
-  const int gchunks = (G + 255) / 256;
-  const int o = (int)(blockIdx.x / gchunks) * 4 + (threadIdx.x >> 6);
-  if (o >= O) return;
-  const int g0 = (int)(blockIdx.x % gchunks) * 256 + (threadIdx.x & 63) * 4;
-  if (g0 >= G) return;
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int k = 0; k < r; ++k) {
-    const float bk = bf16_bits_to_f32(B[(size_t)o * r + k]);
-    const uint16_t* ak = A + (size_t)k * G;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (g0 + j < G) acc[j] = __builtin_fmaf(bk, bf16_bits_to_f32(ak[g0 + j]), acc[j]);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int g = g0 + j;
-    if (g >= G) continue;
-    const size_t at = (size_t)o * G + g;
-    bool clamped;
-    const uint32_t nb = grid_update<FMT>(base[at], __fmul_rn(acc[j], c), ws2, clamped);
-    out[at] = (uint8_t)nb;
-    if (mask) mask[at] = clamped ? 0 : 1;
-  }
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)O * G) return;
+  const int o = (int)(idx / G), g = (int)(idx - (int64_t)o * G);
+  const uint16_t* brow = B + (size_t)o * r;
+  float acc = 0.0f;
+  for (int k = 0; k < r; ++k)
+    acc = __builtin_fmaf(bf16_bits_to_f32(brow[k]), bf16_bits_to_f32(A[(size_t)k * G + g]), acc);
+  bool clamped;
+  const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc, c), ws2, clamped);
+  out[idx] = (uint8_t)nb;
+  if (mask) mask[idx] = clamped ? 0 : 1;
 }
 
 // ------------------------------------------------------------------ dB
-// A wave per row o: lanes stride over the blocks, then a butterfly sum.
-template <int RMAX>
+// A thread per (o, k): dB[o,k] = c sum_g v[o,g] A[k,g] over g in order, with
+// A staged transposed in LDS ([g][k], consecutive k in consecutive lanes) in
+// tiles of kDbTile blocks.  RP lanes per row (RP >= r, a power of two),
+// 256 / RP rows per workgroup.
+constexpr int kDbTile = 256;
+template <int RP>
 __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ dS, const uint8_t* __restrict__ mask,
                                                       const uint16_t* __restrict__ A, int O, int G, int r, float c,
                                                       float* __restrict__ dB) {
-  const int o = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (o >= O) return;
-  const int lane = threadIdx.x & 63;
-  float acc[RMAX];
+  __shared__ float at[kDbTile * RP];                     // [g - g0][k]
+  const int k = threadIdx.x % RP;
+  const int o = blockIdx.x * (256 / RP) + threadIdx.x / RP;
+  const bool active = o < O && k < r;
+  const float* vrow = dS + (size_t)(active ? o : 0) * G;
+  const uint8_t* mrow = mask ? mask + (size_t)(active ? o : 0) * G : nullptr;
+  float acc = 0.0f;
+  for (int g0 = 0; g0 < G; g0 += kDbTile) {
+    const int gn = min(kDbTile, G - g0);
+    __syncthreads();                                     // the previous tile is consumed
+    for (int i = threadIdx.x; i < gn * RP; i += 256) {
+      const int gi = i / RP, kk = i - gi * RP;
+      at[i] = kk < r ? bf16_bits_to_f32(A[(size_t)kk * G + g0 + gi]) : 0.0f;
+    }
+    __syncthreads();
+    if (active) {
+      int gi = 0;
+      for (; gi + 8 <= gn; gi += 8) {                    // 8 loads in flight, then 8 FMAs in order
+        float v[8];
 #pragma unroll
-  for (int k = 0; k < RMAX; ++k) acc[k] = 0.0f;
-  for (int g = lane; g < G; g += 64) {
-    const size_t at = (size_t)o * G + g;
-    const float v = mask ? dS[at] * (float)mask[at] : dS[at];
+        for (int j = 0; j < 8; ++j) v[j] = vrow[g0 + gi + j];
+        if (mrow) {
 #pragma unroll
-    for (int k = 0; k < RMAX; ++k)
-      if (k < r) acc[k] = __builtin_fmaf(v, bf16_bits_to_f32(A[(size_t)k * G + g]), acc[k]);
+          for (int j = 0; j < 8; ++j) v[j] *= (float)mrow[g0 + gi + j];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = __builtin_fmaf(v[j], at[(gi + j) * RP + k], acc);
+      }
+      for (; gi < gn; ++gi) {
+        const int g = g0 + gi;
+        const float v = mrow ? vrow[g] * (float)mrow[g] : vrow[g];
+        acc = __builtin_fmaf(v, at[gi * RP + k], acc);
+      }
+    }
   }
-  float mine = 0.0f;
-#pragma unroll
-  for (int k = 0; k < RMAX; ++k) {
-    if (k >= r) continue;
-    float s = acc[k];
-#pragma unroll
-    for (int w = 32; w >= 1; w >>= 1) s += __shfl_xor(s, w);
-    if (lane == k) mine = s;
-  }
-  if (lane < r) dB[(size_t)o * r + lane] = __fmul_rn(mine, c);
+  if (active) dB[(size_t)o * r + k] = __fmul_rn(acc, c);
 }
 
 // ------------------------------------------------------------------ dA
-// Partial dA over a chunk of kDaRows rows: lanes over blocks, each of the 4
-// waves over a quarter of the rows in order, the waves added in order.
-constexpr int kDaRows = 64;
+// Partial dA over a chunk of kDaRows rows, rows in order: lanes along g, the
+// four waves of a workgroup each own a quarter of the ranks (RMAX / 4).
+constexpr int kDaRows = 32;
 template <int RMAX>
 __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __restrict__ dS,
                                                               const uint8_t* __restrict__ mask,
                                                               const uint16_t* __restrict__ B, int O, int G, int r,
                                                               float* __restrict__ part) {
-  __shared__ float red[4][RMAX][64];
+  constexpr int KW = RMAX / 4;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int gchunks = (G + 63) / 64;
   const int g = (int)(blockIdx.x % gchunks) * 64 + lane;
   const int chunk = (int)(blockIdx.x / gchunks);
-  float acc[RMAX];
+  const int k0 = wave * KW;
+  if (g >= G || k0 >= r) return;
+  float acc[KW];
 #pragma unroll
-  for (int k = 0; k < RMAX; ++k) acc[k] = 0.0f;
-  const int o_begin = chunk * kDaRows + wave * (kDaRows / 4);
-  const int o_end = min(o_begin + kDaRows / 4, O);
-  if (g < G) {
-    for (int o = o_begin; o < o_end; ++o) {
-      const size_t at = (size_t)o * G + g;
-      const float v = mask ? dS[at] * (float)mask[at] : dS[at];
+  for (int j = 0; j < KW; ++j) acc[j] = 0.0f;
+  const int o_end = min((chunk + 1) * kDaRows, O);
+  int o = chunk * kDaRows;
+  for (; o + 8 <= o_end; o += 8) {                       // 8 rows of loads in flight, rows added in order
+    float v[8];
 #pragma unroll
-      for (int k = 0; k < RMAX; ++k)
-        if (k < r) acc[k] = __builtin_fmaf(bf16_bits_to_f32(B[(size_t)o * r + k]), v, acc[k]);
+    for (int u = 0; u < 8; ++u) v[u] = dS[(size_t)(o + u) * G + g];
+    if (mask) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] *= (float)mask[(size_t)(o + u) * G + g];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint16_t* brow = B + (size_t)(o + u) * r + k0;
+#pragma unroll
+      for (int j = 0; j < KW; ++j)
+        if (k0 + j < r) acc[j] = __builtin_fmaf(bf16_bits_to_f32(brow[j]), v[u], acc[j]);
     }
   }
+  for (; o < o_end; ++o) {
+    const size_t at = (size_t)o * G + g;
+    const float v = mask ? dS[at] * (float)mask[at] : dS[at];
+    const uint16_t* brow = B + (size_t)o * r + k0;
 #pragma unroll
-  for (int k = 0; k < RMAX; ++k) red[wave][k][lane] = acc[k];
-  __syncthreads();
-  if (g >= G) return;
-  // thread (wave, lane) adds the four waves' partials for k = wave, wave+4, ...
-  for (int k = wave; k < r; k += 4) {
-    const float s = ((red[0][k][lane] + red[1][k][lane]) + red[2][k][lane]) + red[3][k][lane];
-    part[((size_t)chunk * r + k) * G + g] = s;
+    for (int j = 0; j < KW; ++j)
+      if (k0 + j < r) acc[j] = __builtin_fmaf(bf16_bits_to_f32(brow[j]), v, acc[j]);
   }
+#pragma unroll
+  for (int j = 0; j < KW; ++j)
+    if (k0 + j < r) part[((size_t)chunk * r + k0 + j) * G + g] = acc[j];
 }
 
+// dA[i] = c sum over the chunk partials: a wave per output, lane l adds the
+// chunks l, l + 64, ... in order, then a fixed butterfly across the lanes.
 __global__ __launch_bounds__(256) void qast_da_reduce_kernel(const float* __restrict__ part, int chunks, int r,
                                                              int G, float c, float* __restrict__ dA) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t n = (int64_t)r * G;
   if (i >= n) return;
-  float s = part[i];
-  for (int ch = 1; ch < chunks; ++ch) s += part[(size_t)ch * n + i];
-  dA[i] = __fmul_rn(s, c);
+  const int lane = threadIdx.x & 63;
+  float s = 0.0f;
+  for (int ch = lane; ch < chunks; ch += 64) s += part[(size_t)ch * n + i];
+#pragma unroll
+  for (int w = 32; w >= 1; w >>= 1) s += __shfl_xor(s, w);
+  if (lane == 0) dA[i] = __fmul_rn(s, c);
 }
 
 // ------------------------------------------------------------------ launch
 int qast_scales_launch(int fmt, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
                        float c, float ws2, uint8_t* out, uint8_t* mask, hipStream_t s) {
-  const dim3 grid((unsigned)(((G + 255) / 256) * (int64_t)((O + 3) / 4)));
+  const int64_t n = (int64_t)O * G;
+  const dim3 grid((unsigned)((n + 255) / 256));
   const uint16_t* b = static_cast<const uint16_t*>(B);
   const uint16_t* a = static_cast<const uint16_t*>(A);
   if (fmt == kMX)
@@ -155,15 +178,17 @@ size_t qast_grads_workspace(int O, int G, int r) {
 }
 
 template <int RMAX>
-static void qast_grads_r(int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
-                         const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
-  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + 3) / 4)), dim3(256), 0, s, dS, mask, A, O, G, r, c, dB);
+static int qast_grads_r(int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
+                        const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
+  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + 256 / RMAX - 1) / (256 / RMAX))), dim3(256), 0, s,
+                     dS, mask, A, O, G, r, c, dB);
   const int chunks = (O + kDaRows - 1) / kDaRows;
-  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>, dim3((unsigned)(((G + 63) / 64) * (int64_t)chunks)), dim3(256), 0, s,
-                     dS, mask, B, O, G, r, part);
+  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>, dim3((unsigned)(((G + 63) / 64) * (int64_t)chunks)), dim3(256), 0,
+                     s, dS, mask, B, O, G, r, part);
   const int64_t n = (int64_t)r * G;
-  hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, chunks, r, G, c,
+  hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, part, chunks, r, G, c,
                      dA);
+  return 0;
 }
 
 int qast_grads_launch(int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
@@ -171,9 +196,12 @@ int qast_grads_launch(int O, int G, int r, const float* dS, const uint8_t* mask,
   const uint16_t* b = static_cast<const uint16_t*>(B);
   const uint16_t* a = static_cast<const uint16_t*>(A);
   float* part = static_cast<float*>(workspace);
-  if (r <= 16) qast_grads_r<16>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
-  else if (r <= 32) qast_grads_r<32>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
-  else qast_grads_r<64>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  int rc;
+  if (r <= 8) rc = qast_grads_r<8>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  else if (r <= 16) rc = qast_grads_r<16>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  else if (r <= 32) rc = qast_grads_r<32>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  else rc = qast_grads_r<64>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  if (rc != 0) return rc;
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

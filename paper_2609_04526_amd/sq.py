@@ -230,6 +230,10 @@ def sq_qast_scales(fmt, base_scales, B, A, alpha_over_r, ws2=1.0, scales_out=Non
     return scales_out, mask_out
 
 
+def sq_qast_factor_grads_workspace(O, G, r):
+    return int(load().sq_qast_factor_grads_workspace(O, G, r))
+
+
 def sq_qast_factor_grads(dS, mask, B, A, alpha_over_r, dB=None, dA=None, workspace=None):
     """dB [O, r] and dA [r, G] (fp32) from dS [O, G] through the clamp mask (None: all pass)."""
     O, G = dS.shape
@@ -238,7 +242,7 @@ def sq_qast_factor_grads(dS, mask, B, A, alpha_over_r, dB=None, dA=None, workspa
         dB = torch.empty((O, r), dtype=torch.float32, device=dS.device)
     if dA is None:
         dA = torch.empty((r, G), dtype=torch.float32, device=dS.device)
-    need = int(load().sq_qast_factor_grads_workspace(O, G, r))
+    need = sq_qast_factor_grads_workspace(O, G, r)
     if workspace is None:
         workspace = torch.empty(max(need, 4), dtype=torch.uint8, device=dS.device)
     _dev(dS, mask, B, A, dB, dA, workspace)

@@ -148,8 +148,8 @@ def test_qast_validation(lib):
     assert q(0, 8, 4, 2, FAKE, FAKE, FAKE, nan, 1.0, FAKE, None, None) == -1        # alpha/r
     assert q(1, 8, 4, 2, FAKE, FAKE, FAKE, 1.0, 0.0, FAKE, None, None) == -1        # NV ws2
     assert q(0, 8, 4, 2, FAKE, FAKE + 1, FAKE, 1.0, 1.0, FAKE, None, None) == -3    # bf16 B
-    assert lib.sq_qast_factor_grads_workspace(64, 128, 32) == 1 * 32 * 128 * 4
-    assert lib.sq_qast_factor_grads_workspace(65, 128, 32) == 2 * 32 * 128 * 4
+    assert lib.sq_qast_factor_grads_workspace(32, 128, 32) == 1 * 32 * 128 * 4
+    assert lib.sq_qast_factor_grads_workspace(33, 128, 32) == 2 * 32 * 128 * 4
     assert lib.sq_qast_factor_grads_workspace(64, 128, 0) == 0
     need = lib.sq_qast_factor_grads_workspace(8, 4, 2)
     g = lib.sq_qast_factor_grads
