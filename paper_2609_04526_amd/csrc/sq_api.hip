@@ -68,33 +68,35 @@ int check_merge_plane(int fmt, int64_t n, const uint8_t* scales, const float* de
 }
 
 int run_merge(int n_desc, const sq_merge_desc* d, hipStream_t s) {
-  int64_t total = 0;
-  for (int k = 0; k < n_desc; ++k) total += d[k].n;
-  const int64_t chunk = sq::merge_chunk_for(total);
   sq::MergeBatch batch{};
-  batch.chunk = (int32_t)chunk;
-  int64_t chunks = 0;
+  batch.copy_only = 1;
+  int64_t spans = 0;
   for (int k = 0; k < n_desc; ++k) {
     if (d[k].n == 0) continue;
-    const int64_t c = (d[k].n + chunk - 1) / chunk;
-    if (batch.count == sq::kMergePlanesPerLaunch || chunks + c > INT32_MAX) {
-      if (sq::merge_launch(batch, chunks, s) != 0) return SQ_ERR_HIP;
+    const int64_t unit = d[k].mode == SQ_MERGE_COPY ? sq::kCopySpan : sq::kDeltaSpan;
+    const int64_t c = (d[k].n + unit - 1) / unit;
+    if (batch.count == sq::kMergePlanesPerLaunch || spans + c > INT32_MAX) {
+      batch.spans = (int32_t)spans;
+      if (sq::merge_launch(batch, s) != 0) return SQ_ERR_HIP;
       batch = sq::MergeBatch{};
-      batch.chunk = (int32_t)chunk;
-      chunks = 0;
+      batch.copy_only = 1;
+      spans = 0;
     }
     const int p = batch.count++;
     batch.scales[p] = d[k].scales;
     batch.aux[p] = d[k].mode == SQ_MERGE_DELTA ? static_cast<const void*>(d[k].delta)
                                                : static_cast<const void*>(d[k].src);
     batch.n[p] = d[k].n;
-    batch.chunk_begin[p] = (int32_t)chunks;
+    batch.span_begin[p] = (int32_t)spans;
     batch.ws2[p] = d[k].ws2;
     batch.fmt[p] = (uint8_t)d[k].fmt;
     batch.mode[p] = (uint8_t)d[k].mode;
-    chunks += c;
+    if (d[k].mode != SQ_MERGE_COPY) batch.copy_only = 0;
+    if (d[k].mode == SQ_MERGE_DELTA && d[k].fmt == SQ_NVFP4) batch.nv_delta = 1;
+    spans += c;
   }
-  if (batch.count > 0 && sq::merge_launch(batch, chunks, s) != 0) return SQ_ERR_HIP;
+  batch.spans = (int32_t)spans;
+  if (batch.count > 0 && sq::merge_launch(batch, s) != 0) return SQ_ERR_HIP;
   return SQ_OK;
 }
 

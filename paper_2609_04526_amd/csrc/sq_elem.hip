@@ -34,112 +34,97 @@ __device__ __forceinline__ uint32_t e2m1_round_index(float a) {
 }
 
 // ------------------------------------------------------------------ merge
-// One workgroup per batch.chunk scale bytes of one plane (a multiple of
-// kMergeUnit, chosen per launch so the grid fills the chip).  In each pass a
-// lane issues all of its loads before computing (the plane pointers are
-// restrict: a scale store cannot alias a later load); consecutive lanes touch
-// consecutive 4-byte scale words and 16-byte delta words; delta and copy
-// sources are read once, with streaming (non-temporal) loads.
+// The planes of a launch are cut into spans: kDeltaSpan scale bytes (delta
+// mode: kDeltaSteps steps of 4 scales and a 16-byte fp32 delta per lane) or
+// kCopySpan bytes (copy mode: kCopySteps steps of 16 bytes per lane).  Workgroup w takes spans w, w + grid,
+// w + 2 grid, ...: at any moment the whole grid streams through one window of
+// the planes, which keeps the DRAM accesses of all workgroups together (a
+// workgroup walking a private region of its own streams markedly slower).
+// Consecutive lanes touch consecutive 4-byte scale words and 16-byte delta
+// words; delta and copy sources are read once, with streaming loads.  The
+// plane pointers are restrict: a scale store cannot alias a later load.
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-#ifndef SQ_MERGE_PASS
-#define SQ_MERGE_PASS 8
-#endif
-// Delta merge of the scale bytes [base, end) of one plane, in
-// passes of SQ_MERGE_PASS steps of 4 scales per lane: all loads of a pass are issued before
-// any compute.
+// One delta span: kDeltaSteps steps of 4 scales per lane, all loads issued
+// before any compute.
 template <int FMT>
-__device__ __forceinline__ void merge_delta_chunk(uint8_t* __restrict__ sc, const float* __restrict__ dl,
-                                                  int64_t n, int64_t base, int64_t end, float ws2, int tid) {
-  constexpr int kPass = SQ_MERGE_PASS;
-  constexpr int kPassBytes = kPass * 1024;
-  for (int64_t b = base; b < end && b < n; b += kPassBytes) {
-    if (b + kPassBytes <= n) {
-      uint32_t sv[kPass];
-      f32x4_t dv[kPass];
+__device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const float* __restrict__ dl, int64_t n,
+                                                 int64_t off, float ws2, int tid) {
+  if (off + kDeltaSpan <= n) {
+    uint32_t sv[kDeltaSteps];
+    f32x4_t dv[kDeltaSteps];
 #pragma unroll
-      for (int g = 0; g < kPass; ++g) {
-        const int64_t i = b + g * 1024 + tid * 4;
-        sv[g] = *reinterpret_cast<const uint32_t*>(sc + i);
-        dv[g] = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(dl + i));
-      }
-#pragma unroll
-      for (int g = 0; g < kPass; ++g) {
-        const uint32_t s = sv[g];
-        sv[g] = merge_one_t<FMT>(s & 0xFFu, dv[g][0], ws2) |
-                (merge_one_t<FMT>((s >> 8) & 0xFFu, dv[g][1], ws2) << 8) |
-                (merge_one_t<FMT>((s >> 16) & 0xFFu, dv[g][2], ws2) << 16) |
-                (merge_one_t<FMT>(s >> 24, dv[g][3], ws2) << 24);
-      }
-#pragma unroll
-      for (int g = 0; g < kPass; ++g)
-        *reinterpret_cast<uint32_t*>(sc + b + g * 1024 + tid * 4) = sv[g];
-    } else {
-      for (int64_t k = b + tid; k < n && k < b + kPassBytes; k += 256)
-        sc[k] = (uint8_t)merge_one_t<FMT>(sc[k], dl[k], ws2);
+    for (int g = 0; g < kDeltaSteps; ++g) {
+      const int64_t i = off + g * 1024 + tid * 4;
+      sv[g] = *reinterpret_cast<const uint32_t*>(sc + i);
+      dv[g] = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(dl + i));
     }
+#pragma unroll
+    for (int g = 0; g < kDeltaSteps; ++g) {
+      const uint32_t v = sv[g];
+      sv[g] = merge_one_t<FMT>(v & 0xFFu, dv[g][0], ws2) | (merge_one_t<FMT>((v >> 8) & 0xFFu, dv[g][1], ws2) << 8) |
+              (merge_one_t<FMT>((v >> 16) & 0xFFu, dv[g][2], ws2) << 16) |
+              (merge_one_t<FMT>(v >> 24, dv[g][3], ws2) << 24);
+    }
+#pragma unroll
+    for (int g = 0; g < kDeltaSteps; ++g) *reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4) = sv[g];
+  } else {
+    for (int64_t k = off + tid; k < n && k < off + kDeltaSpan; k += 256)
+      sc[k] = (uint8_t)merge_one_t<FMT>(sc[k], dl[k], ws2);
+  }
+}
+
+// One copy span: kCopySteps steps of 16 bytes per lane, loads first.
+__device__ __forceinline__ void merge_copy_span(uint8_t* __restrict__ sc, const uint8_t* __restrict__ sr, int64_t n,
+                                                int64_t off, int tid) {
+  if (off + kCopySpan <= n) {
+    u32x4_t v[kCopySteps];
+#pragma unroll
+    for (int g = 0; g < kCopySteps; ++g)
+      v[g] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(sr + off + g * 4096 + tid * 16));
+#pragma unroll
+    for (int g = 0; g < kCopySteps; ++g) *reinterpret_cast<u32x4_t*>(sc + off + g * 4096 + tid * 16) = v[g];
+  } else {
+    for (int64_t k = off + tid; k < n && k < off + kCopySpan; k += 256) sc[k] = sr[k];
   }
 }
 
 __global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
   (void)batch_arg;
   // The batch is the kernel's only explicit argument, so it sits at offset 0
-  // of the kernarg segment; reading it there (constant address space) turns a
-  // workgroup-uniform plane index into scalar loads instead of a private copy.
+  // of the kernarg segment; reading it there (constant address space) keeps
+  // the workgroup-uniform plane data in scalar registers.
   const __attribute__((address_space(4))) MergeBatch& batch =
       *(const __attribute__((address_space(4))) MergeBatch*)__builtin_amdgcn_kernarg_segment_ptr();
-  const int chunk = blockIdx.x;
-  // plane of this workgroup: the last plane whose first chunk is <= chunk
-  // (binary search over the workgroup-uniform chunk_begin array)
-  int lo = 0, hi = batch.count - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (batch.chunk_begin[mid] <= chunk) lo = mid;
-    else hi = mid - 1;
-  }
-  const int pi = lo;
-  uint8_t* __restrict__ sc = batch.scales[pi];
-  const int64_t n = batch.n[pi];
-  const int fmt = batch.fmt[pi];
-  const float ws2 = batch.ws2[pi];
-  const int64_t base = (int64_t)(chunk - batch.chunk_begin[pi]) * batch.chunk;
-  const int64_t end = base + batch.chunk;
   const int tid = threadIdx.x;
-  if (batch.mode[pi] == 1) {                                  // copy: 16 bytes per lane per step
-    constexpr int kCopyPass = kMergeUnit / 4096;
-    const uint8_t* __restrict__ sr = static_cast<const uint8_t*>(batch.aux[pi]);
-    for (int64_t b = base; b < end && b < n; b += kMergeUnit) {
-      if (b + kMergeUnit <= n) {
-        u32x4_t v[kCopyPass];
-#pragma unroll
-        for (int g = 0; g < kCopyPass; ++g)
-          v[g] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(sr + b + g * 4096 + tid * 16));
-#pragma unroll
-        for (int g = 0; g < kCopyPass; ++g) *reinterpret_cast<u32x4_t*>(sc + b + g * 4096 + tid * 16) = v[g];
-      } else {
-        for (int64_t k = b + tid; k < n && k < b + kMergeUnit; k += 256) sc[k] = sr[k];
-      }
+  int pi = 0;
+  for (int span = blockIdx.x; span < batch.spans; span += gridDim.x) {
+    // spans only grow, so the plane index only moves forward
+    while (pi + 1 < batch.count && batch.span_begin[pi + 1] <= span) ++pi;
+    uint8_t* __restrict__ sc = batch.scales[pi];
+    const int64_t n = batch.n[pi];
+    const int64_t rel = span - batch.span_begin[pi];
+    if (batch.mode[pi] == 1) {                                // copy
+      merge_copy_span(sc, static_cast<const uint8_t*>(batch.aux[pi]), n, rel * kCopySpan, tid);
+    } else {
+      const float* __restrict__ dl = static_cast<const float*>(batch.aux[pi]);
+      if (batch.fmt[pi] == kNV)
+        merge_delta_span<kNV>(sc, dl, n, rel * kDeltaSpan, batch.ws2[pi], tid);
+      else
+        merge_delta_span<kMX>(sc, dl, n, rel * kDeltaSpan, batch.ws2[pi], tid);
     }
-    return;
   }
-  const float* __restrict__ dl = static_cast<const float*>(batch.aux[pi]);
-  if (fmt == kNV)
-    merge_delta_chunk<kNV>(sc, dl, n, base, end, ws2, tid);
-  else
-    merge_delta_chunk<kMX>(sc, dl, n, base, end, ws2, tid);
 }
 
-int64_t merge_chunk_for(int64_t total) {
-  // about 8 workgroups per CU on 256 CUs, between 1 and 8 units each
-  int64_t units = (total + 2048 * (int64_t)kMergeUnit - 1) / (2048 * (int64_t)kMergeUnit);
-  units = units < 1 ? 1 : (units > 8 ? 8 : units);
-  return units * kMergeUnit;
-}
-
-int merge_launch(const MergeBatch& b, int64_t total_chunks, hipStream_t s) {
-  if (total_chunks <= 0) return 0;
-  hipLaunchKernelGGL(merge_kernel, dim3((unsigned)total_chunks), dim3(256), 0, s, b);
+int merge_launch(const MergeBatch& b, hipStream_t s) {
+  if (b.spans <= 0) return 0;
+  // Measured on the 8B model's planes (medians of interleaved runs): copies
+  // stream best from 2048 workgroups, MXFP4 deltas from 4096, and NVFP4
+  // deltas, whose division keeps more lanes busy, from 8192.
+  const int64_t cap = b.copy_only ? 2048 : (b.nv_delta ? 8192 : 4096);
+  const int64_t grid = b.spans < cap ? b.spans : cap;
+  hipLaunchKernelGGL(merge_kernel, dim3((unsigned)grid), dim3(256), 0, s, b);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

@@ -17,26 +17,35 @@ int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
 size_t gemm_dscale_workspace(int fmt, int T, int O, int I);
 
 // Planes of one merge launch, as arrays (kernel arguments are limited to
-// 4 KiB; this layout fits 112 planes).  Plane p covers workgroups
-// [chunk_begin[p], chunk_begin[p+1]).
+// 4 KiB; this layout fits 112 planes).  Plane p is cut into spans of
+// kDeltaSpan scales (delta mode) or kCopySpan bytes (copy mode) and owns the
+// spans [span_begin[p], span_begin[p+1]).
 constexpr int kMergePlanesPerLaunch = 112;
-constexpr int kMergeUnit = 8192;      // workgroup chunks are multiples of this many scale bytes
+#ifndef SQ_MERGE_DELTA_STEPS
+#define SQ_MERGE_DELTA_STEPS 8
+#endif
+#ifndef SQ_MERGE_COPY_STEPS
+#define SQ_MERGE_COPY_STEPS 8
+#endif
+constexpr int kDeltaSteps = SQ_MERGE_DELTA_STEPS;
+constexpr int kCopySteps = SQ_MERGE_COPY_STEPS;
+constexpr int kDeltaSpan = 1024 * kDeltaSteps;      // 256 lanes x 4 scales per step
+constexpr int kCopySpan = 4096 * kCopySteps;        // 256 lanes x 16 bytes per step
 struct MergeBatch {
   uint8_t* scales[kMergePlanesPerLaunch];
   const void* aux[kMergePlanesPerLaunch];     // fp32 delta (delta mode) or source bytes (copy mode)
   int64_t n[kMergePlanesPerLaunch];
-  int32_t chunk_begin[kMergePlanesPerLaunch];
+  int32_t span_begin[kMergePlanesPerLaunch];
   float ws2[kMergePlanesPerLaunch];
   uint8_t fmt[kMergePlanesPerLaunch];
   uint8_t mode[kMergePlanesPerLaunch];
   int32_t count;
-  int32_t chunk;                      // scale bytes per workgroup (a multiple of kMergeUnit)
+  int32_t spans;                      // spans of all planes
+  int32_t copy_only;                  // every plane is a copy
+  int32_t nv_delta;                   // some plane is an NVFP4 delta merge
 };
 static_assert(sizeof(MergeBatch) <= 4096, "kernel argument budget");
-int merge_launch(const MergeBatch& b, int64_t total_chunks, hipStream_t s);
-// Workgroup chunk for a launch over `total` scale bytes: enough workgroups to
-// fill the chip, each large enough to amortise its set-up.
-int64_t merge_chunk_for(int64_t total);
+int merge_launch(const MergeBatch& b, hipStream_t s);
 
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
