@@ -81,6 +81,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-model-merge", action="store_true")
     p.add_argument("--no-model-step", action="store_true")
+    p.add_argument("--no-lifecycle", action="store_true")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="also run a plain device copy of this many MiB (the copy mode of "
                         "sq_merge_scales: reads N and writes N bytes) to calibrate HBM counters")
@@ -110,30 +111,51 @@ def merged_weight_bf16(codes_d, sb_d, sq):
     return Wm.to(torch.bfloat16).contiguous()
 
 
+def effective_scales_torch(fmt, scale_bytes, ws2):
+    """fp32 effective scales of a scale plane with torch's decoders (input
+    recipes and read-back only; the merge kernels decode on their own)."""
+    if fmt == "mx":
+        return torch.exp2(scale_bytes.float() - 127.0)
+    return scale_bytes.view(torch.float8_e4m3fn).float() * ws2
+
+
 def model_merge(sq, steps):
     """Grouped merges over every scale plane of the 8B model (32 layers x 7
-    linears): MXFP4 delta merge (218,103,808 scales, 6 bytes per scale moved),
-    NVFP4 delta merge (436,207,616 scales, 6 bytes) and the MXFP4 hot swap
-    (copy mode, 2 bytes per scale)."""
+    linears) with a task delta: MXFP4 (218,103,808 scales) and NVFP4
+    (436,207,616 scales), 6 bytes moved per scale, and the MXFP4 hot swap
+    (copy mode, 2 bytes per scale).  Base planes: MXFP4 exponents
+    rint(N(-6, 1.5)), NVFP4 E4M3 of |N(0, 1)| with ws2 = 1/448.  Reports the
+    fraction of scale bytes the merge changed."""
     out = {}
+    ws2 = float(np.float32(1.0 / 448.0))
     for name, fmt, block, mode in (("mx_delta", "mx", 32, "delta"), ("nv_delta", "nv", 16, "delta"),
                                    ("mx_swap", "mx", 32, "copy")):
-        sizes = [o * (i // block) for _ in range(inputs.LLAMA8B_LAYERS) for (_, o, i) in inputs.LLAMA8B_LAYER]
+        shapes = [(o, i // block) for _ in range(inputs.LLAMA8B_LAYERS) for (_, o, i) in inputs.LLAMA8B_LAYER]
+        sizes = [o * g for (o, g) in shapes]
         total = sum(sizes)
         if fmt == "mx":
-            scales = torch.randint(100, 140, (total,), dtype=torch.uint8, device="cuda")
+            base = torch.cat([inputs.device_e8m0_normal_exponents(7000 + k, o, g, -6.0, 1.5).reshape(-1)
+                              for k, (o, g) in enumerate(shapes)])
         else:
-            scales = torch.randint(0x20, 0x70, (total,), dtype=torch.uint8, device="cuda")
-        aux = (torch.randn(total, device="cuda") * 1e-3).float() if mode == "delta" else \
-            torch.randint(100, 140, (total,), dtype=torch.uint8, device="cuda")
+            base = torch.cat([inputs.device_e4m3_abs_normal(7000 + k, o, g).reshape(-1)
+                              for k, (o, g) in enumerate(shapes)])
+        if mode == "delta":
+            aux = inputs.device_task_delta(7500, effective_scales_torch(fmt, base, ws2), fmt).float()
+        else:
+            aux = torch.cat([inputs.device_e8m0_normal_exponents(7600 + k, o, g, -6.0, 1.5).reshape(-1)
+                             for k, (o, g) in enumerate(shapes)])
+        scales = base.clone()
         descs, off = [], 0
         for n in sizes:
-            d = dict(fmt=fmt, scales=scales[off:off + n], ws2=1.0 / 448.0)
+            d = dict(fmt=fmt, scales=scales[off:off + n], ws2=ws2)
             d["delta" if mode == "delta" else "src"] = aux[off:off + n]
             descs.append(d)
             off += n
         group = sq.MergeGroup(descs)
-        for _ in range(3):
+        sq.sq_merge_scales_grouped(group)              # the merge itself: base -> merged
+        torch.cuda.synchronize()
+        changed = float((scales != base).sum().item()) / total
+        for _ in range(2):
             sq.sq_merge_scales_grouped(group)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -146,8 +168,89 @@ def model_merge(sq, steps):
         bps = 6 if mode == "delta" else 2
         gbs = bps * total / (ms * 1e-3) / 1e9
         out[name] = {"scales": total, "planes": len(sizes), "bytes_per_scale": bps, "ms": round(ms, 4),
-                     "GB/s": round(gbs, 1), "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
-        del scales, aux, descs, group
+                     "GB/s": round(gbs, 1), "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "changed_byte_frac": round(changed, 5)}
+        del scales, base, aux, descs, group
+        torch.cuda.empty_cache()
+    out["note"] = ("delta merges are re-applied to the merged planes in the timed repetitions (same bytes "
+                   "moved); the paper reports 4.7-7.7% of scale bytes changed by its task merges (context only)")
+    return out
+
+
+def model_lifecycle(sq, steps=3):
+    """The naive merge's re-quantisation over the whole 8B model: for every
+    linear, the bf16 merged weight W + B A (rank 16, A, B ~ N(0, 0.02), W the
+    dequantised base) re-quantised by rtn_quantize with ties to even and ties
+    away.  Timed over all 224 linears; algorithmic bytes 2 + 0.5 + 1/B per
+    weight.  The diff census counts code nibbles that differ from the base
+    plane (per tie rule) and between the tie rules, and changed scale bytes."""
+    lut = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0],
+                       device="cuda")
+
+    def nibbles(c):
+        return torch.stack((c & 15, c >> 4), dim=-1).reshape(c.shape[0], -1)
+
+    out = {}
+    ws2 = float(np.float32(1.0 / 448.0))
+    for fmt, block in (("mx", 32), ("nv", 16)):
+        items = []
+        for k, (name, o, i) in enumerate(inputs.LLAMA8B_LAYER * inputs.LLAMA8B_LAYERS):
+            G = i // block
+            codes = inputs.device_codes_uniform(8000 + k, o, i)
+            sb = (inputs.device_e8m0_normal_exponents(8300 + k, o, G, -6.0, 1.5) if fmt == "mx"
+                  else inputs.device_e4m3_abs_normal(8300 + k, o, G))
+            g = inputs.device_generator(8600 + k)
+            Bf = torch.randn((o, 16), generator=g, device="cuda") * 0.02
+            Af = torch.randn((16, i), generator=g, device="cuda") * 0.02
+            W = lut[nibbles(codes).long()] * effective_scales_torch(fmt, sb, ws2).repeat_interleave(block, dim=1)
+            Wm = (W + Bf @ Af).to(torch.bfloat16)
+            del W, Bf, Af
+            items.append(dict(codes=codes, sb=sb, Wm=Wm,
+                              ce=torch.empty_like(codes), se=torch.empty_like(sb),
+                              ca=torch.empty_like(codes), sa=torch.empty_like(sb),
+                              w2=torch.empty(1, dtype=torch.float32, device="cuda")))
+        weights = sum(it["Wm"].numel() for it in items)
+        nbytes = weights * (2 + 0.5 + 1.0 / block)
+        res = {"weights": weights, "linears": len(items), "bytes": int(nbytes)}
+        runs = [("even", sq.TIE_EVEN, ws2, "ce", "se"), ("away", sq.TIE_AWAY, ws2, "ca", "sa")]
+        if fmt == "nv":
+            runs.append(("even_ws2_recomputed", sq.TIE_EVEN, 0.0, "ce", "se"))
+        for label, tie, w_in, ck, sk in runs:
+            def run():
+                for it in items:
+                    sq.rtn_quantize(fmt, it["Wm"], tie, w_in, codes=it[ck], scales=it[sk],
+                                    ws2_out=it["w2"] if fmt == "nv" else None)
+            run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(steps):
+                run()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            moved = nbytes + (weights * 2 if w_in == 0.0 else 0)      # the amax pre-pass reads W once more
+            res[label] = {"ms": round(ms, 3), "GB/s": round(moved / (ms * 1e-3) / 1e9, 1),
+                          "frac": round(moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        # census (ties to even and ties away, both with the fixed ws2 for NVFP4)
+        for it in items:
+            sq.rtn_quantize(fmt, it["Wm"], sq.TIE_EVEN, ws2, codes=it["ce"], scales=it["se"],
+                            ws2_out=it["w2"] if fmt == "nv" else None)
+        torch.cuda.synchronize()
+        cen = {"code_nibbles_even_vs_base": 0, "code_nibbles_away_vs_base": 0, "code_nibbles_even_vs_away": 0,
+               "scale_bytes_even_vs_base": 0, "scale_bytes_even_vs_away": 0}
+        for it in items:
+            nb, ne, na = nibbles(it["codes"]), nibbles(it["ce"]), nibbles(it["ca"])
+            cen["code_nibbles_even_vs_base"] += int((ne != nb).sum().item())
+            cen["code_nibbles_away_vs_base"] += int((na != nb).sum().item())
+            cen["code_nibbles_even_vs_away"] += int((ne != na).sum().item())
+            cen["scale_bytes_even_vs_base"] += int((it["se"] != it["sb"]).sum().item())
+            cen["scale_bytes_even_vs_away"] += int((it["se"] != it["sa"]).sum().item())
+        res["census"] = cen
+        res["census_frac_even_vs_base"] = round(cen["code_nibbles_even_vs_base"] / weights, 5)
+        out[fmt] = res
+        del items
+        torch.cuda.empty_cache()
     return out
 
 
@@ -501,6 +604,9 @@ def main():
         out["merge_8b"] = model_merge(sq, 20)
     if not args.no_model_step:
         out["step_8b"] = model_step(sq, 3, 1)
+        torch.cuda.empty_cache()
+    if not args.no_lifecycle:
+        out["lifecycle_8b"] = model_lifecycle(sq)
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(X, dY, codes, sb, delta, src, Wm.float().cpu().numpy())

@@ -16,23 +16,6 @@
 
 namespace sq {
 
-// E2M1 magnitude index (0..7 for 0,.5,1,1.5,2,3,4,6) of |q| with ties to the
-// even mantissa or away from zero; >= 6 saturates, NaN gives 0.
-template <bool AWAY>
-__device__ __forceinline__ uint32_t e2m1_round_index(float a) {
-  uint32_t i = 0;
-  if (AWAY) {
-    i += (a >= 0.25f); i += (a >= 0.75f); i += (a >= 1.25f); i += (a >= 1.75f);
-    i += (a >= 2.5f);  i += (a >= 3.5f);  i += (a >= 5.0f);
-  } else {
-    // a tie goes to whichever neighbour has an even index: 0.25->0, 0.75->1.0,
-    // 1.25->1.0, 1.75->2.0, 2.5->2.0, 3.5->4.0, 5->4.0
-    i += (a > 0.25f); i += (a >= 0.75f); i += (a > 1.25f); i += (a >= 1.75f);
-    i += (a > 2.5f);  i += (a >= 3.5f);  i += (a > 5.0f);
-  }
-  return i;
-}
-
 // ------------------------------------------------------------------ merge
 // The planes of a launch are cut into spans: kDeltaSpan scale bytes (delta
 // mode: kDeltaSteps steps of 4 scales and a 16-byte fp32 delta per lane) or
@@ -140,17 +123,13 @@ __device__ __forceinline__ int ceil_log2_pos(float x) {
   return (int)e - 127 + (frac != 0u);
 }
 
-// One thread per 8 consecutive weights of a row (16 bytes of bf16); the
-// B/8 threads of a block are adjacent lanes and share the block amax.
+// One chunk of 8 consecutive weights of a row (16 bytes of bf16, already
+// loaded); the B/8 lanes of a block are adjacent and share the block amax.
 template <int FMT, bool AWAY>
-__global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W, int64_t n_chunks,
-                                                  const float* ws2_ptr, float ws2_val,
-                                                  uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
+__device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, const float* ws2_ptr, float ws2_val,
+                                          uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
   constexpr int B = ScaleOperand<FMT>::kBlock;
   constexpr int LPB = B / 8;
-  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const bool valid = c < n_chunks;
-  uint4 v = valid ? *reinterpret_cast<const uint4*>(W + 8 * c) : make_uint4(0, 0, 0, 0);
   const uint32_t h[4] = {v.x, v.y, v.z, v.w};
   // amax as a bit pattern: for |x| the integer order of the bits is the
   // numeric order, with NaN above +inf, so NaN propagates like a max.
@@ -188,16 +167,39 @@ __global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W
     eff = __fmul_rn(e4m3_to_f32(sbyte), ws2);
   }
 
-  uint32_t packed = 0;
+  // Codes: gfx950's fp32 -> E2M1 convert rounds |q| to the nearest E2M1
+  // magnitude with ties to even and saturates at 6 (it equals the threshold
+  // rounding on every non-NaN fp32 input); ties away differ from it exactly at
+  // |q| = 0.25, 1.25, 2.5 and 5, where they take the next magnitude.  A NaN q
+  // codes as magnitude 0, and the sign bit is always the sign of w.
+  float q[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    const uint32_t hb = (h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
-    const float w = __uint_as_float(hb << 16);
-    float q;
-    if (FMT == kMX) q = __fmul_rn(w, eff);                  // w / 2^k, one rounding
-    else q = (eff == 0.0f) ? 0.0f : __fdiv_rn(w, eff);
-    const uint32_t mag = e2m1_round_index<AWAY>(fabsf(q));
-    packed |= (mag | ((hb >> 12) & 8u)) << (4 * k);
+    const float w = __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16);
+    if (FMT == kMX) q[k] = __fmul_rn(w, eff);               // w / 2^k, one rounding
+    else q[k] = (eff == 0.0f) ? 0.0f : __fdiv_rn(w, eff);
+  }
+  uint32_t packed = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+    packed |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, q[2 * p], q[2 * p + 1], 1.0f, 0) & 0xFFu) << (8 * p);
+  if (AWAY) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {                           // a tie magnitude is below 6: no carry
+      const float a = fabsf(q[k]);
+      packed += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * k)) : 0u;
+    }
+  }
+  // The convert carries the sign of q, which is the sign of w unless q is NaN
+  // (possible only when the block amax is NaN) or forced to +0 by a zero
+  // NVFP4 scale; only those blocks need the general fix-up.
+  if (am > 0x7F80u || (FMT == kNV && eff == 0.0f)) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint32_t hb = (h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+      const uint32_t mag = (q[k] != q[k]) ? 0u : ((packed >> (4 * k)) & 7u);
+      packed = (packed & ~(15u << (4 * k))) | ((mag | ((hb >> 12) & 8u)) << (4 * k));
+    }
   }
   if (valid) {
     reinterpret_cast<uint32_t*>(codes)[c] = packed;
@@ -205,22 +207,53 @@ __global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W
   }
 }
 
+// Each workgroup takes 512 chunks: a lane loads its two chunks (c and c + 256)
+// before working on either, so two 16-byte loads are in flight per lane.
+template <int FMT, bool AWAY>
+__global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W, int64_t n_chunks,
+                                                  const float* ws2_ptr, float ws2_val,
+                                                  uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
+  const int64_t c0 = (int64_t)blockIdx.x * 512 + threadIdx.x, c1 = c0 + 256;
+  const bool ok0 = c0 < n_chunks, ok1 = c1 < n_chunks;
+  const uint4 v0 = ok0 ? *reinterpret_cast<const uint4*>(W + 8 * c0) : make_uint4(0, 0, 0, 0);
+  const uint4 v1 = ok1 ? *reinterpret_cast<const uint4*>(W + 8 * c1) : make_uint4(0, 0, 0, 0);
+  rtn_chunk<FMT, AWAY>(v0, c0, ok0, ws2_ptr, ws2_val, codes, scales);
+  rtn_chunk<FMT, AWAY>(v1, c1, ok1, ws2_ptr, ws2_val, codes, scales);
+}
+
 __global__ void rtn_amax_init(float* slot) { *reinterpret_cast<uint32_t*>(slot) = 0u; }
 
+// Tensor amax (as bf16 bits) for the recomputed ws2: 4 loads in flight per
+// lane, one integer atomicMax per workgroup (a max of bit patterns is
+// order-independent, so the result is deterministic).
 __global__ __launch_bounds__(256) void rtn_amax(const uint16_t* __restrict__ W, int64_t n_chunks, float* slot) {
+  __shared__ uint32_t red[4];
   uint32_t am = 0;
-  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * 256) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  for (; c + 3 * stride < n_chunks; c += 4 * stride) {
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(W + 8 * (c + u * stride));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t h[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) am = max(am, max(h[k] & 0x7FFFu, (h[k] >> 16) & 0x7FFFu));
+    }
+  }
+  for (; c < n_chunks; c += stride) {
     const uint4 v = *reinterpret_cast<const uint4*>(W + 8 * c);
     const uint32_t h[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      am = max(am, h[k] & 0x7FFFu);
-      am = max(am, (h[k] >> 16) & 0x7FFFu);
-    }
+    for (int k = 0; k < 4; ++k) am = max(am, max(h[k] & 0x7FFFu, (h[k] >> 16) & 0x7FFFu));
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) am = max(am, (uint32_t)__shfl_xor((int)am, off));
-  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<unsigned int*>(slot), am << 16);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = am;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    atomicMax(reinterpret_cast<unsigned int*>(slot), max(max(red[0], red[1]), max(red[2], red[3])) << 16);
 }
 
 __global__ void rtn_ws2_store(float* slot, float v) { *slot = v; }
@@ -242,15 +275,15 @@ int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
       if (ws2_out) hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, ws2_out, ws2_in);
     } else {
       hipLaunchKernelGGL(rtn_amax_init, dim3(1), dim3(1), 0, s, ws2_out);
-      const int64_t want = (n_chunks + 255) / 256;
-      const unsigned grid = (unsigned)(want < 4096 ? (want > 0 ? want : 1) : 4096);
+      const int64_t want = (n_chunks + 1023) / 1024;
+      const unsigned grid = (unsigned)(want < 1024 ? (want > 0 ? want : 1) : 1024);
       hipLaunchKernelGGL(rtn_amax, dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_out);
       hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, ws2_out);
       ws2_ptr = ws2_out;
     }
   }
   if (n_chunks > 0) {
-    const unsigned grid = (unsigned)((n_chunks + 255) / 256);
+    const unsigned grid = (unsigned)((n_chunks + 511) / 512);
     if (fmt == kMX) {
       if (tie == 1) hipLaunchKernelGGL((rtn_kernel<kMX, true>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, 1.0f, codes, scales);
       else hipLaunchKernelGGL((rtn_kernel<kMX, false>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, 1.0f, codes, scales);

@@ -109,3 +109,24 @@ def device_e8m0_normal_exponents(seed: int, O: int, G: int, mean: float, std: fl
     """E8M0 bytes with exponents rint(N(mean, std)) clipped to [-127, 127], on the GPU."""
     e = torch.randn((O, G), generator=device_generator(seed), device="cuda") * std + mean
     return (torch.round(e).clamp_(-127, 127) + 127).to(torch.uint8)
+
+
+def device_task_delta(seed: int, eff: torch.Tensor, fmt: str) -> torch.Tensor:
+    """A task's fp32 scale delta on the device, for effective scales `eff` (fp32):
+    MXFP4: a one-exponent step (up: +eff, down: -eff/2, fair coin) on a seeded 5%
+    of blocks plus N(0, 0.01 eff) jitter (which rounds away on the log grid);
+    NVFP4: N(0, 0.02 eff)."""
+    g = device_generator(seed)
+    if fmt == "mx":
+        pick = torch.rand(eff.shape, generator=g, device="cuda") < 0.05
+        up = torch.rand(eff.shape, generator=g, device="cuda") < 0.5
+        step = torch.where(up, eff, -0.5 * eff)
+        jitter = torch.randn(eff.shape, generator=g, device="cuda") * (0.01 * eff)
+        return torch.where(pick, step, torch.zeros_like(eff)) + jitter
+    return torch.randn(eff.shape, generator=g, device="cuda") * (0.02 * eff)
+
+
+def device_e4m3_abs_normal(seed: int, O: int, G: int) -> torch.Tensor:
+    """E4M3 bytes of |N(0, 1)| samples on the GPU (torch's round-to-nearest-even cast)."""
+    x = torch.randn((O, G), generator=device_generator(seed), device="cuda").abs()
+    return x.to(torch.float8_e4m3fn).view(torch.uint8)

@@ -72,6 +72,34 @@ def test_merge_delta_random_matches_oracle(sq, fmt, n):
     assert guards_intact(buf)
 
 
+@pytest.mark.parametrize("fmt,n", [("mx", 8192 * 5 + 3), ("nv", 8192 * 2 + 4100), ("mx", 8192)])
+def test_merge_delta_full_spans_and_tail(sq, fmt, n):
+    """Planes of several whole workgroup spans (8192 scales) plus a ragged tail."""
+    g = inputs.rng(91 + n)
+    sb = g.integers(90, 150, size=n).astype(np.uint8) if fmt == "mx" else g.integers(0, 0x7E, size=n).astype(np.uint8)
+    ws2 = 1.0 if fmt == "mx" else float(np.float32(1 / 448))
+    eff = codec.effective_scales(fmt, sb, ws2)
+    d = (g.standard_normal(n) * eff * 0.7).astype(np.float32)
+    buf, plane = guarded(sb)
+    sq.sq_merge_scales(fmt, plane, delta=torch.from_numpy(d).cuda(), ws2=ws2)
+    torch.cuda.synchronize()
+    assert np.array_equal(plane.cpu().numpy(), merge.merge_delta(fmt, sb, d, ws2))
+    assert guards_intact(buf)
+
+
+@pytest.mark.parametrize("n", [32768 * 3 + 100, 32768, 32768 * 2 + 16])
+def test_swap_full_spans_and_tail(sq, n):
+    """Copies of several whole workgroup spans (32 KiB) plus a ragged tail."""
+    g = inputs.rng(93 + n)
+    sb = g.integers(0, 256, size=n).astype(np.uint8)
+    src = g.integers(0, 256, size=n).astype(np.uint8)
+    buf, plane = guarded(sb)
+    sq.sq_merge_scales("mx", plane, src=torch.from_numpy(src).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(plane.cpu().numpy(), src)
+    assert guards_intact(buf)
+
+
 @pytest.mark.parametrize("fmt", ["mx", "nv"])
 def test_merge_all_bytes_delta_zero_identity(sq, fmt):
     sb = np.arange(0, 255 if fmt == "mx" else 0x7F, dtype=np.uint8)
@@ -184,6 +212,34 @@ def test_rtn_matches_oracle(sq, fmt, tie, ws2_mode):
         assert w2.cpu().numpy()[0] == rw
     # codes moved relative to the base plane (the naive merge rewrites codes)
     print(f"  {fmt} {tie} {ws2_mode}: code bytes changed vs base {np.mean(rc != codes):.3f}")
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+def test_rtn_8b_gate_projection_sampled_rows(sq, fmt):
+    """14336 x 4096 merged weight (the gate projection): the whole plane is
+    re-quantised on the GPU, and seeded rows are checked byte for byte against
+    the oracle, for both tie rules (and, for NVFP4, the recomputed ws2, which the
+    oracle takes from the whole tensor)."""
+    O, I = 14336, 4096
+    Wb, codes, sb, ws2 = _merged_weight(fmt, O, I, seed=4100)
+    Wd = Wb.cuda()
+    rows = np.sort(np.concatenate([inputs.rng(4101).choice(O, 47, replace=False), [O - 1]]))
+    Wrows = Wb[torch.from_numpy(rows)].float().numpy()
+    modes = [("even", sq.TIE_EVEN, ws2), ("away", sq.TIE_AWAY, ws2)]
+    if fmt == "nv":
+        modes.append(("even", sq.TIE_EVEN, 0.0))
+    for tie, tie_c, w_in in modes:
+        print(f"[rtn 8b] fmt={fmt} tie={tie} ws2_in={w_in}", flush=True)
+        c, s, w2 = sq.rtn_quantize(fmt, Wd, tie_c, w_in)
+        torch.cuda.synchronize()
+        if fmt == "nv" and w_in == 0.0:
+            w_ref = rtn.recompute_ws2(Wb.float().numpy())
+            assert w2.cpu().numpy()[0] == w_ref
+        else:
+            w_ref = w_in if fmt == "nv" else None
+        rc, rs, _ = rtn.quantize(fmt, Wrows, tie, w_ref)
+        assert np.array_equal(c.cpu().numpy()[rows], rc)
+        assert np.array_equal(s.cpu().numpy()[rows], rs)
 
 
 def test_rtn_ties_and_specials(sq):
