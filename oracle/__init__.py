@@ -30,10 +30,13 @@ rtn     round-to-nearest re-quantisation of a bf16 weight, the naive merge
         baseline (§2 "The naive re-quantized merge"; App. "Why the naive merge
         returns the base" for the amax/6 rule; App. "Calibrated PTQ on a sparse
         MoE" for the MXFP4 ceil-log2 rule).
+audit   merge rollback with the applied on-grid delta and byte / nibble diff
+        counts (App. B "Payoff 3: invertible merges and rollback", "Payoff 5:
+        verifiability and provenance").
 qast    one QAST low-rank scale step: Delta_S = (alpha/r) B A, the on-grid
         scale bytes through the merge's grid-and-clamp path, the clamp mask,
         and the factor gradients dB, dA (§3 "Scale-QLoRA forward", "QAST
         makes merge exact by construction", stability recipe (ii)-(iii)).
 """
 
-from . import codec, linear, merge, qast, rtn  # noqa: F401
+from . import audit, codec, linear, merge, qast, rtn  # noqa: F401
