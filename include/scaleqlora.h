@@ -242,6 +242,37 @@ int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS, const uin
                          const void* B, const void* A, float alpha_over_r, float* dB, float* dA,
                          void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Merge rollback (Appendix B, "Payoff 3: invertible merges and rollback"): a
+ * merged scale plane plus the on-grid delta the merge applied restores the
+ * base plane byte for byte, with no retained base.  The delta lives in the
+ * stored field's value domain: the E4M3 value for NVFP4 (ws2 stays out), the
+ * effective scale 2^(b-127) for MXFP4.
+ *
+ * sq_scale_applied_delta: applied[i] = value(after[i]) - value(before[i]),
+ *   one fp32 subtraction (exact when the two values are within 24 binades,
+ *   which covers every pair of finite E4M3 bytes).
+ * sq_scale_rollback: scales[i] = encode(value(scales[i]) - applied[i]), in
+ *   place, with the merge's encoders (E4M3 nearest-even saturating; E8M0
+ *   log-nearest).
+ * before, after, scales: device uint8 [n]; applied: device fp32 [n]; all
+ * 16-byte aligned; n >= 0.
+ */
+int sq_scale_applied_delta(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied,
+                           void* stream);
+int sq_scale_rollback(int fmt, int64_t n, uint8_t* scales, const float* applied, void* stream);
+
+/*
+ * Byte audit (Appendix B, "Payoff 5: verifiability and provenance"): with codes
+ * frozen a scale-merged artifact may differ from its base only in the scale
+ * plane.  Adds to counts[0] the number of bytes i with a[i] != b[i] and to
+ * counts[1] the number of differing 4-bit nibbles (E2M1 codes for a code
+ * plane).  a, b: device uint8 [n], 16-byte aligned; counts: device uint64 [2],
+ * 8-byte aligned, accumulated (the caller zeroes it), exact and
+ * order-independent.
+ */
+int sq_byte_diff(int64_t n, const uint8_t* a, const uint8_t* b, uint64_t* counts, void* stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* sq_status_str(int status);
 

@@ -30,9 +30,9 @@ def _values(fmt: str, b: np.ndarray) -> np.ndarray:
 
 
 def applied_delta(fmt: str, before: np.ndarray, after: np.ndarray) -> np.ndarray:
-    """fp32 on-grid delta value(after) - value(before) (NaN where either byte is NaN)."""
-    d = _values(fmt, after) - _values(fmt, before)           # fp64, exact
-    return d.astype(np.float32)
+    """fp32 on-grid delta value(after) - value(before), one fp32 subtraction (both
+    values are fp32-representable; NaN where either byte is NaN)."""
+    return _values(fmt, after).astype(np.float32) - _values(fmt, before).astype(np.float32)
 
 
 def rollback(fmt: str, merged: np.ndarray, applied: np.ndarray) -> np.ndarray:

@@ -222,6 +222,34 @@ SQ_EXPORT int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS,
                                           static_cast<hipStream_t>(stream)));
 }
 
+SQ_EXPORT int sq_scale_applied_delta(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied,
+                                     void* stream) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  if (n < 0) return SQ_ERR_SHAPE;
+  if (n == 0) return SQ_OK;
+  if (!before || !after || !applied) return SQ_ERR_ARG;
+  if (!aligned(before, 16) || !aligned(after, 16) || !aligned(applied, 16)) return SQ_ERR_ALIGN;
+  return hip_status(sq::applied_launch(fmt, n, before, after, applied, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int sq_scale_rollback(int fmt, int64_t n, uint8_t* scales, const float* applied, void* stream) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  if (n < 0) return SQ_ERR_SHAPE;
+  if (n == 0) return SQ_OK;
+  if (!scales || !applied) return SQ_ERR_ARG;
+  if (!aligned(scales, 16) || !aligned(applied, 16)) return SQ_ERR_ALIGN;
+  return hip_status(sq::rollback_launch(fmt, n, scales, applied, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int sq_byte_diff(int64_t n, const uint8_t* a, const uint8_t* b, uint64_t* counts, void* stream) {
+  if (n < 0) return SQ_ERR_SHAPE;
+  if (!counts) return SQ_ERR_ARG;
+  if (n == 0) return SQ_OK;
+  if (!a || !b) return SQ_ERR_ARG;
+  if (!aligned(a, 16) || !aligned(b, 16) || !aligned(counts, 8)) return SQ_ERR_ALIGN;
+  return hip_status(sq::byte_diff_launch(n, a, b, counts, static_cast<hipStream_t>(stream)));
+}
+
 SQ_EXPORT const char* sq_status_str(int status) {
   switch (status) {
     case SQ_OK: return "SQ_OK";

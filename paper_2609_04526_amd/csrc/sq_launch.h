@@ -58,4 +58,9 @@ size_t qast_grads_workspace(int O, int G, int r);
 int qast_grads_launch(int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
                       float alpha_over_r, float* dB, float* dA, void* workspace, hipStream_t s);
 
+// Rollback and byte audit (sq_audit.hip).
+int applied_launch(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied, hipStream_t s);
+int rollback_launch(int fmt, int64_t n, uint8_t* scales, const float* applied, hipStream_t s);
+int byte_diff_launch(int64_t n, const uint8_t* a, const uint8_t* b, uint64_t* counts, hipStream_t s);
+
 }  // namespace sq

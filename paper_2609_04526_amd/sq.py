@@ -76,6 +76,9 @@ def load():
         "sq_qast_factor_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, ctypes.c_int]),
         "sq_qast_factor_grads": (ctypes.c_int, [_c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p, _c_p,
                                                 ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+        "sq_scale_applied_delta": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_p, _c_p, _c_p, _c_p]),
+        "sq_scale_rollback": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_p, _c_p, _c_p]),
+        "sq_byte_diff": (ctypes.c_int, [_c_i64, _c_p, _c_p, _c_p, _c_p]),
         "sq_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "sq_abi_version": (ctypes.c_int, []),
     }
@@ -251,6 +254,34 @@ def sq_qast_factor_grads(dS, mask, B, A, alpha_over_r, dB=None, dA=None, workspa
                                                                float(alpha_over_r), _ptr(dB), _ptr(dA),
                                                                _ptr(workspace), wsz, _stream()))
     return dB, dA
+
+
+def sq_scale_applied_delta(fmt, before, after, applied=None):
+    """fp32 on-grid delta value(after) - value(before) of two scale planes (same shape)."""
+    fmt = _fmt(fmt)
+    if applied is None:
+        applied = torch.empty(before.shape, dtype=torch.float32, device=before.device)
+    _dev(before, after, applied)
+    _check("sq_scale_applied_delta", load().sq_scale_applied_delta(fmt, before.numel(), _ptr(before), _ptr(after),
+                                                                   _ptr(applied), _stream()))
+    return applied
+
+
+def sq_scale_rollback(fmt, scales, applied):
+    """In place: scales := encode(value(scales) - applied)."""
+    fmt = _fmt(fmt)
+    _dev(scales, applied)
+    _check("sq_scale_rollback", load().sq_scale_rollback(fmt, scales.numel(), _ptr(scales), _ptr(applied), _stream()))
+    return scales
+
+
+def sq_byte_diff(a, b, counts=None):
+    """Adds (differing bytes, differing nibbles) of two byte planes to a device int64 [2] tensor."""
+    if counts is None:
+        counts = torch.zeros(2, dtype=torch.int64, device=a.device)
+    _dev(a, b, counts)
+    _check("sq_byte_diff", load().sq_byte_diff(a.numel(), _ptr(a), _ptr(b), _ptr(counts), _stream()))
+    return counts
 
 
 def abi_version():

@@ -158,3 +158,17 @@ def test_qast_validation(lib):
     assert g(8, 4, 2, FAKE + 2, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, need, None) == -3     # dS
     assert g(8, 4, 2, FAKE, None, FAKE, FAKE, 1.0, None, FAKE, FAKE, need, None) == -1         # dB
     assert g(8, 4, 65, FAKE, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, need, None) == -2
+
+
+def test_rollback_and_audit_validation(lib):
+    assert lib.sq_scale_applied_delta(2, 16, FAKE, FAKE, FAKE, None) == -4
+    assert lib.sq_scale_applied_delta(0, -1, FAKE, FAKE, FAKE, None) == -2
+    assert lib.sq_scale_applied_delta(0, 0, None, None, None, None) == 0          # empty plane
+    assert lib.sq_scale_applied_delta(0, 16, FAKE, None, FAKE, None) == -1
+    assert lib.sq_scale_applied_delta(1, 16, FAKE, FAKE, FAKE + 4, None) == -3
+    assert lib.sq_scale_rollback(0, 16, FAKE + 1, FAKE, None) == -3
+    assert lib.sq_scale_rollback(0, 16, FAKE, None, None) == -1
+    assert lib.sq_byte_diff(16, FAKE, FAKE, None, None) == -1
+    assert lib.sq_byte_diff(16, FAKE, FAKE + 8, FAKE, None) == -3
+    assert lib.sq_byte_diff(16, FAKE, FAKE, FAKE + 4, None) == -3
+    assert lib.sq_byte_diff(0, None, None, FAKE, None) == 0
