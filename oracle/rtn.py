@@ -20,14 +20,27 @@ chosen tie rule (ties to the even mantissa, or half away from zero, App. B
 threat model (a): tools differ in tie-breaking), saturating at 6; the sign bit
 is the sign of w, also when the magnitude rounds to 0.  A NaN q codes as
 magnitude 0.
+
+Deploy-rule variants (App. "Deployment-quantizer sweep" / threat model: rules
+a serving-side quantiser may apply to a continuous merged tensor), in
+quantize_rule: round toward zero (the largest E2M1 magnitude not above |q|),
+stochastic rounding (|q| goes up to the next magnitude with probability equal
+to its fractional position between the two neighbours, drawn from Philox4x64-10
+with the uniform of element e = o*I + i taken as described in philox.py), and
+whole-tensor scaling (one scale for the whole tensor from the tensor amax, by
+the same scale rule, with nearest-even codes).  On-grid values are fixed points
+of truncation and of stochastic rounding, as they are of nearest rounding.
 """
 
 import numpy as np
 
-from . import codec
+from . import codec, philox
 
 TIE_EVEN = "even"
 TIE_AWAY = "away"
+RULE_RTZ = "rtz"
+RULE_STOCHASTIC = "stochastic"
+RULE_WHOLE_TENSOR = "whole_tensor"
 _GRID = codec.E2M1_TABLE[:8]          # 0, .5, 1, 1.5, 2, 3, 4, 6 (magnitude index order)
 
 
@@ -94,5 +107,64 @@ def quantize(fmt: str, W: np.ndarray, tie: str = TIE_EVEN, ws2=None):
             raise ValueError(fmt)
     mag = e2m1_round_magnitude(q, tie)
     sign = np.signbit(Wb).astype(np.uint8) << 3
+    nib = (mag | sign).reshape(O, I)
+    return codec.pack_nibbles(nib), sbytes.reshape(O, G), np.float32(out_ws2)
+
+
+def e2m1_round_rule(q: np.ndarray, rule: str, u: np.ndarray = None) -> np.ndarray:
+    """|q| (fp32) -> E2M1 magnitude index 0..7 under RTZ or stochastic rounding
+    (u: fp32 uniforms in [0, 1) of q's shape).  Saturates at 6; NaN -> 0."""
+    a = np.abs(np.asarray(q, dtype=np.float32).astype(np.float64))
+    nan = np.isnan(a)
+    a = np.where(nan, 0.0, np.minimum(a, 6.0))
+    lo = np.searchsorted(_GRID, a, side="right") - 1            # largest magnitude <= a
+    if rule == RULE_RTZ:
+        idx = lo
+    elif rule == RULE_STOCHASTIC:
+        hi = np.minimum(lo + 1, 7)
+        gap = _GRID[hi] - _GRID[lo]
+        frac = np.where(gap > 0, (a - _GRID[lo]) / np.where(gap > 0, gap, 1.0), 0.0)   # exact
+        idx = np.where(np.asarray(u, dtype=np.float64) < frac, hi, lo)
+    else:
+        raise ValueError(rule)
+    return np.where(nan, 0, idx).astype(np.uint8)
+
+
+def quantize_rule(fmt: str, W: np.ndarray, rule: str, ws2=None, seed: int = 0):
+    """quantize() under a deploy rule: "even" / "away" (nearest, per-block scales),
+    "rtz", "stochastic" (per-block scales, other code rounding) or "whole_tensor"
+    (one scale for the tensor, nearest-even codes).  Same returns as quantize()."""
+    if rule in (TIE_EVEN, TIE_AWAY):
+        return quantize(fmt, W, rule, ws2)
+    W = np.asarray(W, dtype=np.float32)
+    O, I = W.shape
+    block = codec.BLOCK[fmt]
+    G = I // block
+    if rule == RULE_WHOLE_TENSOR:
+        amax_t = np.float32(np.max(np.abs(W))) if W.size else np.float32(0)
+        tiled = np.zeros((O, G, block), np.float32)
+        tiled[:, :, 0] = amax_t                                   # every block sees the tensor amax
+        _, sbytes, out_ws2 = quantize(fmt, tiled.reshape(O, I), TIE_EVEN,
+                                      ws2 if ws2 is not None else (recompute_ws2(W) if fmt == codec.NV else None))
+        eff = codec.effective_scales(fmt, sbytes, out_ws2).astype(np.float32)
+        Wb = W.reshape(O, G, block)
+        with np.errstate(invalid="ignore", divide="ignore", over="ignore"):
+            if fmt == codec.MX:
+                q = (Wb.astype(np.float64) / eff[:, :, None].astype(np.float64)).astype(np.float32)
+            else:
+                q = np.where(eff[:, :, None] == 0, np.float32(0.0), Wb / eff[:, :, None])
+        mag = e2m1_round_magnitude(q, TIE_EVEN)
+    else:
+        codes, sbytes, out_ws2 = quantize(fmt, W, TIE_EVEN, ws2)
+        eff = codec.effective_scales(fmt, sbytes, out_ws2).astype(np.float32)
+        Wb = W.reshape(O, G, block)
+        with np.errstate(invalid="ignore", divide="ignore", over="ignore"):
+            if fmt == codec.MX:
+                q = (Wb.astype(np.float64) / eff[:, :, None].astype(np.float64)).astype(np.float32)
+            else:
+                q = np.where(eff[:, :, None] == 0, np.float32(0.0), Wb / eff[:, :, None])
+        u = philox.uniforms24(O * I, seed).reshape(O, G, block) if rule == RULE_STOCHASTIC else None
+        mag = e2m1_round_rule(q, rule, u)
+    sign = np.signbit(W.reshape(O, G, block)).astype(np.uint8) << 3
     nib = (mag | sign).reshape(O, I)
     return codec.pack_nibbles(nib), sbytes.reshape(O, G), np.float32(out_ws2)
