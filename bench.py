@@ -155,6 +155,31 @@ def model_merge(sq, steps):
         sq.sq_merge_scales_grouped(group)              # the merge itself: base -> merged
         torch.cuda.synchronize()
         changed = float((scales != base).sum().item()) / total
+        rb = None
+        if mode == "delta":
+            # rollback: the applied on-grid delta restores the base byte for byte
+            applied = sq.sq_scale_applied_delta(fmt, base, scales)
+            restored = scales.clone()
+            sq.sq_scale_rollback(fmt, restored, applied)
+            counts = sq.sq_byte_diff(restored, base)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(steps):
+                sq.sq_scale_rollback(fmt, restored, applied)
+            e1.record()
+            torch.cuda.synchronize()
+            rb_ms = e0.elapsed_time(e1) / steps
+            e0.record()
+            for _ in range(steps):
+                sq.sq_byte_diff(restored, base, counts=torch.zeros(2, dtype=torch.int64, device="cuda"))
+            e1.record()
+            torch.cuda.synchronize()
+            diff_ms = e0.elapsed_time(e1) / steps
+            rb = {"restored_bytes_differing": int(counts[0].item()),
+                  "rollback_ms": round(rb_ms, 4), "rollback_GB/s": round(6 * total / (rb_ms * 1e-3) / 1e9, 1),
+                  "audit_ms": round(diff_ms, 4), "audit_GB/s": round(2 * total / (diff_ms * 1e-3) / 1e9, 1)}
+            del applied, restored
         for _ in range(2):
             sq.sq_merge_scales_grouped(group)
         torch.cuda.synchronize()
@@ -170,6 +195,8 @@ def model_merge(sq, steps):
         out[name] = {"scales": total, "planes": len(sizes), "bytes_per_scale": bps, "ms": round(ms, 4),
                      "GB/s": round(gbs, 1), "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "changed_byte_frac": round(changed, 5)}
+        if rb is not None:
+            out[name]["rollback"] = rb
         del scales, base, aux, descs, group
         torch.cuda.empty_cache()
     out["note"] = ("delta merges are re-applied to the merged planes in the timed repetitions (same bytes "
