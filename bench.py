@@ -208,8 +208,9 @@ def model_lifecycle(sq, steps=3):
     """The naive merge's re-quantisation over the whole 8B model: for every
     linear, the bf16 merged weight W + B A (rank 16, A, B ~ N(0, 0.02), W the
     dequantised base) re-quantised by rtn_quantize with ties to even and ties
-    away.  Timed over all 224 linears; algorithmic bytes 2 + 0.5 + 1/B per
-    weight.  The diff census counts code nibbles that differ from the base
+    away, and by rtn_quantize_rule under the deploy-side rules (toward zero,
+    stochastic, whole-tensor scale).  Timed over all 224 linears; algorithmic
+    bytes 2 + 0.5 + 1/B per weight.  The diff census counts code nibbles that differ from the base
     plane (per tie rule) and between the tie rules, and changed scale bytes."""
     lut = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0],
                        device="cuda")
@@ -235,6 +236,7 @@ def model_lifecycle(sq, steps=3):
             items.append(dict(codes=codes, sb=sb, Wm=Wm,
                               ce=torch.empty_like(codes), se=torch.empty_like(sb),
                               ca=torch.empty_like(codes), sa=torch.empty_like(sb),
+                              cr=torch.empty_like(codes), sr=torch.empty_like(sb),
                               w2=torch.empty(1, dtype=torch.float32, device="cuda")))
         weights = sum(it["Wm"].numel() for it in items)
         nbytes = weights * (2 + 0.5 + 1.0 / block)
@@ -242,11 +244,19 @@ def model_lifecycle(sq, steps=3):
         runs = [("even", sq.TIE_EVEN, ws2, "ce", "se"), ("away", sq.TIE_AWAY, ws2, "ca", "sa")]
         if fmt == "nv":
             runs.append(("even_ws2_recomputed", sq.TIE_EVEN, 0.0, "ce", "se"))
+        # deploy-side rules through rtn_quantize_rule (the whole-tensor rule
+        # takes its amax in a pre-pass, so it reads W twice)
+        runs += [("rtz", "rtz", ws2, "cr", "sr"), ("stochastic", "stochastic", ws2, "cr", "sr"),
+                 ("whole_tensor", "whole_tensor", 0.0, "cr", "sr")]
         for label, tie, w_in, ck, sk in runs:
             def run():
                 for it in items:
-                    sq.rtn_quantize(fmt, it["Wm"], tie, w_in, codes=it[ck], scales=it[sk],
-                                    ws2_out=it["w2"] if fmt == "nv" else None)
+                    if isinstance(tie, str):
+                        sq.rtn_quantize_rule(fmt, it["Wm"], tie, w_in if fmt == "nv" else 0.0, 1234,
+                                             codes=it[ck], scales=it[sk], ws2_out=it["w2"])
+                    else:
+                        sq.rtn_quantize(fmt, it["Wm"], tie, w_in, codes=it[ck], scales=it[sk],
+                                        ws2_out=it["w2"] if fmt == "nv" else None)
             run()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -256,9 +266,15 @@ def model_lifecycle(sq, steps=3):
             e1.record()
             torch.cuda.synchronize()
             ms = e0.elapsed_time(e1) / steps
-            moved = nbytes + (weights * 2 if w_in == 0.0 else 0)      # the amax pre-pass reads W once more
+            two_pass = (w_in == 0.0 and fmt == "nv") or tie == "whole_tensor"
+            moved = nbytes + (weights * 2 if two_pass else 0)       # the amax pre-pass reads W once more
             res[label] = {"ms": round(ms, 3), "GB/s": round(moved / (ms * 1e-3) / 1e9, 1),
                           "frac": round(moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+            if ck == "cr":
+                nb_moved = sum(int((nibbles(it["cr"]) != nibbles(it["codes"])).sum().item()) for it in items)
+                sb_moved = sum(int((it["sr"] != it["sb"]).sum().item()) for it in items)
+                res[label]["code_nibbles_vs_base_frac"] = round(nb_moved / weights, 5)
+                res[label]["scale_bytes_vs_base"] = sb_moved
         # census (ties to even and ties away, both with the fixed ws2 for NVFP4)
         for it in items:
             sq.rtn_quantize(fmt, it["Wm"], sq.TIE_EVEN, ws2, codes=it["ce"], scales=it["se"],

@@ -76,6 +76,13 @@ typedef enum { SQ_MXFP4 = 0, SQ_NVFP4 = 1 } sq_format;
 typedef enum { SQ_OUT_F32 = 0, SQ_OUT_BF16 = 1 } sq_out_dtype;
 typedef enum { SQ_TIE_EVEN = 0, SQ_TIE_AWAY = 1 } sq_tie;
 typedef enum { SQ_MERGE_DELTA = 0, SQ_MERGE_COPY = 1 } sq_merge_mode;
+typedef enum {
+  SQ_RULE_NEAREST_EVEN = 0,  /* = rtn_quantize with SQ_TIE_EVEN */
+  SQ_RULE_NEAREST_AWAY = 1,  /* = rtn_quantize with SQ_TIE_AWAY */
+  SQ_RULE_RTZ = 2,           /* codes toward zero, per-block scales */
+  SQ_RULE_STOCHASTIC = 3,    /* codes by stochastic rounding, per-block scales */
+  SQ_RULE_WHOLE_TENSOR = 4   /* one scale from the tensor amax, nearest-even codes */
+} sq_rule;
 
 /*
  * Forward, Y = X W^T (paper Section 2 storage equation; Section 3,
@@ -202,6 +209,34 @@ int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream
  */
 int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int tie,
                  uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream);
+
+/*
+ * Re-quantisation of a bf16 weight under a serving-side rule, the out-of-family
+ * deploy quantisers of the robustness sweep (Appendix B, threat model (a) and
+ * the deployment-quantizer sweep: truncation, stochastic rounding and a
+ * whole-tensor scale alongside the nearest rules).
+ *
+ *   SQ_RULE_NEAREST_EVEN / _AWAY: exactly rtn_quantize with that tie rule.
+ *   SQ_RULE_RTZ: scales as rtn_quantize; each code magnitude is the largest
+ *          E2M1 magnitude not above min(|q|, 6).
+ *   SQ_RULE_STOCHASTIC: scales as rtn_quantize; with lo the truncated
+ *          magnitude and hi the next one (hi = lo at 6), the code takes hi iff
+ *          u_e < (min(|q|, 6) - lo) / (hi - lo), where u_e for element
+ *          e = o*I + i is word e % 4 of Philox4x64-10 at counter (e / 4, 0, 0,
+ *          0) and key (seed, 0), its top 24 bits times 2^-24.  On-grid values
+ *          never move.
+ *   SQ_RULE_WHOLE_TENSOR: every block takes the scale rtn_quantize would give
+ *          a block whose amax is the tensor amax (for NVFP4, ws2 fixed or
+ *          recomputed as in rtn_quantize); codes nearest-even.
+ *   A NaN q codes as magnitude 0 and the sign bit is the sign of w (all rules).
+ *
+ * Arguments as rtn_quantize.  ws2_out (device fp32 scalar, 4-byte aligned) is
+ * required for SQ_RULE_WHOLE_TENSOR (it holds the tensor amax during the call
+ * and the ws2 used at the end, 1 for MXFP4) and wherever rtn_quantize needs it.
+ * seed is used by SQ_RULE_STOCHASTIC only.
+ */
+int rtn_quantize_rule(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int rule, uint64_t seed,
+                      uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream);
 
 /*
  * QAST low-rank scale step (Section 3, "Scale-QLoRA forward": Delta_S =

@@ -46,10 +46,10 @@ def philox4x64_10(c0, c1, c2, c3, k0: int, k1: int):
     return c0, c1, c2, c3
 
 
-def uniforms24(n: int, seed: int) -> np.ndarray:
-    """u_e for e = 0 .. n-1: counter (e // 4, 0, 0, 0), key (seed, 0), output word
-    e % 4, its top 24 bits times 2^-24 (exact in fp32; u in [0, 1))."""
-    e = np.arange(n, dtype=np.uint64)
+def uniforms24(n: int, seed: int, start: int = 0) -> np.ndarray:
+    """u_e for e = start .. start+n-1: counter (e // 4, 0, 0, 0), key (seed, 0),
+    output word e % 4, its top 24 bits times 2^-24 (exact in fp32; u in [0, 1))."""
+    e = np.arange(start, start + n, dtype=np.uint64)
     z = np.zeros_like(e)
     words = philox4x64_10(e >> np.uint64(2), z, z, z, seed, 0)
     w = np.choose((e & np.uint64(3)).astype(np.int64), words)

@@ -130,10 +130,12 @@ def e2m1_round_rule(q: np.ndarray, rule: str, u: np.ndarray = None) -> np.ndarra
     return np.where(nan, 0, idx).astype(np.uint8)
 
 
-def quantize_rule(fmt: str, W: np.ndarray, rule: str, ws2=None, seed: int = 0):
+def quantize_rule(fmt: str, W: np.ndarray, rule: str, ws2=None, seed: int = 0, row0: int = 0):
     """quantize() under a deploy rule: "even" / "away" (nearest, per-block scales),
     "rtz", "stochastic" (per-block scales, other code rounding) or "whole_tensor"
-    (one scale for the tensor, nearest-even codes).  Same returns as quantize()."""
+    (one scale for the tensor, nearest-even codes).  Same returns as quantize().
+    row0: W holds rows row0 .. of a larger tensor of the same width, so the
+    stochastic rule's element index starts at row0 * I."""
     if rule in (TIE_EVEN, TIE_AWAY):
         return quantize(fmt, W, rule, ws2)
     W = np.asarray(W, dtype=np.float32)
@@ -163,7 +165,7 @@ def quantize_rule(fmt: str, W: np.ndarray, rule: str, ws2=None, seed: int = 0):
                 q = (Wb.astype(np.float64) / eff[:, :, None].astype(np.float64)).astype(np.float32)
             else:
                 q = np.where(eff[:, :, None] == 0, np.float32(0.0), Wb / eff[:, :, None])
-        u = philox.uniforms24(O * I, seed).reshape(O, G, block) if rule == RULE_STOCHASTIC else None
+        u = philox.uniforms24(O * I, seed, row0 * I).reshape(O, G, block) if rule == RULE_STOCHASTIC else None
         mag = e2m1_round_rule(q, rule, u)
     sign = np.signbit(W.reshape(O, G, block)).astype(np.uint8) << 3
     nib = (mag | sign).reshape(O, I)

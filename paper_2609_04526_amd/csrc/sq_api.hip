@@ -176,6 +176,23 @@ SQ_EXPORT int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float w
                                    fmt == SQ_NVFP4 ? ws2_out : nullptr, static_cast<hipStream_t>(stream)));
 }
 
+SQ_EXPORT int rtn_quantize_rule(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int rule,
+                                uint64_t seed, uint8_t* codes_out, uint8_t* scales_out, float* ws2_out,
+                                void* stream) {
+  int st = check_layer(fmt, 0, O, I);
+  if (st != SQ_OK) return st;
+  if (rule < SQ_RULE_NEAREST_EVEN || rule > SQ_RULE_WHOLE_TENSOR) return SQ_ERR_ARG;
+  if (!W || !codes_out || !scales_out) return SQ_ERR_ARG;
+  if (ws2_in > 0.0f && !isfinite(ws2_in)) return SQ_ERR_ARG;
+  const bool slot = rule == SQ_RULE_WHOLE_TENSOR || (fmt == SQ_NVFP4 && !(ws2_in > 0.0f));
+  if (slot && !ws2_out) return SQ_ERR_ARG;                   // the amax slot
+  if (ws2_out && !aligned(ws2_out, 4)) return SQ_ERR_ALIGN;
+  if (!aligned(W, 16) || !aligned(codes_out, 4)) return SQ_ERR_ALIGN;
+  float* out = (fmt == SQ_NVFP4 || rule == SQ_RULE_WHOLE_TENSOR) ? ws2_out : nullptr;
+  return hip_status(sq::rtn_rule_launch(fmt, (int)O, (int)I, W, fmt == SQ_NVFP4 ? ws2_in : 0.0f, rule, seed,
+                                        codes_out, scales_out, out, static_cast<hipStream_t>(stream)));
+}
+
 namespace {
 constexpr int kQastRankMax = 64;
 

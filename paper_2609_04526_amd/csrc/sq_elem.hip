@@ -123,10 +123,64 @@ __device__ __forceinline__ int ceil_log2_pos(float x) {
   return (int)e - 127 + (frac != 0u);
 }
 
+// The 128-bit product a * m as (hi, lo) from four 32 x 32 -> 64-bit
+// multiply-adds; no partial sum overflows 64 bits.
+__device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t m, uint64_t& hi, uint64_t& lo) {
+  const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32), m0 = (uint32_t)m, m1 = (uint32_t)(m >> 32);
+  const uint64_t p00 = (uint64_t)a0 * m0;
+  const uint64_t t = (uint64_t)a1 * m0 + (p00 >> 32);
+  const uint64_t u = (uint64_t)a0 * m1 + (uint32_t)t;
+  hi = (uint64_t)a1 * m1 + (t >> 32) + (u >> 32);
+  lo = (u << 32) | (uint32_t)p00;
+}
+
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011) with counter
+// (c, 0, 0, 0) and key (key, 0): ten rounds of two 64 x 64 -> 128-bit
+// products recombined with the other counter words and the key, the key
+// bumped by two Weyl constants between rounds.  Written from the published
+// definition; it feeds the stochastic deploy rule.
+__device__ __forceinline__ void philox4x64_10(uint64_t c, uint64_t key, uint64_t out[4]) {
+  uint64_t x0 = c, x1 = 0, x2 = 0, x3 = 0, k0 = key, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B97F4A7C15ull;
+      k1 += 0xBB67AE8584CAA73Bull;
+    }
+    uint64_t hi0, lo0, hi1, lo1;
+    mulhilo64(x0, 0xD2E7470EE14C6C93ull, hi0, lo0);
+    mulhilo64(x2, 0xCA5A826395121157ull, hi1, lo1);
+    x0 = hi1 ^ x1 ^ k0;
+    x1 = lo1;
+    x2 = hi0 ^ x3 ^ k1;
+    x3 = lo0;
+  }
+  out[0] = x0;
+  out[1] = x1;
+  out[2] = x2;
+  out[3] = x3;
+}
+
+// E2M1 magnitude of index m (0..7): twice the values 0, .5, 1, 1.5, 2, 3, 4, 6
+// sit in the nibbles of 0xC8643210.
+__device__ __forceinline__ float e2m1_mag(uint32_t m) {
+  return (float)((0xC8643210u >> (4u * m)) & 0xFu) * 0.5f;
+}
+
+// Rounding rules of the re-quantiser.  The nearest rules and round-toward-zero
+// and stochastic rounding keep the per-block scale; the whole-tensor rule
+// takes one scale from the tensor amax (the deploy-side quantisers of the
+// out-of-family sweep, Appendix B threat model (a) and the deployment-quantizer
+// sweep).
+enum : int { kRuleEven = 0, kRuleAway = 1, kRuleRtz = 2, kRuleStochastic = 3, kRuleWholeTensor = 4 };
+
 // One chunk of 8 consecutive weights of a row (16 bytes of bf16, already
 // loaded); the B/8 lanes of a block are adjacent and share the block amax.
-template <int FMT, bool AWAY>
+// amax_t: the tensor amax (whole-tensor rule); seed: the Philox key
+// (stochastic rule; element e = 8c + k draws word e % 4 of block e / 4).
+template <int FMT, int RULE>
 __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, const float* ws2_ptr, float ws2_val,
+                                          const float* amax_t, uint64_t seed,
                                           uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
   constexpr int B = ScaleOperand<FMT>::kBlock;
   constexpr int LPB = B / 8;
@@ -134,13 +188,17 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
   // amax as a bit pattern: for |x| the integer order of the bits is the
   // numeric order, with NaN above +inf, so NaN propagates like a max.
   uint32_t am = 0;
+  if (RULE == kRuleWholeTensor) {
+    am = __float_as_uint(*amax_t) >> 16;                    // bf16 bits, written by rtn_amax
+  } else {
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    am = max(am, h[k] & 0x7FFFu);
-    am = max(am, (h[k] >> 16) & 0x7FFFu);
+    for (int k = 0; k < 4; ++k) {
+      am = max(am, h[k] & 0x7FFFu);
+      am = max(am, (h[k] >> 16) & 0x7FFFu);
+    }
+    am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+    if (LPB == 4) am = max(am, (uint32_t)__shfl_xor((int)am, 2));
   }
-  am = max(am, (uint32_t)__shfl_xor((int)am, 1));
-  if (LPB == 4) am = max(am, (uint32_t)__shfl_xor((int)am, 2));
   const float amax = __uint_as_float(am << 16);
   const float sixth = __fdiv_rn(amax, 6.0f);
 
@@ -162,7 +220,11 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
     const float inv = (k == 127) ? __uint_as_float(0x00400000u) : __uint_as_float((uint32_t)(127 - k) << 23);
     eff = (sbyte == 0xFFu) ? __uint_as_float(0x7FC00000u) : inv;   // used as a multiplier below
   } else {
-    const float ws2 = ws2_ptr ? *ws2_ptr : ws2_val;
+    float ws2 = ws2_ptr ? *ws2_ptr : ws2_val;
+    if (RULE == kRuleWholeTensor && !(ws2_val > 0.0f)) {    // recomputed from the same amax
+      ws2 = __fdiv_rn(sixth, 448.0f);
+      if (ws2 == 0.0f) ws2 = 1.0f;
+    }
     sbyte = e4m3_encode_rne_sat(__fdiv_rn(sixth, ws2));
     eff = __fmul_rn(e4m3_to_f32(sbyte), ws2);
   }
@@ -183,11 +245,37 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
 #pragma unroll
   for (int p = 0; p < 4; ++p)
     packed |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, q[2 * p], q[2 * p + 1], 1.0f, 0) & 0xFFu) << (8 * p);
-  if (AWAY) {
+  if (RULE == kRuleAway) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {                           // a tie magnitude is below 6: no carry
       const float a = fabsf(q[k]);
       packed += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * k)) : 0u;
+    }
+  }
+  if (RULE == kRuleRtz || RULE == kRuleStochastic) {
+    // The nearest magnitude is the truncated one or the one above it: step
+    // down where it lies above min(|q|, 6).  Stochastic rounding then goes up
+    // from the truncated magnitude lo iff u * gap < a - m(lo), which is
+    // u < (a - m(lo)) / gap with both sides exact in fp32 (u has 24 bits and
+    // gap is 0 or a power of two; a - m(lo) is a multiple of ulp(a)).
+    uint64_t rw[8];
+    if (RULE == kRuleStochastic) {
+      philox4x64_10((uint64_t)(2 * c), seed, rw);
+      philox4x64_10((uint64_t)(2 * c + 1), seed, rw + 4);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float a = fminf(fabsf(q[k]), 6.0f);
+      uint32_t m = (packed >> (4 * k)) & 7u;
+      const uint32_t dn = (e2m1_mag(m) > a) ? 1u : 0u;
+      m -= dn;
+      uint32_t up = 0;
+      if (RULE == kRuleStochastic) {
+        const float u = (float)(uint32_t)(rw[k] >> 40) * 5.9604644775390625e-08f;   // 2^-24
+        const uint32_t hi = m < 7u ? m + 1u : 7u;
+        up = (__fmul_rn(u, e2m1_mag(hi) - e2m1_mag(m)) < a - e2m1_mag(m)) ? 1u : 0u;
+      }
+      packed = packed - (dn << (4 * k)) + (up << (4 * k));   // stays within the magnitude bits
     }
   }
   // The convert carries the sign of q, which is the sign of w unless q is NaN
@@ -209,16 +297,17 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
 
 // Each workgroup takes 512 chunks: a lane loads its two chunks (c and c + 256)
 // before working on either, so two 16-byte loads are in flight per lane.
-template <int FMT, bool AWAY>
+template <int FMT, int RULE>
 __global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W, int64_t n_chunks,
-                                                  const float* ws2_ptr, float ws2_val,
-                                                  uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
+                                                  const float* ws2_ptr, float ws2_val, const float* amax_t,
+                                                  uint64_t seed, uint8_t* __restrict__ codes,
+                                                  uint8_t* __restrict__ scales) {
   const int64_t c0 = (int64_t)blockIdx.x * 512 + threadIdx.x, c1 = c0 + 256;
   const bool ok0 = c0 < n_chunks, ok1 = c1 < n_chunks;
   const uint4 v0 = ok0 ? *reinterpret_cast<const uint4*>(W + 8 * c0) : make_uint4(0, 0, 0, 0);
   const uint4 v1 = ok1 ? *reinterpret_cast<const uint4*>(W + 8 * c1) : make_uint4(0, 0, 0, 0);
-  rtn_chunk<FMT, AWAY>(v0, c0, ok0, ws2_ptr, ws2_val, codes, scales);
-  rtn_chunk<FMT, AWAY>(v1, c1, ok1, ws2_ptr, ws2_val, codes, scales);
+  rtn_chunk<FMT, RULE>(v0, c0, ok0, ws2_ptr, ws2_val, amax_t, seed, codes, scales);
+  rtn_chunk<FMT, RULE>(v1, c1, ok1, ws2_ptr, ws2_val, amax_t, seed, codes, scales);
 }
 
 __global__ void rtn_amax_init(float* slot) { *reinterpret_cast<uint32_t*>(slot) = 0u; }
@@ -265,32 +354,69 @@ __global__ void rtn_ws2_finalize(float* slot) {
   *slot = ws2;
 }
 
+namespace {
+template <int FMT, int RULE>
+void rtn_grid(int64_t n_chunks, const uint16_t* w, const float* ws2_ptr, float ws2_val, const float* amax_t,
+              uint64_t seed, uint8_t* codes, uint8_t* scales, hipStream_t s) {
+  if (n_chunks <= 0) return;
+  const unsigned grid = (unsigned)((n_chunks + 511) / 512);
+  hipLaunchKernelGGL((rtn_kernel<FMT, RULE>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, ws2_val, amax_t,
+                     seed, codes, scales);
+}
+
+template <int RULE>
+void rtn_fmt(int fmt, int64_t n_chunks, const uint16_t* w, const float* ws2_ptr, float ws2_val, const float* amax_t,
+             uint64_t seed, uint8_t* codes, uint8_t* scales, hipStream_t s) {
+  if (fmt == kMX) rtn_grid<kMX, RULE>(n_chunks, w, ws2_ptr, 1.0f, amax_t, seed, codes, scales, s);
+  else rtn_grid<kNV, RULE>(n_chunks, w, ws2_ptr, ws2_val, amax_t, seed, codes, scales, s);
+}
+
+// The tensor amax (as the bits of an fp32 holding a bf16 value) into *slot.
+void tensor_amax(const uint16_t* w, int64_t n_chunks, float* slot, hipStream_t s) {
+  hipLaunchKernelGGL(rtn_amax_init, dim3(1), dim3(1), 0, s, slot);
+  const int64_t want = (n_chunks + 1023) / 1024;
+  const unsigned grid = (unsigned)(want < 1024 ? (want > 0 ? want : 1) : 1024);
+  hipLaunchKernelGGL(rtn_amax, dim3(grid), dim3(256), 0, s, w, n_chunks, slot);
+}
+}  // namespace
+
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s) {
+  return rtn_rule_launch(fmt, O, I, W, ws2_in, tie == 1 ? kRuleAway : kRuleEven, 0, codes, scales, ws2_out, s);
+}
+
+int rtn_rule_launch(int fmt, int O, int I, const void* W, float ws2_in, int rule, uint64_t seed,
+                    uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s) {
   const int64_t n_chunks = (int64_t)O * I / 8;
   const uint16_t* w = static_cast<const uint16_t*>(W);
+  if (rule == kRuleWholeTensor) {
+    // ws2_out holds the tensor amax while the codes are written, then the
+    // ws2 used (1 for MXFP4); the launches are stream-ordered.
+    tensor_amax(w, n_chunks, ws2_out, s);
+    rtn_fmt<kRuleWholeTensor>(fmt, n_chunks, w, nullptr, fmt == kNV && ws2_in > 0.0f ? ws2_in : 0.0f, ws2_out,
+                              seed, codes, scales, s);
+    if (fmt == kNV && !(ws2_in > 0.0f)) hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, ws2_out);
+    else hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, ws2_out, fmt == kNV ? ws2_in : 1.0f);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+  }
   const float* ws2_ptr = nullptr;
   if (fmt == kNV) {
     if (ws2_in > 0.0f) {
       if (ws2_out) hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, ws2_out, ws2_in);
     } else {
-      hipLaunchKernelGGL(rtn_amax_init, dim3(1), dim3(1), 0, s, ws2_out);
-      const int64_t want = (n_chunks + 1023) / 1024;
-      const unsigned grid = (unsigned)(want < 1024 ? (want > 0 ? want : 1) : 1024);
-      hipLaunchKernelGGL(rtn_amax, dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_out);
+      tensor_amax(w, n_chunks, ws2_out, s);
       hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, ws2_out);
       ws2_ptr = ws2_out;
     }
   }
-  if (n_chunks > 0) {
-    const unsigned grid = (unsigned)((n_chunks + 511) / 512);
-    if (fmt == kMX) {
-      if (tie == 1) hipLaunchKernelGGL((rtn_kernel<kMX, true>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, 1.0f, codes, scales);
-      else hipLaunchKernelGGL((rtn_kernel<kMX, false>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, 1.0f, codes, scales);
-    } else {
-      if (tie == 1) hipLaunchKernelGGL((rtn_kernel<kNV, true>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, ws2_in, codes, scales);
-      else hipLaunchKernelGGL((rtn_kernel<kNV, false>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, ws2_in, codes, scales);
-    }
+  switch (rule) {
+    case kRuleEven: rtn_fmt<kRuleEven>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s); break;
+    case kRuleAway: rtn_fmt<kRuleAway>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s); break;
+    case kRuleRtz: rtn_fmt<kRuleRtz>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s); break;
+    case kRuleStochastic:
+      rtn_fmt<kRuleStochastic>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s);
+      break;
+    default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -49,6 +49,10 @@ int merge_launch(const MergeBatch& b, hipStream_t s);
 
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
+// rule: 0 nearest-even, 1 nearest-away, 2 toward zero, 3 stochastic (Philox
+// key `seed`), 4 whole-tensor scale (ws2_out required: the amax slot).
+int rtn_rule_launch(int fmt, int O, int I, const void* W, float ws2_in, int rule, uint64_t seed,
+                    uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
 
 // QAST low-rank scale step: on-grid scale bytes (+ clamp mask) and the factor
 // gradients; qast_grads_workspace bytes of partial dA planes.

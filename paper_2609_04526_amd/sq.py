@@ -21,6 +21,9 @@ OUT_F32, OUT_BF16 = 0, 1
 TIE_EVEN, TIE_AWAY = 0, 1
 MERGE_DELTA, MERGE_COPY = 0, 1
 FORMATS = {"mx": MXFP4, "nv": NVFP4}
+RULE_NEAREST_EVEN, RULE_NEAREST_AWAY, RULE_RTZ, RULE_STOCHASTIC, RULE_WHOLE_TENSOR = 0, 1, 2, 3, 4
+RULES = {"even": RULE_NEAREST_EVEN, "away": RULE_NEAREST_AWAY, "rtz": RULE_RTZ,
+         "stochastic": RULE_STOCHASTIC, "whole_tensor": RULE_WHOLE_TENSOR}
 BLOCK = {MXFP4: 32, NVFP4: 16}
 
 _c_i64 = ctypes.c_int64
@@ -71,6 +74,8 @@ def load():
         "sq_merge_scales_grouped": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(MergeDesc), _c_p]),
         "rtn_quantize": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
                                         _c_p, _c_p, _c_p, _c_p]),
+        "rtn_quantize_rule": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
+                                             ctypes.c_uint64, _c_p, _c_p, _c_p, _c_p]),
         "sq_qast_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p,
                                           ctypes.c_float, ctypes.c_float, _c_p, _c_p, _c_p]),
         "sq_qast_factor_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, ctypes.c_int]),
@@ -211,6 +216,26 @@ def rtn_quantize(fmt, W, tie=TIE_EVEN, ws2_in=0.0, codes=None, scales=None, ws2_
     _dev(W, codes, scales, ws2_out)
     _check("rtn_quantize", load().rtn_quantize(fmt, O, I, _ptr(W), float(ws2_in), int(tie), _ptr(codes),
                                                _ptr(scales), _ptr(ws2_out), _stream()))
+    return codes, scales, ws2_out
+
+
+def rtn_quantize_rule(fmt, W, rule, ws2_in=0.0, seed=0, codes=None, scales=None, ws2_out=None):
+    """Re-quantisation of bf16 W [O, I] under a deploy rule (RULE_*) -> (codes, scales, ws2_out).
+    ws2_out is allocated where the call needs it (NVFP4, or the whole-tensor rule)."""
+    fmt = _fmt(fmt)
+    rule = RULES.get(rule, rule)
+    O, I = W.shape
+    dev = W.device
+    if codes is None:
+        codes = torch.empty((O, I // 2), dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty((O, I // BLOCK[fmt]), dtype=torch.uint8, device=dev)
+    if (fmt == NVFP4 or rule == RULE_WHOLE_TENSOR) and ws2_out is None:
+        ws2_out = torch.empty(1, dtype=torch.float32, device=dev)
+    _dev(W, codes, scales, ws2_out)
+    _check("rtn_quantize_rule", load().rtn_quantize_rule(fmt, O, I, _ptr(W), float(ws2_in), int(rule),
+                                                         int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(codes),
+                                                         _ptr(scales), _ptr(ws2_out), _stream()))
     return codes, scales, ws2_out
 
 

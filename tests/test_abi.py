@@ -136,6 +136,19 @@ def test_rtn_validation(lib):
     assert lib.rtn_quantize(0, 256, 512, None, 0.0, 0, FAKE, FAKE, None, None) == -1
 
 
+def test_rtn_rule_validation(lib):
+    assert lib.rtn_quantize_rule(0, 256, 500, FAKE, 0.0, 2, 0, FAKE, FAKE, None, None) == -2
+    assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 5, 0, FAKE, FAKE, None, None) == -1
+    assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, -1, 0, FAKE, FAKE, None, None) == -1
+    # the whole-tensor rule needs the amax slot in both formats
+    assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 4, 0, FAKE, FAKE, None, None) == -1
+    assert lib.rtn_quantize_rule(1, 256, 512, FAKE, 0.5, 4, 0, FAKE, FAKE, None, None) == -1
+    assert lib.rtn_quantize_rule(1, 256, 512, FAKE, 0.0, 3, 7, FAKE, FAKE, None, None) == -1
+    assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 4, 0, FAKE, FAKE, MISALIGNED + 2, None) == -3
+    assert lib.rtn_quantize_rule(0, 256, 512, MISALIGNED, 0.0, 2, 0, FAKE, FAKE, None, None) == -3
+    assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 2, 0, FAKE, None, None, None) == -1
+
+
 def test_qast_validation(lib):
     nan = float("nan")
     q = lib.sq_qast_scales

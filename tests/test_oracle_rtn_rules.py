@@ -26,6 +26,11 @@ def test_philox_matches_numpy(key):
     assert np.array_equal(got, ref)
 
 
+def test_uniforms_window_is_a_slice():
+    full = philox.uniforms24(1000, 21)
+    assert np.array_equal(philox.uniforms24(301, 21, start=599), full[599:900])
+
+
 def test_uniforms_are_24_bit_and_uniform():
     u = philox.uniforms24(1 << 16, 11)
     assert u.dtype == np.float32 and np.all(u >= 0) and np.all(u < 1)
@@ -92,3 +97,11 @@ def test_whole_tensor_rule_direct():
     cn, sn, wn = rtn.quantize_rule("nv", W, rtn.RULE_WHOLE_TENSOR)
     assert np.all(sn == sn[0, 0])
     assert sn[0, 0] == codec.e4m3_encode(np.float32(np.float32(amax) / np.float32(6.0)) / wn)
+
+
+def test_row_offset_matches_the_whole_tensor():
+    W = (np.random.default_rng(6).standard_normal((12, 64)) * 0.1).astype(np.float32)
+    W = np.asarray(W.view(np.uint32) & 0xFFFF0000, np.uint32).view(np.float32)
+    c, s, _ = rtn.quantize_rule("mx", W, rtn.RULE_STOCHASTIC, seed=8)
+    c7, s7, _ = rtn.quantize_rule("mx", W[7:9], rtn.RULE_STOCHASTIC, seed=8, row0=7)
+    assert np.array_equal(c7, c[7:9]) and np.array_equal(s7, s[7:9])
