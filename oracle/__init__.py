@@ -37,6 +37,13 @@ qast    one QAST low-rank scale step: Delta_S = (alpha/r) B A, the on-grid
         scale bytes through the merge's grid-and-clamp path, the clamp mask,
         and the factor gradients dB, dA (§3 "Scale-QLoRA forward", "QAST
         makes merge exact by construction", stability recipe (ii)-(iii)).
+qat     the QAT-LoRA weight-space STE comparator: W = base + (alpha/r) B A
+        fake-quantised by the nearest rule, and the factor gradients through
+        the straight-through estimator (§2 related work, "Merge-aware
+        weight-space"; App. "Training cost per step").
+philox  Philox4x64-10, the counter-based generator behind the stochastic
+        deploy rule (rtn.quantize_rule; App. B threat model (a), the
+        deployment-quantizer sweep).
 """
 
-from . import audit, codec, linear, merge, qast, rtn  # noqa: F401
+from . import audit, codec, linear, merge, philox, qast, qat, rtn  # noqa: F401
