@@ -278,6 +278,44 @@ int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS, const uin
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * QAT-LoRA weight-space STE comparator (Section 2 related work, "Merge-aware
+ * weight-space": W <- W + (quantize(W) - W).detach() on W = W_base + (alpha/r)
+ * B A; Appendix "Training cost per step").  The fake-quantised forward weight
+ * is a (codes, scales) pair on the native grid, so sq_fwd and sq_bwd_dx run on
+ * the output of sq_qat_requant directly.
+ *
+ * sq_qat_requant: one fused pass writing the nearest-rule re-quantisation of
+ *   W_eff[o,i] = bf16(fp32(base[o,i] + fp32(alpha_over_r * S[o,i])))
+ *   base[o,i]  = fp32(code[o,i] * eff[o, i/B]), eff as sq_fwd (NVFP4: fp32
+ *                e4m3(byte) * ws2);
+ *   S[o,i]     = sum over k = 0..r-1 in increasing order of B[o,k] A[k,i],
+ *                fp32, each product exact;
+ * with bf16 rounding to nearest even (NaN -> +NaN).  The codes and scales are
+ * exactly what rtn_quantize(fmt, W_eff, SQ_TIE_EVEN, ws2) writes (NVFP4 keeps
+ * the given ws2).  codes, scales: the base [O, I/2], [O, G]; B bf16 [O, r];
+ * A bf16 [r, I] (16-byte aligned); 1 <= r <= 64; O <= 1048560; alpha_over_r
+ * finite; codes_out, scales_out must not overlap the inputs.
+ *
+ * sq_lora_grads: the factor gradients through the straight-through estimator,
+ *   dB = alpha_over_r dY^T X A^T   fp32 [O, r]
+ *   dA = alpha_over_r B^T dY^T X   fp32 [r, I]
+ * computed through the rank (P = X A^T and Q = dY B first), without forming
+ * dY^T X; fp32 accumulation in a fixed order (deterministic).  X bf16 [T, I],
+ * dY bf16 [T, O] (16-byte aligned), B bf16 [O, r], A bf16 [r, I] (16-byte
+ * aligned); 0 <= T <= 8388480 (T = 0 writes zeros); O, I multiples of 8;
+ * 1 <= r <= 64.  workspace: device scratch of at least
+ * sq_lora_grads_workspace(T, O, I, r) bytes, 16-byte aligned, contents
+ * irrelevant (0 bytes when T = 0; 0 is also returned for invalid sizes).
+ */
+int sq_qat_requant(int fmt, int64_t O, int64_t I, int r, const uint8_t* codes, const uint8_t* scales, float ws2,
+                   const void* B, const void* A, float alpha_over_r, uint8_t* codes_out, uint8_t* scales_out,
+                   void* stream);
+size_t sq_lora_grads_workspace(int64_t T, int64_t O, int64_t I, int r);
+int sq_lora_grads(int64_t T, int64_t O, int64_t I, int r, const void* X, const void* dY, const void* B,
+                  const void* A, float alpha_over_r, float* dB, float* dA, void* workspace, size_t workspace_bytes,
+                  void* stream);
+
+/*
  * Merge rollback (Appendix B, "Payoff 3: invertible merges and rollback"): a
  * merged scale plane plus the on-grid delta the merge applied restores the
  * base plane byte for byte, with no retained base.  The delta lives in the

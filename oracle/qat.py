@@ -71,3 +71,14 @@ def lora_grads(X, dY, B, A, alpha_over_r: float):
     dW = dY64.T @ X64
     c = float(np.float32(alpha_over_r))
     return c * (dW @ A64.T), c * (B64.T @ dW)
+
+
+def lora_grads_sampled(X, dY, B, A, alpha_over_r: float, rows, cols):
+    """dB[rows, :] and dA[:, cols] in fp64, each from its own rows / columns of
+    dW = dY^T X: dB[o, :] = c dW[o, :] A^T, dA[:, i] = c B^T dW[:, i]."""
+    X64, dY64 = _f32(X).astype(np.float64), _f32(dY).astype(np.float64)
+    B64, A64 = _f32(B).astype(np.float64), _f32(A).astype(np.float64)
+    c = float(np.float32(alpha_over_r))
+    dW_rows = dY64[:, rows].T @ X64                       # [len(rows), I]
+    dW_cols = dY64.T @ X64[:, cols]                       # [O, len(cols)]
+    return c * (dW_rows @ A64.T), c * (B64.T @ dW_cols)

@@ -239,6 +239,57 @@ SQ_EXPORT int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS,
                                           static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+constexpr int kLoraRankMax = 64;
+constexpr int64_t kRequantRowsMax = int64_t(65535) * 16;     // grid.y of the fused re-quantiser
+constexpr int64_t kLoraTokensMax = int64_t(65535) * 128;     // grid.y of the token-chunk kernel
+
+int check_lora_dims(int64_t T, int64_t O, int64_t I, int r) {
+  if (T < 0 || T > kLoraTokensMax || O < 1 || I < 1 || O > kDimMax || I > kDimMax) return SQ_ERR_SHAPE;
+  if (O % 8 != 0 || I % 8 != 0) return SQ_ERR_SHAPE;
+  if (T * I * 2 > kOperandBytesMax || T * O * 2 > kOperandBytesMax) return SQ_ERR_SHAPE;
+  if (r < 1 || r > kLoraRankMax) return SQ_ERR_SHAPE;
+  return SQ_OK;
+}
+}  // namespace
+
+SQ_EXPORT int sq_qat_requant(int fmt, int64_t O, int64_t I, int r, const uint8_t* codes, const uint8_t* scales,
+                             float ws2, const void* B, const void* A, float alpha_over_r, uint8_t* codes_out,
+                             uint8_t* scales_out, void* stream) {
+  int st = check_layer(fmt, 0, O, I);
+  if (st != SQ_OK) return st;
+  if (r < 1 || r > kLoraRankMax || O > kRequantRowsMax) return SQ_ERR_SHAPE;
+  if (!codes || !scales || !B || !A || !codes_out || !scales_out) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (fmt == SQ_NVFP4 && !ws2_ok(ws2)) return SQ_ERR_ARG;
+  if (!aligned(codes, 4) || !aligned(codes_out, 4) || !aligned(A, 16) || !aligned(B, 2)) return SQ_ERR_ALIGN;
+  return hip_status(sq::qat_requant_launch(fmt, (int)O, (int)I, r, codes, scales, fmt == SQ_NVFP4 ? ws2 : 1.0f, B,
+                                           A, alpha_over_r, codes_out, scales_out,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT size_t sq_lora_grads_workspace(int64_t T, int64_t O, int64_t I, int r) {
+  if (check_lora_dims(T, O, I, r) != SQ_OK) return 0;
+  return sq::lora_grads_workspace((int)T, (int)O, (int)I, r);
+}
+
+SQ_EXPORT int sq_lora_grads(int64_t T, int64_t O, int64_t I, int r, const void* X, const void* dY, const void* B,
+                            const void* A, float alpha_over_r, float* dB, float* dA, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  int st = check_lora_dims(T, O, I, r);
+  if (st != SQ_OK) return st;
+  if (!B || !A || !dB || !dA || (T > 0 && (!X || !dY))) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (!aligned(X, 16) || !aligned(dY, 16) || !aligned(A, 16) || !aligned(B, 2) || !aligned(dB, 4) ||
+      !aligned(dA, 4))
+    return SQ_ERR_ALIGN;
+  const size_t need = sq::lora_grads_workspace((int)T, (int)O, (int)I, r);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return SQ_ERR_WORKSPACE;
+  if (need > 0 && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  return hip_status(sq::lora_grads_launch((int)T, (int)O, (int)I, r, X, dY, B, A, alpha_over_r, dB, dA, workspace,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 SQ_EXPORT int sq_scale_applied_delta(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied,
                                      void* stream) {
   if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;

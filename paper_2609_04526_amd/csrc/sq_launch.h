@@ -54,6 +54,15 @@ int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
 int rtn_rule_launch(int fmt, int O, int I, const void* W, float ws2_in, int rule, uint64_t seed,
                     uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
 
+// QAT-LoRA weight-space STE: fused W_eff + nearest re-quantisation, and the
+// factor gradients through the rank (lora_grads_workspace bytes of scratch).
+int qat_requant_launch(int fmt, int O, int I, int r, const uint8_t* codes, const uint8_t* scales, float ws2,
+                       const void* B, const void* A, float c, uint8_t* codes_out, uint8_t* scales_out,
+                       hipStream_t s);
+size_t lora_grads_workspace(int T, int O, int I, int r);
+int lora_grads_launch(int T, int O, int I, int r, const void* X, const void* dY, const void* B, const void* A,
+                      float c, float* dB, float* dA, void* workspace, hipStream_t s);
+
 // QAST low-rank scale step: on-grid scale bytes (+ clamp mask) and the factor
 // gradients; qast_grads_workspace bytes of partial dA planes.
 int qast_scales_launch(int fmt, int O, int G, int r, const uint8_t* base, const void* B, const void* A,

@@ -1,0 +1,197 @@
+// Round-to-nearest (and deploy-rule) re-quantisation of one chunk of 8 bf16
+// weights into E2M1 codes and the block scale: the device side shared by the
+// RTN kernels and the fused QAT-LoRA re-quantiser.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sq_device.h"
+#include "sq_grid.h"
+
+namespace sq {
+
+// ceil(log2 x) for positive finite fp32 x (subnormals included).
+__device__ __forceinline__ int ceil_log2_pos(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const uint32_t e = u >> 23, frac = u & 0x7FFFFFu;
+  if (e == 0u) {
+    const int p = 31 - __clz(frac);
+    return p - 149 + ((frac & (frac - 1u)) != 0u);
+  }
+  return (int)e - 127 + (frac != 0u);
+}
+
+// The 128-bit product a * m as (hi, lo) from four 32 x 32 -> 64-bit
+// multiply-adds; no partial sum overflows 64 bits.
+__device__ __forceinline__ void mulhilo64(uint64_t a, uint64_t m, uint64_t& hi, uint64_t& lo) {
+  const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32), m0 = (uint32_t)m, m1 = (uint32_t)(m >> 32);
+  const uint64_t p00 = (uint64_t)a0 * m0;
+  const uint64_t t = (uint64_t)a1 * m0 + (p00 >> 32);
+  const uint64_t u = (uint64_t)a0 * m1 + (uint32_t)t;
+  hi = (uint64_t)a1 * m1 + (t >> 32) + (u >> 32);
+  lo = (u << 32) | (uint32_t)p00;
+}
+
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011) with counter
+// (c, 0, 0, 0) and key (key, 0): ten rounds of two 64 x 64 -> 128-bit
+// products recombined with the other counter words and the key, the key
+// bumped by two Weyl constants between rounds.  Written from the published
+// definition; it feeds the stochastic deploy rule.
+__device__ __forceinline__ void philox4x64_10(uint64_t c, uint64_t key, uint64_t out[4]) {
+  uint64_t x0 = c, x1 = 0, x2 = 0, x3 = 0, k0 = key, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B97F4A7C15ull;
+      k1 += 0xBB67AE8584CAA73Bull;
+    }
+    uint64_t hi0, lo0, hi1, lo1;
+    mulhilo64(x0, 0xD2E7470EE14C6C93ull, hi0, lo0);
+    mulhilo64(x2, 0xCA5A826395121157ull, hi1, lo1);
+    x0 = hi1 ^ x1 ^ k0;
+    x1 = lo1;
+    x2 = hi0 ^ x3 ^ k1;
+    x3 = lo0;
+  }
+  out[0] = x0;
+  out[1] = x1;
+  out[2] = x2;
+  out[3] = x3;
+}
+
+// E2M1 magnitude of index m (0..7): twice the values 0, .5, 1, 1.5, 2, 3, 4, 6
+// sit in the nibbles of 0xC8643210.
+__device__ __forceinline__ float e2m1_mag(uint32_t m) {
+  return (float)((0xC8643210u >> (4u * m)) & 0xFu) * 0.5f;
+}
+
+// Rounding rules of the re-quantiser.  The nearest rules and round-toward-zero
+// and stochastic rounding keep the per-block scale; the whole-tensor rule
+// takes one scale from the tensor amax (the deploy-side quantisers of the
+// out-of-family sweep, Appendix B threat model (a) and the deployment-quantizer
+// sweep).
+enum : int { kRuleEven = 0, kRuleAway = 1, kRuleRtz = 2, kRuleStochastic = 3, kRuleWholeTensor = 4 };
+
+// One chunk of 8 consecutive weights of a row (16 bytes of bf16, already
+// loaded); the B/8 lanes of a block are adjacent and share the block amax.
+// amax_t: the tensor amax (whole-tensor rule); seed: the Philox key
+// (stochastic rule; element e = 8c + k draws word e % 4 of block e / 4).
+template <int FMT, int RULE>
+__device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, const float* ws2_ptr, float ws2_val,
+                                          const float* amax_t, uint64_t seed,
+                                          uint8_t* __restrict__ codes, uint8_t* __restrict__ scales) {
+  constexpr int B = ScaleOperand<FMT>::kBlock;
+  constexpr int LPB = B / 8;
+  const uint32_t h[4] = {v.x, v.y, v.z, v.w};
+  // amax as a bit pattern: for |x| the integer order of the bits is the
+  // numeric order, with NaN above +inf, so NaN propagates like a max.
+  uint32_t am = 0;
+  if (RULE == kRuleWholeTensor) {
+    am = __float_as_uint(*amax_t) >> 16;                    // bf16 bits, written by rtn_amax
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      am = max(am, h[k] & 0x7FFFu);
+      am = max(am, (h[k] >> 16) & 0x7FFFu);
+    }
+    am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+    if (LPB == 4) am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+  }
+  const float amax = __uint_as_float(am << 16);
+  const float sixth = __fdiv_rn(amax, 6.0f);
+
+  uint32_t sbyte;
+  float eff;            // effective block scale (what q divides by)
+  if (FMT == kMX) {
+    int k;
+    if (sixth != sixth) {
+      sbyte = 0xFFu;
+      k = 0;
+    } else {
+      if (sixth == 0.0f) k = -127;
+      else if (sixth > 3.4028234e38f) k = 127;
+      else k = ceil_log2_pos(sixth);
+      k = k < -127 ? -127 : (k > 127 ? 127 : k);
+      sbyte = (uint32_t)(k + 127);
+    }
+    // 2^-k as fp32 (2^-127 is subnormal, 2^127 normal): exact
+    const float inv = (k == 127) ? __uint_as_float(0x00400000u) : __uint_as_float((uint32_t)(127 - k) << 23);
+    eff = (sbyte == 0xFFu) ? __uint_as_float(0x7FC00000u) : inv;   // used as a multiplier below
+  } else {
+    float ws2 = ws2_ptr ? *ws2_ptr : ws2_val;
+    if (RULE == kRuleWholeTensor && !(ws2_val > 0.0f)) {    // recomputed from the same amax
+      ws2 = __fdiv_rn(sixth, 448.0f);
+      if (ws2 == 0.0f) ws2 = 1.0f;
+    }
+    sbyte = e4m3_encode_rne_sat(__fdiv_rn(sixth, ws2));
+    eff = __fmul_rn(e4m3_to_f32(sbyte), ws2);
+  }
+
+  // Codes: gfx950's fp32 -> E2M1 convert rounds |q| to the nearest E2M1
+  // magnitude with ties to even and saturates at 6 (it equals the threshold
+  // rounding on every non-NaN fp32 input); ties away differ from it exactly at
+  // |q| = 0.25, 1.25, 2.5 and 5, where they take the next magnitude.  A NaN q
+  // codes as magnitude 0, and the sign bit is always the sign of w.
+  float q[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const float w = __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16);
+    if (FMT == kMX) q[k] = __fmul_rn(w, eff);               // w / 2^k, one rounding
+    else q[k] = (eff == 0.0f) ? 0.0f : __fdiv_rn(w, eff);
+  }
+  uint32_t packed = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+    packed |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, q[2 * p], q[2 * p + 1], 1.0f, 0) & 0xFFu) << (8 * p);
+  if (RULE == kRuleAway) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {                           // a tie magnitude is below 6: no carry
+      const float a = fabsf(q[k]);
+      packed += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * k)) : 0u;
+    }
+  }
+  if (RULE == kRuleRtz || RULE == kRuleStochastic) {
+    // The nearest magnitude is the truncated one or the one above it: step
+    // down where it lies above min(|q|, 6).  Stochastic rounding then goes up
+    // from the truncated magnitude lo iff u * gap < a - m(lo), which is
+    // u < (a - m(lo)) / gap with both sides exact in fp32 (u has 24 bits and
+    // gap is 0 or a power of two; a - m(lo) is a multiple of ulp(a)).
+    uint64_t rw[8];
+    if (RULE == kRuleStochastic) {
+      philox4x64_10((uint64_t)(2 * c), seed, rw);
+      philox4x64_10((uint64_t)(2 * c + 1), seed, rw + 4);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float a = fminf(fabsf(q[k]), 6.0f);
+      uint32_t m = (packed >> (4 * k)) & 7u;
+      const uint32_t dn = (e2m1_mag(m) > a) ? 1u : 0u;
+      m -= dn;
+      uint32_t up = 0;
+      if (RULE == kRuleStochastic) {
+        const float u = (float)(uint32_t)(rw[k] >> 40) * 5.9604644775390625e-08f;   // 2^-24
+        const uint32_t hi = m < 7u ? m + 1u : 7u;
+        up = (__fmul_rn(u, e2m1_mag(hi) - e2m1_mag(m)) < a - e2m1_mag(m)) ? 1u : 0u;
+      }
+      packed = packed - (dn << (4 * k)) + (up << (4 * k));   // stays within the magnitude bits
+    }
+  }
+  // The convert carries the sign of q, which is the sign of w unless q is NaN
+  // (possible only when the block amax is NaN) or forced to +0 by a zero
+  // NVFP4 scale; only those blocks need the general fix-up.
+  if (am > 0x7F80u || (FMT == kNV && eff == 0.0f)) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const uint32_t hb = (h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+      const uint32_t mag = (q[k] != q[k]) ? 0u : ((packed >> (4 * k)) & 7u);
+      packed = (packed & ~(15u << (4 * k))) | ((mag | ((hb >> 12) & 8u)) << (4 * k));
+    }
+  }
+  if (valid) {
+    reinterpret_cast<uint32_t*>(codes)[c] = packed;
+    if ((c % LPB) == 0) scales[c / LPB] = (uint8_t)sbyte;
+  }
+}
+
+}  // namespace sq

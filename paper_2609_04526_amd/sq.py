@@ -76,6 +76,11 @@ def load():
                                         _c_p, _c_p, _c_p, _c_p]),
         "rtn_quantize_rule": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
                                              ctypes.c_uint64, _c_p, _c_p, _c_p, _c_p]),
+        "sq_qat_requant": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, ctypes.c_float,
+                                          _c_p, _c_p, ctypes.c_float, _c_p, _c_p, _c_p]),
+        "sq_lora_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, _c_i64, ctypes.c_int]),
+        "sq_lora_grads": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p, _c_p,
+                                         ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
         "sq_qast_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p,
                                           ctypes.c_float, ctypes.c_float, _c_p, _c_p, _c_p]),
         "sq_qast_factor_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, ctypes.c_int]),
@@ -237,6 +242,47 @@ def rtn_quantize_rule(fmt, W, rule, ws2_in=0.0, seed=0, codes=None, scales=None,
                                                          int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(codes),
                                                          _ptr(scales), _ptr(ws2_out), _stream()))
     return codes, scales, ws2_out
+
+
+def sq_qat_requant(fmt, codes, scales, B, A, alpha_over_r, ws2=1.0, codes_out=None, scales_out=None):
+    """Fake-quantised QAT-LoRA weight quantize(base + alpha_over_r B A) as (codes_out, scales_out).
+    codes uint8 [O, I/2], scales uint8 [O, G], B bf16 [O, r], A bf16 [r, I]."""
+    fmt = _fmt(fmt)
+    O, I = codes.shape[0], codes.shape[1] * 2
+    r = B.shape[1]
+    if codes_out is None:
+        codes_out = torch.empty_like(codes)
+    if scales_out is None:
+        scales_out = torch.empty_like(scales)
+    _dev(codes, scales, B, A, codes_out, scales_out)
+    _check("sq_qat_requant", load().sq_qat_requant(fmt, O, I, r, _ptr(codes), _ptr(scales), float(ws2), _ptr(B),
+                                                   _ptr(A), float(alpha_over_r), _ptr(codes_out),
+                                                   _ptr(scales_out), _stream()))
+    return codes_out, scales_out
+
+
+def sq_lora_grads_workspace(T, O, I, r):
+    return int(load().sq_lora_grads_workspace(T, O, I, r))
+
+
+def sq_lora_grads(X, dY, B, A, alpha_over_r, dB=None, dA=None, workspace=None):
+    """STE factor gradients dB [O, r], dA [r, I] (fp32) of W = base + alpha_over_r B A."""
+    T, I = X.shape
+    O, r = B.shape
+    dev = B.device
+    if dB is None:
+        dB = torch.empty((O, r), dtype=torch.float32, device=dev)
+    if dA is None:
+        dA = torch.empty((r, I), dtype=torch.float32, device=dev)
+    need = sq_lora_grads_workspace(T, O, I, r)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _dev(X, dY, B, A, dB, dA, workspace)
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check("sq_lora_grads", load().sq_lora_grads(T, O, I, r, _ptr(X), _ptr(dY), _ptr(B), _ptr(A),
+                                                 float(alpha_over_r), _ptr(dB), _ptr(dA), _ptr(workspace),
+                                                 nbytes, _stream()))
+    return dB, dA
 
 
 def sq_qast_scales(fmt, base_scales, B, A, alpha_over_r, ws2=1.0, scales_out=None, mask_out=None,

@@ -149,6 +149,44 @@ def test_rtn_rule_validation(lib):
     assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 2, 0, FAKE, None, None, None) == -1
 
 
+def test_qat_validation(lib):
+    assert lib.sq_qat_requant(2, 256, 512, 32, FAKE, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -4
+    assert lib.sq_qat_requant(0, 256, 500, 32, FAKE, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -2
+    assert lib.sq_qat_requant(0, 256, 512, 0, FAKE, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -2
+    assert lib.sq_qat_requant(0, 256, 512, 65, FAKE, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -2
+    assert lib.sq_qat_requant(0, 65535 * 16 + 8, 512, 8, FAKE, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -2
+    assert lib.sq_qat_requant(0, 256, 512, 32, None, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -1
+    assert lib.sq_qat_requant(0, 256, 512, 32, FAKE, FAKE, 1.0, FAKE, FAKE, float("nan"), FAKE, FAKE, None) == -1
+    assert lib.sq_qat_requant(1, 256, 512, 32, FAKE, FAKE, 0.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -1
+    assert lib.sq_qat_requant(0, 256, 512, 32, FAKE, FAKE, 1.0, FAKE, MISALIGNED, 0.5, FAKE, FAKE, None) == -3
+    assert lib.sq_qat_requant(0, 256, 512, 32, FAKE + 1, FAKE, 1.0, FAKE, FAKE, 0.5, FAKE, FAKE, None) == -3
+    # workspace: P^T and Q^T as bf16 hi/lo [2, RW, Tp] (Tp = T rounded up to 64), B^T [RW, O] bf16,
+    # partial sums [splits, N, RW] fp32 for each product (64-token stages, about 256 workgroups each),
+    # then the projections' partial sums over 1024-wide K-chunks [chunks, Tp, RW] fp32
+    assert lib.sq_lora_grads_workspace(256, 128, 512, 32) == \
+        2 * (2 * 32 * 256 * 2) + 32 * 128 * 2 + 4 * 512 * 32 * 4 + 4 * 128 * 32 * 4 + 2 * 256 * 32 * 4
+    assert lib.sq_lora_grads_workspace(0, 128, 512, 32) == 0
+    assert lib.sq_lora_grads_workspace(256, 128, 512, 65) == 0
+    assert lib.sq_lora_grads_workspace(256, 124, 512, 8) == 0
+    need = lib.sq_lora_grads_workspace(256, 128, 512, 33)
+    assert need == 2 * (2 * 64 * 256 * 2) + 64 * 128 * 2 + 4 * 512 * 64 * 4 + 4 * 128 * 64 * 4 + 2 * 256 * 64 * 4
+    # 4096 tokens over a 4096-wide product: 16 column tiles -> 16 splits of 256 tokens
+    assert lib.sq_lora_grads_workspace(4096, 4096, 4096, 32) == \
+        2 * (2 * 32 * 4096 * 2) + 32 * 4096 * 2 + 2 * 16 * 4096 * 32 * 4 + 2 * 4 * 4096 * 32 * 4
+    args = (256, 128, 512, 32, FAKE, FAKE, FAKE, FAKE, 0.5, FAKE, FAKE)
+    assert lib.sq_lora_grads(*args, FAKE, 10, None) == -5
+    assert lib.sq_lora_grads(*args, None, 1 << 30, None) == -5
+    assert lib.sq_lora_grads(*args, MISALIGNED + 4, 1 << 30, None) == -3
+    assert lib.sq_lora_grads(256, 128, 512, 32, MISALIGNED, FAKE, FAKE, FAKE, 0.5, FAKE, FAKE, FAKE, 1 << 30,
+                             None) == -3
+    assert lib.sq_lora_grads(256, 128, 512, 32, None, FAKE, FAKE, FAKE, 0.5, FAKE, FAKE, FAKE, 1 << 30, None) == -1
+    assert lib.sq_lora_grads(256, 128, 512, 32, FAKE, FAKE, FAKE, FAKE, float("inf"), FAKE, FAKE, FAKE, 1 << 30,
+                             None) == -1
+    assert lib.sq_lora_grads(-1, 128, 512, 32, FAKE, FAKE, FAKE, FAKE, 0.5, FAKE, FAKE, FAKE, 1 << 30, None) == -2
+    assert lib.sq_lora_grads(65535 * 128 + 1, 128, 512, 32, FAKE, FAKE, FAKE, FAKE, 0.5, FAKE, FAKE, FAKE,
+                             1 << 30, None) == -2
+
+
 def test_qast_validation(lib):
     nan = float("nan")
     q = lib.sq_qast_scales

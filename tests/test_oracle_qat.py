@@ -106,3 +106,15 @@ def test_low_rank_association():
     X64, dY64, B64, A64 = (v.astype(np.float64) for v in (X, dY, B, A))
     assert np.allclose(dB, 0.5 * dY64.T @ (X64 @ A64.T), rtol=1e-12, atol=1e-12)
     assert np.allclose(dA, 0.5 * (dY64 @ B64).T @ X64, rtol=1e-12, atol=1e-12)
+
+
+def test_sampled_gradients_equal_the_full_ones():
+    T, O, I, r = 30, 16, 48, 3
+    g = np.random.default_rng(6)
+    X, dY = g.standard_normal((T, I)).astype(np.float32), g.standard_normal((T, O)).astype(np.float32)
+    B, A = g.standard_normal((O, r)).astype(np.float32), g.standard_normal((r, I)).astype(np.float32)
+    dB, dA = qat.lora_grads(X, dY, B, A, 0.25)
+    rows, cols = np.array([0, 5, 15]), np.array([1, 47, 20])
+    sB, sA = qat.lora_grads_sampled(X, dY, B, A, 0.25, rows, cols)
+    assert np.allclose(sB, dB[rows], rtol=1e-12, atol=1e-12)
+    assert np.allclose(sA, dA[:, cols], rtol=1e-12, atol=1e-12)
