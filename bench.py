@@ -305,11 +305,15 @@ def model_step(sq, steps, warmup, comparator=True):
     kept per linear, Y and dX go to per-shape buffers.  The step runs every
     forward in layer order, then every backward in reverse order.
 
-    The comparator is the weight-space STE step of QAT-LoRA on layer 0's seven
-    linears (rank 32), reported x32 as an extrapolation: W' = deq(W) + B A,
-    RTN fake-quantisation (rtn_quantize, then a torch dequant), the three dense
-    bf16 GEMMs through torch (hipBLASLt) with dW materialised in fp32, then
-    dB = dW A^T and dA = B^T dW."""
+    The QAST step reruns it with every linear's scales from a rank-32 adapter;
+    the QAT-LoRA step runs the weight-space STE comparator on the native path
+    (fused re-quantisation of W + B A, forward and dX on those codes, factor
+    gradients through the rank).  A second, framework-style comparator repeats
+    the paper's own construction on layer 0's seven linears (rank 32), reported
+    x32 as an extrapolation: W' = deq(W) + B A, RTN fake-quantisation
+    (rtn_quantize, then a torch dequant), the three dense bf16 GEMMs through
+    torch (hipBLASLt) with dW materialised in fp32, then dB = dW A^T and
+    dA = B^T dW."""
     Tm = 4096
     shapes = inputs.LLAMA8B_LAYER
     L = inputs.LLAMA8B_LAYERS
@@ -414,6 +418,47 @@ def model_step(sq, steps, warmup, comparator=True):
     torch.cuda.synchronize()
     qast_ms = e0.elapsed_time(e1) / steps
 
+    # The QAT-LoRA comparator on the native path: every linear's weight
+    # W = deq(W) + B A (rank 32) is re-quantised by the fused kernel before its
+    # forward, the forward and dX run on those codes, and the STE gradients go
+    # to B and A through the rank (dW is never formed).
+    qt = []
+    for n, (name, o, i) in enumerate(shapes * L):
+        g = inputs.device_generator(7000 + n)
+        qt.append(dict(B=(torch.randn((o, r), generator=g, device="cuda") * 0.02).to(torch.bfloat16),
+                       A=(torch.randn((r, i), generator=g, device="cuda") * 0.02).to(torch.bfloat16),
+                       c=torch.empty((o, i // 2), dtype=torch.uint8, device="cuda"),
+                       s=torch.empty((o, i // 32), dtype=torch.uint8, device="cuda"),
+                       dB=torch.empty((o, r), dtype=torch.float32, device="cuda"),
+                       dA=torch.empty((r, i), dtype=torch.float32, device="cuda")))
+    lws = torch.empty(max(sq.sq_lora_grads_workspace(Tm, o, i, r) for (_, o, i) in shapes),
+                      dtype=torch.uint8, device="cuda")
+
+    def run_qat():
+        for l in range(L):
+            for k, (name, o, i) in enumerate(shapes):
+                n = l * len(shapes) + k
+                q = qt[n]
+                sq.sq_qat_requant("mx", codes[n], scales[n], q["B"], q["A"], 1.0, codes_out=q["c"], scales_out=q["s"])
+                sq.sq_fwd("mx", xs[l][name], q["c"], q["s"], 1.0, Y=ybuf[(o, i)])
+        for l in reversed(range(L)):
+            for k, (name, o, i) in reversed(list(enumerate(shapes))):
+                n = l * len(shapes) + k
+                q = qt[n]
+                sq.sq_bwd_dx("mx", dys[n], q["c"], q["s"], 1.0, dX=dxbuf[(o, i)])
+                sq.sq_lora_grads(xs[l][name], dys[n], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"], workspace=lws)
+
+    for _ in range(warmup):
+        run_qat()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        run_qat()
+    e1.record()
+    torch.cuda.synchronize()
+    qat_ms = e0.elapsed_time(e1) / steps
+    del qt, lws
+
     out = {"workload": "MXFP4 8B-shaped model, 32 layers x 7 linears, 4096 tokens: fwd + dX + dS of every linear",
            "ms": round(ms, 3), "TFLOP": round(flops / 1e12, 2),
            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
@@ -423,7 +468,15 @@ def model_step(sq, steps, warmup, comparator=True):
                                  "sq_qast_scales before each forward, sq_qast_factor_grads after each dS",
                          "ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
                          "note": "the paper reports +49 ms per step for QAST on its own hardware and model "
-                                 "(context only)"}}
+                                 "(context only)"},
+           "qat_lora_step": {"what": "QAT-LoRA weight-space STE on the native path, rank 32: sq_qat_requant "
+                                     "(fused W + B A and nearest re-quantisation) before each forward, forward "
+                                     "and dX on the re-quantised codes, sq_lora_grads (STE gradients of B, A "
+                                     "through the rank) after each dX",
+                             "ms": round(qat_ms, 3), "ratio_to_scale_step": round(qat_ms / ms, 3),
+                             "ratio_to_qast_step": round(qat_ms / qast_ms, 3),
+                             "note": "the paper reports QAT-LoRA at 3.9x its QAST step per step on its own "
+                                     "hardware, through framework ops with dW materialised (context only)"}}
     del dys, xs, qa
     if comparator:
         out["weight_space_ste"] = weight_space_ste(sq, codes[:len(shapes)], scales[:len(shapes)], Tm, ms, L)
