@@ -185,6 +185,47 @@ typedef struct sq_merge_desc {
 int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream);
 
 /*
+ * Grouped products over the experts of an MoE layer (Section 3, MoE path: the
+ * expert weights are stacked and every expert's scale adapter is applied in
+ * one batched pass): experts share O and I (and the format) and each has its
+ * own routed tokens, activations, weights and outputs.  Each expert computes
+ * exactly what the single-product entry point computes for it (sq_fwd,
+ * sq_bwd_dx, sq_bwd_dscale), with the same accumulation order per output
+ * element; the whole list runs in one launch per 64 experts.
+ *
+ *   act     sq_fwd_grouped, sq_bwd_dscale_grouped: X_e bf16 [T_e, I];
+ *           sq_bwd_dx_grouped: dY_e bf16 [T_e, O]  (16-byte aligned)
+ *   act2    sq_bwd_dscale_grouped: dY_e bf16 [T_e, O] (16-byte aligned);
+ *           otherwise ignored
+ *   codes   expert e's codes [O, I/2] (4-byte aligned)
+ *   scales  expert e's scale bytes [O, G] (sq_fwd_grouped, sq_bwd_dx_grouped)
+ *   out     Y_e [T_e, O] / dX_e [T_e, I] in the given dtype (16-byte aligned),
+ *           or dS_e fp32 [O, G] (4-byte aligned; all zeros when T_e = 0)
+ *   T       tokens routed to expert e, 0 <= T_e (pointers that only serve
+ *           tokens may be NULL when T_e = 0)
+ *   ws2     expert e's NVFP4 per-tensor scalar (finite, > 0; ignored for
+ *           MXFP4 and by sq_bwd_dscale_grouped)
+ *   reserved must be 0
+ * n_experts >= 0; descs is read during the call only.
+ */
+typedef struct {
+  const void* act;
+  const void* act2;
+  const uint8_t* codes;
+  const uint8_t* scales;
+  void* out;
+  int64_t T;
+  float ws2;
+  int32_t reserved;
+} sq_expert_desc;
+
+int sq_fwd_grouped(int fmt, int64_t O, int64_t I, int n_experts, const sq_expert_desc* descs, int y_dtype,
+                   void* stream);
+int sq_bwd_dx_grouped(int fmt, int64_t O, int64_t I, int n_experts, const sq_expert_desc* descs, int dx_dtype,
+                      void* stream);
+int sq_bwd_dscale_grouped(int fmt, int64_t O, int64_t I, int n_experts, const sq_expert_desc* descs, void* stream);
+
+/*
  * Round-to-nearest re-quantisation of a bf16 weight [O, I] into codes and
  * scales, the naive merge W' = requant(dequant(W) + (alpha/r) BA) (Section 2,
  * "The naive re-quantized merge is the failure mode").

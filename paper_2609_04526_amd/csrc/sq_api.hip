@@ -160,6 +160,74 @@ SQ_EXPORT int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, vo
   return run_merge(n_desc, descs, static_cast<hipStream_t>(stream));
 }
 
+namespace {
+enum GroupedKind { kGroupedFwd, kGroupedDx, kGroupedDs };
+
+int run_grouped(GroupedKind kind, int fmt, int64_t O, int64_t I, int n, const sq_expert_desc* d, int out_dtype,
+                hipStream_t s) {
+  int st = check_layer(fmt, 0, O, I);
+  if (st != SQ_OK) return st;
+  if (n < 0 || (n > 0 && !d)) return SQ_ERR_ARG;
+  if (kind != kGroupedDs && out_dtype != SQ_OUT_F32 && out_dtype != SQ_OUT_BF16) return SQ_ERR_ARG;
+  for (int e = 0; e < n; ++e) {
+    const sq_expert_desc& x = d[e];
+    if (x.reserved != 0) return SQ_ERR_ARG;
+    st = check_layer(fmt, x.T, O, I);
+    if (st != SQ_OK) return st;
+    if (!x.codes) return SQ_ERR_ARG;
+    if (!aligned(x.codes, 4)) return SQ_ERR_ALIGN;
+    if (kind == kGroupedDs) {
+      if (!x.out || (x.T > 0 && (!x.act || !x.act2))) return SQ_ERR_ARG;
+      if (!aligned(x.act, 16) || !aligned(x.act2, 16) || !aligned(x.out, 4)) return SQ_ERR_ALIGN;
+    } else {
+      if (!x.scales || (x.T > 0 && (!x.act || !x.out))) return SQ_ERR_ARG;
+      if (fmt == SQ_NVFP4 && !ws2_ok(x.ws2)) return SQ_ERR_ARG;
+      if (!aligned(x.act, 16) || !aligned(x.out, 16)) return SQ_ERR_ALIGN;
+    }
+  }
+  // one table entry per expert that has work (the forward and dX skip empty experts)
+  sq::ExpertProblem p[sq::kGroupMax];
+  int m = 0;
+  auto flush = [&]() -> int {
+    if (m == 0) return 0;
+    int rc;
+    if (kind == kGroupedFwd) rc = sq::gemm_fwd_grouped(fmt, (int)O, (int)I, m, p, out_dtype == SQ_OUT_BF16, s);
+    else if (kind == kGroupedDx) rc = sq::gemm_dx_grouped(fmt, (int)O, (int)I, m, p, out_dtype == SQ_OUT_BF16, s);
+    else rc = sq::gemm_dscale_grouped(fmt, (int)O, (int)I, m, p, s);
+    m = 0;
+    return rc;
+  };
+  for (int e = 0; e < n; ++e) {
+    const sq_expert_desc& x = d[e];
+    if (kind != kGroupedDs && x.T == 0) continue;
+    p[m].a = x.act;
+    p[m].b = x.act2;
+    p[m].codes = x.codes;
+    p[m].scales = x.scales;
+    p[m].out = x.out;
+    p[m].T = (int)x.T;
+    p[m].ws2 = fmt == SQ_NVFP4 ? x.ws2 : 1.0f;
+    if (++m == sq::kGroupMax && flush() != 0) return SQ_ERR_HIP;
+  }
+  return flush() == 0 ? SQ_OK : SQ_ERR_HIP;
+}
+}  // namespace
+
+SQ_EXPORT int sq_fwd_grouped(int fmt, int64_t O, int64_t I, int n_experts, const sq_expert_desc* descs,
+                             int y_dtype, void* stream) {
+  return run_grouped(kGroupedFwd, fmt, O, I, n_experts, descs, y_dtype, static_cast<hipStream_t>(stream));
+}
+
+SQ_EXPORT int sq_bwd_dx_grouped(int fmt, int64_t O, int64_t I, int n_experts, const sq_expert_desc* descs,
+                                int dx_dtype, void* stream) {
+  return run_grouped(kGroupedDx, fmt, O, I, n_experts, descs, dx_dtype, static_cast<hipStream_t>(stream));
+}
+
+SQ_EXPORT int sq_bwd_dscale_grouped(int fmt, int64_t O, int64_t I, int n_experts, const sq_expert_desc* descs,
+                                    void* stream) {
+  return run_grouped(kGroupedDs, fmt, O, I, n_experts, descs, SQ_OUT_F32, static_cast<hipStream_t>(stream));
+}
+
 SQ_EXPORT int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int tie,
                            uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream) {
   int st = check_layer(fmt, 0, O, I);

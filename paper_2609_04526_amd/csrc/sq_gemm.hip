@@ -81,6 +81,22 @@ struct GemmArgs {
   int ksteps_per;         // DS: K stages per range
 };
 
+// Up to kGroupMax experts per grouped launch, passed by value (kernel
+// arguments stay under 4 KiB).
+struct GemmGroup {
+  GemmArgs base;                  // shared: O, I, G, N (fwd/dx) or M, N (ds), out_bf16
+  const uint16_t* a[kGroupMax];
+  const uint16_t* b[kGroupMax];
+  const uint8_t* codes[kGroupMax];
+  const uint8_t* scales[kGroupMax];
+  void* out[kGroupMax];
+  int T[kGroupMax];
+  float ws2[kGroupMax];
+  int tile_begin[kGroupMax];
+  int count;
+};
+static_assert(sizeof(GemmGroup) <= 4096, "kernel argument budget");
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
@@ -336,8 +352,11 @@ __device__ __forceinline__ void epi_store_bf16(const f32x16 (&acc)[TM][TN], SQ_L
 // ------------------------------------------------------------------ kernel
 // Block tile BM x BN, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN) built
 // from 32x32 MFMA tiles; STAGES LDS stages for the DMA operands.
+// One workgroup's tile: bid is its index among the nb workgroups of one
+// product (the XCD-aware order reads bid % 8 as the XCD, which holds when the
+// product's first workgroup sits at a multiple of 8 in the grid).
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
@@ -378,10 +397,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   // a DS launch with split K runs ksplit workgroups per tile, each over its
   // own range of K stages
   const int tiles = tiles_m * tiles_n;
-  const int split = (MODE == kDs && g.ksplit > 1) ? (int)blockIdx.x / tiles : 0;
+  const int split = (MODE == kDs && g.ksplit > 1) ? bid / tiles : 0;
   int tm, tn;
-  tile_of((MODE == kDs && g.ksplit > 1) ? (int)blockIdx.x - split * tiles : (int)blockIdx.x,
-          (MODE == kDs && g.ksplit > 1) ? tiles : (int)gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_of((MODE == kDs && g.ksplit > 1) ? bid - split * tiles : bid, (MODE == kDs && g.ksplit > 1) ? tiles : nb,
+          tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
   auto stage = [&](auto SC) -> SQ_LDS uint8_t* {
@@ -750,6 +769,40 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
   }
 }
 
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
+  gemm_tile<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>(g, (int)blockIdx.x, (int)gridDim.x);
+}
+
+// Grouped products (one per MoE expert, same O and I, own tokens and
+// weights): expert e owns workgroups [tile_begin[e], tile_begin[e] + tiles of
+// e), its range starting at a multiple of 8; the rest of the range exits.
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup gg) {
+  const int b = (int)blockIdx.x;
+  int lo = 0, hi = gg.count - 1;                 // last e with tile_begin[e] <= b
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (gg.tile_begin[mid] <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  const int e = lo;
+  GemmArgs g = gg.base;
+  g.a = gg.a[e];
+  g.b = gg.b[e];
+  g.codes = gg.codes[e];
+  g.scales = gg.scales[e];
+  g.out = gg.out[e];
+  g.T = gg.T[e];
+  g.ws2 = gg.ws2[e];
+  if (MODE == kDs) g.K = g.T;
+  else g.M = g.T;
+  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  const int local = b - gg.tile_begin[e];
+  if (local >= tiles) return;
+  gemm_tile<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>(g, local, tiles);
+}
+
 // Tile configurations (compile-time; SQ_CFG_* selects one per product for
 // tuning builds).  Each entry: BM, BN, waves along M, waves along N, stages,
 // K per stage.  The large tile is used when its grid still gives every CU a
@@ -810,6 +863,87 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = dx_bf16;
   return fmt == kMX ? launch_sized<kDx, kMX, SQ_CFG_DX>(g, s) : launch_sized<kDx, kNV, SQ_CFG_DX>(g, s);
+}
+
+// ------------------------------------------------------------------ grouped
+// One launch per kGroupMax experts.  Workgroups of expert e start at a
+// multiple of 8 so the XCD-aware order inside each expert still holds.
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
+static int launch_grouped(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
+  using L = SmemLayout<MODE, BM, BN, STAGES, BK>;
+  static_assert(L::kBytes <= 160 * 1024, "LDS budget");
+  int blocks = 0;
+  gg.count = n;
+  for (int e = 0; e < n; ++e) {
+    const int M = MODE == kDs ? gg.base.M : p[e].T;
+    const int tiles = ((M + BM - 1) / BM) * ((gg.base.N + BN - 1) / BN);
+    gg.a[e] = static_cast<const uint16_t*>(p[e].a);
+    gg.b[e] = static_cast<const uint16_t*>(p[e].b);
+    gg.codes[e] = p[e].codes;
+    gg.scales[e] = p[e].scales;
+    gg.out[e] = p[e].out;
+    gg.T[e] = p[e].T;
+    gg.ws2[e] = FMT == kNV ? p[e].ws2 : 1.0f;
+    gg.tile_begin[e] = blocks;
+    blocks += (tiles + 7) / 8 * 8;
+  }
+  if (blocks == 0) return 0;
+  hipLaunchKernelGGL((gemm_grouped_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(blocks),
+                     dim3(64 * WGM * WGN), 0, s, gg);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// The large tile when the experts' tiles fill the chip and (for the forward
+// and dX, whose rows are tokens) an expert averages at least 512 tokens.
+template <int MODE, int FMT, int BM, int BN, int... REST>
+static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
+  int64_t tokens = 0, big = 0;
+  for (int e = 0; e < n; ++e) {
+    tokens += p[e].T;
+    const int M = MODE == kDs ? gg.base.M : p[e].T;
+    big += (int64_t)((M + BM - 1) / BM) * ((gg.base.N + BN - 1) / BN);
+  }
+  const bool large = big >= kCUs && (MODE == kDs || tokens >= (int64_t)512 * n);
+  if (large) return launch_grouped<MODE, FMT, BM, BN, REST...>(gg, p, n, s);
+  return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+}
+
+template <int MODE>
+static int run_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int out_bf16, hipStream_t s) {
+  GemmGroup gg{};
+  gg.base.O = O;
+  gg.base.I = I;
+  gg.base.G = I / (fmt == kMX ? 32 : 16);
+  gg.base.out_bf16 = out_bf16;
+  gg.base.ksplit = 1;
+  if (MODE == kFwdR) { gg.base.N = O; gg.base.K = I; }
+  else if (MODE == kDx) { gg.base.N = I; gg.base.K = O; }
+  else { gg.base.M = I; gg.base.N = O; }
+  for (int e0 = 0; e0 < n; e0 += kGroupMax) {
+    const int m = n - e0 < kGroupMax ? n - e0 : kGroupMax;
+    int rc;
+    if (MODE == kFwdR)
+      rc = fmt == kMX ? grouped_sized<kFwdR, kMX, SQ_CFG_FWD>(gg, p + e0, m, s)
+                      : grouped_sized<kFwdR, kNV, SQ_CFG_FWD>(gg, p + e0, m, s);
+    else if (MODE == kDx)
+      rc = fmt == kMX ? grouped_sized<kDx, kMX, SQ_CFG_DX>(gg, p + e0, m, s)
+                      : grouped_sized<kDx, kNV, SQ_CFG_DX>(gg, p + e0, m, s);
+    else
+      rc = fmt == kMX ? grouped_sized<kDs, kMX, SQ_CFG_DS>(gg, p + e0, m, s)
+                      : grouped_sized<kDs, kNV, SQ_CFG_DS>(gg, p + e0, m, s);
+    if (rc != 0) return rc;
+  }
+  return 0;
+}
+
+int gemm_fwd_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int y_bf16, hipStream_t s) {
+  return run_grouped<kFwdR>(fmt, O, I, n, p, y_bf16, s);
+}
+int gemm_dx_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int dx_bf16, hipStream_t s) {
+  return run_grouped<kDx>(fmt, O, I, n, p, dx_bf16, s);
+}
+int gemm_dscale_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, hipStream_t s) {
+  return run_grouped<kDs>(fmt, O, I, n, p, 0, s);
 }
 
 // Split of the token sum for dS when the large tile leaves CUs idle: each of

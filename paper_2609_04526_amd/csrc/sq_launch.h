@@ -47,6 +47,23 @@ struct MergeBatch {
 static_assert(sizeof(MergeBatch) <= 4096, "kernel argument budget");
 int merge_launch(const MergeBatch& b, hipStream_t s);
 
+// Grouped products over MoE experts that share O and I: each expert has its
+// own tokens (T >= 0), activations, weights and output.  Up to kGroupMax
+// experts per launch; the caller splits longer lists.
+constexpr int kGroupMax = 64;
+struct ExpertProblem {
+  const void* a;            // fwd, ds: X [T, I]; dx: dY [T, O]
+  const void* b;            // ds: dY [T, O]
+  const uint8_t* codes;
+  const uint8_t* scales;
+  void* out;                // fwd: Y [T, O]; dx: dX [T, I]; ds: dS [O, G] fp32
+  int T;
+  float ws2;
+};
+int gemm_fwd_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int y_bf16, hipStream_t s);
+int gemm_dx_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int dx_bf16, hipStream_t s);
+int gemm_dscale_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, hipStream_t s);
+
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
 // rule: 0 nearest-even, 1 nearest-away, 2 toward zero, 3 stochastic (Philox

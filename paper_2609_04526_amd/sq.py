@@ -50,6 +50,20 @@ class MergeDesc(ctypes.Structure):
     ]
 
 
+class ExpertDesc(ctypes.Structure):
+    """Mirror of sq_expert_desc."""
+    _fields_ = [
+        ("act", ctypes.c_void_p),
+        ("act2", ctypes.c_void_p),
+        ("codes", ctypes.c_void_p),
+        ("scales", ctypes.c_void_p),
+        ("out", ctypes.c_void_p),
+        ("T", ctypes.c_int64),
+        ("ws2", ctypes.c_float),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
 _lib = None
 
 
@@ -72,6 +86,12 @@ def load():
         "sq_merge_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_p, _c_p, _c_p, ctypes.c_float,
                                            ctypes.c_int, _c_p]),
         "sq_merge_scales_grouped": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(MergeDesc), _c_p]),
+        "sq_fwd_grouped": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, ctypes.POINTER(ExpertDesc),
+                                          ctypes.c_int, _c_p]),
+        "sq_bwd_dx_grouped": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int,
+                                             ctypes.POINTER(ExpertDesc), ctypes.c_int, _c_p]),
+        "sq_bwd_dscale_grouped": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int,
+                                                 ctypes.POINTER(ExpertDesc), _c_p]),
         "rtn_quantize": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
                                         _c_p, _c_p, _c_p, _c_p]),
         "rtn_quantize_rule": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
@@ -205,6 +225,63 @@ def sq_merge_scales_grouped(planes):
     group = planes if isinstance(planes, MergeGroup) else MergeGroup(planes)
     _check("sq_merge_scales_grouped",
            load().sq_merge_scales_grouped(len(group.planes), group.arr, _stream()))
+
+
+def _expert_table(acts, acts2, codes, scales, outs, ws2):
+    n = len(codes)
+    arr = (ExpertDesc * max(n, 1))()
+    for e in range(n):
+        d = arr[e]
+        d.act = acts[e].data_ptr() if acts[e] is not None and acts[e].numel() else None
+        d.act2 = acts2[e].data_ptr() if acts2 is not None and acts2[e].numel() else None
+        d.codes = codes[e].data_ptr()
+        d.scales = scales[e].data_ptr() if scales is not None else None
+        d.out = outs[e].data_ptr() if outs[e].numel() else None
+        d.T = acts[e].shape[0]
+        d.ws2 = float(ws2[e]) if ws2 is not None else 1.0
+        d.reserved = 0
+    return arr
+
+
+_DTYPE_CODE = {torch.float32: OUT_F32, torch.bfloat16: OUT_BF16}
+
+
+def sq_fwd_grouped(fmt, Xs, codes, scales, ws2=None, out_dtype=torch.float32, Ys=None):
+    """Per-expert Y_e = X_e W_e^T in one grouped launch; Xs[e] bf16 [T_e, I]."""
+    fmt = _fmt(fmt)
+    O, I = codes[0].shape[0], codes[0].shape[1] * 2
+    if Ys is None:
+        Ys = [torch.empty((x.shape[0], O), dtype=out_dtype, device=codes[0].device) for x in Xs]
+    _dev(*Xs, *codes, *scales, *Ys)
+    arr = _expert_table(Xs, None, codes, scales, Ys, ws2)
+    _check("sq_fwd_grouped", load().sq_fwd_grouped(fmt, O, I, len(codes), arr, _DTYPE_CODE[Ys[0].dtype] if Ys
+                                                   else OUT_F32, _stream()))
+    return Ys
+
+
+def sq_bwd_dx_grouped(fmt, dYs, codes, scales, ws2=None, out_dtype=torch.float32, dXs=None):
+    """Per-expert dX_e = dY_e W_e in one grouped launch; dYs[e] bf16 [T_e, O]."""
+    fmt = _fmt(fmt)
+    O, I = codes[0].shape[0], codes[0].shape[1] * 2
+    if dXs is None:
+        dXs = [torch.empty((d.shape[0], I), dtype=out_dtype, device=codes[0].device) for d in dYs]
+    _dev(*dYs, *codes, *scales, *dXs)
+    arr = _expert_table(dYs, None, codes, scales, dXs, ws2)
+    _check("sq_bwd_dx_grouped", load().sq_bwd_dx_grouped(fmt, O, I, len(codes), arr, _DTYPE_CODE[dXs[0].dtype]
+                                                         if dXs else OUT_F32, _stream()))
+    return dXs
+
+
+def sq_bwd_dscale_grouped(fmt, Xs, dYs, codes, dSs=None):
+    """Per-expert dS_e (fp32 [O, G]) in one grouped launch."""
+    fmt = _fmt(fmt)
+    O, I = codes[0].shape[0], codes[0].shape[1] * 2
+    if dSs is None:
+        dSs = [torch.empty((O, I // BLOCK[fmt]), dtype=torch.float32, device=codes[0].device) for _ in codes]
+    _dev(*Xs, *dYs, *codes, *dSs)
+    arr = _expert_table(Xs, dYs, codes, None, dSs, None)
+    _check("sq_bwd_dscale_grouped", load().sq_bwd_dscale_grouped(fmt, O, I, len(codes), arr, _stream()))
+    return dSs
 
 
 def rtn_quantize(fmt, W, tie=TIE_EVEN, ws2_in=0.0, codes=None, scales=None, ws2_out=None):

@@ -46,6 +46,30 @@ def test_merge_desc_layout_matches_header():
     assert sq.MergeDesc.ws2.offset == 32 and sq.MergeDesc.reserved.offset == 44
 
 
+def test_descriptor_layouts_match_the_c_compiler(tmp_path):
+    """sizeof / offsetof of the header's descriptor structs, printed by a C
+    program built with gcc, against the ctypes mirrors."""
+    import subprocess
+    from paper_2609_04526_amd import sq
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "scaleqlora.h"\n'
+        'int main(void) {\n'
+        '  printf("%zu %zu %zu\\n", sizeof(sq_merge_desc), offsetof(sq_merge_desc, ws2),'
+        ' offsetof(sq_merge_desc, reserved));\n'
+        '  printf("%zu %zu %zu %zu\\n", sizeof(sq_expert_desc), offsetof(sq_expert_desc, T),'
+        ' offsetof(sq_expert_desc, ws2), offsetof(sq_expert_desc, reserved));\n'
+        '  return 0;\n}\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    m = [int(v) for v in out[0].split()]
+    e = [int(v) for v in out[1].split()]
+    assert m == [ctypes.sizeof(sq.MergeDesc), sq.MergeDesc.ws2.offset, sq.MergeDesc.reserved.offset]
+    assert e == [ctypes.sizeof(sq.ExpertDesc), sq.ExpertDesc.T.offset, sq.ExpertDesc.ws2.offset,
+                 sq.ExpertDesc.reserved.offset]
+
+
 FAKE = 0x10000            # a 16-byte-aligned address that is never dereferenced
 MISALIGNED = 0x10008
 
@@ -134,6 +158,37 @@ def test_rtn_validation(lib):
     assert lib.rtn_quantize(1, 256, 512, FAKE, float("inf"), 0, FAKE, FAKE, None, None) == -1
     assert lib.rtn_quantize(0, 256, 512, MISALIGNED, 0.0, 0, FAKE, FAKE, None, None) == -3
     assert lib.rtn_quantize(0, 256, 512, None, 0.0, 0, FAKE, FAKE, None, None) == -1
+
+
+def test_grouped_validation(lib):
+    from paper_2609_04526_amd import sq
+
+    def table(*rows):
+        arr = (sq.ExpertDesc * len(rows))()
+        for d, (act, act2, codes, scales, out, T, ws2, res) in zip(arr, rows):
+            d.act, d.act2, d.codes, d.scales, d.out = act, act2, codes, scales, out
+            d.T, d.ws2, d.reserved = T, ws2, res
+        return arr
+
+    ok = (FAKE, FAKE, FAKE, FAKE, FAKE, 64, 1.0, 0)
+    empty = (None, None, FAKE, FAKE, None, 0, 1.0, 0)
+    assert lib.sq_fwd_grouped(0, 256, 512, 0, None, 0, None) == 0            # nothing to do
+    assert lib.sq_fwd_grouped(0, 256, 512, 2, table(empty, empty), 0, None) == 0
+    assert lib.sq_fwd_grouped(0, 256, 512, -1, None, 0, None) == -1
+    assert lib.sq_fwd_grouped(0, 256, 512, 1, None, 0, None) == -1
+    assert lib.sq_fwd_grouped(2, 256, 512, 1, table(ok), 0, None) == -4
+    assert lib.sq_fwd_grouped(0, 256, 500, 1, table(ok), 0, None) == -2
+    assert lib.sq_fwd_grouped(0, 256, 512, 1, table(ok), 5, None) == -1
+    assert lib.sq_fwd_grouped(0, 256, 512, 2, table(ok, ok[:7] + (1,)), 0, None) == -1      # reserved
+    assert lib.sq_fwd_grouped(0, 256, 512, 1, table(ok[:5] + (-1,) + ok[6:]), 0, None) == -2
+    assert lib.sq_fwd_grouped(0, 256, 512, 1, table((None,) + ok[1:]), 0, None) == -1
+    assert lib.sq_fwd_grouped(0, 256, 512, 1, table((MISALIGNED,) + ok[1:]), 0, None) == -3
+    assert lib.sq_fwd_grouped(1, 256, 512, 1, table(ok[:6] + (0.0, 0)), 0, None) == -1     # NVFP4 ws2
+    assert lib.sq_bwd_dx_grouped(0, 256, 512, 1, table(ok[:3] + (None,) + ok[4:]), 0, None) == -1
+    # dS is written even for an expert without tokens, so its output is required
+    assert lib.sq_bwd_dscale_grouped(0, 256, 512, 1, table(empty[:4] + (None,) + empty[5:]), None) == -1
+    assert lib.sq_bwd_dscale_grouped(0, 256, 512, 1, table((FAKE, None) + ok[2:]), None) == -1
+    assert lib.sq_bwd_dscale_grouped(0, 256, 512, 1, table(ok[:4] + (FAKE + 2,) + ok[5:]), None) == -3
 
 
 def test_rtn_rule_validation(lib):
