@@ -319,6 +319,25 @@ int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS, const uin
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The QAST step for the E experts of an MoE layer in the same launches
+ * (Section 3, MoE path: every expert's Delta_S in one batched pass).  The
+ * experts are stacked: base_scales, scales_out, clamp_mask_out, dS [E, O, G];
+ * B [E, O, r]; A [E, r, G]; dB fp32 [E, O, r]; dA fp32 [E, r, G].  Expert e
+ * computes exactly what sq_qast_scales / sq_qast_factor_grads compute for its
+ * planes.  ws2: host array of E per-expert NVFP4 scalars (read during the
+ * call; ignored and may be NULL for MXFP4).  1 <= E <= 65535 and
+ * E*O*G, E*O*r, E*r*G < 2^31; workspace: at least
+ * sq_qast_factor_grads_batched_workspace(E, O, G, r) bytes.
+ */
+int sq_qast_scales_batched(int fmt, int64_t E, int64_t O, int64_t G, int r, const uint8_t* base_scales,
+                           const void* B, const void* A, float alpha_over_r, const float* ws2, uint8_t* scales_out,
+                           uint8_t* clamp_mask_out, void* stream);
+size_t sq_qast_factor_grads_batched_workspace(int64_t E, int64_t O, int64_t G, int r);
+int sq_qast_factor_grads_batched(int64_t E, int64_t O, int64_t G, int r, const float* dS, const uint8_t* clamp_mask,
+                                 const void* B, const void* A, float alpha_over_r, float* dB, float* dA,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * QAT-LoRA weight-space STE comparator (Section 2 related work, "Merge-aware
  * weight-space": W <- W + (quantize(W) - W).detach() on W = W_base + (alpha/r)
  * B A; Appendix "Training cost per step").  The fake-quantised forward weight

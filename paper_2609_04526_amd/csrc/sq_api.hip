@@ -264,47 +264,86 @@ SQ_EXPORT int rtn_quantize_rule(int fmt, int64_t O, int64_t I, const void* W, fl
 namespace {
 constexpr int kQastRankMax = 64;
 
-int check_qast_plane(int64_t O, int64_t G, int r) {
-  if (O < 1 || G < 1 || O > kDimMax || G > kDimMax || O * G > kDimMax) return SQ_ERR_SHAPE;
+int check_qast_plane(int64_t O, int64_t G, int r, int64_t E = 1) {
+  if (E < 1 || E > 65535) return SQ_ERR_SHAPE;
+  if (O < 1 || G < 1 || O > kDimMax || G > kDimMax || E * O * G > kDimMax) return SQ_ERR_SHAPE;
+  if (E * O * r > kDimMax || E * r * G > kDimMax) return SQ_ERR_SHAPE;
   if (r < 1 || r > kQastRankMax) return SQ_ERR_SHAPE;
   return SQ_OK;
+}
+
+int qast_scales_checked(int fmt, int64_t E, int64_t O, int64_t G, int r, const uint8_t* base_scales, const void* B,
+                        const void* A, float alpha_over_r, const float* ws2, uint8_t* scales_out,
+                        uint8_t* clamp_mask_out, void* stream) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  int st = check_qast_plane(O, G, r, E);
+  if (st != SQ_OK) return st;
+  if (!base_scales || !B || !A || !scales_out) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (fmt == SQ_NVFP4) {
+    if (!ws2) return SQ_ERR_ARG;
+    for (int64_t e = 0; e < E; ++e)
+      if (!ws2_ok(ws2[e])) return SQ_ERR_ARG;
+  }
+  if (!aligned(B, 2) || !aligned(A, 2)) return SQ_ERR_ALIGN;
+  return hip_status(sq::qast_scales_launch(fmt, (int)E, (int)O, (int)G, r, base_scales, B, A, alpha_over_r, ws2,
+                                           scales_out, clamp_mask_out, static_cast<hipStream_t>(stream)));
+}
+
+int qast_grads_checked(int64_t E, int64_t O, int64_t G, int r, const float* dS, const uint8_t* clamp_mask,
+                       const void* B, const void* A, float alpha_over_r, float* dB, float* dA, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = check_qast_plane(O, G, r, E);
+  if (st != SQ_OK) return st;
+  if (!dS || !B || !A || !dB || !dA) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (!aligned(dS, 4) || !aligned(B, 2) || !aligned(A, 2) || !aligned(dB, 4) || !aligned(dA, 4))
+    return SQ_ERR_ALIGN;
+  const size_t need = sq::qast_grads_workspace((int)E, (int)O, (int)G, r);
+  if (!workspace || workspace_bytes < need) return SQ_ERR_WORKSPACE;
+  if (!aligned(workspace, 4)) return SQ_ERR_ALIGN;
+  return hip_status(sq::qast_grads_launch((int)E, (int)O, (int)G, r, dS, clamp_mask, B, A, alpha_over_r, dB, dA,
+                                          workspace, static_cast<hipStream_t>(stream)));
 }
 }  // namespace
 
 SQ_EXPORT int sq_qast_scales(int fmt, int64_t O, int64_t G, int r, const uint8_t* base_scales, const void* B,
                              const void* A, float alpha_over_r, float ws2, uint8_t* scales_out,
                              uint8_t* clamp_mask_out, void* stream) {
-  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
-  int st = check_qast_plane(O, G, r);
-  if (st != SQ_OK) return st;
-  if (!base_scales || !B || !A || !scales_out) return SQ_ERR_ARG;
-  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
-  if (fmt == SQ_NVFP4 && !ws2_ok(ws2)) return SQ_ERR_ARG;
-  if (!aligned(B, 2) || !aligned(A, 2)) return SQ_ERR_ALIGN;
-  return hip_status(sq::qast_scales_launch(fmt, (int)O, (int)G, r, base_scales, B, A, alpha_over_r,
-                                           fmt == SQ_NVFP4 ? ws2 : 1.0f, scales_out, clamp_mask_out,
-                                           static_cast<hipStream_t>(stream)));
+  return qast_scales_checked(fmt, 1, O, G, r, base_scales, B, A, alpha_over_r, &ws2, scales_out, clamp_mask_out,
+                             stream);
+}
+
+SQ_EXPORT int sq_qast_scales_batched(int fmt, int64_t E, int64_t O, int64_t G, int r, const uint8_t* base_scales,
+                                     const void* B, const void* A, float alpha_over_r, const float* ws2,
+                                     uint8_t* scales_out, uint8_t* clamp_mask_out, void* stream) {
+  return qast_scales_checked(fmt, E, O, G, r, base_scales, B, A, alpha_over_r, ws2, scales_out, clamp_mask_out,
+                             stream);
 }
 
 SQ_EXPORT size_t sq_qast_factor_grads_workspace(int64_t O, int64_t G, int r) {
   if (check_qast_plane(O, G, r) != SQ_OK) return 0;
-  return sq::qast_grads_workspace((int)O, (int)G, r);
+  return sq::qast_grads_workspace(1, (int)O, (int)G, r);
+}
+
+SQ_EXPORT size_t sq_qast_factor_grads_batched_workspace(int64_t E, int64_t O, int64_t G, int r) {
+  if (check_qast_plane(O, G, r, E) != SQ_OK) return 0;
+  return sq::qast_grads_workspace((int)E, (int)O, (int)G, r);
 }
 
 SQ_EXPORT int sq_qast_factor_grads(int64_t O, int64_t G, int r, const float* dS, const uint8_t* clamp_mask,
                                    const void* B, const void* A, float alpha_over_r, float* dB, float* dA,
                                    void* workspace, size_t workspace_bytes, void* stream) {
-  int st = check_qast_plane(O, G, r);
-  if (st != SQ_OK) return st;
-  if (!dS || !B || !A || !dB || !dA) return SQ_ERR_ARG;
-  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
-  if (!aligned(dS, 4) || !aligned(B, 2) || !aligned(A, 2) || !aligned(dB, 4) || !aligned(dA, 4))
-    return SQ_ERR_ALIGN;
-  const size_t need = sq::qast_grads_workspace((int)O, (int)G, r);
-  if (!workspace || workspace_bytes < need) return SQ_ERR_WORKSPACE;
-  if (!aligned(workspace, 4)) return SQ_ERR_ALIGN;
-  return hip_status(sq::qast_grads_launch((int)O, (int)G, r, dS, clamp_mask, B, A, alpha_over_r, dB, dA, workspace,
-                                          static_cast<hipStream_t>(stream)));
+  return qast_grads_checked(1, O, G, r, dS, clamp_mask, B, A, alpha_over_r, dB, dA, workspace, workspace_bytes,
+                            stream);
+}
+
+SQ_EXPORT int sq_qast_factor_grads_batched(int64_t E, int64_t O, int64_t G, int r, const float* dS,
+                                           const uint8_t* clamp_mask, const void* B, const void* A,
+                                           float alpha_over_r, float* dB, float* dA, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  return qast_grads_checked(E, O, G, r, dS, clamp_mask, B, A, alpha_over_r, dB, dA, workspace, workspace_bytes,
+                            stream);
 }
 
 namespace {

@@ -80,13 +80,18 @@ size_t lora_grads_workspace(int T, int O, int I, int r);
 int lora_grads_launch(int T, int O, int I, int r, const void* X, const void* dY, const void* B, const void* A,
                       float c, float* dB, float* dA, void* workspace, hipStream_t s);
 
-// QAST low-rank scale step: on-grid scale bytes (+ clamp mask) and the factor
-// gradients; qast_grads_workspace bytes of partial dA planes.
-int qast_scales_launch(int fmt, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
-                       float alpha_over_r, float ws2, uint8_t* out, uint8_t* mask, hipStream_t s);
-size_t qast_grads_workspace(int O, int G, int r);
-int qast_grads_launch(int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
-                      float alpha_over_r, float* dB, float* dA, void* workspace, hipStream_t s);
+// QAST low-rank scale step for E stacked experts (E = 1: one plane): on-grid
+// scale bytes (+ clamp mask) and the factor gradients; qast_grads_workspace
+// bytes of partial dA planes.  ws2: E per-expert scalars (NVFP4).
+constexpr int kWs2TableMax = 256;
+struct Ws2Table {
+  float v[kWs2TableMax];
+};
+int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
+                       float c, const float* ws2, uint8_t* out, uint8_t* mask, hipStream_t s);
+size_t qast_grads_workspace(int E, int O, int G, int r);
+int qast_grads_launch(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
+                      float c, float* dB, float* dA, void* workspace, hipStream_t s);
 
 // Rollback and byte audit (sq_audit.hip).
 int applied_launch(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied, hipStream_t s);

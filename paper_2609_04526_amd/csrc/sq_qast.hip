@@ -8,6 +8,10 @@
 //   dB = (alpha/r) (dS * m) A^T        m = 0 where the NVFP4 ceiling clamp bound
 //   dA = (alpha/r) B^T (dS * m)
 //
+// The MoE path stacks E experts (rows e*O .. e*O + O - 1 of every [rows, G]
+// or [rows, r] plane; A as [E, r, G]) and runs every expert's step in the
+// same launches.
+//
 // Delta_S adds the r rank-one terms in increasing k in fp32; each product of
 // two bf16 values is exact in fp32, so the fused multiply-add below rounds
 // exactly like a separate multiply and add, and the scale bytes are fixed bit
@@ -28,20 +32,25 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as
 // ------------------------------------------------------------------ scales
 // One thread per scale (o, g), consecutive threads along g: the A reads are
 // coalesced and a row's B entries are shared by its threads.
+// Experts are stacked: rows e*O .. e*O + O - 1 of base, B, out and mask
+// belong to expert e, whose A is A + e*r*G and whose ws2 is ws2[e].
 template <int FMT>
 __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restrict__ base,
                                                           const uint16_t* __restrict__ B,
-                                                          const uint16_t* __restrict__ A, int O, int G, int r,
-                                                          float c, float ws2, uint8_t* out, uint8_t* mask) {
+                                                          const uint16_t* __restrict__ A, int E, int O, int G, int r,
+                                                          float c, Ws2Table ws2, uint8_t* out, uint8_t* mask) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)O * G) return;
-  const int o = (int)(idx / G), g = (int)(idx - (int64_t)o * G);
-  const uint16_t* brow = B + (size_t)o * r;
+  if (idx >= (int64_t)E * O * G) return;
+  const int64_t row = idx / G;
+  const int g = (int)(idx - row * G);
+  const int e = (int)(row / O);
+  const uint16_t* brow = B + (size_t)row * r;
+  const uint16_t* ae = A + (size_t)e * r * G;
   float acc = 0.0f;
   for (int k = 0; k < r; ++k)
-    acc = __builtin_fmaf(bf16_bits_to_f32(brow[k]), bf16_bits_to_f32(A[(size_t)k * G + g]), acc);
+    acc = __builtin_fmaf(bf16_bits_to_f32(brow[k]), bf16_bits_to_f32(ae[(size_t)k * G + g]), acc);
   bool clamped;
-  const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc, c), ws2, clamped);
+  const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc, c), ws2.v[e], clamped);
   out[idx] = (uint8_t)nb;
   if (mask) mask[idx] = clamped ? 0 : 1;
 }
@@ -57,6 +66,11 @@ __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ 
                                                       const uint16_t* __restrict__ A, int O, int G, int r, float c,
                                                       float* __restrict__ dB) {
   __shared__ float at[kDbTile * RP];                     // [g - g0][k]
+  const int e = blockIdx.y;                              // expert: its rows, its A
+  dS += (size_t)e * O * G;
+  if (mask) mask += (size_t)e * O * G;
+  A += (size_t)e * r * G;
+  dB += (size_t)e * O * r;
   const int k = threadIdx.x % RP;
   const int o = blockIdx.x * (256 / RP) + threadIdx.x / RP;
   const bool active = o < O && k < r;
@@ -104,6 +118,11 @@ __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __res
                                                               const uint16_t* __restrict__ B, int O, int G, int r,
                                                               float* __restrict__ part) {
   constexpr int KW = RMAX / 4;
+  const int e = blockIdx.y;                              // expert: its rows, its partial planes
+  dS += (size_t)e * O * G;
+  if (mask) mask += (size_t)e * O * G;
+  B += (size_t)e * O * r;
+  part += (size_t)e * ((O + kDaRows - 1) / kDaRows) * r * G;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int gchunks = (G + 63) / 64;
   const int g = (int)(blockIdx.x % gchunks) * 64 + lane;
@@ -147,60 +166,70 @@ __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __res
 // dA[i] = c sum over the chunk partials: a wave per output, lane l adds the
 // chunks l, l + 64, ... in order, then a fixed butterfly across the lanes.
 __global__ __launch_bounds__(256) void qast_da_reduce_kernel(const float* __restrict__ part, int chunks, int r,
-                                                             int G, float c, float* __restrict__ dA) {
-  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+                                                             int G, int E, float c, float* __restrict__ dA) {
   const int64_t n = (int64_t)r * G;
-  if (i >= n) return;
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= (int64_t)E * n) return;
+  const int64_t e = i / n, ie = i - e * n;
+  const float* pe = part + (size_t)e * chunks * n;
   const int lane = threadIdx.x & 63;
   float s = 0.0f;
-  for (int ch = lane; ch < chunks; ch += 64) s += part[(size_t)ch * n + i];
+  for (int ch = lane; ch < chunks; ch += 64) s += pe[(size_t)ch * n + ie];
 #pragma unroll
   for (int w = 32; w >= 1; w >>= 1) s += __shfl_xor(s, w);
   if (lane == 0) dA[i] = __fmul_rn(s, c);
 }
 
 // ------------------------------------------------------------------ launch
-int qast_scales_launch(int fmt, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
-                       float c, float ws2, uint8_t* out, uint8_t* mask, hipStream_t s) {
-  const int64_t n = (int64_t)O * G;
-  const dim3 grid((unsigned)((n + 255) / 256));
+int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
+                       float c, const float* ws2, uint8_t* out, uint8_t* mask, hipStream_t s) {
   const uint16_t* b = static_cast<const uint16_t*>(B);
   const uint16_t* a = static_cast<const uint16_t*>(A);
-  if (fmt == kMX)
-    hipLaunchKernelGGL(qast_scales_kernel<kMX>, grid, dim3(256), 0, s, base, b, a, O, G, r, c, ws2, out, mask);
-  else
-    hipLaunchKernelGGL(qast_scales_kernel<kNV>, grid, dim3(256), 0, s, base, b, a, O, G, r, c, ws2, out, mask);
+  for (int e0 = 0; e0 < E; e0 += kWs2TableMax) {          // per-expert ws2 travels by value
+    const int m = E - e0 < kWs2TableMax ? E - e0 : kWs2TableMax;
+    Ws2Table t;
+    for (int e = 0; e < m; ++e) t.v[e] = fmt == kNV ? ws2[e0 + e] : 1.0f;
+    const size_t rows0 = (size_t)e0 * O;
+    const int64_t n = (int64_t)m * O * G;
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (fmt == kMX)
+      hipLaunchKernelGGL(qast_scales_kernel<kMX>, grid, dim3(256), 0, s, base + rows0 * G, b + rows0 * r,
+                         a + (size_t)e0 * r * G, m, O, G, r, c, t, out + rows0 * G, mask ? mask + rows0 * G : nullptr);
+    else
+      hipLaunchKernelGGL(qast_scales_kernel<kNV>, grid, dim3(256), 0, s, base + rows0 * G, b + rows0 * r,
+                         a + (size_t)e0 * r * G, m, O, G, r, c, t, out + rows0 * G, mask ? mask + rows0 * G : nullptr);
+  }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
-size_t qast_grads_workspace(int O, int G, int r) {
-  return (size_t)((O + kDaRows - 1) / kDaRows) * r * G * sizeof(float);
+size_t qast_grads_workspace(int E, int O, int G, int r) {
+  return (size_t)E * ((O + kDaRows - 1) / kDaRows) * r * G * sizeof(float);
 }
 
 template <int RMAX>
-static int qast_grads_r(int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
+static int qast_grads_r(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
                         const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
-  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + 256 / RMAX - 1) / (256 / RMAX))), dim3(256), 0, s,
-                     dS, mask, A, O, G, r, c, dB);
+  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + 256 / RMAX - 1) / (256 / RMAX)), (unsigned)E),
+                     dim3(256), 0, s, dS, mask, A, O, G, r, c, dB);
   const int chunks = (O + kDaRows - 1) / kDaRows;
-  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>, dim3((unsigned)(((G + 63) / 64) * (int64_t)chunks)), dim3(256), 0,
-                     s, dS, mask, B, O, G, r, part);
-  const int64_t n = (int64_t)r * G;
-  hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, part, chunks, r, G, c,
+  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>, dim3((unsigned)(((G + 63) / 64) * (int64_t)chunks), (unsigned)E),
+                     dim3(256), 0, s, dS, mask, B, O, G, r, part);
+  const int64_t n = (int64_t)E * r * G;
+  hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, part, chunks, r, G, E, c,
                      dA);
   return 0;
 }
 
-int qast_grads_launch(int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
+int qast_grads_launch(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
                       float c, float* dB, float* dA, void* workspace, hipStream_t s) {
   const uint16_t* b = static_cast<const uint16_t*>(B);
   const uint16_t* a = static_cast<const uint16_t*>(A);
   float* part = static_cast<float*>(workspace);
   int rc;
-  if (r <= 8) rc = qast_grads_r<8>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
-  else if (r <= 16) rc = qast_grads_r<16>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
-  else if (r <= 32) rc = qast_grads_r<32>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
-  else rc = qast_grads_r<64>(O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  if (r <= 8) rc = qast_grads_r<8>(E, O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  else if (r <= 16) rc = qast_grads_r<16>(E, O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  else if (r <= 32) rc = qast_grads_r<32>(E, O, G, r, dS, mask, b, a, c, dB, dA, part, s);
+  else rc = qast_grads_r<64>(E, O, G, r, dS, mask, b, a, c, dB, dA, part, s);
   if (rc != 0) return rc;
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }

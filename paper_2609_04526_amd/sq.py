@@ -104,6 +104,12 @@ def load():
         "sq_qast_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p,
                                           ctypes.c_float, ctypes.c_float, _c_p, _c_p, _c_p]),
         "sq_qast_factor_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, ctypes.c_int]),
+        "sq_qast_scales_batched": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p,
+                                                  _c_p, ctypes.c_float, _c_p, _c_p, _c_p, _c_p]),
+        "sq_qast_factor_grads_batched_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, _c_i64, ctypes.c_int]),
+        "sq_qast_factor_grads_batched": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p,
+                                                        _c_p, ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t,
+                                                        _c_p]),
         "sq_qast_factor_grads": (ctypes.c_int, [_c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p, _c_p,
                                                 ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
         "sq_scale_applied_delta": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_p, _c_p, _c_p, _c_p]),
@@ -379,6 +385,45 @@ def sq_qast_scales(fmt, base_scales, B, A, alpha_over_r, ws2=1.0, scales_out=Non
                                                    float(alpha_over_r), float(ws2), _ptr(scales_out),
                                                    _ptr(mask_out), _stream()))
     return scales_out, mask_out
+
+
+def sq_qast_scales_batched(fmt, base_scales, B, A, alpha_over_r, ws2=None, scales_out=None, mask_out=None,
+                           want_mask=True):
+    """QAST scale bytes for E stacked experts: base_scales [E, O, G], B [E, O, r],
+    A [E, r, G] (bf16); ws2: E per-expert NVFP4 scalars.  Returns (scales_out, mask)."""
+    fmt = _fmt(fmt)
+    E, O, G = base_scales.shape
+    r = B.shape[2]
+    if scales_out is None:
+        scales_out = torch.empty_like(base_scales)
+    if want_mask and mask_out is None:
+        mask_out = torch.empty_like(base_scales)
+    w = None
+    if fmt == NVFP4:
+        w = (ctypes.c_float * E)(*[float(v) for v in ws2])
+    _dev(base_scales, B, A, scales_out, mask_out)
+    _check("sq_qast_scales_batched", load().sq_qast_scales_batched(
+        fmt, E, O, G, r, _ptr(base_scales), _ptr(B), _ptr(A), float(alpha_over_r),
+        ctypes.cast(w, ctypes.c_void_p) if w is not None else None, _ptr(scales_out), _ptr(mask_out), _stream()))
+    return scales_out, mask_out
+
+
+def sq_qast_factor_grads_batched(dS, mask, B, A, alpha_over_r, dB=None, dA=None, workspace=None):
+    """dB [E, O, r], dA [E, r, G] (fp32) for E stacked experts."""
+    E, O, G = dS.shape
+    r = B.shape[2]
+    if dB is None:
+        dB = torch.empty((E, O, r), dtype=torch.float32, device=dS.device)
+    if dA is None:
+        dA = torch.empty((E, r, G), dtype=torch.float32, device=dS.device)
+    need = int(load().sq_qast_factor_grads_batched_workspace(E, O, G, r))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dS.device)
+    _dev(dS, mask, B, A, dB, dA, workspace)
+    _check("sq_qast_factor_grads_batched", load().sq_qast_factor_grads_batched(
+        E, O, G, r, _ptr(dS), _ptr(mask), _ptr(B), _ptr(A), float(alpha_over_r), _ptr(dB), _ptr(dA),
+        _ptr(workspace), workspace.numel(), _stream()))
+    return dB, dA
 
 
 def sq_qast_factor_grads_workspace(O, G, r):

@@ -160,6 +160,20 @@ def test_rtn_validation(lib):
     assert lib.rtn_quantize(0, 256, 512, None, 0.0, 0, FAKE, FAKE, None, None) == -1
 
 
+def test_qast_batched_validation(lib):
+    ws2 = (ctypes.c_float * 3)(1.0, 0.5, 0.0)
+    assert lib.sq_qast_scales_batched(0, 0, 64, 16, 8, FAKE, FAKE, FAKE, 1.0, None, FAKE, None, None) == -2
+    assert lib.sq_qast_scales_batched(0, 65536, 8, 8, 8, FAKE, FAKE, FAKE, 1.0, None, FAKE, None, None) == -2
+    assert lib.sq_qast_scales_batched(0, 4096, 4096, 256, 8, FAKE, FAKE, FAKE, 1.0, None, FAKE, None, None) == -2
+    assert lib.sq_qast_scales_batched(1, 3, 64, 16, 8, FAKE, FAKE, FAKE, 1.0, None, FAKE, None, None) == -1
+    assert lib.sq_qast_scales_batched(1, 3, 64, 16, 8, FAKE, FAKE, FAKE, 1.0, ctypes.cast(ws2, ctypes.c_void_p),
+                                      FAKE, None, None) == -1              # expert 2's ws2 is 0
+    assert lib.sq_qast_factor_grads_batched_workspace(3, 64, 16, 8) == 3 * 2 * 8 * 16 * 4
+    assert lib.sq_qast_factor_grads_batched_workspace(0, 64, 16, 8) == 0
+    assert lib.sq_qast_factor_grads_batched(3, 64, 16, 8, FAKE, None, FAKE, FAKE, 1.0, FAKE, FAKE, FAKE, 10,
+                                            None) == -5
+
+
 def test_grouped_validation(lib):
     from paper_2609_04526_amd import sq
 

@@ -184,3 +184,37 @@ def test_qast_8b_gate_projection_nv(sq):
     wB, wA = qast.factor_grads(dS, want_m, B, A, 1.0)
     assert normwise(dB.cpu().numpy(), wB) <= TOL
     assert normwise(dA.cpu().numpy(), wA) <= TOL
+
+
+@pytest.mark.parametrize("fmt,E,O,G,r", [("mx", 5, 64, 40, 8), ("nv", 3, 136, 77, 33), ("nv", 260, 8, 16, 4)])
+def test_batched_experts_match_per_expert(sq, fmt, E, O, G, r):
+    """E stacked experts in one launch sequence (260 experts: two tables of
+    per-expert ws2): scale bytes and masks equal the oracle's per expert bit
+    for bit, and the factor gradients equal the single-plane entry's bit for
+    bit (the same order per expert)."""
+    print(f"[qast batched] fmt={fmt} E={E} O={O} G={G} r={r}", flush=True)
+    bases, ws2s, Bs, As = [], [], [], []
+    for e in range(E):
+        base, ws2 = plane(fmt, O, G, 7700 + e)
+        if fmt == "nv":
+            ws2 = float(np.float32(ws2 * (1 + e % 4)))
+        B, A = factors(fmt, base, ws2, r, 7800 + e, push=2.0)
+        bases.append(base), ws2s.append(ws2), Bs.append(B), As.append(A)
+    base_d = torch.from_numpy(np.stack(bases)).cuda()
+    B_d = torch.stack(Bs).cuda()
+    A_d = torch.stack(As).cuda()
+    got, got_m = sq.sq_qast_scales_batched(fmt, base_d, B_d, A_d, 0.5, ws2s if fmt == "nv" else None)
+    g = inputs.rng(7900)
+    dS = (g.standard_normal((E, O, G)) * 1e-2).astype(np.float32)
+    dS_d = torch.from_numpy(dS).cuda()
+    dB, dA = sq.sq_qast_factor_grads_batched(dS_d, got_m, B_d, A_d, 0.25)
+    torch.cuda.synchronize()
+    gs, gm = got.cpu().numpy(), got_m.cpu().numpy()
+    for e in range(E) if E <= 8 else [0, 1, 255, 256, E - 1]:
+        want, want_m = qast.qast_scales(fmt, bases[e], Bs[e], As[e], 0.5, ws2s[e])
+        assert np.array_equal(gs[e], want) and np.array_equal(gm[e], want_m)
+        dB1, dA1 = sq.sq_qast_factor_grads(dS_d[e], got_m[e], B_d[e], A_d[e], 0.25)
+        torch.cuda.synchronize()
+        assert torch.equal(dB1, dB[e]) and torch.equal(dA1, dA[e])
+        wB, wA = qast.factor_grads(dS[e], gm[e], Bs[e], As[e], 0.25)
+        assert normwise(dB[e].cpu().numpy(), wB) <= TOL and normwise(dA[e].cpu().numpy(), wA) <= TOL
