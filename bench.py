@@ -82,6 +82,7 @@ def parse():
     p.add_argument("--no-model-merge", action="store_true")
     p.add_argument("--no-model-step", action="store_true")
     p.add_argument("--no-lifecycle", action="store_true")
+    p.add_argument("--no-moe", action="store_true")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="also run a plain device copy of this many MiB (the copy mode of "
                         "sq_merge_scales: reads N and writes N bytes) to calibrate HBM counters")
@@ -483,6 +484,116 @@ def model_step(sq, steps, warmup, comparator=True):
     return out
 
 
+def model_moe(sq, steps=3, warmup=1):
+    """One scale-only training step of a 30B-A3B-shaped MoE stack in MXFP4: 48
+    layers, each with 128 experts of gate/up [768, 2048] and down [2048, 768];
+    4096 tokens routed top-8 (32768 expert rows per layer, split over the
+    experts by a seeded Dirichlet-multinomial, the same split for every
+    layer).  Per layer and linear: one grouped forward, and in reverse order
+    one grouped dX and one grouped dS, all 128 experts in each launch.  Every
+    layer has its own expert weights; the routed activations and output
+    buffers are shared across layers (values do not change the timing).  The
+    QAST variant adds the batched rank-32 scale step of all experts per linear
+    (sq_qast_scales_batched before the forward, sq_qast_factor_grads_batched
+    after dS)."""
+    L, E, topk, Tm, r = 48, 128, 8, 4096, 32
+    g = inputs.rng(8800)
+    Ts = g.multinomial(Tm * topk, g.dirichlet(np.full(E, 2.0))).tolist()
+    shapes = (("gate", 768, 2048), ("up", 768, 2048), ("down", 2048, 768))
+    acts = {}
+    for (name, o, i) in shapes:
+        acts[name] = dict(X=[inputs.device_bf16_normal(8900 + e, (T, i)) for e, T in enumerate(Ts)],
+                          dY=[inputs.device_bf16_normal(9100 + e, (T, o)) for e, T in enumerate(Ts)],
+                          Y=[torch.empty((T, o), dtype=torch.bfloat16, device="cuda") for T in Ts],
+                          dX=[torch.empty((T, i), dtype=torch.bfloat16, device="cuda") for T in Ts],
+                          dS=[torch.empty((o, i // 32), dtype=torch.float32, device="cuda") for _ in Ts])
+    layers = []
+    for l in range(L):
+        lw = {}
+        for k, (name, o, i) in enumerate(shapes):
+            codes = inputs.device_codes_uniform(9300 + 10 * l + k, E * o, i).view(E, o, i // 2)
+            sc = inputs.device_e8m0_normal_exponents(9600 + 10 * l + k, E * o, i // 32, -6.0, 1.5).view(E, o, i // 32)
+            lw[name] = dict(codes=codes, scales=sc, cl=[codes[e] for e in range(E)], sl=[sc[e] for e in range(E)])
+        layers.append(lw)
+
+    def fwd(l, name, scales=None):
+        a, w = acts[name], layers[l][name]
+        sq.sq_fwd_grouped("mx", a["X"], w["cl"], scales if scales is not None else w["sl"], Ys=a["Y"])
+
+    def bwd(l, name, scales=None):
+        a, w = acts[name], layers[l][name]
+        sq.sq_bwd_dx_grouped("mx", a["dY"], w["cl"], scales if scales is not None else w["sl"], dXs=a["dX"])
+        sq.sq_bwd_dscale_grouped("mx", a["X"], a["dY"], w["cl"], dSs=a["dS"])
+
+    def run():
+        for l in range(L):
+            for (name, _, _) in shapes:
+                fwd(l, name)
+        for l in reversed(range(L)):
+            for (name, _, _) in reversed(shapes):
+                bwd(l, name)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    ms = timed(run)
+    rows = sum(Ts)
+    flops = 6.0 * rows * L * sum(o * i for (_, o, i) in shapes)
+    # QAST: per layer and linear, stacked factors B [E, o, r], A [E, r, G]
+    qa = {}
+    for (name, o, i) in shapes:
+        G = i // 32
+        gg = inputs.device_generator(9900 + o)
+        qa[name] = dict(B=(torch.randn((E, o, r), generator=gg, device="cuda") * 0.02).to(torch.bfloat16),
+                        A=(torch.randn((E, r, G), generator=gg, device="cuda") * 1e-3).to(torch.bfloat16),
+                        sc=torch.empty((E, o, G), dtype=torch.uint8, device="cuda"),
+                        m=torch.empty((E, o, G), dtype=torch.uint8, device="cuda"),
+                        dB=torch.empty((E, o, r), dtype=torch.float32, device="cuda"),
+                        dA=torch.empty((E, r, G), dtype=torch.float32, device="cuda"))
+        qa[name]["sl"] = [qa[name]["sc"][e] for e in range(E)]
+        qa[name]["dSall"] = torch.empty((E, o, G), dtype=torch.float32, device="cuda")
+        acts[name]["dS"] = [qa[name]["dSall"][e] for e in range(E)]
+        qa[name]["ws"] = torch.empty(max(1, int(sq.load().sq_qast_factor_grads_batched_workspace(E, o, G, r))),
+                                     dtype=torch.uint8, device="cuda")
+
+    def run_qast():
+        for l in range(L):
+            for (name, _, _) in shapes:
+                q = qa[name]
+                sq.sq_qast_scales_batched("mx", layers[l][name]["scales"], q["B"], q["A"], 1.0,
+                                          scales_out=q["sc"], mask_out=q["m"])
+                fwd(l, name, q["sl"])
+        for l in reversed(range(L)):
+            for (name, _, _) in reversed(shapes):
+                q = qa[name]
+                bwd(l, name, q["sl"])
+                sq.sq_qast_factor_grads_batched(q["dSall"], q["m"], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"],
+                                                workspace=q["ws"])
+
+    qast_ms = timed(run_qast)
+    out = {"workload": "MXFP4 30B-A3B-shaped MoE stack: 48 layers x 128 experts x {gate, up [768, 2048], "
+                       "down [2048, 768]}, 4096 tokens top-8 (32768 routed rows per layer): grouped fwd + dX + dS",
+           "expert_rows": {"min": int(min(Ts)), "max": int(max(Ts)), "mean": round(rows / E, 1)},
+           "ms": round(ms, 3), "TFLOP": round(flops / 1e12, 2),
+           "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+           "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "qast_step": {"ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
+                         "note": "batched rank-32 QAST scale step of all experts per linear; the paper reports "
+                                 "QAST within noise of its no-STE baseline on its MoE (context only)"}}
+    del layers, acts, qa
+    torch.cuda.empty_cache()
+    return out
+
+
 def dequant_torch(codes, scales):
     """bf16 W from an MXFP4 code plane with torch ops (the comparator's fake-quant
     read-back; the scale-only path never forms W in HBM)."""
@@ -700,6 +811,9 @@ def main():
         out["merge_8b"] = model_merge(sq, 20)
     if not args.no_model_step:
         out["step_8b"] = model_step(sq, 3, 1)
+        torch.cuda.empty_cache()
+    if not args.no_moe:
+        out["moe_30b_a3b"] = model_moe(sq)
         torch.cuda.empty_cache()
     if not args.no_lifecycle:
         out["lifecycle_8b"] = model_lifecycle(sq)

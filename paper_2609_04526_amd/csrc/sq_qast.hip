@@ -17,7 +17,9 @@
 // exactly like a separate multiply and add, and the scale bytes are fixed bit
 // for bit.  The factor gradients accumulate in fp32 in a fixed order (dB: over
 // the blocks in order; dA: rows in order within 32-row chunks, then the chunk
-// partials through a fixed per-lane order and butterfly): deterministic.
+// partials through a fixed per-lane order and butterfly): deterministic.  The
+// backward kernels stage 32-row x 64-block tiles of dS * m in LDS with all of
+// a tile's loads in flight together.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,144 +32,200 @@ namespace sq {
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 // ------------------------------------------------------------------ scales
-// One thread per scale (o, g), consecutive threads along g: the A reads are
-// coalesced and a row's B entries are shared by its threads.
+// A workgroup per tile of 32 rows x 32 blocks of one expert (blockIdx.y): the
+// tile's A columns [RMAX][32] and B rows [32][RMAX] are staged in LDS as fp32
+// (every load issued together; ranks past r are 0 and add exact zeros), and
+// thread (g, row group) adds the r terms of its four rows in increasing k.
 // Experts are stacked: rows e*O .. e*O + O - 1 of base, B, out and mask
 // belong to expert e, whose A is A + e*r*G and whose ws2 is ws2[e].
-template <int FMT>
+constexpr int kScRows = 32;
+constexpr int kScCols = 32;
+
+template <int FMT, int RMAX>
 __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restrict__ base,
                                                           const uint16_t* __restrict__ B,
-                                                          const uint16_t* __restrict__ A, int E, int O, int G, int r,
+                                                          const uint16_t* __restrict__ A, int O, int G, int r,
                                                           float c, Ws2Table ws2, uint8_t* out, uint8_t* mask) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)E * O * G) return;
-  const int64_t row = idx / G;
-  const int g = (int)(idx - row * G);
-  const int e = (int)(row / O);
-  const uint16_t* brow = B + (size_t)row * r;
+  __shared__ float at[RMAX][kScCols + 1];
+  __shared__ float bt[kScRows][RMAX + 1];
+  const int e = blockIdx.y;
+  const size_t rows0 = (size_t)e * O;
   const uint16_t* ae = A + (size_t)e * r * G;
-  float acc = 0.0f;
-  for (int k = 0; k < r; ++k)
-    acc = __builtin_fmaf(bf16_bits_to_f32(brow[k]), bf16_bits_to_f32(ae[(size_t)k * G + g]), acc);
-  bool clamped;
-  const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc, c), ws2.v[e], clamped);
-  out[idx] = (uint8_t)nb;
-  if (mask) mask[idx] = clamped ? 0 : 1;
+  const int gtiles = (G + kScCols - 1) / kScCols;
+  const int o0 = ((int)blockIdx.x / gtiles) * kScRows, g0 = ((int)blockIdx.x % gtiles) * kScCols;
+#pragma unroll
+  for (int u = 0; u < RMAX * kScCols / 256; ++u) {
+    const int i = threadIdx.x + 256 * u, k = i / kScCols, gi = i % kScCols;
+    at[k][gi] = (k < r && g0 + gi < G) ? bf16_bits_to_f32(ae[(size_t)k * G + g0 + gi]) : 0.0f;
+  }
+#pragma unroll
+  for (int u = 0; u < kScRows * RMAX / 256; ++u) {
+    const int i = threadIdx.x + 256 * u, ro = i / RMAX, k = i % RMAX;
+    bt[ro][k] = (k < r && o0 + ro < O) ? bf16_bits_to_f32(B[(rows0 + o0 + ro) * r + k]) : 0.0f;
+  }
+  __syncthreads();
+  const int gi = threadIdx.x % kScCols, rq = (threadIdx.x / kScCols) * 4;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int k = 0; k < RMAX; ++k) {
+    const float a = at[k][gi];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[q] = __builtin_fmaf(bt[rq + q][k], a, acc[q]);
+  }
+  const int g = g0 + gi;
+  if (g >= G) return;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int o = o0 + rq + q;
+    if (o >= O) break;
+    const size_t idx = (rows0 + o) * G + g;
+    bool clamped;
+    const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc[q], c), ws2.v[e], clamped);
+    out[idx] = (uint8_t)nb;
+    if (mask) mask[idx] = clamped ? 0 : 1;
+  }
 }
 
-// ------------------------------------------------------------------ dB
-// A thread per (o, k): dB[o,k] = c sum_g v[o,g] A[k,g] over g in order, with
-// A staged transposed in LDS ([g][k], consecutive k in consecutive lanes) in
-// tiles of kDbTile blocks.  RP lanes per row (RP >= r, a power of two),
-// 256 / RP rows per workgroup.
-constexpr int kDbTile = 256;
-template <int RP>
+// ------------------------------------------------------------------ dB, dA
+// Both backward products stage tiles of v = dS * m (32 rows x 64 blocks, fp32)
+// in LDS with every load of the tile issued together, plus the matching
+// factor tile.  blockIdx.y is the expert (its rows, its A).
+constexpr int kQRows = 32;          // rows per tile
+constexpr int kQCols = 64;          // blocks per tile
+constexpr int kDaRows = kQRows;
+
+__device__ __forceinline__ void stage_v(float (&vt)[kQRows][kQCols + 1], const float* __restrict__ dS,
+                                        const uint8_t* __restrict__ mask, int O, int G, int o0, int g0) {
+#pragma unroll
+  for (int u = 0; u < kQRows * kQCols / 256; ++u) {
+    const int i = threadIdx.x + 256 * u, ro = i / kQCols, gi = i % kQCols;
+    const int o = o0 + ro, g = g0 + gi;
+    float v = 0.0f;
+    if (o < O && g < G) {
+      const size_t at = (size_t)o * G + g;
+      v = dS[at];
+      if (mask) v *= (float)mask[at];
+    }
+    vt[ro][gi] = v;
+  }
+}
+
+// dB[o, k] = c sum over g in increasing order of v[o, g] A[k, g]: a workgroup
+// owns 32 rows and walks the blocks in tiles of 64; thread (k, row group)
+// accumulates 32 / (256 / RMAX) rows of one rank.
+template <int RMAX>
 __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ dS, const uint8_t* __restrict__ mask,
                                                       const uint16_t* __restrict__ A, int O, int G, int r, float c,
                                                       float* __restrict__ dB) {
-  __shared__ float at[kDbTile * RP];                     // [g - g0][k]
-  const int e = blockIdx.y;                              // expert: its rows, its A
+  constexpr int kGroups = 256 / RMAX, kRowsPer = kQRows / kGroups;
+  __shared__ float vt[kQRows][kQCols + 1];
+  __shared__ float at[RMAX][kQCols + 1];
+  const int e = blockIdx.y;
   dS += (size_t)e * O * G;
   if (mask) mask += (size_t)e * O * G;
   A += (size_t)e * r * G;
   dB += (size_t)e * O * r;
-  const int k = threadIdx.x % RP;
-  const int o = blockIdx.x * (256 / RP) + threadIdx.x / RP;
-  const bool active = o < O && k < r;
-  const float* vrow = dS + (size_t)(active ? o : 0) * G;
-  const uint8_t* mrow = mask ? mask + (size_t)(active ? o : 0) * G : nullptr;
-  float acc = 0.0f;
-  for (int g0 = 0; g0 < G; g0 += kDbTile) {
-    const int gn = min(kDbTile, G - g0);
-    __syncthreads();                                     // the previous tile is consumed
-    for (int i = threadIdx.x; i < gn * RP; i += 256) {
-      const int gi = i / RP, kk = i - gi * RP;
-      at[i] = kk < r ? bf16_bits_to_f32(A[(size_t)kk * G + g0 + gi]) : 0.0f;
+  const int o0 = blockIdx.x * kQRows;
+  const int k = threadIdx.x % RMAX, grp = threadIdx.x / RMAX;
+  float acc[kRowsPer];
+#pragma unroll
+  for (int q = 0; q < kRowsPer; ++q) acc[q] = 0.0f;
+  for (int g0 = 0; g0 < G; g0 += kQCols) {
+    __syncthreads();                                     // the previous tiles are consumed
+    stage_v(vt, dS, mask, O, G, o0, g0);
+#pragma unroll
+    for (int u = 0; u < RMAX * kQCols / 256; ++u) {
+      const int i = threadIdx.x + 256 * u, kk = i / kQCols, gi = i % kQCols;
+      at[kk][gi] = (kk < r && g0 + gi < G) ? bf16_bits_to_f32(A[(size_t)kk * G + g0 + gi]) : 0.0f;
     }
     __syncthreads();
-    if (active) {
-      int gi = 0;
-      for (; gi + 8 <= gn; gi += 8) {                    // 8 loads in flight, then 8 FMAs in order
-        float v[8];
+    const int gn = min(kQCols, G - g0);
+    for (int gi = 0; gi < gn; ++gi) {
+      const float a = at[k][gi];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = vrow[g0 + gi + j];
-        if (mrow) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] *= (float)mrow[g0 + gi + j];
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc = __builtin_fmaf(v[j], at[(gi + j) * RP + k], acc);
-      }
-      for (; gi < gn; ++gi) {
-        const int g = g0 + gi;
-        const float v = mrow ? vrow[g] * (float)mrow[g] : vrow[g];
-        acc = __builtin_fmaf(v, at[gi * RP + k], acc);
-      }
+      for (int q = 0; q < kRowsPer; ++q) acc[q] = __builtin_fmaf(vt[grp * kRowsPer + q][gi], a, acc[q]);
     }
   }
-  if (active) dB[(size_t)o * r + k] = __fmul_rn(acc, c);
+  if (k >= r) return;
+#pragma unroll
+  for (int q = 0; q < kRowsPer; ++q) {
+    const int o = o0 + grp * kRowsPer + q;
+    if (o < O) dB[(size_t)o * r + k] = __fmul_rn(acc[q], c);
+  }
 }
 
-// ------------------------------------------------------------------ dA
-// Partial dA over a chunk of kDaRows rows, rows in order: lanes along g, the
-// four waves of a workgroup each own a quarter of the ranks (RMAX / 4).
-constexpr int kDaRows = 32;
+// Partial dA over one 32-row chunk and 64 blocks: part[chunk][k][g] = sum
+// over the chunk's rows in increasing order of B[o, k] v[o, g]; thread
+// (g, rank group) accumulates RMAX / 4 ranks of one block.
 template <int RMAX>
 __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __restrict__ dS,
                                                               const uint8_t* __restrict__ mask,
                                                               const uint16_t* __restrict__ B, int O, int G, int r,
                                                               float* __restrict__ part) {
   constexpr int KW = RMAX / 4;
-  const int e = blockIdx.y;                              // expert: its rows, its partial planes
+  __shared__ float vt[kQRows][kQCols + 1];
+  __shared__ float bt[kQRows][RMAX + 1];
+  const int e = blockIdx.y;
+  const int chunks = (O + kQRows - 1) / kQRows;
   dS += (size_t)e * O * G;
   if (mask) mask += (size_t)e * O * G;
   B += (size_t)e * O * r;
-  part += (size_t)e * ((O + kDaRows - 1) / kDaRows) * r * G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int gchunks = (G + 63) / 64;
-  const int g = (int)(blockIdx.x % gchunks) * 64 + lane;
-  const int chunk = (int)(blockIdx.x / gchunks);
-  const int k0 = wave * KW;
-  if (g >= G || k0 >= r) return;
+  part += (size_t)e * chunks * r * G;
+  const int gtiles = (G + kQCols - 1) / kQCols;
+  const int chunk = (int)blockIdx.x / gtiles, g0 = ((int)blockIdx.x % gtiles) * kQCols;
+  const int o0 = chunk * kQRows;
+  stage_v(vt, dS, mask, O, G, o0, g0);
+#pragma unroll
+  for (int u = 0; u < (kQRows * RMAX + 255) / 256; ++u) {
+    const int i = threadIdx.x + 256 * u;
+    if (i < kQRows * RMAX) {
+      const int ro = i / RMAX, kk = i % RMAX;
+      bt[ro][kk] = (kk < r && o0 + ro < O) ? bf16_bits_to_f32(B[(size_t)(o0 + ro) * r + kk]) : 0.0f;
+    }
+  }
+  __syncthreads();
+  const int gi = threadIdx.x % kQCols, k0 = (threadIdx.x / kQCols) * KW;
   float acc[KW];
 #pragma unroll
   for (int j = 0; j < KW; ++j) acc[j] = 0.0f;
-  const int o_end = min((chunk + 1) * kDaRows, O);
-  int o = chunk * kDaRows;
-  for (; o + 8 <= o_end; o += 8) {                       // 8 rows of loads in flight, rows added in order
-    float v[8];
+  const int on = min(kQRows, O - o0);
+  for (int ro = 0; ro < on; ++ro) {
+    const float v = vt[ro][gi];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = dS[(size_t)(o + u) * G + g];
-    if (mask) {
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] *= (float)mask[(size_t)(o + u) * G + g];
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint16_t* brow = B + (size_t)(o + u) * r + k0;
-#pragma unroll
-      for (int j = 0; j < KW; ++j)
-        if (k0 + j < r) acc[j] = __builtin_fmaf(bf16_bits_to_f32(brow[j]), v[u], acc[j]);
-    }
+    for (int j = 0; j < KW; ++j) acc[j] = __builtin_fmaf(bt[ro][k0 + j], v, acc[j]);
   }
-  for (; o < o_end; ++o) {
-    const size_t at = (size_t)o * G + g;
-    const float v = mask ? dS[at] * (float)mask[at] : dS[at];
-    const uint16_t* brow = B + (size_t)o * r + k0;
-#pragma unroll
-    for (int j = 0; j < KW; ++j)
-      if (k0 + j < r) acc[j] = __builtin_fmaf(bf16_bits_to_f32(brow[j]), v, acc[j]);
-  }
+  if (g0 + gi >= G) return;
 #pragma unroll
   for (int j = 0; j < KW; ++j)
-    if (k0 + j < r) part[((size_t)chunk * r + k0 + j) * G + g] = acc[j];
+    if (k0 + j < r) part[((size_t)chunk * r + k0 + j) * G + g0 + gi] = acc[j];
 }
 
-// dA[i] = c sum over the chunk partials: a wave per output, lane l adds the
-// chunks l, l + 64, ... in order, then a fixed butterfly across the lanes.
+// dA[i] = c sum over the chunk partials.  Up to 64 chunks: a thread per
+// output adds the chunks in order (loads eight at a time); more: a wave per
+// output, lane l adds the chunks l, l + 64, ... in order, then a fixed
+// butterfly across the lanes.  Either order depends only on the shape.
+constexpr int kDaFewChunks = 64;
 __global__ __launch_bounds__(256) void qast_da_reduce_kernel(const float* __restrict__ part, int chunks, int r,
                                                              int G, int E, float c, float* __restrict__ dA) {
   const int64_t n = (int64_t)r * G;
+  if (chunks <= kDaFewChunks) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)E * n) return;
+    const int64_t e = i / n, ie = i - e * n;
+    const float* pe = part + (size_t)e * chunks * n + ie;
+    float s = 0.0f;
+    int ch = 0;
+    for (; ch + 8 <= chunks; ch += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = pe[(size_t)(ch + u) * n];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; ch < chunks; ++ch) s += pe[(size_t)ch * n];
+    dA[i] = __fmul_rn(s, c);
+    return;
+  }
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= (int64_t)E * n) return;
   const int64_t e = i / n, ie = i - e * n;
@@ -190,14 +248,27 @@ int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base,
     Ws2Table t;
     for (int e = 0; e < m; ++e) t.v[e] = fmt == kNV ? ws2[e0 + e] : 1.0f;
     const size_t rows0 = (size_t)e0 * O;
-    const int64_t n = (int64_t)m * O * G;
-    const dim3 grid((unsigned)((n + 255) / 256));
-    if (fmt == kMX)
-      hipLaunchKernelGGL(qast_scales_kernel<kMX>, grid, dim3(256), 0, s, base + rows0 * G, b + rows0 * r,
-                         a + (size_t)e0 * r * G, m, O, G, r, c, t, out + rows0 * G, mask ? mask + rows0 * G : nullptr);
-    else
-      hipLaunchKernelGGL(qast_scales_kernel<kNV>, grid, dim3(256), 0, s, base + rows0 * G, b + rows0 * r,
-                         a + (size_t)e0 * r * G, m, O, G, r, c, t, out + rows0 * G, mask ? mask + rows0 * G : nullptr);
+    const dim3 grid((unsigned)(((O + kScRows - 1) / kScRows) * (int64_t)((G + kScCols - 1) / kScCols)),
+                    (unsigned)m);
+    const uint8_t* bp = base + rows0 * G;
+    const uint16_t* Bp = b + rows0 * r;
+    const uint16_t* Ap = a + (size_t)e0 * r * G;
+    uint8_t* op = out + rows0 * G;
+    uint8_t* mp = mask ? mask + rows0 * G : nullptr;
+#define SQ_QAST_SCALES(F, R) \
+    hipLaunchKernelGGL((qast_scales_kernel<F, R>), grid, dim3(256), 0, s, bp, Bp, Ap, O, G, r, c, t, op, mp)
+    if (fmt == kMX) {
+      if (r <= 8) SQ_QAST_SCALES(kMX, 8);
+      else if (r <= 16) SQ_QAST_SCALES(kMX, 16);
+      else if (r <= 32) SQ_QAST_SCALES(kMX, 32);
+      else SQ_QAST_SCALES(kMX, 64);
+    } else {
+      if (r <= 8) SQ_QAST_SCALES(kNV, 8);
+      else if (r <= 16) SQ_QAST_SCALES(kNV, 16);
+      else if (r <= 32) SQ_QAST_SCALES(kNV, 32);
+      else SQ_QAST_SCALES(kNV, 64);
+    }
+#undef SQ_QAST_SCALES
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
@@ -209,14 +280,15 @@ size_t qast_grads_workspace(int E, int O, int G, int r) {
 template <int RMAX>
 static int qast_grads_r(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
                         const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
-  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + 256 / RMAX - 1) / (256 / RMAX)), (unsigned)E),
-                     dim3(256), 0, s, dS, mask, A, O, G, r, c, dB);
-  const int chunks = (O + kDaRows - 1) / kDaRows;
-  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>, dim3((unsigned)(((G + 63) / 64) * (int64_t)chunks), (unsigned)E),
-                     dim3(256), 0, s, dS, mask, B, O, G, r, part);
+  const int chunks = (O + kQRows - 1) / kQRows;
+  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)chunks, (unsigned)E), dim3(256), 0, s, dS, mask, A, O, G, r,
+                     c, dB);
+  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>,
+                     dim3((unsigned)(((G + kQCols - 1) / kQCols) * (int64_t)chunks), (unsigned)E), dim3(256), 0, s,
+                     dS, mask, B, O, G, r, part);
   const int64_t n = (int64_t)E * r * G;
-  hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, part, chunks, r, G, E, c,
-                     dA);
+  const int64_t rblocks = chunks <= kDaFewChunks ? (n + 255) / 256 : (n + 3) / 4;
+  hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, part, chunks, r, G, E, c, dA);
   return 0;
 }
 
