@@ -83,7 +83,19 @@ __global__ __launch_bounds__(256) void byte_diff_kernel(const uint8_t* __restric
   __shared__ uint32_t red[2][4];
   uint32_t nb = 0, nn = 0;
   const int64_t stride = (int64_t)gridDim.x * 4096;
-  for (int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16; i < n; i += stride) {
+  int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16;
+  for (; i + 3 * stride + 16 <= n; i += 4 * stride) {      // four 16-byte pairs in flight
+    u32x4a_t x[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      x[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4a_t*>(a + i + u * stride)) ^
+             __builtin_nontemporal_load(reinterpret_cast<const u32x4a_t*>(b + i + u * stride));
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) diff_word(x[u][k], nb, nn);
+  }
+  for (; i < n; i += stride) {
     if (i + 16 <= n) {
       const u32x4a_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4a_t*>(a + i)) ^
                          __builtin_nontemporal_load(reinterpret_cast<const u32x4a_t*>(b + i));
