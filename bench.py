@@ -528,22 +528,23 @@ def model_moe(sq, steps=3, warmup=1):
             lw[name] = dict(codes=codes, scales=sc, cl=[codes[e] for e in range(E)], sl=[sc[e] for e in range(E)])
         layers.append(lw)
 
-    def fwd(l, name, scales=None):
-        a, w = acts[name], layers[l][name]
-        sq.sq_fwd_grouped("mx", a["X"], w["cl"], scales if scales is not None else w["sl"], Ys=a["Y"])
-
-    def bwd(l, name, scales=None):
-        a, w = acts[name], layers[l][name]
-        sq.sq_bwd_dx_grouped("mx", a["dY"], w["cl"], scales if scales is not None else w["sl"], dXs=a["dX"])
-        sq.sq_bwd_dscale_grouped("mx", a["X"], a["dY"], w["cl"], dSs=a["dS"])
+    # the expert descriptor tables are built once, as a training loop would
+    tables = {}
+    for l in range(L):
+        for (name, _, _) in shapes:
+            a, w = acts[name], layers[l][name]
+            tables[(l, name)] = (sq.ExpertTable("fwd", "mx", a["X"], w["cl"], w["sl"], a["Y"]),
+                                 sq.ExpertTable("dx", "mx", a["dY"], w["cl"], w["sl"], a["dX"]),
+                                 sq.ExpertTable("ds", "mx", a["X"], w["cl"], None, a["dS"], acts2=a["dY"]))
 
     def run():
         for l in range(L):
             for (name, _, _) in shapes:
-                fwd(l, name)
+                tables[(l, name)][0].run()
         for l in reversed(range(L)):
             for (name, _, _) in reversed(shapes):
-                bwd(l, name)
+                tables[(l, name)][1].run()
+                tables[(l, name)][2].run()
 
     def timed(fn):
         for _ in range(warmup):
@@ -573,9 +574,17 @@ def model_moe(sq, steps=3, warmup=1):
                         dA=torch.empty((E, r, G), dtype=torch.float32, device="cuda"))
         qa[name]["sl"] = [qa[name]["sc"][e] for e in range(E)]
         qa[name]["dSall"] = torch.empty((E, o, G), dtype=torch.float32, device="cuda")
-        acts[name]["dS"] = [qa[name]["dSall"][e] for e in range(E)]
+        qa[name]["dSl"] = [qa[name]["dSall"][e] for e in range(E)]
         qa[name]["ws"] = torch.empty(max(1, int(sq.load().sq_qast_factor_grads_batched_workspace(E, o, G, r))),
                                      dtype=torch.uint8, device="cuda")
+
+    qtables = {}
+    for l in range(L):
+        for (name, _, _) in shapes:
+            a, w, q = acts[name], layers[l][name], qa[name]
+            qtables[(l, name)] = (sq.ExpertTable("fwd", "mx", a["X"], w["cl"], q["sl"], a["Y"]),
+                                  sq.ExpertTable("dx", "mx", a["dY"], w["cl"], q["sl"], a["dX"]),
+                                  sq.ExpertTable("ds", "mx", a["X"], w["cl"], None, q["dSl"], acts2=a["dY"]))
 
     def run_qast():
         for l in range(L):
@@ -583,11 +592,12 @@ def model_moe(sq, steps=3, warmup=1):
                 q = qa[name]
                 sq.sq_qast_scales_batched("mx", layers[l][name]["scales"], q["B"], q["A"], 1.0,
                                           scales_out=q["sc"], mask_out=q["m"])
-                fwd(l, name, q["sl"])
+                qtables[(l, name)][0].run()
         for l in reversed(range(L)):
             for (name, _, _) in reversed(shapes):
                 q = qa[name]
-                bwd(l, name, q["sl"])
+                qtables[(l, name)][1].run()
+                qtables[(l, name)][2].run()
                 sq.sq_qast_factor_grads_batched(q["dSall"], q["m"], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"],
                                                 workspace=q["ws"])
 
@@ -601,7 +611,7 @@ def model_moe(sq, steps=3, warmup=1):
            "qast_step": {"ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
                          "note": "batched rank-32 QAST scale step of all experts per linear; the paper reports "
                                  "QAST within noise of its no-STE baseline on its MoE (context only)"}}
-    del layers, acts, qa
+    del layers, acts, qa, tables, qtables
     torch.cuda.empty_cache()
     return out
 

@@ -252,42 +252,56 @@ def _expert_table(acts, acts2, codes, scales, outs, ws2):
 _DTYPE_CODE = {torch.float32: OUT_F32, torch.bfloat16: OUT_BF16}
 
 
+class ExpertTable:
+    """A prebuilt sq_expert_desc table for repeated grouped calls on the same
+    tensors (building the table is host work that a training loop need not
+    repeat).  Holds references to every tensor it points at."""
+
+    def __init__(self, kind, fmt, acts, codes, scales=None, outs=None, acts2=None, ws2=None,
+                 out_dtype=torch.float32):
+        self.kind, self.fmt = kind, _fmt(fmt)
+        self.O, self.I = codes[0].shape[0], codes[0].shape[1] * 2
+        dev = codes[0].device
+        if outs is None:
+            if kind == "fwd":
+                outs = [torch.empty((x.shape[0], self.O), dtype=out_dtype, device=dev) for x in acts]
+            elif kind == "dx":
+                outs = [torch.empty((d.shape[0], self.I), dtype=out_dtype, device=dev) for d in acts]
+            else:
+                outs = [torch.empty((self.O, self.I // BLOCK[self.fmt]), dtype=torch.float32, device=dev)
+                        for _ in codes]
+        _dev(*acts, *codes, *(scales or []), *outs, *(acts2 or []))
+        self.refs = (acts, codes, scales, outs, acts2)
+        self.outs = outs
+        self.n = len(codes)
+        self.arr = _expert_table(acts, acts2, codes, scales, outs, ws2)
+        self.dtype = _DTYPE_CODE[outs[0].dtype] if (outs and kind != "ds") else OUT_F32
+
+    def run(self):
+        lib = load()
+        if self.kind == "fwd":
+            st = lib.sq_fwd_grouped(self.fmt, self.O, self.I, self.n, self.arr, self.dtype, _stream())
+        elif self.kind == "dx":
+            st = lib.sq_bwd_dx_grouped(self.fmt, self.O, self.I, self.n, self.arr, self.dtype, _stream())
+        else:
+            st = lib.sq_bwd_dscale_grouped(self.fmt, self.O, self.I, self.n, self.arr, _stream())
+        _check(f"sq_{self.kind}_grouped", st)
+        return self.outs
+
+
 def sq_fwd_grouped(fmt, Xs, codes, scales, ws2=None, out_dtype=torch.float32, Ys=None):
     """Per-expert Y_e = X_e W_e^T in one grouped launch; Xs[e] bf16 [T_e, I]."""
-    fmt = _fmt(fmt)
-    O, I = codes[0].shape[0], codes[0].shape[1] * 2
-    if Ys is None:
-        Ys = [torch.empty((x.shape[0], O), dtype=out_dtype, device=codes[0].device) for x in Xs]
-    _dev(*Xs, *codes, *scales, *Ys)
-    arr = _expert_table(Xs, None, codes, scales, Ys, ws2)
-    _check("sq_fwd_grouped", load().sq_fwd_grouped(fmt, O, I, len(codes), arr, _DTYPE_CODE[Ys[0].dtype] if Ys
-                                                   else OUT_F32, _stream()))
-    return Ys
+    return ExpertTable("fwd", fmt, Xs, codes, scales, Ys, None, ws2, out_dtype).run()
 
 
 def sq_bwd_dx_grouped(fmt, dYs, codes, scales, ws2=None, out_dtype=torch.float32, dXs=None):
     """Per-expert dX_e = dY_e W_e in one grouped launch; dYs[e] bf16 [T_e, O]."""
-    fmt = _fmt(fmt)
-    O, I = codes[0].shape[0], codes[0].shape[1] * 2
-    if dXs is None:
-        dXs = [torch.empty((d.shape[0], I), dtype=out_dtype, device=codes[0].device) for d in dYs]
-    _dev(*dYs, *codes, *scales, *dXs)
-    arr = _expert_table(dYs, None, codes, scales, dXs, ws2)
-    _check("sq_bwd_dx_grouped", load().sq_bwd_dx_grouped(fmt, O, I, len(codes), arr, _DTYPE_CODE[dXs[0].dtype]
-                                                         if dXs else OUT_F32, _stream()))
-    return dXs
+    return ExpertTable("dx", fmt, dYs, codes, scales, dXs, None, ws2, out_dtype).run()
 
 
 def sq_bwd_dscale_grouped(fmt, Xs, dYs, codes, dSs=None):
     """Per-expert dS_e (fp32 [O, G]) in one grouped launch."""
-    fmt = _fmt(fmt)
-    O, I = codes[0].shape[0], codes[0].shape[1] * 2
-    if dSs is None:
-        dSs = [torch.empty((O, I // BLOCK[fmt]), dtype=torch.float32, device=codes[0].device) for _ in codes]
-    _dev(*Xs, *dYs, *codes, *dSs)
-    arr = _expert_table(Xs, dYs, codes, None, dSs, None)
-    _check("sq_bwd_dscale_grouped", load().sq_bwd_dscale_grouped(fmt, O, I, len(codes), arr, _stream()))
-    return dSs
+    return ExpertTable("ds", fmt, Xs, codes, None, dSs, dYs).run()
 
 
 def rtn_quantize(fmt, W, tie=TIE_EVEN, ws2_in=0.0, codes=None, scales=None, ws2_out=None):
