@@ -46,9 +46,14 @@
 
 namespace sq {
 
-// The three products (kFwdR: the forward, with W dequantised once per
-// workgroup into a bf16 K-contiguous LDS tile).
-enum Mode { kDx = 1, kDs = 2, kFwdR = 3 };
+// The three products.  Two forms of the forward:
+//   kFwdR  W dequantised once per workgroup into a bf16 K-contiguous LDS tile;
+//   kFwdC  (MXFP4) the packed codes are copied to LDS as they are and every
+//          wave dequantises its own MFMA operand in registers: one
+//          v_cvt_scalef32_pk_bf16_fp4 per code byte, with the E8M0 scale byte
+//          as the convert's scale operand.  LDS carries 4 bits per weight
+//          instead of 16, and no bf16 W tile is written.
+enum Mode { kDx = 1, kDs = 2, kFwdR = 3, kFwdC = 4 };
 
 constexpr int kBK = 64;                 // K per LDS stage
 constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-robin to 8 XCDs
@@ -227,11 +232,48 @@ struct DmaNat {
   }
 };
 
+// Code tile (kFwdC): rows [r0, r0+R) of the packed [O, I/2] code plane, the 32
+// bytes (64 codes) of one K stage per row, stored row after row, 16-byte half
+// h of row r at half h ^ swz_codes(r): the 16 (or 8) lanes a ds_read_b128
+// serves together read 16 consecutive rows at one logical half and so land
+// in 16 distinct 16-byte bank slots.  One wave instruction fills 32 rows
+// (lane l: row l/2, stored half l%2).  Rows past O read zeros from the buffer
+// bound; a half past I is masked on the last stage.
+__device__ __forceinline__ int swz_codes(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
+template <int R, int NT>
+struct DmaCodes {
+  static constexpr int kInst = R * 2 / NT;
+  static_assert(kInst * NT == R * 2, "code rows must split over the waves");
+  uint32_t off[kInst];
+  int klim[kInst];
+  __device__ __forceinline__ void init(int I, int O, int r0, int tid) {
+    const int wave = tid >> 6, lane = tid & 63;
+#pragma unroll
+    for (int q = 0; q < kInst; ++q) {
+      const int r = (q * (NT / 64) + wave) * 32 + (lane >> 1);
+      const int h = (lane & 1) ^ swz_codes(r);
+      const int gr = r0 + r;
+      off[q] = gr < O ? (uint32_t)gr * (uint32_t)(I >> 1) + 16u * (uint32_t)h : kOOB;
+      klim[q] = I - 32 * h;
+    }
+  }
+  template <int Q0, int Q1>
+  __device__ __forceinline__ void issue_part(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint8_t* s, int k0, int wave) const {
+#pragma unroll
+    for (int q = Q0; q < Q1; ++q) {
+      const int blk = q * (NT / 64) + wave;
+      const uint32_t o = (off[q] == kOOB || k0 >= klim[q]) ? kOOB : off[q] + (uint32_t)(k0 >> 1);
+      dma16(rs, s + blk * 1024, o);
+    }
+  }
+};
+
 // 16-byte DMA loads each thread issues per stage (only the mode's own
 // operand layouts are instantiated)
 template <int MODE, int BM, int BN, int NT, int BK>
 __host__ __device__ constexpr int dma_count() {
   if constexpr (MODE == kDx || MODE == kFwdR) return DmaKC<BM, NT>::kInst;
+  else if constexpr (MODE == kFwdC) return DmaKC<BM, NT>::kInst + DmaCodes<BN, NT>::kInst;
   else return DmaNat<BM, NT, BK>::kInst + DmaNat<BN, NT, BK>::kInst;
 }
 
@@ -259,9 +301,14 @@ struct SmemLayout {
   static constexpr int kA = BM * BK * 2;                                      // bytes per A stage
   static constexpr int kB = BK * BN * 2;                                      // bytes per B stage
   static constexpr bool kWReg = MODE == kDx || MODE == kFwdR;                 // W staged through registers
-  static constexpr int kStage = kA + (kWReg ? 0 : kB);                        // DMA bytes per stage
+  static constexpr int kCodes = MODE == kFwdC ? BN * (BK / 2) : 0;            // packed codes per stage
+  static constexpr int kStage = kA + (kWReg || MODE == kFwdC ? 0 : kB) + kCodes;   // DMA bytes per stage
   static constexpr int kWBytes = kWReg ? 2 * kB : 0;                          // bf16 W double buffer
-  static constexpr int kBytes = STAGES * kStage + kWBytes;
+  // kFwdC has no W buffer: its stage arrays are sized to also hold the bf16
+  // output staging of every wave (BM x BN bf16 over the stages)
+  static constexpr int kEpiPer = (BM * BN * 2 + STAGES - 1) / STAGES;
+  static constexpr int kStageAlloc = MODE == kFwdC && kEpiPer > kStage ? kEpiPer : kStage;
+  static constexpr int kBytes = STAGES * kStageAlloc + kWBytes;
 };
 
 // ------------------------------------------------------------------ output
@@ -368,16 +415,16 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   constexpr int kDma = dma_count<MODE, BM, BN, NT, BK>();   // DMA loads per thread per stage
   // One static array per DMA stage (distinct objects, so the compiler can see
   // that a stage being filled does not alias the stage being read).
-  __shared__ __attribute__((aligned(16))) uint8_t lds0[L::kStage];
-  __shared__ __attribute__((aligned(16))) uint8_t lds1[L::kStage];
-  __shared__ __attribute__((aligned(16))) uint8_t lds2[STAGES > 2 ? L::kStage : 16];
-  __shared__ __attribute__((aligned(16))) uint8_t lds3[STAGES > 3 ? L::kStage : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t lds0[L::kStageAlloc];
+  __shared__ __attribute__((aligned(16))) uint8_t lds1[L::kStageAlloc];
+  __shared__ __attribute__((aligned(16))) uint8_t lds2[STAGES > 2 ? L::kStageAlloc : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t lds3[STAGES > 3 ? L::kStageAlloc : 16];
   __shared__ __attribute__((aligned(16))) uint8_t ldsw[kWReg ? L::kWBytes : 16];
   static_assert(STAGES >= 2 && STAGES <= 4, "2 to 4 stages");
   // The bf16 output staging reuses the operand LDS: one WM x WN bf16 region
   // per wave, taken from the stage arrays and the W buffer in turn.
   constexpr int kEpiRegion = WM * WN * 2;
-  constexpr int kEpiPerStage = L::kStage / kEpiRegion, kEpiPerW = (kWReg ? L::kWBytes : 0) / kEpiRegion;
+  constexpr int kEpiPerStage = L::kStageAlloc / kEpiRegion, kEpiPerW = (kWReg ? L::kWBytes : 0) / kEpiRegion;
   constexpr bool kEpiStaged =
       MODE != kDs && WM >= 16 && (WM & (WM - 1)) == 0 && WN % 32 == 0 && STAGES * kEpiPerStage + kEpiPerW >= WGM * WGN;
   auto epi_region = [&](int w) -> SQ_LDS uint16_t* {
@@ -414,6 +461,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   __amdgpu_buffer_rsrc_t ra, rb;
   if constexpr (MODE == kFwdR) {
     ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+  } else if constexpr (MODE == kFwdC) {
+    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+    rb = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
   } else if constexpr (MODE == kDx) {
     ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.O * 2));
   } else {
@@ -437,11 +487,16 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   using DA_kc = std::conditional_t<MODE != kDs, DmaKC<BM, NT>, DmaKC<8 * NT / 64, NT>>;  // unused in DS
   using DA_nat = std::conditional_t<MODE == kDs, DmaNat<BM, NT, BK>, DmaNat<512, NT, 64>>;
   using DB_nat = std::conditional_t<MODE == kDs, DmaNat<BN, NT, BK>, DmaNat<512, NT, 64>>;
+  using DC = std::conditional_t<MODE == kFwdC, DmaCodes<BN, NT>, DmaCodes<NT / 2, NT>>;   // used by kFwdC
   DA_kc dA_kc;
   DA_nat dA_nat;
   DB_nat dB_nat;
+  DC dC;
   if constexpr (MODE == kFwdR) {
     dA_kc.init(g.I, g.T, g.I, m0, tid);
+  } else if constexpr (MODE == kFwdC) {
+    dA_kc.init(g.I, g.T, g.I, m0, tid);
+    dC.init(g.I, g.O, n0, tid);
   } else if constexpr (MODE == kDx) {
     dA_kc.init(g.O, g.T, g.O, m0, tid);
   } else {
@@ -455,6 +510,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     const bool full = k0 + BK <= g.K;
     if constexpr (MODE == kFwdR || MODE == kDx) {
       dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
+    } else if constexpr (MODE == kFwdC) {
+      dA_kc.issue(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
+      dC.template issue_part<0, DC::kInst>(rb, st + L::kA, k0, wave_u);
     } else {
       dA_nat.issue(ra, (SQ_LDS uint16_t*)st, (uint32_t)k0 * (uint32_t)g.I * 2u, wave_u);
       dB_nat.issue(rb, (SQ_LDS uint16_t*)(st + L::kA), (uint32_t)k0 * (uint32_t)g.O * 2u, wave_u);
@@ -468,9 +526,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     SQ_LDS uint8_t* st = stage(SC);
     const int k0 = (kofs + kt) * BK;
     const bool full = k0 + BK <= g.K;
-    if constexpr (MODE == kFwdR || MODE == kDx) {
+    if constexpr (MODE == kFwdR || MODE == kDx || MODE == kFwdC) {
       constexpr int n = decltype(dA_kc)::kInst;
       dA_kc.template issue_part<P * n / 4, (P + 1) * n / 4>(ra, (SQ_LDS uint16_t*)st, k0, full, wave_u);
+      if constexpr (MODE == kFwdC && P == 0) dC.template issue_part<0, DC::kInst>(rb, st + L::kA, k0, wave_u);
     } else if constexpr (MODE == kDs) {
       constexpr int na = decltype(dA_nat)::kInst, nb = decltype(dB_nat)::kInst;
       dA_nat.template issue_part<P * na / 4, (P + 1) * na / 4>(ra, (SQ_LDS uint16_t*)st,
@@ -564,6 +623,37 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     }
   };
 
+  // ---- kFwdC: the E8M0 scale bytes of the wave's code rows.  Lane (n, h) of
+  // 32-row slice j uses row n0 + wn0 + 32 j + n, block 2 kt + h (the 32 codes
+  // of that block are the lane's half of stage kt).  One 16-byte load per
+  // slice brings the row's 16 blocks of 8 stages; the next 16 bytes are
+  // loaded during the last of those stages, into the same registers, once
+  // that stage's scale operands have been taken.  The launcher takes this
+  // path only when G is a multiple of 16 (I % 512 == 0), so chunks never run
+  // past a row and the stage count is a multiple of 8.  A row outside the
+  // layer reads at an offset past the plane: zeros.
+  constexpr int kSc = MODE == kFwdC ? TN : 1;
+  u32x4 scw[kSc];
+  uint32_t sc0[kSc];
+  __amdgpu_buffer_rsrc_t rs_sc;
+  if constexpr (MODE == kFwdC) {
+    static_assert(FMT == kMX && STAGES == 2 && BK == 64, "register dequantisation: MXFP4, two 64-deep stages");
+    rs_sc = make_rsrc(g.scales, (uint32_t)((size_t)g.O * g.G));
+#pragma unroll
+    for (int j = 0; j < kSc; ++j) {
+      const int row = n0 + wn0 + 32 * j + (lane & 31);
+      sc0[j] = row < g.O ? (uint32_t)row * (uint32_t)g.G : kOOB;
+    }
+  }
+  auto load_sc = [&](int chunk) {
+    if constexpr (MODE == kFwdC) {
+#pragma unroll
+      for (int j = 0; j < kSc; ++j)
+        scw[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                               rs_sc, (int)(sc0[j] + 16u * (uint32_t)chunk), 0, 0));
+    }
+  };
+
   // ---- one K stage: wait for its data, refill the oldest stage, multiply
   auto step = [&](auto SC, int kt) {
     constexpr int S = decltype(SC)::value;
@@ -616,7 +706,46 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       }
     };
     SQ_LDS uint8_t* st = stage(SC);
-    if constexpr (MODE == kFwdR) {
+    if constexpr (MODE == kFwdC) {
+      // The lanes of half h (= lane / 32) take k = 32 h + 8 kk .. + 7 of the
+      // stage in slice kk, for both operands: the sum over the stage's 64 k
+      // is the same, and a lane's 32 k are one 16-byte run of codes under one
+      // scale.  A: 16-byte chunk 4 h + kk of its K-contiguous row.
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint8_t* cs = st + L::kA;
+      const int h = lane >> 5;
+      // scale byte 2 (kt % 8) + h of the slice's 16-byte chunk
+      const int q = (kt >> 1) & 3;
+      const uint32_t sh = 8u * (2u * (uint32_t)(kt & 1) + (uint32_t)h);
+      u32x4 cw[TN];
+      float sop[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = wn0 + 32 * j + (lane & 31);
+        cw[j] = *(const SQ_LDS u32x4*)(cs + r * (kBK / 2) + 16 * (h ^ swz_codes(r)));
+        const uint32_t w = q == 0 ? scw[j][0] : q == 1 ? scw[j][1] : q == 2 ? scw[j][2] : scw[j][3];
+        sop[j] = e8m0_as_scale_operand((w >> sh) & 0xFFu);
+      }
+      if ((kt & 7) == 7 && kt + 1 < nk) load_sc((kt + 1) >> 3);
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        bf16x8 fa[TM], fb[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 4 * h + kk));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const uint4 d = dequant8_mx(cw[j][kk], sop[j]);
+          __builtin_memcpy(&fb[j], &d, 16);
+        }
+        before_mfma(kk);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+    } else if constexpr (MODE == kFwdR) {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = wbuf(kt);
 #pragma unroll
@@ -682,6 +811,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       load_w(0, std::integral_constant<int, 0>{});
       commit_w(0, std::integral_constant<int, 0>{});
     }
+  }
+  if constexpr (MODE == kFwdC) {
+    if (0 < nk) load_sc(0);
   }
   __builtin_amdgcn_sched_barrier(0);
   if (0 < nk) issue_dma(std::integral_constant<int, 0>{}, 0);
@@ -817,6 +949,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup 
 #ifndef SQ_CFG_DS
 #define SQ_CFG_DS 256, 256, 4, 2, 2, 64
 #endif
+#ifndef SQ_CFG_FWDC
+#define SQ_CFG_FWDC 256, 256, 4, 2, 2, 64
+#endif
 #ifndef SQ_CFG_SMALL
 #define SQ_CFG_SMALL 128, 128, 2, 2, 2, 64
 #endif
@@ -850,6 +985,10 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
   g.M = T; g.N = O; g.K = I;
   g.ws2 = (fmt == kNV) ? ws2 : 1.0f;
   g.out_bf16 = y_bf16;
+  // registers dequantise when the code and scale planes are 16-byte aligned
+  // and every row's scales split into 16-byte runs
+  if (fmt == kMX && g.G % 16 == 0 && ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(scales)) & 15) == 0)
+    return launch_sized<kFwdC, kMX, SQ_CFG_FWDC>(g, s);
   return fmt == kMX ? launch_sized<kFwdR, kMX, SQ_CFG_FWD>(g, s) : launch_sized<kFwdR, kNV, SQ_CFG_FWD>(g, s);
 }
 

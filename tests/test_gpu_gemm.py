@@ -122,6 +122,28 @@ def test_bf16_outputs_are_rounded_f32_outputs(sq, fmt, T, O, I):
         assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("T,O,I", [(300, 264, 1024), (4100, 4104, 512), (64, 256, 512), (130, 72, 1536)])
+def test_mx_forward_both_dequant_paths(sq, T, O, I):
+    """An MXFP4 forward with 16-byte aligned codes and scales and I a multiple
+    of 512 dequantises each wave's operand in registers; codes that are only
+    4-byte aligned take the path that dequantises W once into LDS.  Both
+    match the oracle."""
+    X, dY, codes, sb, ws2 = make_layer("mx", T, O, I, seed=2300 + T)
+    Xc, sc = X.cuda(), torch.from_numpy(sb).cuda()
+    c16 = torch.from_numpy(codes).cuda()
+    buf = torch.empty(codes.size + 16, dtype=torch.uint8, device="cuda")
+    c4 = buf[4:4 + codes.size].view(codes.shape)
+    c4.copy_(c16)
+    assert c16.data_ptr() % 16 == 0 and c4.data_ptr() % 16 == 4
+    print(f"[gemm] mx forward, both dequant paths, T={T} O={O} I={I}", flush=True)
+    ya = sq.sq_fwd("mx", Xc, c16, sc).cpu().numpy()
+    yb = sq.sq_fwd("mx", Xc, c4, sc).cpu().numpy()
+    ref = linear.forward(X.double().numpy(), linear.dequant("mx", codes, sb, ws2))
+    ea, eb = normwise(ya, ref), normwise(yb, ref)
+    print(f"  normwise errors: registers {ea:.2e}, LDS {eb:.2e}")
+    assert ea <= TOL and eb <= TOL
+
+
 def test_zero_tokens_gives_zero_dscale(sq):
     O, I = 64, 128
     codes = torch.from_numpy(inputs.codes_uniform(5, O, I)).cuda()
