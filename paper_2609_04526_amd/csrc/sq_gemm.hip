@@ -69,6 +69,11 @@ constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: r
 #ifndef SQ_FWD_W_AHEAD2
 #define SQ_FWD_W_AHEAD2 1
 #endif
+// SQ_SCHED_LATE 1: the stage barrier sits before the MFMAs of the last slice
+// of a stage (operand reads run one slice ahead, across the barrier).
+#ifndef SQ_SCHED_LATE
+#define SQ_SCHED_LATE 1
+#endif
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -106,9 +111,38 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint3
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
-// 16 bytes per lane, global -> LDS; lane l writes dst + 16 l.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, SQ_LDS void* dst, uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, (int)voff, 0, 0, 0);
+// Buffer descriptor of the global -> LDS copies: base, num_records = bytes
+// (offsets at or past it read zeros), raw buffer flags.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+struct DmaRsrc {
+  i32x4 v;
+};
+__device__ __forceinline__ DmaRsrc make_dma_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  DmaRsrc r;
+  r.v = i32x4{__builtin_amdgcn_readfirstlane((int)(uint32_t)a), __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32) & 0xFFFF),
+              __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000};
+  return r;
+}
+
+// 16 bytes per lane, global -> LDS; lane l writes dst + 16 l.  Written as
+// the instruction itself: the compiler's wait insertion cannot tell the LDS
+// tile a copy fills from the tile being read, and would otherwise stall
+// every later LDS read until the copy lands.  The loop waits for the copies
+// explicitly (vmcnt) before the barrier that publishes a stage.
+#ifndef SQ_DMA_ASM
+#define SQ_DMA_ASM 1
+#endif
+__device__ __forceinline__ void dma16(DmaRsrc r, SQ_LDS void* dst, uint32_t voff) {
+#if SQ_DMA_ASM
+  const int lds = __builtin_amdgcn_readfirstlane((int)(uint32_t)reinterpret_cast<uintptr_t>(dst));
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff), "s"(r.v)
+               : "memory", "m0");
+#else
+  __amdgpu_buffer_rsrc_t b = __builtin_amdgcn_make_buffer_rsrc(
+      reinterpret_cast<void*>((uint64_t)(uint32_t)r.v[0] | ((uint64_t)(uint32_t)r.v[1] << 32)), (short)0, r.v[2], r.v[3]);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(b, dst, 16, (int)voff, 0, 0, 0);
+#endif
 }
 
 // Wait until at most n vector-memory loads of this wave are outstanding and
@@ -178,12 +212,12 @@ struct DmaKC {
       klim[q] = kdim - c * 8;
     }
   }
-  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int k0, bool full,
+  __device__ __forceinline__ void issue(DmaRsrc rs, SQ_LDS uint16_t* s, int k0, bool full,
                                         int wave) const {
     issue_part<0, kInst>(rs, s, k0, full, wave);
   }
   template <int Q0, int Q1>
-  __device__ __forceinline__ void issue_part(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, int k0, bool full,
+  __device__ __forceinline__ void issue_part(DmaRsrc rs, SQ_LDS uint16_t* s, int k0, bool full,
                                              int wave) const {
 #pragma unroll
     for (int q = Q0; q < Q1; ++q) {
@@ -216,12 +250,12 @@ struct DmaNat {
       off[q] = gm < mdim ? (uint32_t)((size_t)k * ld + gm) * 2u : kOOB;
     }
   }
-  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
+  __device__ __forceinline__ void issue(DmaRsrc rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
                                         int wave) const {
     issue_part<0, kInst>(rs, s, kstep_bytes, wave);
   }
   template <int Q0, int Q1>
-  __device__ __forceinline__ void issue_part(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
+  __device__ __forceinline__ void issue_part(DmaRsrc rs, SQ_LDS uint16_t* s, uint32_t kstep_bytes,
                                              int wave) const {
 #pragma unroll
     for (int q = Q0; q < Q1; ++q) {
@@ -258,7 +292,7 @@ struct DmaCodes {
     }
   }
   template <int Q0, int Q1>
-  __device__ __forceinline__ void issue_part(__amdgpu_buffer_rsrc_t rs, SQ_LDS uint8_t* s, int k0, int wave) const {
+  __device__ __forceinline__ void issue_part(DmaRsrc rs, SQ_LDS uint8_t* s, int k0, int wave) const {
 #pragma unroll
     for (int q = Q0; q < Q1; ++q) {
       const int blk = q * (NT / 64) + wave;
@@ -282,8 +316,21 @@ __host__ __device__ constexpr int dma_count() {
 // enumerated in groups of kGroupM tile-rows (column by column inside a group)
 // and each XCD is given one contiguous stretch of that order, so the
 // workgroups that share an L2 also share operand panels.
-constexpr int kGroupM = 8;
+#ifndef SQ_GROUPM_FWD
+#define SQ_GROUPM_FWD 8
+#endif
+#ifndef SQ_GROUPM_DX
+#define SQ_GROUPM_DX 8
+#endif
+#ifndef SQ_GROUPM_DS
+#define SQ_GROUPM_DS 8
+#endif
+template <int MODE>
+constexpr int group_m() {
+  return MODE == kDs ? SQ_GROUPM_DS : MODE == kDx ? SQ_GROUPM_DX : SQ_GROUPM_FWD;
+}
 
+template <int kGroupM>
 __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int x = bid % kXcds, q = nb / kXcds, r = nb % kXcds;
   const int idx = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + bid / kXcds;
@@ -296,7 +343,7 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
   tn = in / gm;
 }
 
-template <int MODE, int BM, int BN, int STAGES, int BK>
+template <int MODE, int BM, int BN, int STAGES, int BK, int NW>
 struct SmemLayout {
   static constexpr int kA = BM * BK * 2;                                      // bytes per A stage
   static constexpr int kB = BK * BN * 2;                                      // bytes per B stage
@@ -305,8 +352,10 @@ struct SmemLayout {
   static constexpr int kStage = kA + (kWReg || MODE == kFwdC ? 0 : kB) + kCodes;   // DMA bytes per stage
   static constexpr int kWBytes = kWReg ? 2 * kB : 0;                          // bf16 W double buffer
   // kFwdC has no W buffer: its stage arrays are sized to also hold the bf16
-  // output staging of every wave (BM x BN bf16 over the stages)
-  static constexpr int kEpiPer = (BM * BN * 2 + STAGES - 1) / STAGES;
+  // output staging of every wave (one (BM x BN / NW) bf16 region per wave,
+  // whole regions per stage array)
+  static constexpr int kEpiRegion = BM * BN * 2 / NW;
+  static constexpr int kEpiPer = (NW + STAGES - 1) / STAGES * kEpiRegion;
   static constexpr int kStageAlloc = MODE == kFwdC && kEpiPer > kStage ? kEpiPer : kStage;
   static constexpr int kBytes = STAGES * kStageAlloc + kWBytes;
 };
@@ -410,7 +459,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   constexpr int B = ScaleOperand<FMT>::kBlock;
   static_assert(MODE == kDs || BK == kBK, "K-contiguous tiles use 64-wide stages");
   static_assert(BK == 32 || BK == 64, "stage depth");
-  using L = SmemLayout<MODE, BM, BN, STAGES, BK>;
+  using L = SmemLayout<MODE, BM, BN, STAGES, BK, WGM * WGN>;
   constexpr bool kWReg = L::kWReg;
   constexpr int kDma = dma_count<MODE, BM, BN, NT, BK>();   // DMA loads per thread per stage
   // One static array per DMA stage (distinct objects, so the compiler can see
@@ -446,7 +495,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   const int tiles = tiles_m * tiles_n;
   const int split = (MODE == kDs && g.ksplit > 1) ? bid / tiles : 0;
   int tm, tn;
-  tile_of((MODE == kDs && g.ksplit > 1) ? bid - split * tiles : bid, (MODE == kDs && g.ksplit > 1) ? tiles : nb,
+  tile_of<group_m<MODE>()>((MODE == kDs && g.ksplit > 1) ? bid - split * tiles : bid, (MODE == kDs && g.ksplit > 1) ? tiles : nb,
           tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
@@ -458,17 +507,17 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     else return (SQ_LDS uint8_t*)lds3;
   };
 
-  __amdgpu_buffer_rsrc_t ra, rb;
+  DmaRsrc ra, rb;
   if constexpr (MODE == kFwdR) {
-    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+    ra = make_dma_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
   } else if constexpr (MODE == kFwdC) {
-    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
-    rb = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
+    ra = make_dma_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+    rb = make_dma_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
   } else if constexpr (MODE == kDx) {
-    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.O * 2));
+    ra = make_dma_rsrc(g.a, (uint32_t)((size_t)g.T * g.O * 2));
   } else {
-    ra = make_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
-    rb = make_rsrc(g.b, (uint32_t)((size_t)g.T * g.O * 2));
+    ra = make_dma_rsrc(g.a, (uint32_t)((size_t)g.T * g.I * 2));
+    rb = make_dma_rsrc(g.b, (uint32_t)((size_t)g.T * g.O * 2));
   }
 
   f32x16 acc[TM][TN];
@@ -637,7 +686,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   uint32_t sc0[kSc];
   __amdgpu_buffer_rsrc_t rs_sc;
   if constexpr (MODE == kFwdC) {
-    static_assert(FMT == kMX && STAGES == 2 && BK == 64, "register dequantisation: MXFP4, two 64-deep stages");
+    static_assert(FMT == kMX && BK == 64, "register dequantisation: MXFP4, 64-deep stages");
     rs_sc = make_rsrc(g.scales, (uint32_t)((size_t)g.O * g.G));
 #pragma unroll
     for (int j = 0; j < kSc; ++j) {
@@ -805,6 +854,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     }
   };
 
+  constexpr bool kLate = MODE == kFwdC || (SQ_SCHED_LATE && MODE == kDs);
+  if constexpr (!kLate) {
   // ---- prologue: the first STAGES-1 stages in flight
   if constexpr (kWReg) {
     if (nk > 0) {
@@ -837,6 +888,174 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     if constexpr (STAGES > 3) {
       if (kt0 + 3 < nk) step(std::integral_constant<int, 3>{}, kt0 + 3);
     }
+  }
+  } else {
+  // ---- Late-barrier schedule.  The operands of slice kk + 1 are read from
+  // LDS while slice kk multiplies, and the barrier that publishes stage
+  // kt + 1 sits before the MFMAs of stage kt's last slice: those MFMAs cover
+  // the latency of stage kt + 1's first reads, so the matrix cores do not
+  // drain at every barrier.  Right after the barrier the buffer of stage kt
+  // is free: half of the DMA of stage kt + STAGES goes out there, the other
+  // half in the first slice of stage kt + 1, so each stage's copy has
+  // STAGES - 1 stages to land.  A W tile (kFwdR, kDx) for stage kt + 1 is
+  // committed to LDS before the barrier of stage kt.
+  struct Frag {
+    bf16x8 a[TM];
+    bf16x8 b[TN];
+    uint32_t cd[MODE == kFwdC ? TN : 1];     // kFwdC: this slice's 8 codes per row slice
+  };
+  Frag F0, F1;
+  u32x4 cst[MODE == kFwdC ? TN : 1];         // kFwdC: the stage's codes, read with slice 0
+  float sop[MODE == kFwdC ? TN : 1];         // kFwdC: the stage's scale operands
+  const int h32 = lane >> 5;
+
+  auto read = [&](auto SC, int kt, auto KK, Frag& f) {
+    constexpr int kk = decltype(KK)::value;
+    SQ_LDS uint8_t* st = stage(SC);
+    if constexpr (MODE == kFwdC) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        f.a[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 4 * h32 + kk));
+      if constexpr (kk == 0) {
+        const SQ_LDS uint8_t* cs = st + L::kA;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int r = wn0 + 32 * j + (lane & 31);
+          cst[j] = *(const SQ_LDS u32x4*)(cs + r * (kBK / 2) + 16 * (h32 ^ swz_codes(r)));
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) f.cd[j] = cst[j][kk];
+    } else if constexpr (MODE == kFwdR) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = wbuf(kt);
+      const int chunk = 2 * kk + h32;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) f.a[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), chunk));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) f.b[j] = *(const SQ_LDS bf16x8*)(b + kc_off(wn0 + j * 32 + (lane & 31), chunk));
+    } else if constexpr (MODE == kDx) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = wbuf(kt);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        f.a[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 2 * kk + h32));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) f.b[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+    } else {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) f.a[i] = nat_frag<BM>(a, kk, wm0 + i * 32, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) f.b[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+    }
+  };
+  auto mma = [&](Frag& f) {
+    if constexpr (MODE == kFwdC) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const uint4 d = dequant8_mx(f.cd[j], sop[j]);
+        __builtin_memcpy(&f.b[j], &d, 16);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+  };
+  // kFwdC: scale operands of stage kt, byte 2 (kt % 8) + h of the slice's
+  // 16-byte chunk; the next chunk is loaded during the chunk's last stage
+  auto take_scales = [&](int kt) {
+    if constexpr (MODE == kFwdC) {
+      const int q = (kt >> 1) & 3;
+      const uint32_t sh = 8u * (2u * (uint32_t)(kt & 1) + (uint32_t)h32);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const uint32_t w = q == 0 ? scw[j][0] : q == 1 ? scw[j][1] : q == 2 ? scw[j][2] : scw[j][3];
+        sop[j] = e8m0_as_scale_operand((w >> sh) & 0xFFu);
+      }
+      if ((kt & 7) == 7 && kt + 1 < nk) load_sc((kt + 1) >> 3);
+    }
+  };
+  // DMA quarters [Q0, Q0 + 2) of stage kt into buffer SC
+  auto dma_half = [&](auto SC, int kt, auto Q0) {
+    constexpr int q = decltype(Q0)::value;
+    dma_part(SC, kt, std::integral_constant<int, q>{});
+    dma_part(SC, kt, std::integral_constant<int, q + 1>{});
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  // DMA loads a thread issues for the stages after kt + 1 (the wait at the
+  // barrier leaves those in flight; anything issued later is younger still)
+  constexpr int kAhead = (STAGES - 2) * kDma < 63 ? (STAGES - 2) * kDma : 63;
+
+  auto step2 = [&](auto SC, int kt) {
+    constexpr int S = decltype(SC)::value;
+    using SN = std::integral_constant<int, (S + 1) % STAGES>;            // stage kt + 1
+    using SP = std::integral_constant<int, (S + STAGES - 1) % STAGES>;   // stage kt + STAGES - 1
+    take_scales(kt);
+    // slice 0 (operands in F0): read slice 1; the second half of stage
+    // kt + STAGES - 1's DMA and the W loads go out here
+    read(SC, kt, I1{}, F1);
+    if (kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
+    if constexpr (kWAhead == 2) load_w(kt + 2, std::integral_constant<int, S % 2>{});
+    else if constexpr (kWReg) {
+      if (kt + 1 < nk) load_w(kt + 1, I0{});
+    }
+    mma(F0);
+    read(SC, kt, I2{}, F0);
+    mma(F1);
+    read(SC, kt, I3{}, F1);
+    mma(F0);
+    // publish stage kt + 1: its W tile, then everyone's DMA and LDS writes
+    if constexpr (kWReg) {
+      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
+    }
+    wait_vm_lgkm0<kAhead>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < nk) read(SN{}, kt + 1, I0{}, F0);
+    if (kt + STAGES < nk) dma_half(SC, kt + STAGES, I0{});
+    mma(F1);
+  };
+
+  // prologue: stage 0 in LDS and its slice 0 read, then the DMA of stages
+  // 1 .. STAGES - 2 and the first half of stage STAGES - 1
+  if (nk > 0) {
+    if constexpr (kWReg) {
+      load_w(0, I0{});
+      commit_w(0, I0{});
+    }
+    if constexpr (kWAhead == 2) load_w(1, I1{});
+    if constexpr (MODE == kFwdC) load_sc(0);
+    issue_dma(I0{}, 0);
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    read(I0{}, 0, I0{}, F0);
+    if constexpr (STAGES > 2) {
+      if (1 < nk) issue_dma(I1{}, 1);
+    }
+    if constexpr (STAGES > 3) {
+      if (2 < nk) issue_dma(I2{}, 2);
+    }
+    if (STAGES - 1 < nk) dma_half(std::integral_constant<int, STAGES - 1>{}, STAGES - 1, I0{});
+  }
+  for (int kt0 = 0; kt0 < nk; kt0 += STAGES) {
+    step2(I0{}, kt0);
+    if (kt0 + 1 < nk) step2(I1{}, kt0 + 1);
+    if constexpr (STAGES > 2) {
+      if (kt0 + 2 < nk) step2(I2{}, kt0 + 2);
+    }
+    if constexpr (STAGES > 3) {
+      if (kt0 + 3 < nk) step2(I3{}, kt0 + 3);
+    }
+  }
   }
 
   wait_vm_lgkm0<0>();   // loads issued past the last stage have landed before LDS is reused
@@ -959,7 +1178,7 @@ constexpr int kCUs = 256;   // MI355X compute units
 
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 static int launch_gemm(const GemmArgs& g, hipStream_t s) {
-  using L = SmemLayout<MODE, BM, BN, STAGES, BK>;
+  using L = SmemLayout<MODE, BM, BN, STAGES, BK, WGM * WGN>;
   static_assert(L::kBytes <= 160 * 1024, "LDS budget");
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles == 0) return 0;
@@ -975,6 +1194,17 @@ static int launch_sized(const GemmArgs& g, hipStream_t s) {
   return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
 }
 
+// The MXFP4 forward dequantises in registers (kFwdC) when every row's scales
+// split into 16-byte runs and the code and scale planes are 16-byte aligned;
+// the grouped forward makes the same choice as the single one, so an
+// expert's output equals the single product's bit for bit.
+static bool regs_dequant_ok(int G, const ExpertProblem* p, int n) {
+  if (G % 16 != 0) return false;
+  for (int e = 0; e < n; ++e)
+    if (((reinterpret_cast<uintptr_t>(p[e].codes) | reinterpret_cast<uintptr_t>(p[e].scales)) & 15) != 0) return false;
+  return true;
+}
+
 // ------------------------------------------------------------------ entry
 int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
              const uint8_t* scales, float ws2, void* Y, int y_bf16, hipStream_t s) {
@@ -987,8 +1217,10 @@ int gemm_fwd(int fmt, int T, int O, int I, const void* X, const uint8_t* codes,
   g.out_bf16 = y_bf16;
   // registers dequantise when the code and scale planes are 16-byte aligned
   // and every row's scales split into 16-byte runs
-  if (fmt == kMX && g.G % 16 == 0 && ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(scales)) & 15) == 0)
-    return launch_sized<kFwdC, kMX, SQ_CFG_FWDC>(g, s);
+  ExpertProblem one{};
+  one.codes = codes;
+  one.scales = scales;
+  if (fmt == kMX && regs_dequant_ok(g.G, &one, 1)) return launch_sized<kFwdC, kMX, SQ_CFG_FWDC>(g, s);
   return fmt == kMX ? launch_sized<kFwdR, kMX, SQ_CFG_FWD>(g, s) : launch_sized<kFwdR, kNV, SQ_CFG_FWD>(g, s);
 }
 
@@ -1009,7 +1241,7 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
 // multiple of 8 so the XCD-aware order inside each expert still holds.
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 static int launch_grouped(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
-  using L = SmemLayout<MODE, BM, BN, STAGES, BK>;
+  using L = SmemLayout<MODE, BM, BN, STAGES, BK, WGM * WGN>;
   static_assert(L::kBytes <= 160 * 1024, "LDS budget");
   int blocks = 0;
   gg.count = n;
@@ -1061,7 +1293,9 @@ static int run_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int
   for (int e0 = 0; e0 < n; e0 += kGroupMax) {
     const int m = n - e0 < kGroupMax ? n - e0 : kGroupMax;
     int rc;
-    if (MODE == kFwdR)
+    if (MODE == kFwdR && fmt == kMX && regs_dequant_ok(gg.base.G, p + e0, m))
+      rc = grouped_sized<kFwdC, kMX, SQ_CFG_FWDC>(gg, p + e0, m, s);
+    else if (MODE == kFwdR)
       rc = fmt == kMX ? grouped_sized<kFwdR, kMX, SQ_CFG_FWD>(gg, p + e0, m, s)
                       : grouped_sized<kFwdR, kNV, SQ_CFG_FWD>(gg, p + e0, m, s);
     else if (MODE == kDx)
