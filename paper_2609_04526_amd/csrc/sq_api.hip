@@ -69,17 +69,15 @@ int check_merge_plane(int fmt, int64_t n, const uint8_t* scales, const float* de
 
 int run_merge(int n_desc, const sq_merge_desc* d, hipStream_t s) {
   sq::MergeBatch batch{};
-  batch.copy_only = 1;
   int64_t spans = 0;
   for (int k = 0; k < n_desc; ++k) {
     if (d[k].n == 0) continue;
-    const int64_t unit = d[k].mode == SQ_MERGE_COPY ? sq::kCopySpan : sq::kDeltaSpan;
+    const int64_t unit = d[k].mode == SQ_MERGE_COPY ? sq::kCopySpan : sq::delta_span(d[k].fmt);
     const int64_t c = (d[k].n + unit - 1) / unit;
     if (batch.count == sq::kMergePlanesPerLaunch || spans + c > INT32_MAX) {
       batch.spans = (int32_t)spans;
       if (sq::merge_launch(batch, s) != 0) return SQ_ERR_HIP;
       batch = sq::MergeBatch{};
-      batch.copy_only = 1;
       spans = 0;
     }
     const int p = batch.count++;
@@ -91,8 +89,8 @@ int run_merge(int n_desc, const sq_merge_desc* d, hipStream_t s) {
     batch.ws2[p] = d[k].ws2;
     batch.fmt[p] = (uint8_t)d[k].fmt;
     batch.mode[p] = (uint8_t)d[k].mode;
-    if (d[k].mode != SQ_MERGE_COPY) batch.copy_only = 0;
-    if (d[k].mode == SQ_MERGE_DELTA && d[k].fmt == SQ_NVFP4) batch.nv_delta = 1;
+    batch.kinds |= d[k].mode == SQ_MERGE_COPY ? sq::kMergeCopy
+                                              : (d[k].fmt == SQ_NVFP4 ? sq::kMergeNvDelta : sq::kMergeMxDelta);
     spans += c;
   }
   batch.spans = (int32_t)spans;

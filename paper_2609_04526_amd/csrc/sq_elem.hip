@@ -17,9 +17,14 @@
 
 namespace sq {
 
+// merge tuning knobs (build-time)
+#ifndef SQ_MERGE_NT_STORE
+#define SQ_MERGE_NT_STORE 0
+#endif
+
 // ------------------------------------------------------------------ merge
-// The planes of a launch are cut into spans: kDeltaSpan scale bytes (delta
-// mode: kDeltaSteps steps of 4 scales and a 16-byte fp32 delta per lane) or
+// The planes of a launch are cut into spans: delta_span(fmt) scale bytes (delta
+// mode: delta_steps(fmt) steps of 4 scales and a 16-byte fp32 delta per lane) or
 // kCopySpan bytes (copy mode: kCopySteps steps of 16 bytes per lane).  Workgroup w takes spans w, w + grid,
 // w + 2 grid, ...: at any moment the whole grid streams through one window of
 // the planes, which keeps the DRAM accesses of all workgroups together (a
@@ -28,13 +33,14 @@ namespace sq {
 // words; delta and copy sources are read once, with streaming loads.  The
 // plane pointers are restrict: a scale store cannot alias a later load.
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef sq_f32x4 f32x4_t;
 
-// One delta span: kDeltaSteps steps of 4 scales per lane, all loads issued
-// before any compute.
-template <int FMT>
+// One delta span: delta_steps(FMT) steps of 4 scales per lane, all loads
+// issued before any compute.
+template <int FMT, int FAST>
 __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const float* __restrict__ dl, int64_t n,
-                                                 int64_t off, float ws2, int tid) {
+                                                 int64_t off, const Ws2Div& ws2, int tid) {
+  constexpr int kDeltaSteps = delta_steps(FMT), kDeltaSpan = delta_span(FMT);
   if (off + kDeltaSpan <= n) {
     uint32_t sv[kDeltaSteps];
     f32x4_t dv[kDeltaSteps];
@@ -47,12 +53,21 @@ __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const
 #pragma unroll
     for (int g = 0; g < kDeltaSteps; ++g) {
       const uint32_t v = sv[g];
-      sv[g] = merge_one_t<FMT>(v & 0xFFu, dv[g][0], ws2) | (merge_one_t<FMT>((v >> 8) & 0xFFu, dv[g][1], ws2) << 8) |
-              (merge_one_t<FMT>((v >> 16) & 0xFFu, dv[g][2], ws2) << 16) |
-              (merge_one_t<FMT>(v >> 24, dv[g][3], ws2) << 24);
+      if constexpr (FMT == kNV)
+        sv[g] = nv_merge_word<FAST>(v, dv[g], ws2);
+      else
+        sv[g] = merge_one_t<FMT>(v & 0xFFu, dv[g][0], ws2) | (merge_one_t<FMT>((v >> 8) & 0xFFu, dv[g][1], ws2) << 8) |
+                (merge_one_t<FMT>((v >> 16) & 0xFFu, dv[g][2], ws2) << 16) |
+                (merge_one_t<FMT>(v >> 24, dv[g][3], ws2) << 24);
     }
 #pragma unroll
-    for (int g = 0; g < kDeltaSteps; ++g) *reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4) = sv[g];
+    for (int g = 0; g < kDeltaSteps; ++g) {
+#if SQ_MERGE_NT_STORE
+      __builtin_nontemporal_store(sv[g], reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4));
+#else
+      *reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4) = sv[g];
+#endif
+    }
   } else {
     for (int64_t k = off + tid; k < n && k < off + kDeltaSpan; k += 256)
       sc[k] = (uint8_t)merge_one_t<FMT>(sc[k], dl[k], ws2);
@@ -74,6 +89,10 @@ __device__ __forceinline__ void merge_copy_span(uint8_t* __restrict__ sc, const 
   }
 }
 
+// KINDS: the plane kinds this instance handles (a launch whose planes are all
+// of one kind gets an instance with that kind's code alone, and so that
+// kind's register budget and occupancy).
+template <int KINDS>
 __global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
   (void)batch_arg;
   // The batch is the kernel's only explicit argument, so it sits at offset 0
@@ -89,14 +108,17 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
     uint8_t* __restrict__ sc = batch.scales[pi];
     const int64_t n = batch.n[pi];
     const int64_t rel = span - batch.span_begin[pi];
-    if (batch.mode[pi] == 1) {                                // copy
+    const float* __restrict__ dl = static_cast<const float*>(batch.aux[pi]);
+    if ((KINDS & kMergeCopy) && batch.mode[pi] == 1) {
       merge_copy_span(sc, static_cast<const uint8_t*>(batch.aux[pi]), n, rel * kCopySpan, tid);
-    } else {
-      const float* __restrict__ dl = static_cast<const float*>(batch.aux[pi]);
-      if (batch.fmt[pi] == kNV)
-        merge_delta_span<kNV>(sc, dl, n, rel * kDeltaSpan, batch.ws2[pi], tid);
+    } else if ((KINDS & kMergeNvDelta) && (KINDS == kMergeNvDelta || batch.fmt[pi] == kNV)) {
+      const Ws2Div w = make_ws2_div(batch.ws2[pi]);
+      if (w.fast)
+        merge_delta_span<kNV, 1>(sc, dl, n, rel * delta_span(kNV), w, tid);
       else
-        merge_delta_span<kMX>(sc, dl, n, rel * kDeltaSpan, batch.ws2[pi], tid);
+        merge_delta_span<kNV, 0>(sc, dl, n, rel * delta_span(kNV), w, tid);
+    } else if (KINDS & kMergeMxDelta) {
+      merge_delta_span<kMX, 0>(sc, dl, n, rel * delta_span(kMX), make_ws2_div(1.0f), tid);
     }
   }
 }
@@ -105,10 +127,22 @@ int merge_launch(const MergeBatch& b, hipStream_t s) {
   if (b.spans <= 0) return 0;
   // Measured on the 8B model's planes (medians of interleaved runs): copies
   // stream best from 2048 workgroups, MXFP4 deltas from 4096, and NVFP4
-  // deltas, whose division keeps more lanes busy, from 8192.
-  const int64_t cap = b.copy_only ? 2048 : (b.nv_delta ? 8192 : 4096);
-  const int64_t grid = b.spans < cap ? b.spans : cap;
-  hipLaunchKernelGGL(merge_kernel, dim3((unsigned)grid), dim3(256), 0, s, b);
+  // deltas (16-step spans, a longer grid step per scale) from 16384.
+#ifndef SQ_MERGE_NV_GRID
+#define SQ_MERGE_NV_GRID 16384
+#endif
+#ifndef SQ_MERGE_MX_GRID
+#define SQ_MERGE_MX_GRID 4096
+#endif
+  const int64_t cap = b.kinds == kMergeCopy ? 2048 : ((b.kinds & kMergeNvDelta) ? SQ_MERGE_NV_GRID : SQ_MERGE_MX_GRID);
+  const dim3 grid((unsigned)(b.spans < cap ? b.spans : cap));
+  switch (b.kinds) {
+    case kMergeCopy: hipLaunchKernelGGL(merge_kernel<kMergeCopy>, grid, dim3(256), 0, s, b); break;
+    case kMergeMxDelta: hipLaunchKernelGGL(merge_kernel<kMergeMxDelta>, grid, dim3(256), 0, s, b); break;
+    case kMergeNvDelta: hipLaunchKernelGGL(merge_kernel<kMergeNvDelta>, grid, dim3(256), 0, s, b); break;
+    default:
+      hipLaunchKernelGGL(merge_kernel<kMergeCopy | kMergeMxDelta | kMergeNvDelta>, grid, dim3(256), 0, s, b);
+  }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

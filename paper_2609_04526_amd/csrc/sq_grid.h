@@ -47,6 +47,66 @@ __device__ __forceinline__ uint32_t e4m3_encode_rne_sat(float x) {
   return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, c, 0, false) & 0xFFu;
 }
 
+// ------------------------------------------------------------------ NVFP4 step
+// A tensor's ws2 with what the NVFP4 grid step needs of it: the ceiling
+// fp32(448 ws2) and r = fp32(1 / ws2), correctly rounded.
+struct Ws2Div {
+  float ws2, r, cap;
+  bool fast;      // ws2 in [2^-64, 2^64]: divide through r (below)
+};
+__device__ __forceinline__ Ws2Div make_ws2_div(float ws2) {
+  Ws2Div w;
+  w.ws2 = ws2;
+  w.r = __fdiv_rn(1.0f, ws2);
+  w.cap = __fmul_rn(448.0f, ws2);
+  w.fast = ws2 >= 0x1p-64f && ws2 <= 0x1p64f;
+  return w;
+}
+
+// fp32(e2 / ws2), correctly rounded (nearest even).  q0 = fp32(e2 r) is
+// within two ulps of the quotient; a Newton step with the remainder
+// e2 - ws2 q0 taken by a fused multiply-add makes it faithful, and a second
+// one rounds it correctly (Markstein's theorem: a faithful quotient corrected
+// through the correctly rounded reciprocal).  That needs the remainders to
+// stay clear of underflow; with ws2 in [2^-64, 2^64] they do for every
+// quotient at or above 2^-26, and smaller quotients round to a signed zero
+// on the E4M3 grid whichever way their last bit goes.  Zeros keep their sign
+// and a quotient past the fp32 range stays infinite (q0); NaN stays NaN.
+// Other ws2 divide directly.
+// FAST = 1 or 0 takes that path without looking at w.fast (callers that
+// branch once per plane); -1 looks.
+template <int FAST = -1>
+__device__ __forceinline__ float div_ws2(float e2, const Ws2Div& w) {
+  if (FAST == 0 || (FAST < 0 && !w.fast)) return __fdiv_rn(e2, w.ws2);
+  const float q0 = __fmul_rn(e2, w.r);
+  const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, w.ws2, e2), w.r, q0);
+  const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, w.ws2, e2), w.r, q1);
+  return (e2 == 0.0f || __builtin_isinf(q0)) ? q0 : q2;
+}
+
+// q = fp32(e2 / ws2) of the NVFP4 step for stored byte b (given as the low
+// byte of `word` shifted to byte SEL) and delta d; `clamped` reports whether
+// the ceiling bound.  The result is at most fp32(cap / ws2) < 449.
+template <int SEL, int FAST = -1>
+__device__ __forceinline__ float nv_step_q(uint32_t word, float d, const Ws2Div& w, bool& clamped) {
+  const float e = __fmul_rn(__builtin_amdgcn_cvt_f32_fp8((int)word, SEL), w.ws2);
+  float e2 = __fadd_rn(e, d);
+  clamped = e2 > w.cap;                       // NaN compares false and is kept
+  e2 = clamped ? w.cap : e2;
+  return div_ws2<FAST>(e2, w);
+}
+
+// Step results go to E4M3 through gfx950's fp8 convert (nearest even).  They
+// lie below 449, whose nearest E4M3 value is 448, so only the lower side needs
+// the clamp at -448 that makes the convert saturate; NaN compares false and
+// passes.  The convert writes NaN as 0xFF: e4m3_nan_canon turns every NaN
+// byte (0x7F or 0xFF; finite values stop at 0x7E / 0xFE) into 0x7F.
+__device__ __forceinline__ float e4m3_prep(float q) { return q < -448.0f ? -448.0f : q; }
+__device__ __forceinline__ uint32_t e4m3_nan_canon(uint32_t w) {
+  const uint32_t nan_bytes = ((w & 0x7F7F7F7Fu) + 0x01010101u) & 0x80808080u;   // bit 7 of each NaN byte
+  return w & ~nan_bytes;
+}
+
 // ------------------------------------------------------------------ update
 // New scale byte for eff' = eff + d rounded onto the grid (round_grid of
 // Section 3); `clamped` reports whether the NVFP4 ceiling min(eff', 448 ws2)
@@ -55,23 +115,33 @@ __device__ __forceinline__ uint32_t e4m3_encode_rne_sat(float x) {
 //          q = fp32(e2 / ws2), b' = E4M3 nearest-even, saturating.
 //   MXFP4: e2 = fp32(2^(b-127) + d), b' = E8M0 of 2^round(log2 e2).
 template <int FMT>
-__device__ __forceinline__ uint32_t grid_update(uint32_t b, float d, float ws2, bool& clamped) {
+__device__ __forceinline__ uint32_t grid_update(uint32_t b, float d, const Ws2Div& w, bool& clamped) {
   if (FMT == kNV) {
-    const float e = __fmul_rn(e4m3_to_f32(b), ws2);
-    float e2 = __fadd_rn(e, d);
-    const float cap = __fmul_rn(448.0f, ws2);
-    clamped = e2 > cap;                         // NaN compares false and is kept
-    e2 = clamped ? cap : e2;
-    return e4m3_encode_rne_sat(__fdiv_rn(e2, ws2));
+    const float q = e4m3_prep(nv_step_q<0>(b, d, w, clamped));
+    return e4m3_nan_canon((uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(q, q, 0, false) & 0xFFu);
   }
   clamped = false;
   return e8m0_encode_log(__fadd_rn(e8m0_to_f32(b), d));
 }
 
 template <int FMT>
-__device__ __forceinline__ uint32_t merge_one_t(uint32_t b, float d, float ws2) {
+__device__ __forceinline__ uint32_t merge_one_t(uint32_t b, float d, const Ws2Div& w) {
   bool clamped;
-  return grid_update<FMT>(b, d, ws2, clamped);
+  return grid_update<FMT>(b, d, w, clamped);
+}
+
+// NVFP4 step of the four bytes of `word` (byte k with delta d[k]).  The same
+// arithmetic as grid_update<kNV>, byte for byte; two converts pack the word.
+typedef float sq_f32x4 __attribute__((ext_vector_type(4)));
+template <int FAST>
+__device__ __forceinline__ uint32_t nv_merge_word(uint32_t word, sq_f32x4 d, const Ws2Div& w) {
+  bool c;
+  const float q0 = e4m3_prep(nv_step_q<0, FAST>(word, d[0], w, c));
+  const float q1 = e4m3_prep(nv_step_q<1, FAST>(word, d[1], w, c));
+  const float q2 = e4m3_prep(nv_step_q<2, FAST>(word, d[2], w, c));
+  const float q3 = e4m3_prep(nv_step_q<3, FAST>(word, d[3], w, c));
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false);
+  return e4m3_nan_canon((uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(q2, q3, lo, true));
 }
 
 }  // namespace sq

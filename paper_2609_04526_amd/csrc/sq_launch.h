@@ -18,18 +18,24 @@ size_t gemm_dscale_workspace(int fmt, int T, int O, int I);
 
 // Planes of one merge launch, as arrays (kernel arguments are limited to
 // 4 KiB; this layout fits 112 planes).  Plane p is cut into spans of
-// kDeltaSpan scales (delta mode) or kCopySpan bytes (copy mode) and owns the
-// spans [span_begin[p], span_begin[p+1]).
+// delta_span(fmt) scales (delta mode) or kCopySpan bytes (copy mode) and owns
+// the spans [span_begin[p], span_begin[p+1]).
 constexpr int kMergePlanesPerLaunch = 112;
-#ifndef SQ_MERGE_DELTA_STEPS
-#define SQ_MERGE_DELTA_STEPS 8
+enum MergeKind { kMergeCopy = 1, kMergeMxDelta = 2, kMergeNvDelta = 4 };
+#ifndef SQ_MERGE_DELTA_STEPS_MX
+#define SQ_MERGE_DELTA_STEPS_MX 8
+#endif
+#ifndef SQ_MERGE_DELTA_STEPS_NV
+#define SQ_MERGE_DELTA_STEPS_NV 16
 #endif
 #ifndef SQ_MERGE_COPY_STEPS
 #define SQ_MERGE_COPY_STEPS 8
 #endif
-constexpr int kDeltaSteps = SQ_MERGE_DELTA_STEPS;
+// steps of 4 scales (and a 16-byte fp32 delta) per lane in one delta span;
+// NVFP4's longer grid step hides better behind more loads in flight
+constexpr int delta_steps(int fmt) { return fmt == 1 ? SQ_MERGE_DELTA_STEPS_NV : SQ_MERGE_DELTA_STEPS_MX; }
+constexpr int delta_span(int fmt) { return 1024 * delta_steps(fmt); }   // 256 lanes x 4 scales per step
 constexpr int kCopySteps = SQ_MERGE_COPY_STEPS;
-constexpr int kDeltaSpan = 1024 * kDeltaSteps;      // 256 lanes x 4 scales per step
 constexpr int kCopySpan = 4096 * kCopySteps;        // 256 lanes x 16 bytes per step
 struct MergeBatch {
   uint8_t* scales[kMergePlanesPerLaunch];
@@ -41,8 +47,7 @@ struct MergeBatch {
   uint8_t mode[kMergePlanesPerLaunch];
   int32_t count;
   int32_t spans;                      // spans of all planes
-  int32_t copy_only;                  // every plane is a copy
-  int32_t nv_delta;                   // some plane is an NVFP4 delta merge
+  int32_t kinds;                      // planes present: kMergeCopy | kMergeMxDelta | kMergeNvDelta
 };
 static_assert(sizeof(MergeBatch) <= 4096, "kernel argument budget");
 int merge_launch(const MergeBatch& b, hipStream_t s);

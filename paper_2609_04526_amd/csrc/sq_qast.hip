@@ -74,13 +74,14 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
   }
   const int g = g0 + gi;
   if (g >= G) return;
+  const Ws2Div wd = make_ws2_div(ws2.v[e]);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int o = o0 + rq + q;
     if (o >= O) break;
     const size_t idx = (rows0 + o) * G + g;
     bool clamped;
-    const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc[q], c), ws2.v[e], clamped);
+    const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc[q], c), wd, clamped);
     out[idx] = (uint8_t)nb;
     if (mask) mask[idx] = clamped ? 0 : 1;
   }

@@ -72,9 +72,10 @@ def test_merge_delta_random_matches_oracle(sq, fmt, n):
     assert guards_intact(buf)
 
 
-@pytest.mark.parametrize("fmt,n", [("mx", 8192 * 5 + 3), ("nv", 8192 * 2 + 4100), ("mx", 8192)])
+@pytest.mark.parametrize("fmt,n", [("mx", 8192 * 5 + 3), ("nv", 16384 * 2 + 4100), ("mx", 8192), ("nv", 16384)])
 def test_merge_delta_full_spans_and_tail(sq, fmt, n):
-    """Planes of several whole workgroup spans (8192 scales) plus a ragged tail."""
+    """Planes of several whole workgroup spans (8192 MXFP4 or 16384 NVFP4
+    scales) plus a ragged tail."""
     g = inputs.rng(91 + n)
     sb = g.integers(90, 150, size=n).astype(np.uint8) if fmt == "mx" else g.integers(0, 0x7E, size=n).astype(np.uint8)
     ws2 = 1.0 if fmt == "mx" else float(np.float32(1 / 448))
@@ -118,6 +119,60 @@ def test_merge_special_values(sq):
     sq.sq_merge_scales("mx", plane, delta=torch.from_numpy(d).cuda())
     torch.cuda.synchronize()
     assert np.array_equal(plane.cpu().numpy(), merge.merge_delta("mx", sb, d))
+
+
+@pytest.mark.parametrize("ws2", [float(np.float32(1 / 448)), 0.37, 3.0e-3, 2.0 ** -70, 2.0 ** 70])
+def test_merge_nv_special_values(sq, ws2):
+    """NVFP4: NaN bytes (0x7F, 0xFF), negative bytes, signed zeros, NaN and
+    infinite deltas, deltas far past the ceiling and far below zero; ws2 both
+    inside and outside the range where the division runs through 1/ws2."""
+    w = np.float32(ws2)
+    sb = np.array([0x00, 0x80, 0x7F, 0xFF, 0x7E, 0xFE, 0x01, 0x81, 0x38, 0xB8, 0x40, 0x08], dtype=np.uint8)
+    ds = np.array([0.0, -0.0, np.nan, -np.nan, np.inf, -np.inf, 3.0e38, -3.0e38, 1e-45, -1e-45,
+                   float(w) * 1000, -float(w) * 1000, float(w) * 0.0009765625, -float(w) * 0.0009765625],
+                  dtype=np.float32)
+    b = np.repeat(sb, ds.size)
+    d = np.tile(ds, sb.size)
+    b = np.tile(b, 3)
+    d = np.tile(d, 3)
+    buf, plane = guarded(b)
+    print(f"[merge nv special] ws2={ws2} n={b.size}", flush=True)
+    sq.sq_merge_scales("nv", plane, delta=torch.from_numpy(d).cuda(), ws2=ws2)
+    torch.cuda.synchronize()
+    got = plane.cpu().numpy()
+    ref = merge.merge_delta("nv", b, d, ws2)
+    bad = np.flatnonzero(got != ref)
+    assert bad.size == 0, [(int(b[i]), float(d[i]), int(got[i]), int(ref[i])) for i in bad[:8]]
+    assert guards_intact(buf)
+
+
+@pytest.mark.parametrize("ws2", [float(np.float32(1 / 448)), 0.0123, 2.0 ** -60, 5.5e17])
+def test_merge_nv_quotients_at_e4m3_midpoints(sq, ws2):
+    """NVFP4 deltas that put e2 / ws2 within a few fp32 ulps of every E4M3
+    rounding midpoint (and of the values themselves), positive and negative:
+    an ulp of error in the division would move bytes across a midpoint."""
+    w = np.float32(ws2)
+    vals = codec.E4M3_TABLE[:0x7F].astype(np.float64)
+    pos = np.unique(vals[vals >= 0])
+    mids = (pos[:-1] + pos[1:]) / 2
+    targets = np.concatenate([mids, pos, -mids, -pos]).astype(np.float32)
+    k = np.arange(-6, 7)
+    t = targets[:, None]
+    q = (t.astype(np.float64) * (1.0 + k[None, :] * 2.0 ** -23)).astype(np.float32).ravel()
+    g = inputs.rng(4242)
+    base = g.integers(0, 0x7F, size=q.size).astype(np.uint8)
+    e = (codec.E4M3_TABLE[base].astype(np.float32) * w).astype(np.float32)
+    e2_target = (q.astype(np.float64) * float(w)).astype(np.float32)
+    d = (e2_target.astype(np.float64) - e.astype(np.float64)).astype(np.float32)
+    buf, plane = guarded(base)
+    print(f"[merge nv midpoints] ws2={ws2} n={base.size}", flush=True)
+    sq.sq_merge_scales("nv", plane, delta=torch.from_numpy(d).cuda(), ws2=ws2)
+    torch.cuda.synchronize()
+    got = plane.cpu().numpy()
+    ref = merge.merge_delta("nv", base, d, ws2)
+    bad = np.flatnonzero(got != ref)
+    assert bad.size == 0, [(int(base[i]), float(d[i]), int(got[i]), int(ref[i])) for i in bad[:8]]
+    assert guards_intact(buf)
 
 
 def test_swap_and_grouped_merge_leave_codes_untouched(sq):
