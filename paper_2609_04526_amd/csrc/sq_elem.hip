@@ -113,7 +113,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
       merge_copy_span(sc, static_cast<const uint8_t*>(batch.aux[pi]), n, rel * kCopySpan, tid);
     } else if ((KINDS & kMergeNvDelta) && (KINDS == kMergeNvDelta || batch.fmt[pi] == kNV)) {
       const Ws2Div w = make_ws2_div(batch.ws2[pi]);
-      if (w.fast)
+      if (w.div.fast)
         merge_delta_span<kNV, 1>(sc, dl, n, rel * delta_span(kNV), w, tid);
       else
         merge_delta_span<kNV, 0>(sc, dl, n, rel * delta_span(kNV), w, tid);
@@ -149,6 +149,9 @@ int merge_launch(const MergeBatch& b, hipStream_t s) {
 // ------------------------------------------------------------------ RTN
 // Each workgroup takes 512 chunks: a lane loads its two chunks (c and c + 256)
 // before working on either, so two 16-byte loads are in flight per lane.
+// (A grid-stride form with 2 to 8 chunks per lane in flight ran slower on the
+// 8B model's weights: the per-chunk work is long enough that short-lived
+// workgroups keep more loads in flight across the chip.)
 template <int FMT, int RULE>
 __global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W, int64_t n_chunks,
                                                   const float* ws2_ptr, float ws2_val, const float* amax_t,

@@ -47,41 +47,53 @@ __device__ __forceinline__ uint32_t e4m3_encode_rne_sat(float x) {
   return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, c, 0, false) & 0xFFu;
 }
 
+// ------------------------------------------------------------------ division
+// A divisor with its correctly rounded reciprocal r = fp32(1 / d).
+struct RcpDivisor {
+  float d, r;
+  bool fast;      // d in [2^-64, 2^64]: divide through r (div_exact)
+};
+__device__ __forceinline__ RcpDivisor make_rcp_divisor(float d) {
+  RcpDivisor v;
+  v.d = d;
+  v.r = __fdiv_rn(1.0f, d);
+  v.fast = d >= 0x1p-64f && d <= 0x1p64f;
+  return v;
+}
+
+// fp32(x / d), correctly rounded (nearest even).  q0 = fp32(x r) is within
+// two ulps of the quotient; a Newton step with the remainder x - d q0 taken by
+// a fused multiply-add makes it faithful, and a second one rounds it correctly
+// (Markstein's theorem: a faithful quotient corrected through the correctly
+// rounded reciprocal).  That needs the remainders to stay clear of underflow;
+// with d in [2^-64, 2^64] they do for every quotient at or above 2^-26, and
+// the callers round smaller quotients to a signed zero (E4M3 or E2M1)
+// whichever way their last bit goes.  Zeros keep their sign and a quotient
+// past the fp32 range stays infinite (q0); NaN stays NaN.  Other divisors
+// divide directly.  FAST = 1 or 0 takes that path without looking at
+// v.fast (callers that branch once per plane); -1 looks.
+template <int FAST = -1>
+__device__ __forceinline__ float div_exact(float x, const RcpDivisor& v) {
+  if (FAST == 0 || (FAST < 0 && !v.fast)) return __fdiv_rn(x, v.d);
+  const float q0 = __fmul_rn(x, v.r);
+  const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, v.d, x), v.r, q0);
+  const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, v.d, x), v.r, q1);
+  return (x == 0.0f || __builtin_isinf(q0)) ? q0 : q2;
+}
+
 // ------------------------------------------------------------------ NVFP4 step
-// A tensor's ws2 with what the NVFP4 grid step needs of it: the ceiling
-// fp32(448 ws2) and r = fp32(1 / ws2), correctly rounded.
+// A tensor's ws2 with what the NVFP4 grid step needs of it: the divisor and
+// the ceiling fp32(448 ws2).
 struct Ws2Div {
-  float ws2, r, cap;
-  bool fast;      // ws2 in [2^-64, 2^64]: divide through r (below)
+  RcpDivisor div;
+  float ws2, cap;
 };
 __device__ __forceinline__ Ws2Div make_ws2_div(float ws2) {
   Ws2Div w;
+  w.div = make_rcp_divisor(ws2);
   w.ws2 = ws2;
-  w.r = __fdiv_rn(1.0f, ws2);
   w.cap = __fmul_rn(448.0f, ws2);
-  w.fast = ws2 >= 0x1p-64f && ws2 <= 0x1p64f;
   return w;
-}
-
-// fp32(e2 / ws2), correctly rounded (nearest even).  q0 = fp32(e2 r) is
-// within two ulps of the quotient; a Newton step with the remainder
-// e2 - ws2 q0 taken by a fused multiply-add makes it faithful, and a second
-// one rounds it correctly (Markstein's theorem: a faithful quotient corrected
-// through the correctly rounded reciprocal).  That needs the remainders to
-// stay clear of underflow; with ws2 in [2^-64, 2^64] they do for every
-// quotient at or above 2^-26, and smaller quotients round to a signed zero
-// on the E4M3 grid whichever way their last bit goes.  Zeros keep their sign
-// and a quotient past the fp32 range stays infinite (q0); NaN stays NaN.
-// Other ws2 divide directly.
-// FAST = 1 or 0 takes that path without looking at w.fast (callers that
-// branch once per plane); -1 looks.
-template <int FAST = -1>
-__device__ __forceinline__ float div_ws2(float e2, const Ws2Div& w) {
-  if (FAST == 0 || (FAST < 0 && !w.fast)) return __fdiv_rn(e2, w.ws2);
-  const float q0 = __fmul_rn(e2, w.r);
-  const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, w.ws2, e2), w.r, q0);
-  const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, w.ws2, e2), w.r, q1);
-  return (e2 == 0.0f || __builtin_isinf(q0)) ? q0 : q2;
 }
 
 // q = fp32(e2 / ws2) of the NVFP4 step for stored byte b (given as the low
@@ -93,7 +105,7 @@ __device__ __forceinline__ float nv_step_q(uint32_t word, float d, const Ws2Div&
   float e2 = __fadd_rn(e, d);
   clamped = e2 > w.cap;                       // NaN compares false and is kept
   e2 = clamped ? w.cap : e2;
-  return div_ws2<FAST>(e2, w);
+  return div_exact<FAST>(e2, w.div);
 }
 
 // Step results go to E4M3 through gfx950's fp8 convert (nearest even).  They

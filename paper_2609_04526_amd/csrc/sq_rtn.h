@@ -134,11 +134,13 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
   // |q| = 0.25, 1.25, 2.5 and 5, where they take the next magnitude.  A NaN q
   // codes as magnitude 0, and the sign bit is always the sign of w.
   float q[8];
+  RcpDivisor ed;                                            // NVFP4: q = w / eff, exactly (div_exact)
+  if (FMT == kNV) ed = make_rcp_divisor(eff);
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     const float w = __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16);
     if (FMT == kMX) q[k] = __fmul_rn(w, eff);               // w / 2^k, one rounding
-    else q[k] = (eff == 0.0f) ? 0.0f : __fdiv_rn(w, eff);
+    else q[k] = (eff == 0.0f) ? 0.0f : div_exact(w, ed);
   }
   uint32_t packed = 0;
 #pragma unroll
