@@ -1272,8 +1272,10 @@ static int launch_grouped(GemmGroup& gg, const ExpertProblem* p, int n, hipStrea
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
-// The large tile when the experts' tiles fill the chip and (for the forward
-// and dX, whose rows are tokens) an expert averages at least 512 tokens.
+// The large tile when the experts' tiles fill the chip and an expert averages
+// at least 512 tokens (rows of the forward and dX, the contraction of dS:
+// shorter token sums leave a 256 x 256 dS tile a few stages between its
+// prologue and epilogue, where two 128 x 128 workgroups per CU do better).
 template <int MODE, int FMT, int BM, int BN, int... REST>
 static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
   int64_t tokens = 0, big = 0;
@@ -1282,7 +1284,7 @@ static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream
     const int M = MODE == kDs ? gg.base.M : p[e].T;
     big += (int64_t)((M + BM - 1) / BM) * ((gg.base.N + BN - 1) / BN);
   }
-  const bool large = big >= kCUs && (MODE == kDs || tokens >= (int64_t)512 * n);
+  const bool large = big >= kCUs && tokens >= (int64_t)512 * n;
   if (large) return launch_grouped<MODE, FMT, BM, BN, REST...>(gg, p, n, s);
   return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
 }
