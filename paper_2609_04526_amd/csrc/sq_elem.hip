@@ -18,9 +18,6 @@
 namespace sq {
 
 // merge tuning knobs (build-time)
-#ifndef SQ_MERGE_NT_STORE
-#define SQ_MERGE_NT_STORE 0
-#endif
 
 // ------------------------------------------------------------------ merge
 // The planes of a launch are cut into spans: delta_span(fmt) scale bytes (delta
@@ -36,7 +33,10 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef sq_f32x4 f32x4_t;
 
 // One delta span: delta_steps(FMT) steps of 4 scales per lane, all loads
-// issued before any compute.
+// issued before any compute.  Scale bytes are written with streaming stores;
+// NVFP4 planes (2x the bytes of MXFP4's, well past the 256 MB last-level
+// cache between whole-model merges) also read them with streaming loads,
+// which on MXFP4 planes measured slower.
 template <int FMT, int FAST>
 __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const float* __restrict__ dl, int64_t n,
                                                  int64_t off, const Ws2Div& ws2, int tid) {
@@ -47,7 +47,10 @@ __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const
 #pragma unroll
     for (int g = 0; g < kDeltaSteps; ++g) {
       const int64_t i = off + g * 1024 + tid * 4;
-      sv[g] = *reinterpret_cast<const uint32_t*>(sc + i);
+      if constexpr (FMT == kNV)
+        sv[g] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(sc + i));
+      else
+        sv[g] = *reinterpret_cast<const uint32_t*>(sc + i);
       dv[g] = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(dl + i));
     }
 #pragma unroll
@@ -61,13 +64,8 @@ __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const
                 (merge_one_t<FMT>(v >> 24, dv[g][3], ws2) << 24);
     }
 #pragma unroll
-    for (int g = 0; g < kDeltaSteps; ++g) {
-#if SQ_MERGE_NT_STORE
+    for (int g = 0; g < kDeltaSteps; ++g)
       __builtin_nontemporal_store(sv[g], reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4));
-#else
-      *reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4) = sv[g];
-#endif
-    }
   } else {
     for (int64_t k = off + tid; k < n && k < off + kDeltaSpan; k += 256)
       sc[k] = (uint8_t)merge_one_t<FMT>(sc[k], dl[k], ws2);
