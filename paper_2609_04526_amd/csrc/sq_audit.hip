@@ -9,8 +9,8 @@
 // per-tensor ws2 is common to both sides and stays out), 2^(b-127) for
 // MXFP4.  Two such values within 24 binades differ by an fp32-representable
 // amount, so the subtraction is exact and rollback re-encodes the exact base.
-// All three stream with the merge's grid-stride order: 4 scales (or 16 bytes)
-// per lane per step, the whole grid inside one window of the planes.
+// All three stream with the merge's grid-stride order, the whole grid inside
+// one window of the planes.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -32,22 +32,48 @@ __device__ __forceinline__ uint32_t field_encode(float v) {
   return FMT == kNV ? e4m3_encode_rne_sat(v) : e8m0_encode_log(v);
 }
 
+// Both kernels take spans of kAuditSteps x 1024 scales: a lane issues all
+// kAuditSteps of its 4-scale loads before computing, and workgroup w takes
+// spans w, w + grid, ...  Outputs are written with streaming stores, and the
+// scale planes of NVFP4 (the larger ones) are read with streaming loads, as
+// in the merge.
+#ifndef SQ_AUDIT_STEPS
+#define SQ_AUDIT_STEPS 8
+#endif
+constexpr int kAuditSteps = SQ_AUDIT_STEPS;
+constexpr int64_t kAuditSpan = 1024 * kAuditSteps;
+
+template <int FMT>
+__device__ __forceinline__ uint32_t load_scales4(const uint8_t* p) {
+  if constexpr (FMT == kNV) return __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
+  else return *reinterpret_cast<const uint32_t*>(p);
+}
+
 template <int FMT>
 __global__ __launch_bounds__(256) void applied_kernel(const uint8_t* __restrict__ before,
                                                       const uint8_t* __restrict__ after, float* __restrict__ applied,
                                                       int64_t n) {
-  const int64_t stride = (int64_t)gridDim.x * 1024;
-  for (int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4; i < n; i += stride) {
-    if (i + 4 <= n) {
-      const uint32_t b0 = *reinterpret_cast<const uint32_t*>(before + i);
-      const uint32_t b1 = *reinterpret_cast<const uint32_t*>(after + i);
-      f32x4a_t d;
+  const int tid = threadIdx.x;
+  for (int64_t off = (int64_t)blockIdx.x * kAuditSpan; off < n; off += (int64_t)gridDim.x * kAuditSpan) {
+    if (off + kAuditSpan <= n) {
+      uint32_t b0[kAuditSteps], b1[kAuditSteps];
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        d[k] = __fsub_rn(field_value<FMT>((b1 >> (8 * k)) & 0xFFu), field_value<FMT>((b0 >> (8 * k)) & 0xFFu));
-      *reinterpret_cast<f32x4a_t*>(applied + i) = d;
+      for (int g = 0; g < kAuditSteps; ++g) {
+        const int64_t i = off + g * 1024 + tid * 4;
+        b0[g] = load_scales4<FMT>(before + i);
+        b1[g] = load_scales4<FMT>(after + i);
+      }
+#pragma unroll
+      for (int g = 0; g < kAuditSteps; ++g) {
+        f32x4a_t d;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          d[k] = __fsub_rn(field_value<FMT>((b1[g] >> (8 * k)) & 0xFFu), field_value<FMT>((b0[g] >> (8 * k)) & 0xFFu));
+        __builtin_nontemporal_store(d, reinterpret_cast<f32x4a_t*>(applied + off + g * 1024 + tid * 4));
+      }
     } else {
-      for (int64_t k = i; k < n; ++k) applied[k] = __fsub_rn(field_value<FMT>(after[k]), field_value<FMT>(before[k]));
+      for (int64_t k = off + tid; k < n && k < off + kAuditSpan; k += 256)
+        applied[k] = __fsub_rn(field_value<FMT>(after[k]), field_value<FMT>(before[k]));
     }
   }
 }
@@ -55,18 +81,28 @@ __global__ __launch_bounds__(256) void applied_kernel(const uint8_t* __restrict_
 template <int FMT>
 __global__ __launch_bounds__(256) void rollback_kernel(uint8_t* __restrict__ sc, const float* __restrict__ applied,
                                                        int64_t n) {
-  const int64_t stride = (int64_t)gridDim.x * 1024;
-  for (int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4; i < n; i += stride) {
-    if (i + 4 <= n) {
-      const uint32_t b = *reinterpret_cast<const uint32_t*>(sc + i);
-      const f32x4a_t d = __builtin_nontemporal_load(reinterpret_cast<const f32x4a_t*>(applied + i));
-      uint32_t out = 0;
+  const int tid = threadIdx.x;
+  for (int64_t off = (int64_t)blockIdx.x * kAuditSpan; off < n; off += (int64_t)gridDim.x * kAuditSpan) {
+    if (off + kAuditSpan <= n) {
+      uint32_t b[kAuditSteps];
+      f32x4a_t d[kAuditSteps];
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        out |= field_encode<FMT>(__fsub_rn(field_value<FMT>((b >> (8 * k)) & 0xFFu), d[k])) << (8 * k);
-      *reinterpret_cast<uint32_t*>(sc + i) = out;
+      for (int g = 0; g < kAuditSteps; ++g) {
+        const int64_t i = off + g * 1024 + tid * 4;
+        b[g] = load_scales4<FMT>(sc + i);
+        d[g] = __builtin_nontemporal_load(reinterpret_cast<const f32x4a_t*>(applied + i));
+      }
+#pragma unroll
+      for (int g = 0; g < kAuditSteps; ++g) {
+        uint32_t out = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          out |= field_encode<FMT>(__fsub_rn(field_value<FMT>((b[g] >> (8 * k)) & 0xFFu), d[g][k])) << (8 * k);
+        __builtin_nontemporal_store(out, reinterpret_cast<uint32_t*>(sc + off + g * 1024 + tid * 4));
+      }
     } else {
-      for (int64_t k = i; k < n; ++k) sc[k] = (uint8_t)field_encode<FMT>(__fsub_rn(field_value<FMT>(sc[k]), applied[k]));
+      for (int64_t k = off + tid; k < n && k < off + kAuditSpan; k += 256)
+        sc[k] = (uint8_t)field_encode<FMT>(__fsub_rn(field_value<FMT>(sc[k]), applied[k]));
     }
   }
 }
@@ -123,9 +159,17 @@ static unsigned stream_grid(int64_t n, int64_t per_wg) {
   return (unsigned)(want < 4096 ? (want > 0 ? want : 1) : 4096);
 }
 
+#ifndef SQ_AUDIT_GRID
+#define SQ_AUDIT_GRID 16384
+#endif
+static unsigned span_grid(int64_t n) {
+  const int64_t want = (n + kAuditSpan - 1) / kAuditSpan;
+  return (unsigned)(want < SQ_AUDIT_GRID ? want : SQ_AUDIT_GRID);
+}
+
 int applied_launch(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied, hipStream_t s) {
   if (n <= 0) return 0;
-  const unsigned g = stream_grid(n, 1024);
+  const unsigned g = span_grid(n);
   if (fmt == kMX) hipLaunchKernelGGL(applied_kernel<kMX>, dim3(g), dim3(256), 0, s, before, after, applied, n);
   else hipLaunchKernelGGL(applied_kernel<kNV>, dim3(g), dim3(256), 0, s, before, after, applied, n);
   return hipGetLastError() == hipSuccess ? 0 : -1;
@@ -133,7 +177,7 @@ int applied_launch(int fmt, int64_t n, const uint8_t* before, const uint8_t* aft
 
 int rollback_launch(int fmt, int64_t n, uint8_t* scales, const float* applied, hipStream_t s) {
   if (n <= 0) return 0;
-  const unsigned g = stream_grid(n, 1024);
+  const unsigned g = span_grid(n);
   if (fmt == kMX) hipLaunchKernelGGL(rollback_kernel<kMX>, dim3(g), dim3(256), 0, s, scales, applied, n);
   else hipLaunchKernelGGL(rollback_kernel<kNV>, dim3(g), dim3(256), 0, s, scales, applied, n);
   return hipGetLastError() == hipSuccess ? 0 : -1;
