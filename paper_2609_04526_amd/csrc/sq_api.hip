@@ -68,16 +68,21 @@ int check_merge_plane(int fmt, int64_t n, const uint8_t* scales, const float* de
 }
 
 int run_merge(int n_desc, const sq_merge_desc* d, hipStream_t s) {
+  int64_t total = 0;
+  for (int k = 0; k < n_desc; ++k) total += d[k].n;
+  const bool small = total < sq::kMergeSmallScales;
   sq::MergeBatch batch{};
+  batch.small = small;
   int64_t spans = 0;
   for (int k = 0; k < n_desc; ++k) {
     if (d[k].n == 0) continue;
-    const int64_t unit = d[k].mode == SQ_MERGE_COPY ? sq::kCopySpan : sq::delta_span(d[k].fmt);
+    const int64_t unit = d[k].mode == SQ_MERGE_COPY ? sq::copy_span(small) : sq::delta_span(d[k].fmt, small);
     const int64_t c = (d[k].n + unit - 1) / unit;
     if (batch.count == sq::kMergePlanesPerLaunch || spans + c > INT32_MAX) {
       batch.spans = (int32_t)spans;
       if (sq::merge_launch(batch, s) != 0) return SQ_ERR_HIP;
       batch = sq::MergeBatch{};
+      batch.small = small;
       spans = 0;
     }
     const int p = batch.count++;

@@ -20,9 +20,10 @@ namespace sq {
 // merge tuning knobs (build-time)
 
 // ------------------------------------------------------------------ merge
-// The planes of a launch are cut into spans: delta_span(fmt) scale bytes (delta
-// mode: delta_steps(fmt) steps of 4 scales and a 16-byte fp32 delta per lane) or
-// kCopySpan bytes (copy mode: kCopySteps steps of 16 bytes per lane).  Workgroup w takes spans w, w + grid,
+// The planes of a launch are cut into spans: delta_span(fmt, small) scale bytes
+// (delta mode: delta_steps(fmt, small) steps of 4 scales and a 16-byte fp32
+// delta per lane) or copy_span(small) bytes (copy mode: copy_steps(small)
+// steps of 16 bytes per lane).  Workgroup w takes spans w, w + grid,
 // w + 2 grid, ...: at any moment the whole grid streams through one window of
 // the planes, which keeps the DRAM accesses of all workgroups together (a
 // workgroup walking a private region of its own streams markedly slower).
@@ -37,10 +38,10 @@ typedef sq_f32x4 f32x4_t;
 // NVFP4 planes (2x the bytes of MXFP4's, well past the 256 MB last-level
 // cache between whole-model merges) also read them with streaming loads,
 // which on MXFP4 planes measured slower.
-template <int FMT, int FAST>
+template <int FMT, int FAST, bool SMALL>
 __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const float* __restrict__ dl, int64_t n,
                                                  int64_t off, const Ws2Div& ws2, int tid) {
-  constexpr int kDeltaSteps = delta_steps(FMT), kDeltaSpan = delta_span(FMT);
+  constexpr int kDeltaSteps = delta_steps(FMT, SMALL), kDeltaSpan = delta_span(FMT, SMALL);
   if (off + kDeltaSpan <= n) {
     uint32_t sv[kDeltaSteps];
     f32x4_t dv[kDeltaSteps];
@@ -72,9 +73,11 @@ __device__ __forceinline__ void merge_delta_span(uint8_t* __restrict__ sc, const
   }
 }
 
-// One copy span: kCopySteps steps of 16 bytes per lane, loads first.
+// One copy span: copy_steps(SMALL) steps of 16 bytes per lane, loads first.
+template <bool SMALL>
 __device__ __forceinline__ void merge_copy_span(uint8_t* __restrict__ sc, const uint8_t* __restrict__ sr, int64_t n,
                                                 int64_t off, int tid) {
+  constexpr int kCopySteps = copy_steps(SMALL), kCopySpan = copy_span(SMALL);
   if (off + kCopySpan <= n) {
     u32x4_t v[kCopySteps];
 #pragma unroll
@@ -90,7 +93,7 @@ __device__ __forceinline__ void merge_copy_span(uint8_t* __restrict__ sc, const 
 // KINDS: the plane kinds this instance handles (a launch whose planes are all
 // of one kind gets an instance with that kind's code alone, and so that
 // kind's register budget and occupancy).
-template <int KINDS>
+template <int KINDS, bool SMALL>
 __global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
   (void)batch_arg;
   // The batch is the kernel's only explicit argument, so it sits at offset 0
@@ -108,15 +111,15 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeBatch batch_arg) {
     const int64_t rel = span - batch.span_begin[pi];
     const float* __restrict__ dl = static_cast<const float*>(batch.aux[pi]);
     if ((KINDS & kMergeCopy) && batch.mode[pi] == 1) {
-      merge_copy_span(sc, static_cast<const uint8_t*>(batch.aux[pi]), n, rel * kCopySpan, tid);
+      merge_copy_span<SMALL>(sc, static_cast<const uint8_t*>(batch.aux[pi]), n, rel * copy_span(SMALL), tid);
     } else if ((KINDS & kMergeNvDelta) && (KINDS == kMergeNvDelta || batch.fmt[pi] == kNV)) {
       const Ws2Div w = make_ws2_div(batch.ws2[pi]);
       if (w.div.fast)
-        merge_delta_span<kNV, 1>(sc, dl, n, rel * delta_span(kNV), w, tid);
+        merge_delta_span<kNV, 1, SMALL>(sc, dl, n, rel * delta_span(kNV, SMALL), w, tid);
       else
-        merge_delta_span<kNV, 0>(sc, dl, n, rel * delta_span(kNV), w, tid);
+        merge_delta_span<kNV, 0, SMALL>(sc, dl, n, rel * delta_span(kNV, SMALL), w, tid);
     } else if (KINDS & kMergeMxDelta) {
-      merge_delta_span<kMX, 0>(sc, dl, n, rel * delta_span(kMX), make_ws2_div(1.0f), tid);
+      merge_delta_span<kMX, 0, SMALL>(sc, dl, n, rel * delta_span(kMX, SMALL), make_ws2_div(1.0f), tid);
     }
   }
 }
@@ -134,12 +137,24 @@ int merge_launch(const MergeBatch& b, hipStream_t s) {
 #endif
   const int64_t cap = b.kinds == kMergeCopy ? 2048 : ((b.kinds & kMergeNvDelta) ? SQ_MERGE_NV_GRID : SQ_MERGE_MX_GRID);
   const dim3 grid((unsigned)(b.spans < cap ? b.spans : cap));
+  if (b.small) {
+    // few scales in all: one-step spans, one workgroup each
+    const dim3 all((unsigned)b.spans);
+    switch (b.kinds) {
+      case kMergeCopy: hipLaunchKernelGGL((merge_kernel<kMergeCopy, true>), all, dim3(256), 0, s, b); break;
+      case kMergeMxDelta: hipLaunchKernelGGL((merge_kernel<kMergeMxDelta, true>), all, dim3(256), 0, s, b); break;
+      case kMergeNvDelta: hipLaunchKernelGGL((merge_kernel<kMergeNvDelta, true>), all, dim3(256), 0, s, b); break;
+      default:
+        hipLaunchKernelGGL((merge_kernel<kMergeCopy | kMergeMxDelta | kMergeNvDelta, true>), all, dim3(256), 0, s, b);
+    }
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+  }
   switch (b.kinds) {
-    case kMergeCopy: hipLaunchKernelGGL(merge_kernel<kMergeCopy>, grid, dim3(256), 0, s, b); break;
-    case kMergeMxDelta: hipLaunchKernelGGL(merge_kernel<kMergeMxDelta>, grid, dim3(256), 0, s, b); break;
-    case kMergeNvDelta: hipLaunchKernelGGL(merge_kernel<kMergeNvDelta>, grid, dim3(256), 0, s, b); break;
+    case kMergeCopy: hipLaunchKernelGGL((merge_kernel<kMergeCopy, false>), grid, dim3(256), 0, s, b); break;
+    case kMergeMxDelta: hipLaunchKernelGGL((merge_kernel<kMergeMxDelta, false>), grid, dim3(256), 0, s, b); break;
+    case kMergeNvDelta: hipLaunchKernelGGL((merge_kernel<kMergeNvDelta, false>), grid, dim3(256), 0, s, b); break;
     default:
-      hipLaunchKernelGGL(merge_kernel<kMergeCopy | kMergeMxDelta | kMergeNvDelta>, grid, dim3(256), 0, s, b);
+      hipLaunchKernelGGL((merge_kernel<kMergeCopy | kMergeMxDelta | kMergeNvDelta, false>), grid, dim3(256), 0, s, b);
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -18,8 +18,8 @@ size_t gemm_dscale_workspace(int fmt, int T, int O, int I);
 
 // Planes of one merge launch, as arrays (kernel arguments are limited to
 // 4 KiB; this layout fits 112 planes).  Plane p is cut into spans of
-// delta_span(fmt) scales (delta mode) or kCopySpan bytes (copy mode) and owns
-// the spans [span_begin[p], span_begin[p+1]).
+// delta_span(fmt, small) scales (delta mode) or copy_span(small) bytes (copy
+// mode) and owns the spans [span_begin[p], span_begin[p+1]).
 constexpr int kMergePlanesPerLaunch = 112;
 enum MergeKind { kMergeCopy = 1, kMergeMxDelta = 2, kMergeNvDelta = 4 };
 #ifndef SQ_MERGE_DELTA_STEPS_MX
@@ -31,12 +31,20 @@ enum MergeKind { kMergeCopy = 1, kMergeMxDelta = 2, kMergeNvDelta = 4 };
 #ifndef SQ_MERGE_COPY_STEPS
 #define SQ_MERGE_COPY_STEPS 8
 #endif
-// steps of 4 scales (and a 16-byte fp32 delta) per lane in one delta span;
-// NVFP4's longer grid step hides better behind more loads in flight
-constexpr int delta_steps(int fmt) { return fmt == 1 ? SQ_MERGE_DELTA_STEPS_NV : SQ_MERGE_DELTA_STEPS_MX; }
-constexpr int delta_span(int fmt) { return 1024 * delta_steps(fmt); }   // 256 lanes x 4 scales per step
-constexpr int kCopySteps = SQ_MERGE_COPY_STEPS;
-constexpr int kCopySpan = 4096 * kCopySteps;        // 256 lanes x 16 bytes per step
+// Steps of 4 scales (and a 16-byte fp32 delta) per lane in one delta span;
+// NVFP4's longer grid step hides better behind more loads in flight.  A
+// launch over few scales (below kMergeSmallScales in all) takes one-step
+// spans instead, so that it still spreads over the CUs.
+#ifndef SQ_MERGE_SMALL_SCALES
+#define SQ_MERGE_SMALL_SCALES (int64_t(1) << 24)
+#endif
+constexpr int64_t kMergeSmallScales = SQ_MERGE_SMALL_SCALES;
+constexpr int delta_steps(int fmt, bool small = false) {
+  return small ? 1 : (fmt == 1 ? SQ_MERGE_DELTA_STEPS_NV : SQ_MERGE_DELTA_STEPS_MX);
+}
+constexpr int delta_span(int fmt, bool small = false) { return 1024 * delta_steps(fmt, small); }   // 256 lanes x 4 scales per step
+constexpr int copy_steps(bool small = false) { return small ? 1 : SQ_MERGE_COPY_STEPS; }
+constexpr int copy_span(bool small = false) { return 4096 * copy_steps(small); }    // 256 lanes x 16 bytes per step
 struct MergeBatch {
   uint8_t* scales[kMergePlanesPerLaunch];
   const void* aux[kMergePlanesPerLaunch];     // fp32 delta (delta mode) or source bytes (copy mode)
@@ -48,6 +56,7 @@ struct MergeBatch {
   int32_t count;
   int32_t spans;                      // spans of all planes
   int32_t kinds;                      // planes present: kMergeCopy | kMergeMxDelta | kMergeNvDelta
+  int32_t small;                      // one-step spans (the whole call covers few scales)
 };
 static_assert(sizeof(MergeBatch) <= 4096, "kernel argument budget");
 int merge_launch(const MergeBatch& b, hipStream_t s);

@@ -72,10 +72,16 @@ def test_merge_delta_random_matches_oracle(sq, fmt, n):
     assert guards_intact(buf)
 
 
-@pytest.mark.parametrize("fmt,n", [("mx", 8192 * 5 + 3), ("nv", 16384 * 2 + 4100), ("mx", 8192), ("nv", 16384)])
+LARGE = 1 << 24       # calls over this many scales in all take the multi-step spans
+
+
+@pytest.mark.parametrize("fmt,n", [("mx", 8192 * 5 + 3), ("nv", 16384 * 2 + 4100), ("mx", 8192), ("nv", 16384),
+                                   ("mx", 1024 * 7 + 1), ("nv", 1024),
+                                   ("mx", LARGE + 8192 * 5 + 3), ("nv", LARGE + 16384 * 2 + 4100)])
 def test_merge_delta_full_spans_and_tail(sq, fmt, n):
-    """Planes of several whole workgroup spans (8192 MXFP4 or 16384 NVFP4
-    scales) plus a ragged tail."""
+    """Planes of several whole workgroup spans plus a ragged tail: one-step
+    spans of 1024 scales below LARGE scales, multi-step spans (8192 MXFP4 or
+    16384 NVFP4 scales) above."""
     g = inputs.rng(91 + n)
     sb = g.integers(90, 150, size=n).astype(np.uint8) if fmt == "mx" else g.integers(0, 0x7E, size=n).astype(np.uint8)
     ws2 = 1.0 if fmt == "mx" else float(np.float32(1 / 448))
@@ -88,9 +94,10 @@ def test_merge_delta_full_spans_and_tail(sq, fmt, n):
     assert guards_intact(buf)
 
 
-@pytest.mark.parametrize("n", [32768 * 3 + 100, 32768, 32768 * 2 + 16])
+@pytest.mark.parametrize("n", [32768 * 3 + 100, 32768, 32768 * 2 + 16, 4096 * 5 + 7, LARGE + 32768 * 2 + 100])
 def test_swap_full_spans_and_tail(sq, n):
-    """Copies of several whole workgroup spans (32 KiB) plus a ragged tail."""
+    """Copies of several whole workgroup spans (4 KiB one-step spans below
+    LARGE bytes, 32 KiB above) plus a ragged tail."""
     g = inputs.rng(93 + n)
     sb = g.integers(0, 256, size=n).astype(np.uint8)
     src = g.integers(0, 256, size=n).astype(np.uint8)
@@ -175,14 +182,18 @@ def test_merge_nv_quotients_at_e4m3_midpoints(sq, ws2):
     assert guards_intact(buf)
 
 
-def test_swap_and_grouped_merge_leave_codes_untouched(sq):
+@pytest.mark.parametrize("rows", [1, 256])
+def test_swap_and_grouped_merge_leave_codes_untouched(sq, rows):
     """A model-like set of planes: swap some, merge others, in one grouped call;
-    the code planes (held next to them) keep their bytes."""
+    the code planes (held next to them) keep their bytes.  rows = 256 puts the
+    call above LARGE scales (multi-step spans)."""
     planes = []
     refs = []
     code_planes = []
     shapes = [("mx", 64, 4096), ("nv", 96, 4096), ("mx", 32, 14336), ("nv", 40, 14336), ("mx", 8, 1024)]
+    assert (sum(O * I // codec.BLOCK[f] for f, O, I in shapes) * rows > LARGE) == (rows > 1)
     for k, (fmt, O, I) in enumerate(shapes):
+        O *= rows
         B = codec.BLOCK[fmt]
         if fmt == "mx":
             sb = inputs.e8m0_normal_exponents(500 + k, O, I // B, -6, 1.5)
