@@ -220,9 +220,10 @@ def model_merge(sq, steps):
 def model_lifecycle(sq, steps=3):
     """The naive merge's re-quantisation over the whole 8B model: for every
     linear, the bf16 merged weight W + B A (rank 16, A, B ~ N(0, 0.02), W the
-    dequantised base) re-quantised by rtn_quantize with ties to even and ties
-    away, and by rtn_quantize_rule under the deploy-side rules (toward zero,
-    stochastic, whole-tensor scale).  Timed over all 224 linears; algorithmic
+    dequantised base) re-quantised with ties to even and ties away, and under
+    the deploy-side rules (toward zero, stochastic, whole-tensor scale), each
+    as one rtn_quantize_grouped call over all 224 linears (and nearest-even
+    once more as one rtn_quantize call per linear).  Algorithmic
     bytes 2 + 0.5 + 1/B per weight.  The diff census counts code nibbles that differ from the base
     plane (per tie rule) and between the tie rules, and changed scale bytes."""
     lut = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0],
@@ -261,15 +262,21 @@ def model_lifecycle(sq, steps=3):
         # takes its amax in a pre-pass, so it reads W twice)
         runs += [("rtz", "rtz", ws2, "cr", "sr"), ("stochastic", "stochastic", ws2, "cr", "sr"),
                  ("whole_tensor", "whole_tensor", 0.0, "cr", "sr")]
+        # the same nearest-even re-quantisation through one call per linear,
+        # to show what sharing launches saves
+        runs.append(("even_per_linear_calls", sq.TIE_EVEN, ws2, "ce", "se"))
         for label, tie, w_in, ck, sk in runs:
+            rule = tie if isinstance(tie, str) else ("even" if tie == sq.TIE_EVEN else "away")
+            group = sq.RtnGroup(fmt, rule, [dict(W=it["Wm"], codes=it[ck], scales=it[sk], ws2_out=it["w2"],
+                                                 ws2_in=w_in if fmt == "nv" else 0.0, seed=1234) for it in items])
+
             def run():
-                for it in items:
-                    if isinstance(tie, str):
-                        sq.rtn_quantize_rule(fmt, it["Wm"], tie, w_in if fmt == "nv" else 0.0, 1234,
-                                             codes=it[ck], scales=it[sk], ws2_out=it["w2"])
-                    else:
+                if label.endswith("per_linear_calls"):
+                    for it in items:
                         sq.rtn_quantize(fmt, it["Wm"], tie, w_in, codes=it[ck], scales=it[sk],
                                         ws2_out=it["w2"] if fmt == "nv" else None)
+                else:
+                    sq.rtn_quantize_grouped(fmt, rule, group)
             run()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -289,9 +296,8 @@ def model_lifecycle(sq, steps=3):
                 res[label]["code_nibbles_vs_base_frac"] = round(nb_moved / weights, 5)
                 res[label]["scale_bytes_vs_base"] = sb_moved
         # census (ties to even and ties away, both with the fixed ws2 for NVFP4)
-        for it in items:
-            sq.rtn_quantize(fmt, it["Wm"], sq.TIE_EVEN, ws2, codes=it["ce"], scales=it["se"],
-                            ws2_out=it["w2"] if fmt == "nv" else None)
+        sq.rtn_quantize_grouped(fmt, "even", [dict(W=it["Wm"], codes=it["ce"], scales=it["se"], ws2_out=it["w2"],
+                                                   ws2_in=ws2 if fmt == "nv" else 0.0) for it in items])
         torch.cuda.synchronize()
         cen = {"code_nibbles_even_vs_base": 0, "code_nibbles_away_vs_base": 0, "code_nibbles_even_vs_away": 0,
                "scale_bytes_even_vs_base": 0, "scale_bytes_even_vs_away": 0}

@@ -285,6 +285,32 @@ int rtn_quantize(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int
 int rtn_quantize_rule(int fmt, int64_t O, int64_t I, const void* W, float ws2_in, int rule, uint64_t seed,
                       uint8_t* codes_out, uint8_t* scales_out, float* ws2_out, void* stream);
 
+/* One weight of a grouped re-quantisation: the per-weight arguments of
+ * rtn_quantize_rule. */
+typedef struct sq_rtn_desc {
+  int64_t O, I;             /* weight shape [O, I] */
+  const void* W;            /* device bf16 [O, I], 16-byte aligned */
+  uint8_t* codes_out;       /* device [O, I/2], 4-byte aligned */
+  uint8_t* scales_out;      /* device [O, I/B] */
+  float* ws2_out;           /* device fp32 scalar, 4-byte aligned, or NULL (as rtn_quantize_rule) */
+  float ws2_in;             /* NVFP4 per-tensor ws2 (> 0), or <= 0 to recompute */
+  int32_t reserved;         /* must be 0 */
+  uint64_t seed;            /* Philox key of SQ_RULE_STOCHASTIC */
+} sq_rtn_desc;
+
+/*
+ * rtn_quantize_rule over many weights of one format under one rule (the
+ * naive merge re-quantises every linear of the model, Section 2): each
+ * weight's codes, scales and ws2_out are exactly those of its own
+ * rtn_quantize_rule call, and the weights share launches (up to 56 per
+ * launch) instead of taking one each.  descs is a HOST array of n
+ * descriptors, read during the call only, each validated like a
+ * rtn_quantize_rule call; outputs must not overlap one another or any W, and
+ * a weight that needs its ws2_out slot (whole-tensor rule, or NVFP4 with
+ * ws2_in <= 0) must not share it with another weight (SQ_ERR_ARG).
+ */
+int rtn_quantize_grouped(int fmt, int rule, int n, const sq_rtn_desc* descs, void* stream);
+
 /*
  * QAST low-rank scale step (Section 3, "Scale-QLoRA forward": Delta_S =
  * (alpha/r) B A with A block-level, eff' = eff + Delta_S; "QAST makes merge

@@ -5,6 +5,9 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "../../include/scaleqlora.h"
 #include "sq_launch.h"
 
@@ -262,6 +265,34 @@ SQ_EXPORT int rtn_quantize_rule(int fmt, int64_t O, int64_t I, const void* W, fl
   float* out = (fmt == SQ_NVFP4 || rule == SQ_RULE_WHOLE_TENSOR) ? ws2_out : nullptr;
   return hip_status(sq::rtn_rule_launch(fmt, (int)O, (int)I, W, fmt == SQ_NVFP4 ? ws2_in : 0.0f, rule, seed,
                                         codes_out, scales_out, out, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int rtn_quantize_grouped(int fmt, int rule, int n, const sq_rtn_desc* descs, void* stream) {
+  if (fmt != SQ_MXFP4 && fmt != SQ_NVFP4) return SQ_ERR_FORMAT;
+  if (rule < SQ_RULE_NEAREST_EVEN || rule > SQ_RULE_WHOLE_TENSOR) return SQ_ERR_ARG;
+  if (n < 0 || (n > 0 && !descs)) return SQ_ERR_ARG;
+  std::vector<sq::RtnItem> items((size_t)n);
+  std::vector<const float*> slots;
+  for (int k = 0; k < n; ++k) {
+    const sq_rtn_desc& d = descs[k];
+    int st = check_layer(fmt, 0, d.O, d.I);
+    if (st != SQ_OK) return st;
+    if (d.reserved != 0) return SQ_ERR_ARG;
+    if (!d.W || !d.codes_out || !d.scales_out) return SQ_ERR_ARG;
+    if (d.ws2_in > 0.0f && !isfinite(d.ws2_in)) return SQ_ERR_ARG;
+    const bool slot = rule == SQ_RULE_WHOLE_TENSOR || (fmt == SQ_NVFP4 && !(d.ws2_in > 0.0f));
+    if (slot && !d.ws2_out) return SQ_ERR_ARG;
+    if (d.ws2_out && !aligned(d.ws2_out, 4)) return SQ_ERR_ALIGN;
+    if (!aligned(d.W, 16) || !aligned(d.codes_out, 4)) return SQ_ERR_ALIGN;
+    if (slot) slots.push_back(d.ws2_out);
+    float* out = (fmt == SQ_NVFP4 || rule == SQ_RULE_WHOLE_TENSOR) ? d.ws2_out : nullptr;
+    items[(size_t)k] = sq::RtnItem{d.O, d.I, d.W, d.codes_out, d.scales_out, out,
+                                   fmt == SQ_NVFP4 ? d.ws2_in : 0.0f, d.seed};
+  }
+  std::sort(slots.begin(), slots.end());
+  if (std::adjacent_find(slots.begin(), slots.end()) != slots.end()) return SQ_ERR_ARG;   // a shared amax slot
+  if (n == 0) return SQ_OK;
+  return hip_status(sq::rtn_grouped_launch(fmt, rule, n, items.data(), static_cast<hipStream_t>(stream)));
 }
 
 namespace {

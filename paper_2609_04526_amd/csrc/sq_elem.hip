@@ -160,22 +160,51 @@ int merge_launch(const MergeBatch& b, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------ RTN
-// Each workgroup takes 512 chunks: a lane loads its two chunks (c and c + 256)
-// before working on either, so two 16-byte loads are in flight per lane.
-// (A grid-stride form with 2 to 8 chunks per lane in flight ran slower on the
-// 8B model's weights: the per-chunk work is long enough that short-lived
-// workgroups keep more loads in flight across the chip.)
+// Each workgroup takes 512 chunks of one weight: a lane loads its two chunks
+// (c and c + 256) before working on either, so two 16-byte loads are in
+// flight per lane.  (A grid-stride form with 2 to 8 chunks per lane in flight
+// ran slower on the 8B model's weights: the per-chunk work is long enough
+// that short-lived workgroups keep more loads in flight across the chip.)
+// One launch covers up to kRtnPerLaunch weights, so a whole model takes a
+// few launches instead of one per weight, each with its own ramp and tail.
 template <int FMT, int RULE>
-__global__ __launch_bounds__(256) void rtn_kernel(const uint16_t* __restrict__ W, int64_t n_chunks,
-                                                  const float* ws2_ptr, float ws2_val, const float* amax_t,
-                                                  uint64_t seed, uint8_t* __restrict__ codes,
-                                                  uint8_t* __restrict__ scales) {
-  const int64_t c0 = (int64_t)blockIdx.x * 512 + threadIdx.x, c1 = c0 + 256;
+__global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
+  (void)batch_arg;
+  // read through the kernarg segment (constant address space): the
+  // workgroup-uniform table stays in scalar registers
+  const __attribute__((address_space(4))) RtnBatch& b =
+      *(const __attribute__((address_space(4))) RtnBatch*)__builtin_amdgcn_kernarg_segment_ptr();
+  const int wg = (int)blockIdx.x;
+  int lo = 0, hi = b.count - 1;                 // the last weight whose spans start at or before wg
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (b.span_begin[mid] <= wg) lo = mid;
+    else hi = mid - 1;
+  }
+  const int p = lo;
+  const int64_t n_chunks = b.n_chunks[p];
+  const uint16_t* __restrict__ W = b.w[p];
+  uint8_t* codes = b.codes[p];
+  uint8_t* scales = b.scales[p];
+  const int64_t c0 = (int64_t)(wg - b.span_begin[p]) * kRtnSpan + threadIdx.x, c1 = c0 + 256;
   const bool ok0 = c0 < n_chunks, ok1 = c1 < n_chunks;
   const uint4 v0 = ok0 ? *reinterpret_cast<const uint4*>(W + 8 * c0) : make_uint4(0, 0, 0, 0);
   const uint4 v1 = ok1 ? *reinterpret_cast<const uint4*>(W + 8 * c1) : make_uint4(0, 0, 0, 0);
-  rtn_chunk<FMT, RULE>(v0, c0, ok0, ws2_ptr, ws2_val, amax_t, seed, codes, scales);
-  rtn_chunk<FMT, RULE>(v1, c1, ok1, ws2_ptr, ws2_val, amax_t, seed, codes, scales);
+  // scale bytes of whole groups of four blocks leave as 4-byte stores when
+  // the plane is 4-byte aligned
+  constexpr int kGroup = 4 * (ScaleOperand<FMT>::kBlock / 8);
+  const int64_t pack = (reinterpret_cast<uintptr_t>(scales) & 3) == 0 ? n_chunks / kGroup * kGroup : 0;
+  const float* ws2_ptr = b.ws2_ptr[p];
+  const float ws2_val = b.ws2_val[p];
+  const float* amax_t = b.amax_t[p];
+  const uint64_t seed = b.seed[p];
+  // the NVFP4 ws2 and its reciprocal, once for both chunks (a per-workgroup
+  // table of the 128 effective scales' reciprocals timed no faster)
+  constexpr bool kHoist = FMT == kNV && RULE != kRuleWholeTensor;
+  RcpDivisor wd;
+  if (kHoist) wd = make_rcp_divisor(ws2_ptr ? *ws2_ptr : ws2_val);
+  rtn_chunk<FMT, RULE>(v0, c0, ok0, ws2_ptr, ws2_val, amax_t, seed, codes, scales, pack, kHoist ? &wd : nullptr);
+  rtn_chunk<FMT, RULE>(v1, c1, ok1, ws2_ptr, ws2_val, amax_t, seed, codes, scales, pack, kHoist ? &wd : nullptr);
 }
 
 __global__ void rtn_amax_init(float* slot) { *reinterpret_cast<uint32_t*>(slot) = 0u; }
@@ -224,19 +253,22 @@ __global__ void rtn_ws2_finalize(float* slot) {
 
 namespace {
 template <int FMT, int RULE>
-void rtn_grid(int64_t n_chunks, const uint16_t* w, const float* ws2_ptr, float ws2_val, const float* amax_t,
-              uint64_t seed, uint8_t* codes, uint8_t* scales, hipStream_t s) {
-  if (n_chunks <= 0) return;
-  const unsigned grid = (unsigned)((n_chunks + 511) / 512);
-  hipLaunchKernelGGL((rtn_kernel<FMT, RULE>), dim3(grid), dim3(256), 0, s, w, n_chunks, ws2_ptr, ws2_val, amax_t,
-                     seed, codes, scales);
+int rtn_batch(const RtnBatch& b, hipStream_t s) {
+  if (b.spans <= 0) return 0;
+  hipLaunchKernelGGL((rtn_kernel<FMT, RULE>), dim3((unsigned)b.spans), dim3(256), 0, s, b);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
-template <int RULE>
-void rtn_fmt(int fmt, int64_t n_chunks, const uint16_t* w, const float* ws2_ptr, float ws2_val, const float* amax_t,
-             uint64_t seed, uint8_t* codes, uint8_t* scales, hipStream_t s) {
-  if (fmt == kMX) rtn_grid<kMX, RULE>(n_chunks, w, ws2_ptr, 1.0f, amax_t, seed, codes, scales, s);
-  else rtn_grid<kNV, RULE>(n_chunks, w, ws2_ptr, ws2_val, amax_t, seed, codes, scales, s);
+template <int FMT>
+int rtn_batch_rule(int rule, const RtnBatch& b, hipStream_t s) {
+  switch (rule) {
+    case kRuleEven: return rtn_batch<FMT, kRuleEven>(b, s);
+    case kRuleAway: return rtn_batch<FMT, kRuleAway>(b, s);
+    case kRuleRtz: return rtn_batch<FMT, kRuleRtz>(b, s);
+    case kRuleStochastic: return rtn_batch<FMT, kRuleStochastic>(b, s);
+    case kRuleWholeTensor: return rtn_batch<FMT, kRuleWholeTensor>(b, s);
+    default: return -1;
+  }
 }
 
 // The tensor amax (as the bits of an fp32 holding a bf16 value) into *slot.
@@ -248,6 +280,70 @@ void tensor_amax(const uint16_t* w, int64_t n_chunks, float* slot, hipStream_t s
 }
 }  // namespace
 
+int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream_t s) {
+  const bool nv = fmt == kNV;
+  // pre-passes: the tensor amax of every weight that needs one (whole-tensor
+  // rule, or a recomputed NVFP4 ws2), each into its own ws2_out slot
+  for (int k = 0; k < n; ++k) {
+    const RtnItem& it = items[k];
+    const int64_t n_chunks = it.O * it.I / 8;
+    const uint16_t* w = static_cast<const uint16_t*>(it.W);
+    if (rule == kRuleWholeTensor) {
+      tensor_amax(w, n_chunks, it.ws2_out, s);            // ws2_out holds the amax while the codes are written
+    } else if (nv && !(it.ws2_in > 0.0f)) {
+      tensor_amax(w, n_chunks, it.ws2_out, s);
+      hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, it.ws2_out);
+    } else if (nv && it.ws2_out) {
+      hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, it.ws2_out, it.ws2_in);
+    }
+  }
+  RtnBatch batch{};
+  int64_t spans = 0;
+  auto flush = [&]() -> int {
+    batch.spans = (int32_t)spans;
+    const int rc = nv ? rtn_batch_rule<kNV>(rule, batch, s) : rtn_batch_rule<kMX>(rule, batch, s);
+    batch = RtnBatch{};
+    spans = 0;
+    return rc;
+  };
+  for (int k = 0; k < n; ++k) {
+    const RtnItem& it = items[k];
+    const int64_t n_chunks = it.O * it.I / 8;
+    if (n_chunks == 0) continue;
+    const int64_t c = (n_chunks + kRtnSpan - 1) / kRtnSpan;
+    if (batch.count == kRtnPerLaunch || spans + c > INT32_MAX)
+      if (flush() != 0) return -1;
+    const int p = batch.count++;
+    batch.w[p] = static_cast<const uint16_t*>(it.W);
+    batch.codes[p] = it.codes;
+    batch.scales[p] = it.scales;
+    batch.n_chunks[p] = n_chunks;
+    batch.seed[p] = it.seed;
+    batch.span_begin[p] = (int32_t)spans;
+    if (rule == kRuleWholeTensor) {
+      batch.amax_t[p] = it.ws2_out;
+      batch.ws2_val[p] = nv ? (it.ws2_in > 0.0f ? it.ws2_in : 0.0f) : 1.0f;
+    } else if (nv) {
+      batch.ws2_ptr[p] = it.ws2_in > 0.0f ? nullptr : it.ws2_out;
+      batch.ws2_val[p] = it.ws2_in;
+    } else {
+      batch.ws2_val[p] = 1.0f;
+    }
+    spans += c;
+  }
+  if (batch.count > 0 && flush() != 0) return -1;
+  if (rule == kRuleWholeTensor) {
+    // then the ws2 used: recomputed from the amax (NVFP4 without ws2_in), else
+    // ws2_in (NVFP4) or 1 (MXFP4)
+    for (int k = 0; k < n; ++k) {
+      const RtnItem& it = items[k];
+      if (nv && !(it.ws2_in > 0.0f)) hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, it.ws2_out);
+      else hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, it.ws2_out, nv ? it.ws2_in : 1.0f);
+    }
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s) {
   return rtn_rule_launch(fmt, O, I, W, ws2_in, tie == 1 ? kRuleAway : kRuleEven, 0, codes, scales, ws2_out, s);
@@ -255,38 +351,8 @@ int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
 
 int rtn_rule_launch(int fmt, int O, int I, const void* W, float ws2_in, int rule, uint64_t seed,
                     uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s) {
-  const int64_t n_chunks = (int64_t)O * I / 8;
-  const uint16_t* w = static_cast<const uint16_t*>(W);
-  if (rule == kRuleWholeTensor) {
-    // ws2_out holds the tensor amax while the codes are written, then the
-    // ws2 used (1 for MXFP4); the launches are stream-ordered.
-    tensor_amax(w, n_chunks, ws2_out, s);
-    rtn_fmt<kRuleWholeTensor>(fmt, n_chunks, w, nullptr, fmt == kNV && ws2_in > 0.0f ? ws2_in : 0.0f, ws2_out,
-                              seed, codes, scales, s);
-    if (fmt == kNV && !(ws2_in > 0.0f)) hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, ws2_out);
-    else hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, ws2_out, fmt == kNV ? ws2_in : 1.0f);
-    return hipGetLastError() == hipSuccess ? 0 : -1;
-  }
-  const float* ws2_ptr = nullptr;
-  if (fmt == kNV) {
-    if (ws2_in > 0.0f) {
-      if (ws2_out) hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, ws2_out, ws2_in);
-    } else {
-      tensor_amax(w, n_chunks, ws2_out, s);
-      hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, ws2_out);
-      ws2_ptr = ws2_out;
-    }
-  }
-  switch (rule) {
-    case kRuleEven: rtn_fmt<kRuleEven>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s); break;
-    case kRuleAway: rtn_fmt<kRuleAway>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s); break;
-    case kRuleRtz: rtn_fmt<kRuleRtz>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s); break;
-    case kRuleStochastic:
-      rtn_fmt<kRuleStochastic>(fmt, n_chunks, w, ws2_ptr, ws2_in, nullptr, seed, codes, scales, s);
-      break;
-    default: return -1;
-  }
-  return hipGetLastError() == hipSuccess ? 0 : -1;
+  const RtnItem it{O, I, W, codes, scales, ws2_out, ws2_in, seed};
+  return rtn_grouped_launch(fmt, rule, 1, &it, s);
 }
 
 }  // namespace sq

@@ -78,6 +78,39 @@ int gemm_fwd_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int y
 int gemm_dx_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int dx_bf16, hipStream_t s);
 int gemm_dscale_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, hipStream_t s);
 
+// One weight of a grouped re-quantisation (the arguments of one single call).
+struct RtnItem {
+  int64_t O, I;
+  const void* W;
+  uint8_t* codes;
+  uint8_t* scales;
+  float* ws2_out;
+  float ws2_in;
+  uint64_t seed;
+};
+// Weights of one re-quantisation launch (one format, one rule), as arrays
+// within the 4 KiB kernel-argument limit.  Weight p owns the workgroups
+// [span_begin[p], span_begin[p+1]), 512 chunks of 8 weights each.
+constexpr int kRtnPerLaunch = 56;
+constexpr int kRtnSpan = 512;
+struct RtnBatch {
+  const uint16_t* w[kRtnPerLaunch];
+  uint8_t* codes[kRtnPerLaunch];
+  uint8_t* scales[kRtnPerLaunch];
+  const float* ws2_ptr[kRtnPerLaunch];    // recomputed ws2 (NVFP4), else null
+  const float* amax_t[kRtnPerLaunch];     // tensor amax (whole-tensor rule), else null
+  int64_t n_chunks[kRtnPerLaunch];
+  uint64_t seed[kRtnPerLaunch];
+  int32_t span_begin[kRtnPerLaunch];
+  float ws2_val[kRtnPerLaunch];
+  int32_t count;
+  int32_t spans;
+};
+// Re-quantises n weights under one rule (as rtn_rule_launch on each, in
+// launches of up to kRtnPerLaunch weights); every weight that needs an amax
+// slot has its own ws2_out.
+int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream_t s);
+
 int rtn_launch(int fmt, int O, int I, const void* W, float ws2_in, int tie,
                uint8_t* codes, uint8_t* scales, float* ws2_out, hipStream_t s);
 // rule: 0 nearest-even, 1 nearest-away, 2 toward zero, 3 stochastic (Philox

@@ -64,6 +64,21 @@ class ExpertDesc(ctypes.Structure):
     ]
 
 
+class RtnDesc(ctypes.Structure):
+    """Mirror of sq_rtn_desc."""
+    _fields_ = [
+        ("O", ctypes.c_int64),
+        ("I", ctypes.c_int64),
+        ("W", ctypes.c_void_p),
+        ("codes_out", ctypes.c_void_p),
+        ("scales_out", ctypes.c_void_p),
+        ("ws2_out", ctypes.c_void_p),
+        ("ws2_in", ctypes.c_float),
+        ("reserved", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
+    ]
+
+
 _lib = None
 
 
@@ -96,6 +111,8 @@ def load():
                                         _c_p, _c_p, _c_p, _c_p]),
         "rtn_quantize_rule": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_p, ctypes.c_float, ctypes.c_int,
                                              ctypes.c_uint64, _c_p, _c_p, _c_p, _c_p]),
+        "rtn_quantize_grouped": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(RtnDesc),
+                                                _c_p]),
         "sq_qat_requant": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, ctypes.c_float,
                                           _c_p, _c_p, ctypes.c_float, _c_p, _c_p, _c_p]),
         "sq_lora_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, _c_i64, ctypes.c_int]),
@@ -339,6 +356,32 @@ def rtn_quantize_rule(fmt, W, rule, ws2_in=0.0, seed=0, codes=None, scales=None,
                                                          int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(codes),
                                                          _ptr(scales), _ptr(ws2_out), _stream()))
     return codes, scales, ws2_out
+
+
+class RtnGroup:
+    """A prepared descriptor table for rtn_quantize_grouped (built once, reused
+    across calls; the tensors it names must stay alive).  weights: dicts with
+    keys W, codes, scales and optionally ws2_out, ws2_in, seed."""
+
+    def __init__(self, fmt, rule, weights):
+        self.fmt = _fmt(fmt)
+        self.rule = RULES.get(rule, rule)
+        self.weights = weights
+        self.arr = (RtnDesc * max(len(weights), 1))()
+        for k, w in enumerate(weights):
+            O, I = w["W"].shape
+            _dev(w["W"], w["codes"], w["scales"], w.get("ws2_out"))
+            self.arr[k] = RtnDesc(O, I, w["W"].data_ptr(), w["codes"].data_ptr(), w["scales"].data_ptr(),
+                                  w["ws2_out"].data_ptr() if w.get("ws2_out") is not None else 0,
+                                  float(w.get("ws2_in", 0.0)), 0, int(w.get("seed", 0)) & 0xFFFFFFFFFFFFFFFF)
+
+
+def rtn_quantize_grouped(fmt, rule, weights):
+    """rtn_quantize_rule over many weights (an RtnGroup, or the list of dicts
+    RtnGroup takes) in shared launches; outputs are written in place."""
+    group = weights if isinstance(weights, RtnGroup) else RtnGroup(fmt, rule, weights)
+    _check("rtn_quantize_grouped", load().rtn_quantize_grouped(group.fmt, group.rule, len(group.weights),
+                                                               group.arr, _stream()))
 
 
 def sq_qat_requant(fmt, codes, scales, B, A, alpha_over_r, ws2=1.0, codes_out=None, scales_out=None):

@@ -59,6 +59,8 @@ def test_descriptor_layouts_match_the_c_compiler(tmp_path):
         ' offsetof(sq_merge_desc, reserved));\n'
         '  printf("%zu %zu %zu %zu\\n", sizeof(sq_expert_desc), offsetof(sq_expert_desc, T),'
         ' offsetof(sq_expert_desc, ws2), offsetof(sq_expert_desc, reserved));\n'
+        '  printf("%zu %zu %zu %zu %zu\\n", sizeof(sq_rtn_desc), offsetof(sq_rtn_desc, ws2_out),'
+        ' offsetof(sq_rtn_desc, ws2_in), offsetof(sq_rtn_desc, reserved), offsetof(sq_rtn_desc, seed));\n'
         '  return 0;\n}\n')
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
@@ -68,6 +70,9 @@ def test_descriptor_layouts_match_the_c_compiler(tmp_path):
     assert m == [ctypes.sizeof(sq.MergeDesc), sq.MergeDesc.ws2.offset, sq.MergeDesc.reserved.offset]
     assert e == [ctypes.sizeof(sq.ExpertDesc), sq.ExpertDesc.T.offset, sq.ExpertDesc.ws2.offset,
                  sq.ExpertDesc.reserved.offset]
+    r = [int(v) for v in out[2].split()]
+    assert r == [ctypes.sizeof(sq.RtnDesc), sq.RtnDesc.ws2_out.offset, sq.RtnDesc.ws2_in.offset,
+                 sq.RtnDesc.reserved.offset, sq.RtnDesc.seed.offset]
 
 
 FAKE = 0x10000            # a 16-byte-aligned address that is never dereferenced
@@ -216,6 +221,34 @@ def test_rtn_rule_validation(lib):
     assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 4, 0, FAKE, FAKE, MISALIGNED + 2, None) == -3
     assert lib.rtn_quantize_rule(0, 256, 512, MISALIGNED, 0.0, 2, 0, FAKE, FAKE, None, None) == -3
     assert lib.rtn_quantize_rule(0, 256, 512, FAKE, 0.0, 2, 0, FAKE, None, None, None) == -1
+
+
+def test_rtn_grouped_validation(lib):
+    from paper_2609_04526_amd import sq
+
+    def table(*rows):
+        arr = (sq.RtnDesc * len(rows))()
+        for k, r in enumerate(rows):
+            arr[k] = sq.RtnDesc(*r)
+        return arr
+
+    ok = (256, 512, FAKE, FAKE, FAKE, FAKE + 256, 0.0, 0, 0)
+    assert lib.rtn_quantize_grouped(0, 0, 0, None, None) == 0                    # nothing to do
+    assert lib.rtn_quantize_grouped(2, 0, 1, table(ok), None) == -4
+    assert lib.rtn_quantize_grouped(0, 5, 1, table(ok), None) == -1
+    assert lib.rtn_quantize_grouped(0, 0, -1, table(ok), None) == -1
+    assert lib.rtn_quantize_grouped(0, 0, 1, None, None) == -1
+    assert lib.rtn_quantize_grouped(0, 0, 2, table(ok, (256, 500) + ok[2:]), None) == -2
+    assert lib.rtn_quantize_grouped(0, 0, 1, table(ok[:7] + (1, 0)), None) == -1     # reserved
+    assert lib.rtn_quantize_grouped(0, 0, 1, table(ok[:2] + (MISALIGNED,) + ok[3:]), None) == -3
+    assert lib.rtn_quantize_grouped(0, 0, 1, table(ok[:3] + (FAKE + 2,) + ok[4:]), None) == -3
+    assert lib.rtn_quantize_grouped(0, 0, 1, table(ok[:4] + (None,) + ok[5:]), None) == -1
+    # an amax slot is required (whole tensor; NVFP4 recompute), aligned and not shared
+    assert lib.rtn_quantize_grouped(0, 4, 1, table(ok[:5] + (None,) + ok[6:]), None) == -1
+    assert lib.rtn_quantize_grouped(1, 0, 1, table(ok[:5] + (None,) + ok[6:]), None) == -1
+    assert lib.rtn_quantize_grouped(1, 0, 1, table(ok[:5] + (FAKE + 2,) + ok[6:]), None) == -3
+    assert lib.rtn_quantize_grouped(1, 0, 2, table(ok, ok), None) == -1
+    assert lib.rtn_quantize_grouped(1, 0, 1, table(ok[:6] + (float("inf"),) + ok[7:]), None) == -1
 
 
 def test_qat_validation(lib):

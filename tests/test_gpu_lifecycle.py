@@ -326,6 +326,39 @@ def test_rtn_ties_and_specials(sq):
         assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(c.cpu().numpy(), rc)
 
 
+@pytest.mark.parametrize("ws2", [2.0 ** -70, 2.0 ** -64, 3e-3, float(np.float32(1 / 448)), 2.0 ** 64, 2.0 ** 70, 0.0])
+def test_rtn_tiny_blocks_and_extreme_ws2(sq, ws2):
+    """Block amax values on both sides of 2^-120 (where amax / 6 leaves the
+    reciprocal path for a full division), bf16 subnormals, zeros, and a
+    per-tensor ws2 inside and outside [2^-64, 2^64] (0: recomputed), in both
+    formats against the oracle."""
+    O, I = 16, 512
+    g = inputs.rng(4300)
+    W = (g.standard_normal((O, I)) * 0.02).astype(np.float32)
+    exps = [-125, -122, -121, -120, -119, -118, -100, -76, -60, -30, 0, 10, 60, 100, 110, 120]
+    for o, e in enumerate(exps):
+        W[o] *= np.float32(2.0 ** e) / np.float32(0.05)
+        W[o, 32:64] = 0.0                                   # an all-zero block
+    W[3, 64:96] = np.float32(2.0 ** -131)                   # bf16 subnormal blocks
+    W[4, 96:128] = -np.float32(2.0 ** -133)
+    Wb = torch.from_numpy(W).to(torch.bfloat16)
+    Wf = Wb.float().numpy()
+    for fmt in ("mx", "nv"):
+        if fmt == "mx" and ws2 != 0.0:
+            continue
+        ws2_in = float(np.float32(ws2)) if fmt == "nv" else 0.0
+        print(f"[rtn tiny] fmt={fmt} ws2={ws2_in}", flush=True)
+        for tie, tc in (("even", sq.TIE_EVEN), ("away", sq.TIE_AWAY)):
+            c, s, w2 = sq.rtn_quantize(fmt, Wb.cuda(), tc, ws2_in)
+            torch.cuda.synchronize()
+            rc, rs, rw = rtn.quantize(fmt, Wf, tie, ws2_in if (fmt == "nv" and ws2_in > 0) else None)
+            assert np.array_equal(s.cpu().numpy(), rs), np.argwhere(s.cpu().numpy() != rs)[:5]
+            assert np.array_equal(c.cpu().numpy(), rc)
+            if fmt == "nv":
+                got = w2.cpu().numpy()[0]
+                assert got == rw or (np.isnan(got) and np.isnan(rw))
+
+
 def test_rtn_delta_zero_fixed_point(sq):
     O, I = 64, 256
     codes = inputs.codes_uniform(4100, O, I)

@@ -154,3 +154,82 @@ def test_8b_gate_projection_sampled_rows(sq, fmt):
     if fmt == "nv":
         assert w2.cpu().numpy()[0] == rw
 
+
+
+ALL_RULES = ["even", "away", "rtz", "stochastic", "whole_tensor"]
+GROUP_SHAPES = [(264, 1056), (8, 32), (96, 512), (1024, 4096), (8, 1024), (40, 3584)]
+
+
+def _group_weights(sq, fmt, shapes, seed, ws2_in, unaligned=()):
+    """Merged weights with output buffers for a grouped call and for single
+    calls; planes listed in `unaligned` get scale planes at an odd address."""
+    out = []
+    for k, (O, I) in enumerate(shapes):
+        Wb, _ = _merged_weight(fmt, O, I, seed=seed + 7 * k)
+        G = I // codec.BLOCK[fmt]
+        sbuf = torch.full((O * G + 1,), 0xA5, dtype=torch.uint8, device="cuda")
+        sc = sbuf[1:].view(O, G) if k in unaligned else sbuf[:O * G].view(O, G)
+        out.append(dict(W=Wb.cuda(), codes=torch.empty((O, I // 2), dtype=torch.uint8, device="cuda"),
+                        scales=sc, ws2_out=torch.full((1,), -1.0, device="cuda"), ws2_in=ws2_in,
+                        seed=0x9E37_79B9_7F4A_7C15 * (k + 1) & 0xFFFFFFFFFFFFFFFF, sbuf=sbuf))
+    return out
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+@pytest.mark.parametrize("rule", ALL_RULES)
+@pytest.mark.parametrize("ws2_mode", ["fixed", "recompute"])
+def test_grouped_equals_single_calls(sq, fmt, rule, ws2_mode):
+    """rtn_quantize_grouped over weights of several shapes (one with its scale
+    plane at an odd address, so its scale bytes leave one by one) equals one
+    rtn_quantize_rule call per weight, byte for byte, ws2_out included."""
+    if fmt == "mx" and ws2_mode == "recompute":
+        pytest.skip("MXFP4 has no per-tensor scalar")
+    ws2_in = float(np.float32(1 / 448)) if (fmt == "nv" and ws2_mode == "fixed") else 0.0
+    print(f"[grouped] fmt={fmt} rule={rule} ws2={ws2_mode}", flush=True)
+    ws = _group_weights(sq, fmt, GROUP_SHAPES, 6000, ws2_in, unaligned=(2,))
+    sq.rtn_quantize_grouped(fmt, rule, ws)
+    torch.cuda.synchronize()
+    for w in ws:
+        c, s, w2 = sq.rtn_quantize_rule(fmt, w["W"], rule, ws2_in, w["seed"])
+        torch.cuda.synchronize()
+        assert torch.equal(w["codes"], c) and torch.equal(w["scales"], s)
+        if w2 is not None:
+            assert torch.equal(w["ws2_out"], w2)
+        # the canary byte beside the plane is untouched
+        canary = 0 if w["scales"].data_ptr() != w["sbuf"].data_ptr() else -1
+        assert int(w["sbuf"][canary]) == 0xA5
+
+
+def test_grouped_matches_oracle(sq):
+    """One grouped NVFP4 call (recomputed ws2) against the oracle directly."""
+    ws = _group_weights(sq, "nv", [(264, 1056), (96, 512)], 6100, 0.0)
+    sq.rtn_quantize_grouped("nv", "even", ws)
+    torch.cuda.synchronize()
+    for w in ws:
+        rc, rs, rw = rtn.quantize_rule("nv", w["W"].float().cpu().numpy(), "even", None, 0)
+        assert np.array_equal(w["codes"].cpu().numpy(), rc) and np.array_equal(w["scales"].cpu().numpy(), rs)
+        assert w["ws2_out"].cpu().numpy()[0] == rw
+
+
+def test_grouped_more_weights_than_one_launch(sq):
+    """61 weights (one launch takes 56), NVFP4 with every ws2 recomputed."""
+    shapes = [(8 * (1 + k % 5), 16 * (2 + (k * 7) % 9)) for k in range(61)]
+    ws = _group_weights(sq, "nv", shapes, 6200, 0.0, unaligned=(3, 60))
+    sq.rtn_quantize_grouped("nv", "stochastic", ws)
+    torch.cuda.synchronize()
+    for w in ws:
+        c, s, w2 = sq.rtn_quantize_rule("nv", w["W"], "stochastic", 0.0, w["seed"])
+        torch.cuda.synchronize()
+        assert torch.equal(w["codes"], c) and torch.equal(w["scales"], s) and torch.equal(w["ws2_out"], w2)
+
+
+def test_grouped_rejects_a_shared_amax_slot(sq):
+    ws = _group_weights(sq, "nv", [(8, 32), (8, 64)], 6300, 0.0)
+    ws[1]["ws2_out"] = ws[0]["ws2_out"]
+    with pytest.raises(sq.SqError):
+        sq.rtn_quantize_grouped("nv", "even", ws)
+    # with a fixed ws2 the slots only receive it, so sharing one is allowed
+    for w in ws:
+        w["ws2_in"] = float(np.float32(1 / 448))
+    sq.rtn_quantize_grouped("nv", "even", ws)
+    torch.cuda.synchronize()
