@@ -77,7 +77,8 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=100,
+                   help="untimed steps first; the clock settles after some tens of milliseconds of load")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-model-merge", action="store_true")
     p.add_argument("--no-model-step", action="store_true")
@@ -701,7 +702,7 @@ def model_mlp_nv(sq, steps=10):
                  "ds": lambda: sq.sq_bwd_dscale("nv", X, dY, codes, dS=dS)}
         flop = 2.0 * Tm * o * i
         for prod, fn in calls.items():
-            for _ in range(2):
+            for _ in range(5):               # the first launches after the input generation run slower
                 fn()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -767,7 +768,7 @@ def cpu_baseline(X, dY, codes, sb, delta, src, Wm_host):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     from paper_2609_04526_amd import sq
     sq.load()

@@ -66,6 +66,9 @@ constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: r
 #ifndef SQ_DMA_SPREAD
 #define SQ_DMA_SPREAD 2
 #endif
+#ifndef SQ_DX_W_BRANCHFREE
+#define SQ_DX_W_BRANCHFREE 1
+#endif
 #ifndef SQ_FWD_W_AHEAD2
 #define SQ_FWD_W_AHEAD2 1
 #endif
@@ -621,6 +624,20 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   __amdgpu_buffer_rsrc_t rw_codes, rw_scales;
   uint32_t wc0[kWAhead == 2 ? kWPer : 1], ws0[kWAhead == 2 ? kWPer : 1];
   int wklim = 0;
+  // dX W items: item p of thread tid is row kt*64 + tid/(BN/8) + p*NT/(BN/8)
+  // of W^T's stage and the 8 columns from n0 + (tid % (BN/8))*8, the same
+  // columns for every p; a column block outside the layer is marked kOOB and
+  // a row past O reads at kOOB, so the loads take no branches.
+  constexpr bool kDxFree = MODE == kDx && SQ_DX_W_BRANCHFREE;
+  uint32_t dxc = 0, dxs = 0;
+  if constexpr (kDxFree) {
+    static_assert(NT % (BN / 8) == 0, "every item of a thread keeps its columns");
+    rw_codes = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
+    rw_scales = make_rsrc(g.scales, (uint32_t)((size_t)g.O * g.G));
+    const int i = n0 + (tid % (BN / 8)) * 8;
+    dxc = i < g.I ? (uint32_t)(i >> 1) : kOOB;
+    dxs = i < g.I ? (uint32_t)(i / B) : kOOB;
+  }
   if constexpr (kWAhead == 2) {
     rw_codes = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
     rw_scales = make_rsrc(g.scales, (uint32_t)((size_t)g.O * g.G));
@@ -642,6 +659,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
           const bool in = kt * kBK < wklim;
           const uint32_t oc = in ? wc0[p] + (uint32_t)kt * (kBK / 2) : kOOB;
           const uint32_t os = in ? ws0[p] + (uint32_t)kt * (kBK / B) : kOOB;
+          w_reg[u][p] = __builtin_amdgcn_raw_buffer_load_b32(rw_codes, (int)oc, 0, 0);
+          w_sb[u][p] = __builtin_amdgcn_raw_buffer_load_b8(rw_scales, (int)os, 0, 0);
+          continue;
+        }
+        if constexpr (kDxFree) {
+          const int o = kt * kBK + tid / (BN / 8) + p * (NT / (BN / 8));
+          const bool in = o < g.O && dxc != kOOB;
+          const uint32_t oc = in ? (uint32_t)o * (uint32_t)(g.I >> 1) + dxc : kOOB;
+          const uint32_t os = in ? (uint32_t)o * (uint32_t)g.G + dxs : kOOB;
           w_reg[u][p] = __builtin_amdgcn_raw_buffer_load_b32(rw_codes, (int)oc, 0, 0);
           w_sb[u][p] = __builtin_amdgcn_raw_buffer_load_b8(rw_scales, (int)os, 0, 0);
           continue;
