@@ -69,6 +69,9 @@ constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: r
 #ifndef SQ_DX_W_BRANCHFREE
 #define SQ_DX_W_BRANCHFREE 1
 #endif
+#ifndef SQ_DX_W_AHEAD2
+#define SQ_DX_W_AHEAD2 0
+#endif
 #ifndef SQ_FWD_W_AHEAD2
 #define SQ_FWD_W_AHEAD2 1
 #endif
@@ -92,6 +95,9 @@ struct GemmArgs {
   int out_bf16;
   int ksplit;             // DS: K (token) ranges per tile; >1 writes partial planes to `out`
   int ksteps_per;         // DS: K stages per range
+  // the launch covers output rows [m_off, m_off + m_cnt) and columns
+  // [n_off, n_off + n_cnt) (a count of 0: up to M or N)
+  int m_off, m_cnt, n_off, n_cnt;
 };
 
 // Up to kGroupMax experts per grouped launch, passed by value (kernel
@@ -497,7 +503,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
-  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int tiles_m = ((g.m_cnt ? g.m_cnt : g.M) + BM - 1) / BM, tiles_n = ((g.n_cnt ? g.n_cnt : g.N) + BN - 1) / BN;
   // a DS launch with split K runs ksplit workgroups per tile, each over its
   // own range of K stages
   const int tiles = tiles_m * tiles_n;
@@ -505,7 +511,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   int tm, tn;
   tile_of<group_m<MODE>()>((MODE == kDs && g.ksplit > 1) ? bid - split * tiles : bid, (MODE == kDs && g.ksplit > 1) ? tiles : nb,
           tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = g.m_off + tm * BM, n0 = g.n_off + tn * BN;
 
   auto stage = [&](auto SC) -> SQ_LDS uint8_t* {
     constexpr int S = decltype(SC)::value;
@@ -605,7 +611,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // The forward fetches W two stages ahead through branch-free buffer loads
   // (an item outside the layer reads at an offset past the operand: zeros),
   // so the wait before a dequantisation leaves the newer loads in flight.
-  constexpr int kWAhead = (MODE == kFwdR && SQ_FWD_W_AHEAD2) ? 2 : 1;
+  constexpr int kWAhead = ((MODE == kFwdR && SQ_FWD_W_AHEAD2) || (MODE == kDx && SQ_DX_W_AHEAD2)) ? 2 : 1;
   static_assert(kWAhead == 1 || STAGES == 2, "two W register sets alternate with the stage parity");
   uint32_t w_reg[kWAhead][kWPer], w_sb[kWAhead][kWPer];
   auto w_item = [&](int p, int kt, int& o, int& i) {
@@ -622,7 +628,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // kt*64 + (idx%8)*8, so each item keeps byte offsets at kt = 0 (past the
   // operand for rows outside the layer) and a column limit.
   __amdgpu_buffer_rsrc_t rw_codes, rw_scales;
-  uint32_t wc0[kWAhead == 2 ? kWPer : 1], ws0[kWAhead == 2 ? kWPer : 1];
+  constexpr bool kFwdAhead = MODE == kFwdR && kWAhead == 2;
+  uint32_t wc0[kFwdAhead ? kWPer : 1], ws0[kFwdAhead ? kWPer : 1];
   int wklim = 0;
   // dX W items: item p of thread tid is row kt*64 + tid/(BN/8) + p*NT/(BN/8)
   // of W^T's stage and the 8 columns from n0 + (tid % (BN/8))*8, the same
@@ -638,7 +645,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     dxc = i < g.I ? (uint32_t)(i >> 1) : kOOB;
     dxs = i < g.I ? (uint32_t)(i / B) : kOOB;
   }
-  if constexpr (kWAhead == 2) {
+  if constexpr (kFwdAhead) {
     rw_codes = make_rsrc(g.codes, (uint32_t)((size_t)g.O * g.I / 2));
     rw_scales = make_rsrc(g.scales, (uint32_t)((size_t)g.O * g.G));
     const int c8 = (tid % 8) * 8;
@@ -655,7 +662,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     if constexpr (kWReg) {
 #pragma unroll
       for (int p = 0; p < kWPer; ++p) {
-        if constexpr (kWAhead == 2) {
+        if constexpr (kFwdAhead) {
           const bool in = kt * kBK < wklim;
           const uint32_t oc = in ? wc0[p] + (uint32_t)kt * (kBK / 2) : kOOB;
           const uint32_t os = in ? ws0[p] + (uint32_t)kt * (kBK / B) : kOOB;
@@ -1214,18 +1221,60 @@ template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int B
 static int launch_gemm(const GemmArgs& g, hipStream_t s) {
   using L = SmemLayout<MODE, BM, BN, STAGES, BK, WGM * WGN>;
   static_assert(L::kBytes <= 160 * 1024, "LDS budget");
-  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  const int tiles = (((g.m_cnt ? g.m_cnt : g.M) + BM - 1) / BM) * (((g.n_cnt ? g.n_cnt : g.N) + BN - 1) / BN);
   if (tiles == 0) return 0;
   const int blocks = tiles * (MODE == kDs && g.ksplit > 1 ? g.ksplit : 1);
   hipLaunchKernelGGL((gemm_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(blocks), dim3(64 * WGM * WGN), 0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+#ifndef SQ_CFG_HALF_N
+#define SQ_CFG_HALF_N 256, 128, 4, 2, 2, 64
+#endif
+#ifndef SQ_CFG_HALF_M
+#define SQ_CFG_HALF_M 128, 256, 2, 4, 2, 64
+#endif
+#ifndef SQ_TAIL_SPLIT
+#define SQ_TAIL_SPLIT 1
+#endif
+
+// A grid of 256 x 256 tiles that ends in a partial wave (at most half the
+// CUs busy) leaves the other CUs idle while it runs.  When that last partial
+// wave is whole tile-columns (or tile-rows) of the output, those columns
+// (rows) go to a second launch of 256 x 128 (128 x 256) tiles of 8 waves of
+// 64 x 64, twice as many workgroups, which fill the chip.  The first launch
+// keeps the whole waves.  On the 8B MLP products at 4096 tokens (896 tiles,
+// three waves and a half) this took 4-5% off the forward and dX; 4 waves of
+// 64 x 128 in the second launch gained about half as much.  Each output
+// element is still summed in one workgroup in K order, so results do not
+// depend on the split.
 template <int MODE, int FMT, int BM, int BN, int... REST>
 static int launch_sized(const GemmArgs& g, hipStream_t s) {
-  const int64_t big = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  if (big >= kCUs) return launch_gemm<MODE, FMT, BM, BN, REST...>(g, s);
-  return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
+  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  const int64_t big = (int64_t)tm * tn;
+  if (big < kCUs) return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
+  const int rem = (int)(big % kCUs);
+  if (SQ_TAIL_SPLIT && BM == 256 && BN == 256 && rem > 0 && rem <= kCUs / 2 && g.ksplit <= 1) {
+    if (rem % tm == 0) {                                  // the last rem / tm tile-columns
+      const int cols = (tn - rem / tm) * BN;
+      GemmArgs a = g, b = g;
+      a.n_cnt = cols;
+      b.n_off = cols;
+      b.n_cnt = g.N - cols;
+      const int rc = launch_gemm<MODE, FMT, BM, BN, REST...>(a, s);
+      return rc != 0 ? rc : launch_gemm<MODE, FMT, SQ_CFG_HALF_N>(b, s);
+    }
+    if (rem % tn == 0) {                                  // the last rem / tn tile-rows
+      const int rows = (tm - rem / tn) * BM;
+      GemmArgs a = g, b = g;
+      a.m_cnt = rows;
+      b.m_off = rows;
+      b.m_cnt = g.M - rows;
+      const int rc = launch_gemm<MODE, FMT, BM, BN, REST...>(a, s);
+      return rc != 0 ? rc : launch_gemm<MODE, FMT, SQ_CFG_HALF_M>(b, s);
+    }
+  }
+  return launch_gemm<MODE, FMT, BM, BN, REST...>(g, s);
 }
 
 // The MXFP4 forward dequantises in registers (kFwdC) when every row's scales

@@ -79,6 +79,13 @@ SHAPES = [
     # few tiles and many token stages: dS splits the token sum (workspace)
     ("mx", 1000, 264, 512),
     ("nv", 700, 520, 256),
+    # 256 x 256 grids ending in a short partial wave of whole tile-columns
+    # (forward, dX) or tile-rows (dS), with ragged edges: those go to a second
+    # launch of 256 x 128 or 128 x 256 tiles
+    ("mx", 4096, 4360, 64),
+    ("nv", 4096, 64, 4368),
+    ("mx", 64, 4096, 4384),
+    ("nv", 64, 4096, 4368),
 ]
 
 
@@ -223,6 +230,33 @@ def test_parity_8b_key_value_projection_mx(sq):
     """1024 x 4096 MXFP4 key/value projection, 4096 tokens: the forward and
     dS grids are too small for the large tile and take the small one."""
     _sampled_check(sq, "mx", 4096, 1024, 4096, seed=2500)
+
+
+@pytest.mark.parametrize("fmt,O,I", [("mx", 14336, 4096), ("mx", 4096, 14336), ("nv", 4096, 14336)])
+def test_tail_split_equals_slices(sq, fmt, O, I):
+    """8B MLP shapes at 4096 tokens (896 tiles of 256 x 256: three whole waves
+    and a half wave, which runs as 256 x 128 tiles): the forward and dX equal,
+    bit for bit, the same products over 2048-wide slices of W, which take the
+    128 x 128 tile (each output element is summed in K order either way)."""
+    T = 4096
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed=3500 + O)
+    B = codec.BLOCK[fmt]
+    Xd, dYd = X.cuda(), dY.cuda()
+    cd, sd = torch.from_numpy(codes).cuda(), torch.from_numpy(sb).cuda()
+    Y = sq.sq_fwd(fmt, Xd, cd, sd, ws2, out_dtype=torch.float32)
+    dX = sq.sq_bwd_dx(fmt, dYd, cd, sd, ws2, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for o0 in range(0, O, 2048):
+        Ys = sq.sq_fwd(fmt, Xd, cd[o0:o0 + 2048].contiguous(), sd[o0:o0 + 2048].contiguous(), ws2,
+                       out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(Y[:, o0:o0 + 2048], Ys), o0
+    for i0 in range(0, I, 2048):
+        c = cd[:, i0 // 2:(i0 + 2048) // 2].contiguous()
+        s_ = sd[:, i0 // B:(i0 + 2048) // B].contiguous()
+        dXs = sq.sq_bwd_dx(fmt, dYd, c, s_, ws2, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(dX[:, i0:i0 + 2048], dXs), i0
 
 
 @pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336)])
