@@ -317,6 +317,59 @@ def model_lifecycle(sq, steps=3):
     return out
 
 
+def model_step_fused(sq, codes, scales, dys, xs, Tm, L, steps, warmup, flops):
+    """The same step with the projections that share an input stored stacked,
+    as fused-projection layouts keep them: q/k/v as one [6144, 4096] weight and
+    gate/up as one [28672, 4096] weight (codes and scale rows concatenated;
+    dY of the stacked product is the per-linear dY side by side).  Each
+    stacked weight takes one forward, one dX (which is the sum of the
+    projections' dX, what the shared input needs) and one dS, whose row
+    ranges are the projections' dS.  The same flops in 4 + 4 + 4 products per
+    layer instead of 7 + 7 + 7."""
+    n_lin = len(inputs.LLAMA8B_LAYER)
+    groups = (("qkv", (0, 1, 2)), ("o", (3,)), ("gate_up", (4, 5)), ("down", (6,)))
+    layers = []
+    for l in range(L):
+        ent = []
+        for name, ks in groups:
+            ns = [l * n_lin + k for k in ks]
+            c = torch.cat([codes[n] for n in ns]) if len(ns) > 1 else codes[ns[0]]
+            sc = torch.cat([scales[n] for n in ns]) if len(ns) > 1 else scales[ns[0]]
+            dy = torch.cat([dys[n] for n in ns], dim=1) if len(ns) > 1 else dys[ns[0]]
+            x = xs[l][inputs.LLAMA8B_LAYER[ks[0]][0]]
+            o, i = c.shape[0], x.shape[1]
+            ent.append(dict(c=c, sc=sc, dy=dy, x=x, o=o, i=i,
+                            ds=torch.empty((o, i // 32), dtype=torch.float32, device="cuda")))
+        layers.append(ent)
+    yb = {e["o"]: torch.empty((Tm, e["o"]), dtype=torch.bfloat16, device="cuda") for e in layers[0]}
+    xb = {e["i"]: torch.empty((Tm, e["i"]), dtype=torch.bfloat16, device="cuda") for e in layers[0]}
+
+    def run():
+        for l in range(L):
+            for e in layers[l]:
+                sq.sq_fwd("mx", e["x"], e["c"], e["sc"], 1.0, Y=yb[e["o"]])
+        for l in reversed(range(L)):
+            for e in reversed(layers[l]):
+                sq.sq_bwd_dx("mx", e["dy"], e["c"], e["sc"], 1.0, dX=xb[e["i"]])
+                sq.sq_bwd_dscale("mx", e["x"], e["dy"], e["c"], dS=e["ds"])
+
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    del layers, yb, xb
+    torch.cuda.empty_cache()
+    return {"what": "q/k/v and gate/up stacked into one weight each (fused projections), 171.5 TFLOP as above",
+            "ms": round(ms, 3), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+
+
 def model_step(sq, steps, warmup, comparator=True):
     """One scale-only training step of the whole 8B-shaped model in MXFP4: 32
     layers x {q, k, v, o, gate, up, down}, 4096 tokens, every linear's forward,
@@ -396,6 +449,7 @@ def model_step(sq, steps, warmup, comparator=True):
             torch.cuda.synchronize()
             t = a.elapsed_time(b) / L
             per[f"{name}_{prod}"] = {"ms": round(t, 4), "TFLOP/s": round(2.0 * Tm * o * i / (t * 1e-3) / 1e12, 1)}
+    fused = model_step_fused(sq, codes, scales, dys, xs, Tm, L, steps, warmup, flops)
     # The QAST step: every linear's scales come from its rank-32 adapter
     # (on-grid bytes + clamp mask), the products run on those bytes, and dS
     # turns into dB, dA.
@@ -484,6 +538,7 @@ def model_step(sq, steps, warmup, comparator=True):
            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
            "per_linear_one_layer": per,
+           "fused_projections": fused,
            "qast_step": {"what": "the same step with every linear's scales from a rank-32 adapter: "
                                  "sq_qast_scales before each forward, sq_qast_factor_grads after each dS",
                          "ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
