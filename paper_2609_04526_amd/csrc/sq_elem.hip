@@ -160,9 +160,9 @@ int merge_launch(const MergeBatch& b, hipStream_t s) {
 }
 
 // ------------------------------------------------------------------ RTN
-// Each workgroup takes 512 chunks of one weight: a lane loads its two chunks
-// (c and c + 256) before working on either, so two 16-byte loads are in
-// flight per lane.  (A grid-stride form with 2 to 8 chunks per lane in flight
+// Each workgroup takes 256 rtn_chunks(FMT, RULE) chunks of one weight: a lane
+// loads its chunks (c, c + 256, ...) before working on any, so that many
+// 16-byte loads are in flight per lane.  (A grid-stride form with 2 to 8 chunks per lane in flight
 // ran slower on the 8B model's weights: the per-chunk work is long enough
 // that short-lived workgroups keep more loads in flight across the chip.)
 // One launch covers up to kRtnPerLaunch weights, so a whole model takes a
@@ -186,10 +186,14 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
   const uint16_t* __restrict__ W = b.w[p];
   uint8_t* codes = b.codes[p];
   uint8_t* scales = b.scales[p];
-  const int64_t c0 = (int64_t)(wg - b.span_begin[p]) * kRtnSpan + threadIdx.x, c1 = c0 + 256;
-  const bool ok0 = c0 < n_chunks, ok1 = c1 < n_chunks;
-  const uint4 v0 = ok0 ? *reinterpret_cast<const uint4*>(W + 8 * c0) : make_uint4(0, 0, 0, 0);
-  const uint4 v1 = ok1 ? *reinterpret_cast<const uint4*>(W + 8 * c1) : make_uint4(0, 0, 0, 0);
+  constexpr int kRtnChunks = rtn_chunks(FMT, RULE);
+  const int64_t c0 = (int64_t)(wg - b.span_begin[p]) * rtn_span(FMT, RULE) + threadIdx.x;
+  uint4 v[kRtnChunks];
+#pragma unroll
+  for (int u = 0; u < kRtnChunks; ++u) {
+    const int64_t c = c0 + 256 * u;
+    v[u] = c < n_chunks ? *reinterpret_cast<const uint4*>(W + 8 * c) : make_uint4(0, 0, 0, 0);
+  }
   // scale bytes of whole groups of four blocks leave as 4-byte stores when
   // the plane is 4-byte aligned
   constexpr int kGroup = 4 * (ScaleOperand<FMT>::kBlock / 8);
@@ -203,8 +207,12 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
   constexpr bool kHoist = FMT == kNV && RULE != kRuleWholeTensor;
   RcpDivisor wd;
   if (kHoist) wd = make_rcp_divisor(ws2_ptr ? *ws2_ptr : ws2_val);
-  rtn_chunk<FMT, RULE>(v0, c0, ok0, ws2_ptr, ws2_val, amax_t, seed, codes, scales, pack, kHoist ? &wd : nullptr);
-  rtn_chunk<FMT, RULE>(v1, c1, ok1, ws2_ptr, ws2_val, amax_t, seed, codes, scales, pack, kHoist ? &wd : nullptr);
+#pragma unroll
+  for (int u = 0; u < kRtnChunks; ++u) {
+    const int64_t c = c0 + 256 * u;
+    rtn_chunk<FMT, RULE>(v[u], c, c < n_chunks, ws2_ptr, ws2_val, amax_t, seed, codes, scales, pack,
+                         kHoist ? &wd : nullptr);
+  }
 }
 
 __global__ void rtn_amax_init(float* slot) { *reinterpret_cast<uint32_t*>(slot) = 0u; }
@@ -310,7 +318,8 @@ int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream
     const RtnItem& it = items[k];
     const int64_t n_chunks = it.O * it.I / 8;
     if (n_chunks == 0) continue;
-    const int64_t c = (n_chunks + kRtnSpan - 1) / kRtnSpan;
+    const int64_t span = rtn_span(fmt, rule);
+    const int64_t c = (n_chunks + span - 1) / span;
     if (batch.count == kRtnPerLaunch || spans + c > INT32_MAX)
       if (flush() != 0) return -1;
     const int p = batch.count++;
