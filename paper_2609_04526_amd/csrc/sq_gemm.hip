@@ -72,6 +72,9 @@ constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: r
 #ifndef SQ_DX_W_AHEAD2
 #define SQ_DX_W_AHEAD2 0
 #endif
+#ifndef SQ_SCHED_LATE_DX
+#define SQ_SCHED_LATE_DX 0
+#endif
 #ifndef SQ_FWD_W_AHEAD2
 #define SQ_FWD_W_AHEAD2 1
 #endif
@@ -892,7 +895,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     }
   };
 
-  constexpr bool kLate = MODE == kFwdC || (SQ_SCHED_LATE && MODE == kDs);
+  constexpr bool kLate = MODE == kFwdC || (SQ_SCHED_LATE && MODE == kDs) || (SQ_SCHED_LATE_DX && MODE == kDx);
   if constexpr (!kLate) {
   // ---- prologue: the first STAGES-1 stages in flight
   if constexpr (kWReg) {
