@@ -332,12 +332,16 @@ __host__ __device__ constexpr int dma_count() {
 // Workgroup w runs on XCD w % 8, and each XCD has its own L2.  Tiles are
 // enumerated in groups of kGroupM tile-rows (column by column inside a group)
 // and each XCD is given one contiguous stretch of that order, so the
-// workgroups that share an L2 also share operand panels.
+// workgroups that share an L2 also share operand panels.  With 32 tiles per
+// XCD, a height of 4 gives each XCD 4 activation panels (2 MiB each at 4096
+// tokens) and 8 code panels (0.5 MiB): 96 MiB fetched per 4096^3 forward or
+// dX against 144 MiB at height 8, in the same time.  For dS both operands are
+// 2 MiB panels and heights 4 and 8 fetch the same.
 #ifndef SQ_GROUPM_FWD
-#define SQ_GROUPM_FWD 8
+#define SQ_GROUPM_FWD 4
 #endif
 #ifndef SQ_GROUPM_DX
-#define SQ_GROUPM_DX 8
+#define SQ_GROUPM_DX 4
 #endif
 #ifndef SQ_GROUPM_DS
 #define SQ_GROUPM_DS 8
