@@ -757,7 +757,7 @@ def model_mlp_nv(sq, steps=10):
                  "ds": lambda: sq.sq_bwd_dscale("nv", X, dY, codes, dS=dS)}
         flop = 2.0 * Tm * o * i
         for prod, fn in calls.items():
-            for _ in range(5):               # the first launches after the input generation run slower
+            for _ in range(30):              # the first launches after the input generation run slower
                 fn()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
