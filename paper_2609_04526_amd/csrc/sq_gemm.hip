@@ -1038,6 +1038,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // DMA loads a thread issues for the stages after kt + 1 (the wait at the
   // barrier leaves those in flight; anything issued later is younger still)
   constexpr int kAhead = (STAGES - 2) * kDma < 63 ? (STAGES - 2) * kDma : 63;
+  // kFwdC tiles with fewer 32-row code slices than waves leave the code DMA to
+  // the first waves; the others issue one load per stage fewer
+  constexpr bool kCodesSplit = MODE == kFwdC && DC::kWaveInst < NT / 64;
+  constexpr int kDmaLow = kCodesSplit ? kDma - DC::kInst : kDma;
+  constexpr int kAheadLow = (STAGES - 2) * kDmaLow < 63 ? (STAGES - 2) * kDmaLow : 63;
+  const bool codes_wave = !kCodesSplit || wave_u < DC::kWaveInst;
 
   auto step2 = [&](auto SC, int kt) {
     constexpr int S = decltype(SC)::value;
@@ -1061,7 +1067,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     if constexpr (kWReg) {
       if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
     }
-    wait_vm_lgkm0<kAhead>();
+    // stage kt + 1 has landed once at most kAhead (kAheadLow) loads are
+    // outstanding, if the DMA of stages kt + 2 .. kt + STAGES - 1 all went out
+    // after it; in the last stages fewer did, and everything is waited for
+    if (kt + STAGES - 1 < nk) {
+      if (codes_wave) wait_vm_lgkm0<kAhead>();
+      else wait_vm_lgkm0<kAheadLow>();
+    } else {
+      wait_vm_lgkm0<0>();
+    }
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if (kt + 1 < nk) read(SN{}, kt + 1, I0{}, F0);
@@ -1235,6 +1249,11 @@ static int launch_gemm(const GemmArgs& g, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// The MXFP4 forward's small tile keeps four stages in flight (80 KiB of LDS:
+// its code tiles are a quarter of a bf16 W tile).
+#ifndef SQ_CFG_SMALL_FWDC
+#define SQ_CFG_SMALL_FWDC 128, 128, 2, 4, 4, 64
+#endif
 #ifndef SQ_CFG_HALF_N
 #define SQ_CFG_HALF_N 256, 128, 4, 2, 2, 64
 #endif
@@ -1259,7 +1278,10 @@ template <int MODE, int FMT, int BM, int BN, int... REST>
 static int launch_sized(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
   const int64_t big = (int64_t)tm * tn;
-  if (big < kCUs) return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
+  if (big < kCUs) {
+    if constexpr (MODE == kFwdC) return launch_gemm<MODE, FMT, SQ_CFG_SMALL_FWDC>(g, s);
+    else return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
+  }
   const int rem = (int)(big % kCUs);
   if (SQ_TAIL_SPLIT && BM == 256 && BN == 256 && rem > 0 && rem <= kCUs / 2 && g.ksplit <= 1) {
     if (rem % tm == 0) {                                  // the last rem / tm tile-columns
@@ -1368,7 +1390,8 @@ static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream
   }
   const bool large = big >= kCUs && tokens >= (int64_t)512 * n;
   if (large) return launch_grouped<MODE, FMT, BM, BN, REST...>(gg, p, n, s);
-  return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+  if constexpr (MODE == kFwdC) return launch_grouped<MODE, FMT, SQ_CFG_SMALL_FWDC>(gg, p, n, s);
+  else return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
 }
 
 template <int MODE>

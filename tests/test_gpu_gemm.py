@@ -79,6 +79,10 @@ SHAPES = [
     # few tiles and many token stages: dS splits the token sum (workspace)
     ("mx", 1000, 264, 512),
     ("nv", 700, 520, 256),
+    # the MXFP4 forward's small tile with its four-stage pipeline over 16 and
+    # 32 stages (its last stages wait for every load)
+    ("mx", 256, 256, 1024),
+    ("mx", 520, 264, 2048),
     # 256 x 256 grids ending in a short partial wave of whole tile-columns
     # (forward, dX) or tile-rows (dS), with ragged edges: those go to a second
     # launch of 256 x 128 or 128 x 256 tiles
