@@ -87,6 +87,7 @@ SHAPES = [
     # (forward, dX) or tile-rows (dS), with ragged edges: those go to a second
     # launch of 256 x 128 or 128 x 256 tiles
     ("mx", 4096, 4360, 64),
+    ("nv", 4096, 4360, 64),
     ("nv", 4096, 64, 4368),
     ("mx", 64, 4096, 4384),
     ("nv", 64, 4096, 4368),
@@ -133,7 +134,8 @@ def test_bf16_outputs_are_rounded_f32_outputs(sq, fmt, T, O, I):
         assert np.array_equal(got, want)
 
 
-@pytest.mark.parametrize("T,O,I", [(300, 264, 1024), (4100, 4104, 512), (64, 256, 512), (130, 72, 1536)])
+@pytest.mark.parametrize("T,O,I", [(300, 264, 1024), (4100, 4104, 512), (64, 256, 512), (130, 72, 1536),
+                                   (4096, 4360, 512)])
 def test_mx_forward_both_dequant_paths(sq, T, O, I):
     """An MXFP4 forward with 16-byte aligned codes and scales and I a multiple
     of 512 dequantises each wave's operand in registers; codes that are only
