@@ -192,7 +192,13 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
 #pragma unroll
   for (int u = 0; u < kRtnChunks; ++u) {
     const int64_t c = c0 + 256 * u;
-    v[u] = c < n_chunks ? *reinterpret_cast<const uint4*>(W + 8 * c) : make_uint4(0, 0, 0, 0);
+    // the weight is read once: streaming (non-temporal) loads
+    if (c < n_chunks) {
+      const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(W + 8 * c));
+      v[u] = make_uint4(t[0], t[1], t[2], t[3]);
+    } else {
+      v[u] = make_uint4(0, 0, 0, 0);
+    }
   }
   // scale bytes of whole groups of four blocks leave as 4-byte stores when
   // the plane is 4-byte aligned

@@ -217,7 +217,7 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
     const uint32_t b2 = (uint32_t)__shfl_down((int)sbyte, 2 * LPB);
     const uint32_t b3 = (uint32_t)__shfl_down((int)sbyte, 3 * LPB);
     if (valid) {
-      reinterpret_cast<uint32_t*>(codes)[c] = packed;
+      __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t*>(codes) + c);   // streaming store
       if (c < pack_below) {
         if ((c % kGroup) == 0)
           reinterpret_cast<uint32_t*>(scales)[c / kGroup] = sbyte | (b1 << 8) | (b2 << 16) | (b3 << 24);
