@@ -90,12 +90,14 @@ struct RtnItem {
 };
 // Weights of one re-quantisation launch (one format, one rule), as arrays
 // within the 4 KiB kernel-argument limit.  Weight p owns the workgroups
-// [span_begin[p], span_begin[p+1]), 512 chunks of 8 weights each.
+// [span_begin[p], span_begin[p+1]), rtn_span(fmt, rule) chunks of 8 weights
+// each.
 constexpr int kRtnPerLaunch = 56;
 // Chunks of 8 weights per lane: MXFP4 nearest-even (the lightest per-chunk
 // work) streams best with two, every other format and rule with four (more
 // loads in flight behind the longer arithmetic): 3.6-3.7 -> 3.9-4.0 TB/s for
-// NVFP4 nearest-even over the 8B model, 5.7 -> 5.5 for MXFP4 nearest-even.
+// NVFP4 nearest-even over the 8B model, while MXFP4 nearest-even went
+// 5.7 -> 5.5 with four.
 constexpr int rtn_chunks(int fmt, int rule) { return (fmt == 0 && rule == 0) ? 2 : 4; }
 constexpr int rtn_span(int fmt, int rule) { return 256 * rtn_chunks(fmt, rule); }
 struct RtnBatch {
