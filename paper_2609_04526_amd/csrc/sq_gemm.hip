@@ -1260,6 +1260,19 @@ static int launch_gemm(const GemmArgs& g, hipStream_t s) {
 #ifndef SQ_CFG_HALF_M
 #define SQ_CFG_HALF_M 128, 256, 2, 4, 2, 64
 #endif
+// Per-product knobs for the second launch: dS's half tiles run three stages
+// (144 KiB of LDS; the split dS products of the 8B MLP 389.5 -> 385.7 us);
+// four stages for the MXFP4 forward's half tile timed slower (383.5 ->
+// 393.7 us).
+#ifndef SQ_CFG_HALF_N_FWDC
+#define SQ_CFG_HALF_N_FWDC SQ_CFG_HALF_N
+#endif
+#ifndef SQ_CFG_HALF_N_DS
+#define SQ_CFG_HALF_N_DS 256, 128, 4, 2, 3, 64
+#endif
+#ifndef SQ_CFG_HALF_M_DS
+#define SQ_CFG_HALF_M_DS 128, 256, 2, 4, 3, 64
+#endif
 #ifndef SQ_TAIL_SPLIT
 #define SQ_TAIL_SPLIT 1
 #endif
@@ -1291,7 +1304,10 @@ static int launch_sized(const GemmArgs& g, hipStream_t s) {
       b.n_off = cols;
       b.n_cnt = g.N - cols;
       const int rc = launch_gemm<MODE, FMT, BM, BN, REST...>(a, s);
-      return rc != 0 ? rc : launch_gemm<MODE, FMT, SQ_CFG_HALF_N>(b, s);
+      if (rc != 0) return rc;
+      if constexpr (MODE == kFwdC) return launch_gemm<MODE, FMT, SQ_CFG_HALF_N_FWDC>(b, s);
+      else if constexpr (MODE == kDs) return launch_gemm<MODE, FMT, SQ_CFG_HALF_N_DS>(b, s);
+      else return launch_gemm<MODE, FMT, SQ_CFG_HALF_N>(b, s);
     }
     if (rem % tn == 0) {                                  // the last rem / tn tile-rows
       const int rows = (tm - rem / tn) * BM;
@@ -1300,7 +1316,9 @@ static int launch_sized(const GemmArgs& g, hipStream_t s) {
       b.m_off = rows;
       b.m_cnt = g.M - rows;
       const int rc = launch_gemm<MODE, FMT, BM, BN, REST...>(a, s);
-      return rc != 0 ? rc : launch_gemm<MODE, FMT, SQ_CFG_HALF_M>(b, s);
+      if (rc != 0) return rc;
+      if constexpr (MODE == kDs) return launch_gemm<MODE, FMT, SQ_CFG_HALF_M_DS>(b, s);
+      else return launch_gemm<MODE, FMT, SQ_CFG_HALF_M>(b, s);
     }
   }
   return launch_gemm<MODE, FMT, BM, BN, REST...>(g, s);
