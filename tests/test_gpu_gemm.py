@@ -91,6 +91,8 @@ SHAPES = [
     ("nv", 4096, 64, 4368),
     ("mx", 64, 4096, 4384),
     ("nv", 64, 4096, 4368),
+    ("mx", 64, 4360, 4096),
+    ("nv", 64, 4360, 4096),
 ]
 
 
