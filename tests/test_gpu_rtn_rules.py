@@ -233,3 +233,26 @@ def test_grouped_rejects_a_shared_amax_slot(sq):
         w["ws2_in"] = float(np.float32(1 / 448))
     sq.rtn_quantize_grouped("nv", "even", ws)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+def test_grouped_8b_layer_equals_single_calls(sq, fmt):
+    """The seven linears of one 8B layer (q, k, v, o, gate, up, down), bf16
+    weights drawn on the device, re-quantised in one grouped call and one call
+    each: identical bytes."""
+    B = codec.BLOCK[fmt]
+    ws = []
+    for k, (name, O, I) in enumerate(inputs.LLAMA8B_LAYER):
+        W = (inputs.device_bf16_normal(7000 + k, (O, I)).float() * 0.02).to(torch.bfloat16)
+        ws.append(dict(W=W, codes=torch.empty((O, I // 2), dtype=torch.uint8, device="cuda"),
+                       scales=torch.empty((O, I // B), dtype=torch.uint8, device="cuda"),
+                       ws2_out=torch.empty(1, device="cuda"), ws2_in=0.0))
+    print(f"[grouped 8b] fmt={fmt}", flush=True)
+    sq.rtn_quantize_grouped(fmt, "even", ws)
+    torch.cuda.synchronize()
+    for w in ws:
+        c, s, w2 = sq.rtn_quantize(fmt, w["W"], sq.TIE_EVEN, 0.0)
+        torch.cuda.synchronize()
+        assert torch.equal(w["codes"], c) and torch.equal(w["scales"], s)
+        if fmt == "nv":
+            assert torch.equal(w["ws2_out"], w2)
