@@ -56,11 +56,3 @@ def merge_copy(scale_bytes: np.ndarray, src: np.ndarray) -> np.ndarray:
         raise ValueError("src must match the scale plane")
     return src.copy()
 
-
-def round_grid_value(fmt: str, s: np.ndarray, ws2: float = 1.0) -> np.ndarray:
-    """round_grid(s) as a value (fp64), through the same encoders as the merge."""
-    s = np.asarray(s, dtype=np.float32)
-    if fmt == codec.NV:
-        w = np.float32(ws2)
-        return codec.E4M3_TABLE[codec.e4m3_encode(s / w)] * float(w)
-    return codec.E8M0_TABLE[codec.e8m0_encode_log(s)]

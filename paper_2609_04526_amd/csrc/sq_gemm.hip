@@ -60,29 +60,6 @@ constexpr int kXcds = 8;                // MI355X: workgroups are dealt round-ro
 constexpr uint32_t kOOB = 0x80000000u;  // a buffer offset past every operand: reads zero
 
 #define SQ_LDS __attribute__((address_space(3)))
-// Schedule knobs for tuning builds: SQ_DMA_SPREAD 0 issues a stage's DMA at
-// the barrier, 1 one quarter per MFMA slice, 2 two quarters in each of the
-// first two slices; SQ_FWD_W_AHEAD2 1 fetches the forward's W two stages ahead.
-#ifndef SQ_DMA_SPREAD
-#define SQ_DMA_SPREAD 2
-#endif
-#ifndef SQ_DX_W_BRANCHFREE
-#define SQ_DX_W_BRANCHFREE 1
-#endif
-#ifndef SQ_DX_W_AHEAD2
-#define SQ_DX_W_AHEAD2 0
-#endif
-#ifndef SQ_SCHED_LATE_DX
-#define SQ_SCHED_LATE_DX 0
-#endif
-#ifndef SQ_FWD_W_AHEAD2
-#define SQ_FWD_W_AHEAD2 1
-#endif
-// SQ_SCHED_LATE 1: the stage barrier sits before the MFMAs of the last slice
-// of a stage (operand reads run one slice ahead, across the barrier).
-#ifndef SQ_SCHED_LATE
-#define SQ_SCHED_LATE 1
-#endif
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -142,19 +119,10 @@ __device__ __forceinline__ DmaRsrc make_dma_rsrc(const void* p, uint32_t bytes) 
 // tile a copy fills from the tile being read, and would otherwise stall
 // every later LDS read until the copy lands.  The loop waits for the copies
 // explicitly (vmcnt) before the barrier that publishes a stage.
-#ifndef SQ_DMA_ASM
-#define SQ_DMA_ASM 1
-#endif
 __device__ __forceinline__ void dma16(DmaRsrc r, SQ_LDS void* dst, uint32_t voff) {
-#if SQ_DMA_ASM
   const int lds = __builtin_amdgcn_readfirstlane((int)(uint32_t)reinterpret_cast<uintptr_t>(dst));
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(voff), "s"(r.v)
                : "memory", "m0");
-#else
-  __amdgpu_buffer_rsrc_t b = __builtin_amdgcn_make_buffer_rsrc(
-      reinterpret_cast<void*>((uint64_t)(uint32_t)r.v[0] | ((uint64_t)(uint32_t)r.v[1] << 32)), (short)0, r.v[2], r.v[3]);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(b, dst, 16, (int)voff, 0, 0, 0);
-#endif
 }
 
 // Wait until at most n vector-memory loads of this wave are outstanding and
@@ -337,18 +305,9 @@ __host__ __device__ constexpr int dma_count() {
 // tokens) and 8 code panels (0.5 MiB): 96 MiB fetched per 4096^3 forward or
 // dX against 144 MiB at height 8, in the same time.  For dS both operands are
 // 2 MiB panels and heights 4 and 8 fetch the same.
-#ifndef SQ_GROUPM_FWD
-#define SQ_GROUPM_FWD 4
-#endif
-#ifndef SQ_GROUPM_DX
-#define SQ_GROUPM_DX 4
-#endif
-#ifndef SQ_GROUPM_DS
-#define SQ_GROUPM_DS 8
-#endif
 template <int MODE>
 constexpr int group_m() {
-  return MODE == kDs ? SQ_GROUPM_DS : MODE == kDx ? SQ_GROUPM_DX : SQ_GROUPM_FWD;
+  return MODE == kDs ? 8 : 4;
 }
 
 template <int kGroupM>
@@ -608,7 +567,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
                                                               (uint32_t)k0 * (uint32_t)g.O * 2u, wave_u);
     }
   };
-  constexpr bool kSpread = SQ_DMA_SPREAD && STAGES == 2;
+  // The forward and dX (kFwdR, kDx) run the two-stage schedule of `step`;
+  // the MXFP4 register forward and dS run the late-barrier schedule of `step2`.
+  constexpr bool kLate = MODE == kFwdC || MODE == kDs;
+  static_assert(kLate || STAGES == 2, "the early-barrier schedule keeps two stages");
 
   // ---- W through registers (DX: W^T tile [64 o][BN i]; FWDR: W tile
   // [BN o][64 i]), one dword of 8 codes along i per item, dequantised and
@@ -618,19 +580,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // The forward fetches W two stages ahead through branch-free buffer loads
   // (an item outside the layer reads at an offset past the operand: zeros),
   // so the wait before a dequantisation leaves the newer loads in flight.
-  constexpr int kWAhead = ((MODE == kFwdR && SQ_FWD_W_AHEAD2) || (MODE == kDx && SQ_DX_W_AHEAD2)) ? 2 : 1;
-  static_assert(kWAhead == 1 || STAGES == 2, "two W register sets alternate with the stage parity");
+  constexpr int kWAhead = MODE == kFwdR ? 2 : 1;
   uint32_t w_reg[kWAhead][kWPer], w_sb[kWAhead][kWPer];
-  auto w_item = [&](int p, int kt, int& o, int& i) {
-    const int idx = tid + p * NT;
-    if constexpr (MODE == kDx) {
-      o = kt * kBK + idx / (BN / 8);
-      i = n0 + (idx % (BN / 8)) * 8;
-    } else {
-      o = n0 + idx / 8;
-      i = kt * kBK + (idx % 8) * 8;
-    }
-  };
   // Forward W items: row o = n0 + idx/8 is fixed, the 8 columns start at
   // kt*64 + (idx%8)*8, so each item keeps byte offsets at kt = 0 (past the
   // operand for rows outside the layer) and a column limit.
@@ -642,7 +593,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // of W^T's stage and the 8 columns from n0 + (tid % (BN/8))*8, the same
   // columns for every p; a column block outside the layer is marked kOOB and
   // a row past O reads at kOOB, so the loads take no branches.
-  constexpr bool kDxFree = MODE == kDx && SQ_DX_W_BRANCHFREE;
+  constexpr bool kDxFree = MODE == kDx;
   uint32_t dxc = 0, dxs = 0;
   if constexpr (kDxFree) {
     static_assert(NT % (BN / 8) == 0, "every item of a thread keeps its columns");
@@ -684,16 +635,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
           const uint32_t os = in ? (uint32_t)o * (uint32_t)g.G + dxs : kOOB;
           w_reg[u][p] = __builtin_amdgcn_raw_buffer_load_b32(rw_codes, (int)oc, 0, 0);
           w_sb[u][p] = __builtin_amdgcn_raw_buffer_load_b8(rw_scales, (int)os, 0, 0);
-          continue;
-        }
-        int o, i;
-        w_item(p, kt, o, i);
-        if (o < g.O && i < g.I) {
-          w_reg[u][p] = *reinterpret_cast<const uint32_t*>(g.codes + (size_t)o * (g.I >> 1) + (i >> 1));
-          w_sb[u][p] = g.scales[(size_t)o * g.G + i / B];
-        } else {
-          w_reg[u][p] = 0u;
-          w_sb[u][p] = 0x38u;
         }
       }
     }
@@ -752,45 +693,23 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   auto step = [&](auto SC, int kt) {
     constexpr int S = decltype(SC)::value;
     constexpr int SNEXT = (S + STAGES - 1) % STAGES;          // stage that receives kt + STAGES - 1
-    // stage kt is complete once only the DMA of later stages is outstanding
-    if constexpr (kSpread) {
-      wait_vm_lgkm0<0>();           // the last DMA quarter was issued at the end of the previous step
-    } else if constexpr (kWAhead == 2) {
-      wait_vm_lgkm0<2 * kWPer>();   // the W loads of stage kt+1 may still be out
-    } else {
-      const int later = min(STAGES - 2, nk - 1 - kt);
-      if (later >= 2) wait_vm_lgkm0<(2 * kDma < 63 ? 2 * kDma : 63)>();
-      else if (later == 1) wait_vm_lgkm0<kDma>();
-      else wait_vm_lgkm0<0>();
-    }
+    // stage kt is complete once every load this thread issued has landed:
+    // the last DMA quarter went out at the end of the previous step, and the
+    // W registers of stage kt + 1 (kt + 2 for kFwdR) are loaded after this wait
+    wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (kSpread) {
-      if constexpr (kWAhead == 2) load_w(kt + 2, std::integral_constant<int, S % 2>{});
-      else if constexpr (kWReg) {
-        if (kt + 1 < nk) load_w(kt + 1, std::integral_constant<int, 0>{});
-      }
-    } else if constexpr (kWAhead == 2) {
-      // issued every step, past the end too, so every step has the same
-      // loads; the DMA goes first, so the wait for it at the next step start
-      // leaves these W loads in flight
-      issue_dma(std::integral_constant<int, SNEXT>{}, kt + STAGES - 1);
-      __builtin_amdgcn_sched_barrier(0);
-      load_w(kt + 2, std::integral_constant<int, S % 2>{});
-    } else {
-      if constexpr (kWReg) {
-        if (kt + 1 < nk) load_w(kt + 1, std::integral_constant<int, 0>{});
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (kt + STAGES - 1 < nk) issue_dma(std::integral_constant<int, SNEXT>{}, kt + STAGES - 1);
+    if constexpr (kWAhead == 2) load_w(kt + 2, std::integral_constant<int, S % 2>{});
+    else if constexpr (kWReg) {
+      if (kt + 1 < nk) load_w(kt + 1, std::integral_constant<int, 0>{});
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    // quarter q of the next stage's DMA is issued between the operand reads
-    // and the MFMAs of slice slot_of(q)
-    auto slot_of = [](int q) { return SQ_DMA_SPREAD == 1 ? q : q / 2; };
+    // quarters 2 s and 2 s + 1 of the next stage's DMA are issued between the
+    // operand reads and the MFMAs of slice s (s = 0, 1)
+    auto slot_of = [](int q) { return q / 2; };
     auto before_mfma = [&](int kk) {
-      if constexpr (kSpread) {
+      if constexpr (!kLate) {
         if (kWAhead == 2 || kt + STAGES - 1 < nk) {
           if (slot_of(0) == kk) dma_part(std::integral_constant<int, SNEXT>{}, kt + 1, std::integral_constant<int, 0>{});
           if (slot_of(1) == kk) dma_part(std::integral_constant<int, SNEXT>{}, kt + 1, std::integral_constant<int, 1>{});
@@ -800,46 +719,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       }
     };
     SQ_LDS uint8_t* st = stage(SC);
-    if constexpr (MODE == kFwdC) {
-      // The lanes of half h (= lane / 32) take k = 32 h + 8 kk .. + 7 of the
-      // stage in slice kk, for both operands: the sum over the stage's 64 k
-      // is the same, and a lane's 32 k are one 16-byte run of codes under one
-      // scale.  A: 16-byte chunk 4 h + kk of its K-contiguous row.
-      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
-      const SQ_LDS uint8_t* cs = st + L::kA;
-      const int h = lane >> 5;
-      // scale byte 2 (kt % 8) + h of the slice's 16-byte chunk
-      const int q = (kt >> 1) & 3;
-      const uint32_t sh = 8u * (2u * (uint32_t)(kt & 1) + (uint32_t)h);
-      u32x4 cw[TN];
-      float sop[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn0 + 32 * j + (lane & 31);
-        cw[j] = *(const SQ_LDS u32x4*)(cs + r * (kBK / 2) + 16 * (h ^ swz_codes(r)));
-        const uint32_t w = q == 0 ? scw[j][0] : q == 1 ? scw[j][1] : q == 2 ? scw[j][2] : scw[j][3];
-        sop[j] = e8m0_as_scale_operand((w >> sh) & 0xFFu);
-      }
-      if ((kt & 7) == 7 && kt + 1 < nk) load_sc((kt + 1) >> 3);
-#pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        bf16x8 fa[TM], fb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 4 * h + kk));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const uint4 d = dequant8_mx(cw[j][kk], sop[j]);
-          __builtin_memcpy(&fb[j], &d, 16);
-        }
-        before_mfma(kk);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-      }
-    } else if constexpr (MODE == kFwdR) {
+    if constexpr (MODE == kFwdR) {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = wbuf(kt);
 #pragma unroll
@@ -879,27 +759,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
       if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
-    } else {
-      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
-      const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
-#pragma unroll
-      for (int kk = 0; kk < BK / 16; ++kk) {
-        bf16x8 fa[TM], fb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) fa[i] = nat_frag<BM>(a, kk, wm0 + i * 32, lane);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) fb[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
-        before_mfma(kk);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-      }
     }
   };
 
-  constexpr bool kLate = MODE == kFwdC || (SQ_SCHED_LATE && MODE == kDs) || (SQ_SCHED_LATE_DX && MODE == kDx);
   if constexpr (!kLate) {
   // ---- prologue: the first STAGES-1 stages in flight
   if constexpr (kWReg) {
@@ -908,31 +770,16 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       commit_w(0, std::integral_constant<int, 0>{});
     }
   }
-  if constexpr (MODE == kFwdC) {
-    if (0 < nk) load_sc(0);
-  }
   __builtin_amdgcn_sched_barrier(0);
   if (0 < nk) issue_dma(std::integral_constant<int, 0>{}, 0);
   if constexpr (kWAhead == 2) {
     if (0 < nk) load_w(1, std::integral_constant<int, 1>{});
   }
-  if constexpr (STAGES > 2) {
-    if (1 < nk) issue_dma(std::integral_constant<int, 1>{}, 1);
-  }
-  if constexpr (STAGES > 3) {
-    if (2 < nk) issue_dma(std::integral_constant<int, 2>{}, 2);
-  }
   __builtin_amdgcn_sched_barrier(0);
 
-  for (int kt0 = 0; kt0 < nk; kt0 += STAGES) {
+  for (int kt0 = 0; kt0 < nk; kt0 += 2) {
     step(std::integral_constant<int, 0>{}, kt0);
     if (kt0 + 1 < nk) step(std::integral_constant<int, 1>{}, kt0 + 1);
-    if constexpr (STAGES > 2) {
-      if (kt0 + 2 < nk) step(std::integral_constant<int, 2>{}, kt0 + 2);
-    }
-    if constexpr (STAGES > 3) {
-      if (kt0 + 3 < nk) step(std::integral_constant<int, 3>{}, kt0 + 3);
-    }
   }
   } else {
   // ---- Late-barrier schedule.  The operands of slice kk + 1 are read from
@@ -972,22 +819,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) f.cd[j] = cst[j][kk];
-    } else if constexpr (MODE == kFwdR) {
-      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
-      const SQ_LDS uint16_t* b = wbuf(kt);
-      const int chunk = 2 * kk + h32;
-#pragma unroll
-      for (int i = 0; i < TM; ++i) f.a[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), chunk));
-#pragma unroll
-      for (int j = 0; j < TN; ++j) f.b[j] = *(const SQ_LDS bf16x8*)(b + kc_off(wn0 + j * 32 + (lane & 31), chunk));
-    } else if constexpr (MODE == kDx) {
-      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
-      const SQ_LDS uint16_t* b = wbuf(kt);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        f.a[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 2 * kk + h32));
-#pragma unroll
-      for (int j = 0; j < TN; ++j) f.b[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
     } else {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
@@ -1054,19 +885,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     // kt + STAGES - 1's DMA and the W loads go out here
     read(SC, kt, I1{}, F1);
     if (kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
-    if constexpr (kWAhead == 2) load_w(kt + 2, std::integral_constant<int, S % 2>{});
-    else if constexpr (kWReg) {
-      if (kt + 1 < nk) load_w(kt + 1, I0{});
-    }
     mma(F0);
     read(SC, kt, I2{}, F0);
     mma(F1);
     read(SC, kt, I3{}, F1);
     mma(F0);
-    // publish stage kt + 1: its W tile, then everyone's DMA and LDS writes
-    if constexpr (kWReg) {
-      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
-    }
+    // publish stage kt + 1: everyone's DMA
     // stage kt + 1 has landed once at most kAhead (kAheadLow) loads are
     // outstanding, if the DMA of stages kt + 2 .. kt + STAGES - 1 all went out
     // after it; in the last stages fewer did, and everything is waited for
@@ -1086,11 +910,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // prologue: stage 0 in LDS and its slice 0 read, then the DMA of stages
   // 1 .. STAGES - 2 and the first half of stage STAGES - 1
   if (nk > 0) {
-    if constexpr (kWReg) {
-      load_w(0, I0{});
-      commit_w(0, I0{});
-    }
-    if constexpr (kWAhead == 2) load_w(1, I1{});
     if constexpr (MODE == kFwdC) load_sc(0);
     issue_dma(I0{}, 0);
     wait_vm_lgkm0<0>();
@@ -1213,29 +1032,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup 
   gemm_tile<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>(g, local, tiles);
 }
 
-// Tile configurations (compile-time; SQ_CFG_* selects one per product for
-// tuning builds).  Each entry: BM, BN, waves along M, waves along N, stages,
+// Tile configurations.  Each entry: BM, BN, waves along M, waves along N, stages,
 // K per stage.  The large tile is used when its grid still gives every CU a
 // workgroup; smaller grids (the 1024-wide key/value projections, MoE experts
 // of a few hundred rows) take the 128 x 128 tile, with four times as many
 // workgroups.  That tile runs 8 waves of 64 x 32 (two workgroups fit a CU):
 // against 4 waves of 64 x 64, the key/value forward gained 16% and the MoE
 // stack 10%.
-#ifndef SQ_CFG_FWD
 #define SQ_CFG_FWD 256, 256, 4, 2, 2, 64
-#endif
-#ifndef SQ_CFG_DX
 #define SQ_CFG_DX 256, 256, 4, 2, 2, 64
-#endif
-#ifndef SQ_CFG_DS
 #define SQ_CFG_DS 256, 256, 4, 2, 2, 64
-#endif
-#ifndef SQ_CFG_FWDC
 #define SQ_CFG_FWDC 256, 256, 4, 2, 2, 64
-#endif
-#ifndef SQ_CFG_SMALL
 #define SQ_CFG_SMALL 128, 128, 2, 4, 2, 64
-#endif
 constexpr int kCUs = 256;   // MI355X compute units
 
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
@@ -1251,31 +1059,16 @@ static int launch_gemm(const GemmArgs& g, hipStream_t s) {
 
 // The MXFP4 forward's small tile keeps four stages in flight (80 KiB of LDS:
 // its code tiles are a quarter of a bf16 W tile).
-#ifndef SQ_CFG_SMALL_FWDC
 #define SQ_CFG_SMALL_FWDC 128, 128, 2, 4, 4, 64
-#endif
-#ifndef SQ_CFG_HALF_N
 #define SQ_CFG_HALF_N 256, 128, 4, 2, 2, 64
-#endif
-#ifndef SQ_CFG_HALF_M
 #define SQ_CFG_HALF_M 128, 256, 2, 4, 2, 64
-#endif
 // Per-product knobs for the second launch: dS's half tiles run three stages
 // (144 KiB of LDS; the split dS products of the 8B MLP 389.5 -> 385.7 us);
 // four stages for the MXFP4 forward's half tile timed slower (383.5 ->
 // 393.7 us).
-#ifndef SQ_CFG_HALF_N_FWDC
 #define SQ_CFG_HALF_N_FWDC SQ_CFG_HALF_N
-#endif
-#ifndef SQ_CFG_HALF_N_DS
 #define SQ_CFG_HALF_N_DS 256, 128, 4, 2, 3, 64
-#endif
-#ifndef SQ_CFG_HALF_M_DS
 #define SQ_CFG_HALF_M_DS 128, 256, 2, 4, 3, 64
-#endif
-#ifndef SQ_TAIL_SPLIT
-#define SQ_TAIL_SPLIT 1
-#endif
 
 // A grid of 256 x 256 tiles that ends in a partial wave (at most half the
 // CUs busy) leaves the other CUs idle while it runs.  When that last partial
@@ -1296,7 +1089,7 @@ static int launch_sized(const GemmArgs& g, hipStream_t s) {
     else return launch_gemm<MODE, FMT, SQ_CFG_SMALL>(g, s);
   }
   const int rem = (int)(big % kCUs);
-  if (SQ_TAIL_SPLIT && BM == 256 && BN == 256 && rem > 0 && rem <= kCUs / 2 && g.ksplit <= 1) {
+  if (BM == 256 && BN == 256 && rem > 0 && rem <= kCUs / 2 && g.ksplit <= 1) {
     if (rem % tm == 0) {                                  // the last rem / tm tile-columns
       const int cols = (tn - rem / tm) * BN;
       GemmArgs a = g, b = g;

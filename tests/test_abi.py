@@ -325,3 +325,84 @@ def test_rollback_and_audit_validation(lib):
     assert lib.sq_byte_diff(16, FAKE, FAKE + 8, FAKE, None) == -3
     assert lib.sq_byte_diff(16, FAKE, FAKE, FAKE + 4, None) == -3
     assert lib.sq_byte_diff(0, None, None, FAKE, None) == 0
+
+
+# ---------------------------------------------------------------- binding checks
+# The C ABI sees bare pointers, so the Python binding checks dtype, contiguity
+# and shape agreement before any call.  These run on CPU tensors: the checks
+# come before the device check, and nothing reaches the library.
+def _layer_cpu(T=8, O=16, I=64, fmt="mx"):
+    import torch
+    B = 32 if fmt == "mx" else 16
+    X = torch.zeros((T, I), dtype=torch.bfloat16)
+    dY = torch.zeros((T, O), dtype=torch.bfloat16)
+    codes = torch.zeros((O, I // 2), dtype=torch.uint8)
+    scales = torch.zeros((O, I // B), dtype=torch.uint8)
+    return X, dY, codes, scales
+
+
+def _cases():
+    import torch
+    from paper_2609_04526_amd import sq
+    X, dY, codes, scales = _layer_cpu()
+    return [
+        ("fwd: X fp32", lambda: sq.sq_fwd("mx", X.float(), codes, scales)),
+        ("fwd: X transposed view", lambda: sq.sq_fwd("mx", torch.zeros((64, 8), dtype=torch.bfloat16).t(),
+                                                       codes, scales)),
+        ("fwd: Y int32", lambda: sq.sq_fwd("mx", X, codes, scales, Y=torch.zeros((8, 16), dtype=torch.int32))),
+        ("fwd: Y too small", lambda: sq.sq_fwd("mx", X, codes, scales, Y=torch.zeros((8, 8)))),
+        ("fwd: scales too few blocks", lambda: sq.sq_fwd("mx", X, codes, scales[:, :1].contiguous())),
+        ("fwd: codes for another I", lambda: sq.sq_fwd("mx", X, codes[:, :16].contiguous(), scales)),
+        ("fwd: I not a multiple of the block", lambda: sq.sq_fwd("mx", X[:, :48].contiguous(),
+                                                                   codes[:, :24].contiguous(), scales)),
+        ("dx: dY fp16", lambda: sq.sq_bwd_dx("mx", dY.half(), codes, scales)),
+        ("dx: dX wrong shape", lambda: sq.sq_bwd_dx("mx", dY, codes, scales, dX=torch.zeros((8, 32)))),
+        ("dx: codes rows != dY columns", lambda: sq.sq_bwd_dx("mx", dY[:, :8].contiguous(), codes, scales)),
+        ("ds: codes rows != dY columns", lambda: sq.sq_bwd_dscale("mx", X, dY[:, :8].contiguous(), codes)),
+        ("ds: dY rows != X rows", lambda: sq.sq_bwd_dscale("mx", X, dY[:4].contiguous(), codes)),
+        ("ds: dS bf16", lambda: sq.sq_bwd_dscale("mx", X, dY, codes,
+                                                 dS=torch.zeros((16, 2), dtype=torch.bfloat16))),
+        ("ds: dS too small", lambda: sq.sq_bwd_dscale("mx", X, dY, codes, dS=torch.zeros((16, 1)))),
+        ("merge: delta shorter", lambda: sq.sq_merge_scales("mx", scales.reshape(-1),
+                                                            delta=torch.zeros(scales.numel() - 1))),
+        ("merge: delta fp64", lambda: sq.sq_merge_scales("mx", scales.reshape(-1),
+                                                         delta=torch.zeros(scales.numel(), dtype=torch.float64))),
+        ("swap: src shorter", lambda: sq.sq_merge_scales("mx", scales.reshape(-1),
+                                                         src=torch.zeros(3, dtype=torch.uint8))),
+        ("rtn: W fp32", lambda: sq.rtn_quantize("mx", torch.zeros((16, 64)))),
+        ("rtn: codes_out too small", lambda: sq.rtn_quantize("mx", torch.zeros((16, 64), dtype=torch.bfloat16),
+                                                             codes=torch.zeros((16, 16), dtype=torch.uint8))),
+        ("grouped fwd: outputs per expert", lambda: sq.sq_fwd_grouped("mx", [X, X], [codes, codes],
+                                                                      [scales, scales], Ys=[torch.zeros((8, 16))])),
+        ("grouped ds: dS wrong shape", lambda: sq.sq_bwd_dscale_grouped("mx", [X], [dY], [codes],
+                                                                        dSs=[torch.zeros((16, 4))])),
+        ("qat: A wrong shape", lambda: sq.sq_qat_requant("mx", codes, scales,
+                                                         torch.zeros((16, 4), dtype=torch.bfloat16),
+                                                         torch.zeros((4, 32), dtype=torch.bfloat16), 1.0)),
+        ("lora: dY rows != X rows", lambda: sq.sq_lora_grads(X, dY[:4].contiguous(),
+                                                             torch.zeros((16, 4), dtype=torch.bfloat16),
+                                                             torch.zeros((4, 64), dtype=torch.bfloat16), 1.0)),
+        ("qast: A wrong shape", lambda: sq.sq_qast_scales("mx", scales, torch.zeros((16, 4), dtype=torch.bfloat16),
+                                                          torch.zeros((4, 3), dtype=torch.bfloat16), 1.0)),
+        ("qast grads: mask wrong shape", lambda: sq.sq_qast_factor_grads(
+            torch.zeros((16, 2)), torch.zeros((16, 3), dtype=torch.uint8),
+            torch.zeros((16, 4), dtype=torch.bfloat16), torch.zeros((4, 2), dtype=torch.bfloat16), 1.0)),
+        ("rollback: applied shorter", lambda: sq.sq_scale_rollback("mx", scales.reshape(-1), torch.zeros(3))),
+        ("byte diff: b shorter", lambda: sq.sq_byte_diff(scales.reshape(-1), torch.zeros(3, dtype=torch.uint8))),
+    ]
+
+
+@pytest.mark.parametrize("k", range(27))
+def test_binding_rejects_bad_tensors(k):
+    cases = _cases()
+    assert len(cases) == 27
+    name, call = cases[k]
+    with pytest.raises(ValueError):
+        call()
+
+
+def test_binding_rejects_host_tensors_that_pass_the_checks():
+    from paper_2609_04526_amd import sq
+    X, dY, codes, scales = _layer_cpu()
+    with pytest.raises(ValueError, match="device tensors"):
+        sq.sq_fwd("mx", X, codes, scales)

@@ -1,10 +1,14 @@
 """GPU parity of sq_fwd / sq_bwd_dx / sq_bwd_dscale against the oracle.
 
-Small and ragged shapes are compared element by element on full outputs
-(normwise relative error <= 2e-3, the bound the target sets for bf16 inputs
-with fp32 accumulation; the measured error is printed).  Full-size 8B shapes
-are compared on seeded sampled rows that the oracle computes one by one, plus
-the exact identity sum(eff * dS) = <dY, Y> = <X, dX> over the full outputs."""
+Small and ragged shapes are compared on full outputs; full-size 8B shapes
+(and the stacked q/k/v and gate/up projections) on 16 seeded rows and 16
+seeded columns of every output, half of them drawn from the last 2048 rows or
+columns, where a grid ending in a partial wave runs its second launch of half
+tiles.  Two gates apply to every compared fp32 output: the normwise relative
+error <= 2e-3 that the target sets for bf16 inputs with fp32 accumulation,
+and a per-element bound of twice the fp32 summation bound gamma_K * sum|terms|
+(tests/parity_check.py), which a single wrong element fails.  The full-size
+checks add the exact identity sum(eff * dS) = <dY, Y> = <X, dX>."""
 
 import numpy as np
 import pytest
@@ -13,6 +17,7 @@ import torch
 from conftest import ensure_library, gpu_ready
 from oracle import codec, linear
 from paper_2609_04526_amd import inputs
+from parity_check import assert_elements
 
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not gpu_ready(), reason="needs a GPU")]
 
@@ -93,7 +98,29 @@ SHAPES = [
     ("nv", 64, 4096, 4368),
     ("mx", 64, 4360, 4096),
     ("nv", 64, 4360, 4096),
+    # the same dS half tiles over 4 token stages, so their three-stage
+    # pipeline reaches its steady-state waits (128 x 256 half tiles for the
+    # last input-feature rows, 256 x 128 for the last output columns)
+    ("mx", 256, 4360, 4096),
+    ("nv", 256, 4360, 4096),
+    ("mx", 256, 4096, 4384),
+    ("nv", 256, 4096, 4368),
 ]
+
+
+def abs_sums(fmt, Xd, dYd, codes, W):
+    """sum_k |terms| of every output element of Y, dX and dS."""
+    aX, adY, aW = np.abs(Xd), np.abs(dYd), np.abs(W)
+    B = codec.BLOCK[fmt]
+    O, I = W.shape
+    aS = (np.abs(linear.code_values(codes)) * (adY.T @ aX)).reshape(O, I // B, B).sum(axis=2)
+    return aX @ aW.T, adY @ aW, aS
+
+
+def depths(fmt, T, O, I):
+    """Roundings per output element of Y, dX, dS (the K sums plus the NVFP4
+    epilogue multiply; dS adds the code multiply and the block sum)."""
+    return I + 2, O + 2, T + codec.BLOCK[fmt] + 2
 
 
 @pytest.mark.parametrize("fmt,T,O,I", SHAPES)
@@ -104,9 +131,15 @@ def test_parity_full_outputs(sq, fmt, T, O, I):
     W = linear.dequant(fmt, codes, sb, ws2)
     eY = normwise(Y, linear.forward(Xd, W))
     eX = normwise(dX, linear.backward_dx(dYd, W))
-    eS = normwise(dS, linear.backward_dscale(fmt, Xd, dYd, codes))
+    rS = linear.backward_dscale(fmt, Xd, dYd, codes)
+    eS = normwise(dS, rS)
     print(f"  normwise errors Y {eY:.2e} dX {eX:.2e} dS {eS:.2e}")
     assert eY <= TOL and eX <= TOL and eS <= TOL
+    aY, aXo, aS = abs_sums(fmt, Xd, dYd, codes, W)
+    kY, kX, kS = depths(fmt, T, O, I)
+    assert_elements(Y, linear.forward(Xd, W), aY, kY, "Y")
+    assert_elements(dX, linear.backward_dx(dYd, W), aXo, kX, "dX")
+    assert_elements(dS, rS, aS, kS, "dS")
 
 
 @pytest.mark.parametrize("fmt", ["mx", "nv"])
@@ -157,6 +190,10 @@ def test_mx_forward_both_dequant_paths(sq, T, O, I):
     ea, eb = normwise(ya, ref), normwise(yb, ref)
     print(f"  normwise errors: registers {ea:.2e}, LDS {eb:.2e}")
     assert ea <= TOL and eb <= TOL
+    W = linear.dequant("mx", codes, sb, ws2)
+    absY = np.abs(X.double().numpy()) @ np.abs(W).T
+    assert_elements(ya, ref, absY, I + 2, "Y (registers)")
+    assert_elements(yb, ref, absY, I + 2, "Y (LDS)")
 
 
 def test_zero_tokens_gives_zero_dscale(sq):
@@ -204,29 +241,77 @@ def test_nan_scale_propagates(sq):
     assert np.all(np.isfinite(np.delete(Y, 3, axis=1)))
 
 
-def _sampled_check(sq, fmt, T, O, I, seed, mx_exp=None, n_rows=6):
-    kw = {} if mx_exp is None else {"mx_exp": mx_exp}
-    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed, **kw)
-    if mx_exp is None and fmt == "mx":
+def _pick(g, n, total, tail=2048):
+    """n distinct indices below total: half from the last `tail`, half from the rest."""
+    lo = max(total - tail, 0)
+    a = g.choice(np.arange(lo, total), n // 2, replace=False)
+    rest = np.setdiff1d(np.arange(total), a)
+    b = g.choice(rest, n - n // 2, replace=False)
+    return np.sort(np.concatenate([a, b]))
+
+
+def _sampled_check(sq, fmt, T, O, I, seed, n=16):
+    """16 rows and 16 columns of Y, dX and dS against the oracle computed for
+    just those elements, each under both gates, plus the full-output identity."""
+    X, dY, codes, sb, ws2 = make_layer(fmt, T, O, I, seed)
+    if fmt == "mx":
         sb = inputs.e8m0_normal_exponents(seed + 3, O, I // 32, -6.0, 1.5)
-    Y, dX, dS = run_all(sq, fmt, X, dY, codes, sb, ws2)
+    B = codec.BLOCK[fmt]
+    G = I // B
+    print(f"[gemm] sampled parity fmt={fmt} T={T} O={O} I={I}", flush=True)
+    Xc, dYc, cc, sc = to_dev(X, dY, codes, sb)
+    Yg = sq.sq_fwd(fmt, Xc, cc, sc, ws2, torch.float32)
+    dXg = sq.sq_bwd_dx(fmt, dYc, cc, sc, ws2, torch.float32)
+    dSg = sq.sq_bwd_dscale(fmt, Xc, dYc, cc)
+    torch.cuda.synchronize()
     g = inputs.rng(seed + 99)
-    rows_t = g.choice(T, n_rows, replace=False)
-    rows_o = g.choice(O, n_rows, replace=False)
+    t_rows, o_cols, i_cols = _pick(g, n, T), _pick(g, n, O), _pick(g, n, I)
+    o_rows, b_cols = _pick(g, n, O), _pick(g, n, G, 2048 // B)
+
+    def take_rows(t, idx):
+        return t[torch.from_numpy(idx).cuda()].cpu().numpy()
+
+    def take_cols(t, idx):
+        return t[:, torch.from_numpy(idx).cuda()].cpu().numpy()
+
     W = linear.dequant(fmt, codes, sb, ws2)
-    Xd = X.double().numpy()
-    dYd = dY.double().numpy()
-    eY = normwise(Y[rows_t], linear.forward(Xd[rows_t], W))
-    eX = normwise(dX[rows_t], linear.backward_dx(dYd[rows_t], W))
-    eS = normwise(dS[rows_o], linear.backward_dscale(fmt, Xd, dYd[:, rows_o], codes[rows_o]))
-    eff = codec.effective_scales(fmt, sb, ws2)
-    a = float(np.sum(eff * dS.astype(np.float64)))
-    b = float(np.sum(dYd * Y.astype(np.float64)))
-    c = float(np.sum(Xd * dX.astype(np.float64)))
-    scale = float(np.sqrt(np.sum(dYd ** 2) * np.sum(Y.astype(np.float64) ** 2)))
-    print(f"  sampled normwise Y {eY:.2e} dX {eX:.2e} dS {eS:.2e}; identity {a:.6e} {b:.6e} {c:.6e}")
-    assert eY <= TOL and eX <= TOL and eS <= TOL
-    assert abs(a - b) <= TOL * scale and abs(c - b) <= TOL * scale
+    aW = np.abs(W)
+    Xd, dYd = X.double().numpy(), dY.double().numpy()
+    aX, adY = np.abs(Xd), np.abs(dYd)
+    kY, kX, kS = depths(fmt, T, O, I)
+    errs = []
+
+    def gate(got, ref, absref, depth, what):
+        errs.append(normwise(got, ref))
+        assert errs[-1] <= TOL, (what, errs[-1])
+        assert_elements(got, ref, absref, depth, what)
+
+    # Y rows t and columns o
+    gate(take_rows(Yg, t_rows), linear.forward(Xd[t_rows], W), aX[t_rows] @ aW.T, kY, "Y rows")
+    gate(take_cols(Yg, o_cols), linear.forward(Xd, W[o_cols]), aX @ aW[o_cols].T, kY, "Y columns")
+    # dX rows t and columns i
+    gate(take_rows(dXg, t_rows), linear.backward_dx(dYd[t_rows], W), adY[t_rows] @ aW, kX, "dX rows")
+    gate(take_cols(dXg, i_cols), linear.backward_dx(dYd, W[:, i_cols]), adY @ aW[:, i_cols], kX, "dX columns")
+    # dS rows o (all blocks of those outputs) and block columns b (all outputs)
+    cv = np.abs(linear.code_values(codes[o_rows]))
+    aS = (cv * (adY[:, o_rows].T @ aX)).reshape(n, G, B).sum(axis=2)
+    gate(take_rows(dSg, o_rows), linear.backward_dscale(fmt, Xd, dYd[:, o_rows], codes[o_rows]), aS, kS, "dS rows")
+    ref_cols, abs_cols = [], []
+    for b in b_cols:
+        cb = codes[:, b * B // 2:(b + 1) * B // 2]
+        ref_cols.append(linear.backward_dscale(fmt, Xd[:, b * B:(b + 1) * B], dYd, cb)[:, 0])
+        abs_cols.append((np.abs(linear.code_values(cb)) * (adY.T @ aX[:, b * B:(b + 1) * B])).sum(axis=1))
+    gate(take_cols(dSg, b_cols), np.stack(ref_cols, 1), np.stack(abs_cols, 1), kS, "dS block columns")
+
+    # sum(eff * dS) = <dY, Y> = <X, dX> over the full outputs, in fp64 on the device
+    eff = torch.from_numpy(codec.effective_scales(fmt, sb, ws2)).cuda()
+    a = float((eff * dSg.double()).sum())
+    b_ = float((dYc.double() * Yg.double()).sum())
+    c = float((Xc.double() * dXg.double()).sum())
+    scale = float(torch.sqrt((dYc.double() ** 2).sum() * (Yg.double() ** 2).sum()))
+    print(f"  sampled normwise errors (Y r/c, dX r/c, dS r/c) {' '.join(f'{e:.1e}' for e in errs)}; "
+          f"identity {a:.6e} {b_:.6e} {c:.6e}")
+    assert abs(a - b_) <= TOL * scale and abs(c - b_) <= TOL * scale
 
 
 def test_parity_8b_attention_projection_mx(sq):
@@ -238,6 +323,15 @@ def test_parity_8b_key_value_projection_mx(sq):
     """1024 x 4096 MXFP4 key/value projection, 4096 tokens: the forward and
     dS grids are too small for the large tile and take the small one."""
     _sampled_check(sq, "mx", 4096, 1024, 4096, seed=2500)
+
+
+@pytest.mark.parametrize("O,I", [(14336, 4096), (4096, 14336), (6144, 4096), (28672, 4096)])
+def test_parity_8b_mlp_and_stacked_mx(sq, O, I):
+    """The MXFP4 shapes of the 8B model step at 4096 tokens: gate/up
+    (14336 x 4096) and down (4096 x 14336), whose grids end in a half wave of
+    whole tile-columns or tile-rows, and the stacked q/k/v (6144 x 4096) and
+    gate/up (28672 x 4096) weights of the fused-projection layout."""
+    _sampled_check(sq, "mx", 4096, O, I, seed=4000 + O + I)
 
 
 @pytest.mark.parametrize("fmt,O,I", [("mx", 14336, 4096), ("mx", 4096, 14336), ("nv", 4096, 14336)])
