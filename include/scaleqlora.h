@@ -145,6 +145,24 @@ int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I,
 size_t sq_bwd_dscale_workspace(int fmt, int64_t T, int64_t O, int64_t I);
 
 /*
+ * sq_bwd_dscale without a workspace, for callers that cannot allocate device
+ * memory: code being captured into a HIP graph, tight serving and training
+ * loops, harnesses that forbid allocation.  It computes exactly what
+ * sq_bwd_dscale computes (same kernels, same summation order, bitwise equal
+ * dS) and allocates nothing: when the token sum is split, the partial dS
+ * planes live in a static device array of the library, SQ_DSCALE_SCRATCH_BYTES
+ * per device (every shape's plan fits in it; a larger need would return
+ * SQ_ERR_WORKSPACE).  The array is shared by every call on a device and keeps
+ * the last call's partial planes; calls that overlap on one device (on
+ * different streams, or from different threads without ordering) race on it
+ * and must be serialised by the caller.  Arguments and errors otherwise as
+ * sq_bwd_dscale.
+ */
+#define SQ_DSCALE_SCRATCH_BYTES ((size_t)4 << 20)
+int sq_bwd_dscale_noalloc(int fmt, int64_t T, int64_t O, int64_t I,
+                          const void* X, const void* dY, const uint8_t* codes, float* dS, void* stream);
+
+/*
  * Scale-plane merge or swap, in place, over n scale bytes (Section 3, "QAST
  * makes merge exact by construction": the merge writes the on-grid scale byte
  * training used and copies the codes; stability recipe items (ii)-(iii): the

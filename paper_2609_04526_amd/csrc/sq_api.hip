@@ -13,6 +13,8 @@
 
 #define SQ_EXPORT extern "C" __attribute__((visibility("default")))
 
+static_assert(SQ_DSCALE_SCRATCH_BYTES == sq::kDscaleScratchBytes, "header and library agree on the scratch size");
+
 namespace {
 
 constexpr int64_t kDimMax = (int64_t(1) << 31) - 1;
@@ -144,6 +146,19 @@ SQ_EXPORT int sq_bwd_dscale(int fmt, int64_t T, int64_t O, int64_t I, const void
   if (need > 0 && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
   return hip_status(sq::gemm_dscale(fmt, (int)T, (int)O, (int)I, X, dY, codes, dS, workspace,
                                     static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int sq_bwd_dscale_noalloc(int fmt, int64_t T, int64_t O, int64_t I, const void* X, const void* dY,
+                                    const uint8_t* codes, float* dS, void* stream) {
+  int st = check_layer(fmt, T, O, I);
+  if (st != SQ_OK) return st;
+  if (!codes || !dS) return SQ_ERR_ARG;
+  if (T > 0 && (!X || !dY)) return SQ_ERR_ARG;
+  if (!aligned(X, 16) || !aligned(dY, 16) || !aligned(codes, 4) || !aligned(dS, 4)) return SQ_ERR_ALIGN;
+  if (sq_bwd_dscale_workspace(fmt, T, O, I) > SQ_DSCALE_SCRATCH_BYTES) return SQ_ERR_WORKSPACE;
+  const int rc = sq::gemm_dscale_static(fmt, (int)T, (int)O, (int)I, X, dY, codes, dS,
+                                        static_cast<hipStream_t>(stream));
+  return rc == -2 ? SQ_ERR_WORKSPACE : hip_status(rc);
 }
 
 SQ_EXPORT int sq_merge_scales(int fmt, int64_t n, uint8_t* scales, const float* delta, const uint8_t* src,

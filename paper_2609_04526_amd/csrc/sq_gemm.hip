@@ -39,6 +39,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "sq_device.h"
@@ -1285,8 +1287,57 @@ __global__ __launch_bounds__(256) void ds_reduce_kernel(const float* __restrict_
   dS[i4] = acc.x; dS[i4 + 1] = acc.y; dS[i4 + 2] = acc.z; dS[i4 + 3] = acc.w;
 }
 
+static int gemm_dscale_ws(int fmt, int T, int O, int I, const void* X, const void* dY, const uint8_t* codes,
+                          float* dS, void* workspace, hipStream_t s);
+
 int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
                 const uint8_t* codes, float* dS, void* workspace, hipStream_t s) {
+  return gemm_dscale_ws(fmt, T, O, I, X, dY, codes, dS, workspace, s);
+}
+
+// ------------------------------------------------------------------ static scratch
+// The split token sum of dS with its partial planes in a fixed device array
+// instead of a caller workspace, for callers that cannot allocate.  Its size
+// bounds every plan: a layer is split only when its 256 x 256 tiles number
+// fewer than the CUs, into splits <= 256 / tiles ranges, so the partial planes
+// hold splits * O * I / B fp32 values <= 256 * 65536 / B * 4 bytes, 4 MiB for
+// B = 16.  Each device holds its own copy of the array until the process ends;
+// its device address is looked up once per device.
+static __device__ __align__(256) uint8_t scratch[kDscaleScratchBytes];
+static_assert((size_t)kCUs * 256 * 256 / 16 * sizeof(float) <= kDscaleScratchBytes,
+              "the static scratch holds the partial planes of every split plan");
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the current device (nullptr on a HIP error).
+void* scratch_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+}  // namespace
+
+int gemm_dscale_static(int fmt, int T, int O, int I, const void* X, const void* dY, const uint8_t* codes, float* dS,
+                       hipStream_t s) {
+  if (gemm_dscale_workspace(fmt, T, O, I) > kDscaleScratchBytes) return -2;
+  void* ws = scratch_ptr();
+  if (!ws) return -1;
+  return gemm_dscale_ws(fmt, T, O, I, X, dY, codes, dS, ws, s);
+}
+
+static int gemm_dscale_ws(int fmt, int T, int O, int I, const void* X, const void* dY, const uint8_t* codes,
+                          float* dS, void* workspace, hipStream_t s) {
   GemmArgs g{};
   g.a = static_cast<const uint16_t*>(X);
   g.b = static_cast<const uint16_t*>(dY);

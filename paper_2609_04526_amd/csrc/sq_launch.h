@@ -15,6 +15,11 @@ int gemm_dscale(int fmt, int T, int O, int I, const void* X, const void* dY,
                 const uint8_t* codes, float* dS, void* workspace, hipStream_t s);
 // Workspace bytes gemm_dscale needs (partial dS planes of a split token sum).
 size_t gemm_dscale_workspace(int fmt, int T, int O, int I);
+// gemm_dscale with the partial planes in the library's static device scratch
+// (kDscaleScratchBytes per device); -2 if the plan would need more.
+constexpr size_t kDscaleScratchBytes = size_t(4) << 20;
+int gemm_dscale_static(int fmt, int T, int O, int I, const void* X, const void* dY,
+                       const uint8_t* codes, float* dS, hipStream_t s);
 
 // Planes of one merge launch, as arrays (kernel arguments are limited to
 // 4 KiB; this layout fits 112 planes).  Plane p is cut into spans of

@@ -98,6 +98,8 @@ def load():
         "sq_bwd_dscale": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p,
                                          _c_p, ctypes.c_size_t, _c_p]),
         "sq_bwd_dscale_workspace": (ctypes.c_size_t, [ctypes.c_int, _c_i64, _c_i64, _c_i64]),
+        "sq_bwd_dscale_noalloc": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p,
+                                                 _c_p]),
         "sq_merge_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_p, _c_p, _c_p, ctypes.c_float,
                                            ctypes.c_int, _c_p]),
         "sq_merge_scales_grouped": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(MergeDesc), _c_p]),
@@ -281,6 +283,22 @@ def sq_bwd_dscale(fmt, X, dY, codes, dS=None, workspace=None):
     wsz = workspace.numel() if workspace is not None else 0
     _check("sq_bwd_dscale", load().sq_bwd_dscale(fmt, T, O, I, _ptr(X), _ptr(dY), _ptr(codes), _ptr(dS),
                                                  _ptr(workspace), wsz, _stream()))
+    return dS
+
+
+def sq_bwd_dscale_noalloc(fmt, X, dY, codes, dS):
+    """sq_bwd_dscale with the library's static device scratch instead of a
+    workspace (the caller passes dS; nothing is allocated)."""
+    fmt = _fmt(fmt)
+    T, I = _dims2(X, "X")
+    O = _dims2(dY, "dY")[1]
+    _need(X, "X", _BF16)
+    _need(dY, "dY", _BF16, (T, O))
+    G = _layer(fmt, O, I, codes)
+    _need(dS, "dS", _F32, (O, G))
+    _dev(X, dY, codes, dS)
+    _check("sq_bwd_dscale_noalloc", load().sq_bwd_dscale_noalloc(fmt, T, O, I, _ptr(X), _ptr(dY), _ptr(codes),
+                                                                 _ptr(dS), _stream()))
     return dS
 
 
