@@ -426,6 +426,34 @@ int sq_lora_grads(int64_t T, int64_t O, int64_t I, int r, const void* X, const v
                   void* stream);
 
 /*
+ * The QAT-LoRA comparator over the E experts of an MoE layer (Section 3, MoE
+ * path, with the weight-space adapter in place of the scale adapter; Appendix
+ * "Training cost per step": the MoE comparison).  Expert e computes exactly
+ * what the single call computes for its weight, bit for bit.
+ *
+ * sq_qat_requant_batched: E stacked experts: codes [E, O, I/2], scales
+ *   [E, O, G], B bf16 [E, O, r], A bf16 [E, r, I], codes_out, scales_out as
+ *   codes, scales; ws2: host array of E per-expert NVFP4 scalars (read during
+ *   the call; ignored and may be NULL for MXFP4).  1 <= E <= 65535, E*O*I/2,
+ *   E*O*r and E*r*I below 2^31; otherwise as sq_qat_requant.
+ * sq_lora_grads_batched: T is a host array of E token counts (T_e >= 0, read
+ *   during the call).  X bf16 [sum T_e, I] and dY bf16 [sum T_e, O] hold the
+ *   experts' routed token rows one expert after another (the rows of expert
+ *   e start after those of experts 0 .. e-1); B bf16 [E, O, r], A bf16
+ *   [E, r, I]; dB fp32 [E, O, r], dA fp32 [E, r, I] (an expert without tokens
+ *   gets zeros).  workspace: at least sq_lora_grads_batched_workspace bytes
+ *   (the sum of each expert's sq_lora_grads_workspace), 16-byte aligned.
+ *   Otherwise as sq_lora_grads.
+ */
+int sq_qat_requant_batched(int fmt, int64_t E, int64_t O, int64_t I, int r, const uint8_t* codes,
+                           const uint8_t* scales, const float* ws2, const void* B, const void* A, float alpha_over_r,
+                           uint8_t* codes_out, uint8_t* scales_out, void* stream);
+size_t sq_lora_grads_batched_workspace(int64_t E, const int64_t* T, int64_t O, int64_t I, int r);
+int sq_lora_grads_batched(int64_t E, const int64_t* T, int64_t O, int64_t I, int r, const void* X, const void* dY,
+                          const void* B, const void* A, float alpha_over_r, float* dB, float* dA, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/*
  * Merge rollback (Appendix B, "Payoff 3: invertible merges and rollback"): a
  * merged scale plane plus the on-grid delta the merge applied restores the
  * base plane byte for byte, with no retained base.  The delta lives in the

@@ -2,8 +2,9 @@
 
     python -m paper_2609_04526_amd.build
 
-Compiles every .hip source under csrc/ into one shared library next to this
-file.  Always recompiles (a few tens of seconds)."""
+Compiles every .hip source under csrc/ (one hipcc process per source, in
+parallel) and links them into one shared library next to this file.  Always
+recompiles."""
 
 import os
 import subprocess
@@ -36,19 +37,36 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-o", tmp, *sources()]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _compile(src, obj, extra):
+    cmd = [HIPCC, *FLAGS, *extra, "-c", "-o", obj, src]
     res = subprocess.run(cmd, capture_output=True, text=True)
-    err = "\n".join(l for l in res.stderr.splitlines() if "packed-fp32-ops" not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    return cmd, res
+
+
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile every .hip source to an object (in parallel), then link the
+    shared library.  `defines` adds -D flags (probe builds only)."""
+    import concurrent.futures
+    import tempfile
+    extra = [f"-D{d}" for d in defines]
+    with tempfile.TemporaryDirectory(prefix="sq_build_") as tmpdir:
+        srcs = sources()
+        objs = [os.path.join(tmpdir, os.path.basename(src) + ".o") for src in srcs]
+        with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+            results = list(ex.map(lambda so: _compile(so[0], so[1], extra), zip(srcs, objs)))
+        for cmd, res in results:
+            err = "\n".join(l for l in res.stderr.splitlines() if "packed-fp32-ops" not in l)
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            if res.returncode != 0:
+                raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
+        tmp = out + ".tmp"
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"link failed ({res.returncode}):\n{res.stderr}")
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -419,9 +419,28 @@ SQ_EXPORT int sq_qat_requant(int fmt, int64_t O, int64_t I, int r, const uint8_t
   if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
   if (fmt == SQ_NVFP4 && !ws2_ok(ws2)) return SQ_ERR_ARG;
   if (!aligned(codes, 4) || !aligned(codes_out, 4) || !aligned(A, 16) || !aligned(B, 2)) return SQ_ERR_ALIGN;
-  return hip_status(sq::qat_requant_launch(fmt, (int)O, (int)I, r, codes, scales, fmt == SQ_NVFP4 ? ws2 : 1.0f, B,
-                                           A, alpha_over_r, codes_out, scales_out,
-                                           static_cast<hipStream_t>(stream)));
+  const float w = fmt == SQ_NVFP4 ? ws2 : 1.0f;
+  return hip_status(sq::qat_requant_launch(fmt, 1, (int)O, (int)I, r, codes, scales, &w, B, A, alpha_over_r,
+                                           codes_out, scales_out, static_cast<hipStream_t>(stream)));
+}
+
+SQ_EXPORT int sq_qat_requant_batched(int fmt, int64_t E, int64_t O, int64_t I, int r, const uint8_t* codes,
+                                     const uint8_t* scales, const float* ws2, const void* B, const void* A,
+                                     float alpha_over_r, uint8_t* codes_out, uint8_t* scales_out, void* stream) {
+  int st = check_layer(fmt, 0, O, I);
+  if (st != SQ_OK) return st;
+  if (E < 1 || E > 65535 || r < 1 || r > kLoraRankMax || O > kRequantRowsMax) return SQ_ERR_SHAPE;
+  if (E * O * I / 2 > kDimMax || E * O * r > kDimMax || E * r * I > kDimMax) return SQ_ERR_SHAPE;
+  if (!codes || !scales || !B || !A || !codes_out || !scales_out) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (fmt == SQ_NVFP4) {
+    if (!ws2) return SQ_ERR_ARG;
+    for (int64_t e = 0; e < E; ++e)
+      if (!ws2_ok(ws2[e])) return SQ_ERR_ARG;
+  }
+  if (!aligned(codes, 4) || !aligned(codes_out, 4) || !aligned(A, 16) || !aligned(B, 2)) return SQ_ERR_ALIGN;
+  return hip_status(sq::qat_requant_launch(fmt, (int)E, (int)O, (int)I, r, codes, scales, ws2, B, A, alpha_over_r,
+                                           codes_out, scales_out, static_cast<hipStream_t>(stream)));
 }
 
 SQ_EXPORT size_t sq_lora_grads_workspace(int64_t T, int64_t O, int64_t I, int r) {
@@ -444,6 +463,45 @@ SQ_EXPORT int sq_lora_grads(int64_t T, int64_t O, int64_t I, int r, const void* 
   if (need > 0 && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
   return hip_status(sq::lora_grads_launch((int)T, (int)O, (int)I, r, X, dY, B, A, alpha_over_r, dB, dA, workspace,
                                           static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+int check_lora_batch(int64_t E, const int64_t* T, int64_t O, int64_t I, int r) {
+  if (E < 1 || E > 65535 || !T) return E < 1 || E > 65535 ? SQ_ERR_SHAPE : SQ_ERR_ARG;
+  int64_t total = 0;
+  for (int64_t e = 0; e < E; ++e) {
+    int st = check_lora_dims(T[e], O, I, r);
+    if (st != SQ_OK) return st;
+    total += T[e];
+  }
+  if (total * I * 2 > kOperandBytesMax || total * O * 2 > kOperandBytesMax) return SQ_ERR_SHAPE;
+  if (E * O * r > kDimMax || E * r * I > kDimMax) return SQ_ERR_SHAPE;
+  return SQ_OK;
+}
+}  // namespace
+
+SQ_EXPORT size_t sq_lora_grads_batched_workspace(int64_t E, const int64_t* T, int64_t O, int64_t I, int r) {
+  if (check_lora_batch(E, T, O, I, r) != SQ_OK) return 0;
+  return sq::lora_grads_batched_workspace((int)E, T, (int)O, (int)I, r);
+}
+
+SQ_EXPORT int sq_lora_grads_batched(int64_t E, const int64_t* T, int64_t O, int64_t I, int r, const void* X,
+                                    const void* dY, const void* B, const void* A, float alpha_over_r, float* dB,
+                                    float* dA, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_lora_batch(E, T, O, I, r);
+  if (st != SQ_OK) return st;
+  int64_t total = 0;
+  for (int64_t e = 0; e < E; ++e) total += T[e];
+  if (!B || !A || !dB || !dA || (total > 0 && (!X || !dY))) return SQ_ERR_ARG;
+  if (!isfinite(alpha_over_r)) return SQ_ERR_ARG;
+  if (!aligned(X, 16) || !aligned(dY, 16) || !aligned(A, 16) || !aligned(B, 2) || !aligned(dB, 4) ||
+      !aligned(dA, 4))
+    return SQ_ERR_ALIGN;
+  const size_t need = sq::lora_grads_batched_workspace((int)E, T, (int)O, (int)I, r);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return SQ_ERR_WORKSPACE;
+  if (need > 0 && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  return hip_status(sq::lora_grads_batched_launch((int)E, T, (int)O, (int)I, r, X, dY, B, A, alpha_over_r, dB, dA,
+                                                  workspace, static_cast<hipStream_t>(stream)));
 }
 
 SQ_EXPORT int sq_scale_applied_delta(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied,

@@ -132,12 +132,6 @@ int rtn_rule_launch(int fmt, int O, int I, const void* W, float ws2_in, int rule
 
 // QAT-LoRA weight-space STE: fused W_eff + nearest re-quantisation, and the
 // factor gradients through the rank (lora_grads_workspace bytes of scratch).
-int qat_requant_launch(int fmt, int O, int I, int r, const uint8_t* codes, const uint8_t* scales, float ws2,
-                       const void* B, const void* A, float c, uint8_t* codes_out, uint8_t* scales_out,
-                       hipStream_t s);
-size_t lora_grads_workspace(int T, int O, int I, int r);
-int lora_grads_launch(int T, int O, int I, int r, const void* X, const void* dY, const void* B, const void* A,
-                      float c, float* dB, float* dA, void* workspace, hipStream_t s);
 
 // QAST low-rank scale step for E stacked experts (E = 1: one plane): on-grid
 // scale bytes (+ clamp mask) and the factor gradients; qast_grads_workspace
@@ -151,6 +145,22 @@ int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base,
 size_t qast_grads_workspace(int E, int O, int G, int r);
 int qast_grads_launch(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const void* B, const void* A,
                       float c, float* dB, float* dA, void* workspace, hipStream_t s);
+
+// QAT-LoRA weight-space STE: fused W_eff + nearest re-quantisation of E
+// stacked experts (ws2: E per-expert scalars, NVFP4), and the factor
+// gradients through the rank of E experts whose token rows are stacked
+// expert-major (T: E token counts; lora_grads_batched_workspace bytes of
+// scratch).  The single-weight forms are E = 1.
+int qat_requant_launch(int fmt, int E, int O, int I, int r, const uint8_t* codes, const uint8_t* scales,
+                       const float* ws2, const void* B, const void* A, float c, uint8_t* codes_out,
+                       uint8_t* scales_out, hipStream_t s);
+size_t lora_grads_workspace(int T, int O, int I, int r);
+int lora_grads_launch(int T, int O, int I, int r, const void* X, const void* dY, const void* B, const void* A,
+                      float c, float* dB, float* dA, void* workspace, hipStream_t s);
+size_t lora_grads_batched_workspace(int E, const int64_t* T, int O, int I, int r);
+int lora_grads_batched_launch(int E, const int64_t* T, int O, int I, int r, const void* X, const void* dY,
+                              const void* B, const void* A, float c, float* dB, float* dA, void* workspace,
+                              hipStream_t s);
 
 // Rollback and byte audit (sq_audit.hip).
 int applied_launch(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied, hipStream_t s);

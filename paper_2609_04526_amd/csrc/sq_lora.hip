@@ -34,15 +34,27 @@ constexpr int kReqRankTile = 32;    // ranks staged in LDS at a time
 
 // The rank is walked in tiles of 32 (A tile [32][512] and B tile [16][32] in
 // LDS), k in increasing order throughout; ranks past r read as 0, which adds
-// exact zeros.
+// exact zeros.  grid.z is the expert of a stack (expert e0 + z, planes
+// [E, O, *] contiguous, its ws2 in the table).
 template <int FMT>
 __global__ __launch_bounds__(256) void qat_requant_kernel(const uint8_t* __restrict__ codes,
-                                                          const uint8_t* __restrict__ scales, float ws2,
+                                                          const uint8_t* __restrict__ scales, Ws2Table ws2t,
                                                           const uint16_t* __restrict__ B,
                                                           const uint16_t* __restrict__ A, int O, int I, int r,
                                                           float c, uint8_t* __restrict__ codes_out,
-                                                          uint8_t* __restrict__ scales_out) {
+                                                          uint8_t* __restrict__ scales_out, int e0) {
   constexpr int BLK = ScaleOperand<FMT>::kBlock;
+  {
+    const int64_t e = (int64_t)e0 + blockIdx.z;
+    const int64_t code_plane = (int64_t)O * (I / 2), scale_plane = (int64_t)O * (I / BLK);
+    codes += e * code_plane;
+    codes_out += e * code_plane;
+    scales += e * scale_plane;
+    scales_out += e * scale_plane;
+    B += e * O * r;
+    A += e * r * I;
+  }
+  const float ws2 = FMT == kMX ? 1.0f : ws2t.v[blockIdx.z];
   __shared__ __align__(16) uint16_t a_lds[kReqRankTile][kReqCols];
   __shared__ __align__(16) uint16_t b_lds[kReqRows][kReqRankTile];
   const int tid = threadIdx.x;
@@ -132,60 +144,91 @@ __global__ __launch_bounds__(256) void qat_requant_kernel(const uint8_t* __restr
   }
 }
 
-int qat_requant_launch(int fmt, int O, int I, int r, const uint8_t* codes, const uint8_t* scales, float ws2,
-                       const void* B, const void* A, float c, uint8_t* codes_out, uint8_t* scales_out,
-                       hipStream_t s) {
-  const dim3 grid((unsigned)((I + kReqCols - 1) / kReqCols), (unsigned)((O + kReqRows - 1) / kReqRows));
+int qat_requant_launch(int fmt, int E, int O, int I, int r, const uint8_t* codes, const uint8_t* scales,
+                       const float* ws2, const void* B, const void* A, float c, uint8_t* codes_out,
+                       uint8_t* scales_out, hipStream_t s) {
   const uint16_t* b = static_cast<const uint16_t*>(B);
   const uint16_t* a = static_cast<const uint16_t*>(A);
-  if (fmt == kMX)
-    hipLaunchKernelGGL(qat_requant_kernel<kMX>, grid, dim3(256), 0, s, codes, scales, 1.0f, b, a, O, I, r, c,
-                       codes_out, scales_out);
-  else
-    hipLaunchKernelGGL(qat_requant_kernel<kNV>, grid, dim3(256), 0, s, codes, scales, ws2, b, a, O, I, r, c,
-                       codes_out, scales_out);
-  return hipGetLastError() == hipSuccess ? 0 : -1;
+  for (int e0 = 0; e0 < E; e0 += kWs2TableMax) {
+    const int n = E - e0 < kWs2TableMax ? E - e0 : kWs2TableMax;
+    Ws2Table t{};
+    for (int k = 0; k < n; ++k) t.v[k] = fmt == kMX ? 1.0f : ws2[e0 + k];
+    const dim3 grid((unsigned)((I + kReqCols - 1) / kReqCols), (unsigned)((O + kReqRows - 1) / kReqRows),
+                    (unsigned)n);
+    if (fmt == kMX)
+      hipLaunchKernelGGL(qat_requant_kernel<kMX>, grid, dim3(256), 0, s, codes, scales, t, b, a, O, I, r, c,
+                         codes_out, scales_out, e0);
+    else
+      hipLaunchKernelGGL(qat_requant_kernel<kNV>, grid, dim3(256), 0, s, codes, scales, t, b, a, O, I, r, c,
+                         codes_out, scales_out, e0);
+    if (hipGetLastError() != hipSuccess) return -1;
+  }
+  return 0;
 }
 
 // ------------------------------------------------------------ thin_n
 // Partial products part[kc][t][j] = sum over K-chunk kc of L[t, k] Rt[j, k]
-// for two independent products per launch (P = X A^T and Q = dY B share
-// M = T, the rank and the padded token count).  bf16 operands, both
-// contiguous along K (a multiple of 8); rows of Rt at or past r and rows of L
-// at or past M read as 0.  A workgroup owns 32 rows and one K-chunk; its 8
-// waves take the chunk's 16-wide steps round-robin and reduce through LDS in
-// a fixed order.  thin_n_finish then sums the chunks in order and writes the
-// transposed bf16 hi/lo pair Lt[hl][j][t].
+// for a list of independent products per launch (each expert has two,
+// P = X A^T and Q = dY B, which share its tokens M, the rank and its padded
+// token count).  bf16 operands, both contiguous along K (a multiple of 8);
+// rows of Rt at or past r and rows of L at or past M read as 0.  A workgroup
+// owns 32 rows and one K-chunk of one product; its 8 waves take the chunk's
+// 16-wide steps round-robin and reduce through LDS in a fixed order.
+// thin_n_finish then sums the chunks in order and writes the transposed bf16
+// hi/lo pair Lt[hl][j][t].
 constexpr int kThinWaves = 8;
 constexpr int kThinKChunk = 1024;
+constexpr int kLoraExperts = 32;    // experts per launch set (two products each)
 
-struct ThinNPair {
-  const uint16_t* L[2];
-  const uint16_t* Rt[2];
-  float* part[2];                   // [chunks][Tp][RW]
-  uint16_t* Lt[2];                  // [2][RW][Tp]
-  int K[2];
-  int chunks[2];
+struct ThinNProb {
+  const uint16_t* L;                // [M, K]
+  const uint16_t* Rt;               // [RW, K]
+  float* part;                      // [chunks][Tp][RW]
+  uint16_t* Lt;                     // [2][RW][Tp]
+  int K, chunks, M, Tp;
+  int blk0;                         // first thin_n workgroup of the product
+  int fblk0;                        // first thin_n_finish workgroup
 };
+struct ThinNList {
+  ThinNProb p[2 * kLoraExperts];
+  int n;
+};
+static_assert(sizeof(ThinNList) <= 4096, "kernel argument budget");
+
+// The last product whose first workgroup is at or before b (first[] ascending).
+template <typename F>
+__device__ __forceinline__ int find_product(int b, int n, F first) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (first(mid) <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
 
 template <int NT>
-__global__ __launch_bounds__(512) void thin_n_kernel(ThinNPair pr, int M, int r, int Tp) {
+__global__ __launch_bounds__(512) void thin_n_kernel(ThinNList pl, int r) {
   constexpr int RW = 32 * NT;
   __shared__ float red[kThinWaves / 2][32][RW + 1];
-  const int pi = (int)blockIdx.y < pr.chunks[0] ? 0 : 1;
-  const int kc = (int)blockIdx.y - (pi ? pr.chunks[0] : 0);
-  const int K = pr.K[pi];
+  const int b = (int)blockIdx.x;
+  const int pi = find_product(b, pl.n, [&](int q) { return pl.p[q].blk0; });
+  const ThinNProb& pr = pl.p[pi];
+  const int rows = pr.Tp / 32;
+  const int local = b - pr.blk0;
+  const int kc = local / rows;
+  const int K = pr.K, M = pr.M, Tp = pr.Tp;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int row0 = blockIdx.x * 32;
+  const int row0 = (local % rows) * 32;
   const int lr = lane & 31, kh = lane >> 5;
   const bool row_ok = row0 + lr < M;
-  const uint16_t* lp = pr.L[pi] + (int64_t)(row0 + lr) * K + 8 * kh;
+  const uint16_t* lp = pr.L + (int64_t)(row0 + lr) * K + 8 * kh;
   const uint16_t* rp[NT];
   bool r_ok[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     r_ok[t] = 32 * t + lr < r;
-    rp[t] = pr.Rt[pi] + (int64_t)(32 * t + lr) * K + 8 * kh;
+    rp[t] = pr.Rt + (int64_t)(32 * t + lr) * K + 8 * kh;
   }
   f32x16 acc[NT];
 #pragma unroll
@@ -238,7 +281,7 @@ __global__ __launch_bounds__(512) void thin_n_kernel(ThinNPair pr, int M, int r,
       }
   }
   __syncthreads();
-  float* out = pr.part[pi] + ((int64_t)kc * Tp + row0) * RW;
+  float* out = pr.part + ((int64_t)kc * Tp + row0) * RW;
   for (int e = tid; e < 32 * RW; e += 512) {
     const int row = e / RW, j = e % RW;
     out[e] = ((red[0][row][j] + red[1][row][j]) + red[2][row][j]) + red[3][row][j];
@@ -250,13 +293,16 @@ __global__ __launch_bounds__(512) void thin_n_kernel(ThinNPair pr, int M, int r,
 // takes 32 tokens of one product (RW / 8 sums per thread, their loads issued
 // together) and transposes them through LDS.
 template <int RW>
-__global__ __launch_bounds__(256) void thin_n_finish_kernel(ThinNPair pr, int Tp) {
+__global__ __launch_bounds__(256) void thin_n_finish_kernel(ThinNList pl) {
   constexpr int kPer = 32 * RW / 256;
   __shared__ float t_s[32][RW + 1];
-  const int pi = blockIdx.y;
-  const int t0 = blockIdx.x * 32;
-  const float* part = pr.part[pi] + (int64_t)t0 * RW;
-  const int chunks = pr.chunks[pi];
+  const int b = (int)blockIdx.x;
+  const int pi = find_product(b, pl.n, [&](int q) { return pl.p[q].fblk0; });
+  const ThinNProb& pr = pl.p[pi];
+  const int Tp = pr.Tp;
+  const int t0 = (b - pr.fblk0) * 32;
+  const float* part = pr.part + (int64_t)t0 * RW;
+  const int chunks = pr.chunks;
   float sum[kPer];
 #pragma unroll
   for (int u = 0; u < kPer; ++u) sum[u] = 0.0f;
@@ -273,7 +319,7 @@ __global__ __launch_bounds__(256) void thin_n_finish_kernel(ThinNPair pr, int Tp
     t_s[e / RW][e % RW] = sum[u];
   }
   __syncthreads();
-  uint16_t* Lt = pr.Lt[pi];
+  uint16_t* Lt = pr.Lt;
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
     const int e = threadIdx.x + 256 * u;
@@ -339,32 +385,33 @@ __device__ __forceinline__ void tm_load(const uint16_t* __restrict__ R, const ui
 }
 
 // One product of the token contraction: Lt hi/lo [2][RW][Tp], R [T, N];
-// blocks = tiles * splits, block b takes column tile b % tiles and token
-// range b / tiles.  trans: partials as [split][N][RW] (the output is [N, r]),
-// else [split][RW][N].
+// tiles * splits workgroups from blk0 on, local workgroup b takes column tile
+// b % tiles and token range b / tiles.  trans: partials as [split][N][RW]
+// (the output is [N, r]), else [split][RW][N].
 struct TmProblem {
   const uint16_t* Lt;
   const uint16_t* R;
   float* part;
-  int N, tiles, tps, splits, trans;
+  int N, tiles, tps, splits, trans, T, Tp, blk0;
 };
-struct TmPair {
-  TmProblem p[2];
-  int blocks0;                      // blocks of problem 0; the rest are problem 1's
+struct TmList {
+  TmProblem p[2 * kLoraExperts];
+  int n;
 };
+static_assert(sizeof(TmList) <= 4096, "kernel argument budget");
 
 template <int JT>
-__global__ __launch_bounds__(256) void thin_m_kernel(TmPair pr, int T, int Tp) {
+__global__ __launch_bounds__(256) void thin_m_kernel(TmList pl) {
   constexpr int RW = 32 * JT;
   constexpr int kAChunks = 2 * RW * (kTmTok / 8) / 256;   // 16-byte A chunks per thread per stage
   __shared__ __align__(16) uint16_t rt[kTmTok * kTmCols];
   __shared__ __align__(16) uint16_t at[2 * RW * kTmTok];
-  const int pi = (int)blockIdx.x < pr.blocks0 ? 0 : 1;
-  const TmProblem& P = pr.p[pi];
+  const int pi = find_product((int)blockIdx.x, pl.n, [&](int q) { return pl.p[q].blk0; });
+  const TmProblem& P = pl.p[pi];
   const uint16_t* __restrict__ Lt = P.Lt;
   const uint16_t* __restrict__ R = P.R;
-  const int N = P.N;
-  const int local = (int)blockIdx.x - (pi ? pr.blocks0 : 0);
+  const int N = P.N, T = P.T, Tp = P.Tp;
+  const int local = (int)blockIdx.x - P.blk0;
   const int tile = local % P.tiles, split = local / P.tiles;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int n0 = tile * kTmCols;
@@ -441,35 +488,56 @@ __global__ __launch_bounds__(256) void thin_m_kernel(TmPair pr, int T, int Tp) {
     }
 }
 
-// dA[j, i] = c * sum over splits (in order) of partA[s][j][i] (i < I, j < r),
-// then dB[o, j] = c * sum over splits of partB[s][o][j]: one thread per output.
-__global__ __launch_bounds__(256) void thin_m_reduce_kernel(const float* __restrict__ partA, int splitsA,
-                                                            const float* __restrict__ partB, int splitsB, int RW,
-                                                            int r, int I, int O, float c, float* __restrict__ dA,
-                                                            float* __restrict__ dB) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+// Per expert: dA[j, i] = c * sum over splits (in order) of partA[s][j][i]
+// (i < I, j < r), then dB[o, j] = c * sum over splits of partB[s][o][j]: one
+// thread per output.  An expert without tokens (no splits) gets zeros.
+struct RedProb {
+  const float* partA;
+  const float* partB;
+  float* dA;
+  float* dB;
+  int splitsA, splitsB, blk0;
+};
+struct RedList {
+  RedProb p[kLoraExperts];
+  int n;
+};
+static_assert(sizeof(RedList) <= 4096, "kernel argument budget");
+
+__global__ __launch_bounds__(256) void thin_m_reduce_kernel(RedList pl, int RW, int r, int I, int O, float c) {
+  const int ei = find_product((int)blockIdx.x, pl.n, [&](int q) { return pl.p[q].blk0; });
+  const RedProb& P = pl.p[ei];
+  const int64_t e = (int64_t)((int)blockIdx.x - P.blk0) * 256 + threadIdx.x;
   const int64_t nA = (int64_t)r * I;
   if (e < nA) {
     const int j = (int)(e / I), i = (int)(e % I);
     float s = 0.0f;
-    for (int q = 0; q < splitsA; ++q) s += partA[((int64_t)q * RW + j) * I + i];
-    dA[e] = __fmul_rn(c, s);
+    for (int q = 0; q < P.splitsA; ++q) s += P.partA[((int64_t)q * RW + j) * I + i];
+    P.dA[e] = P.splitsA ? __fmul_rn(c, s) : 0.0f;
     return;
   }
   const int64_t f = e - nA;
   if (f >= (int64_t)r * O) return;
   const int o = (int)(f / r), j = (int)(f % r);
   float s = 0.0f;
-  for (int q = 0; q < splitsB; ++q) s += partB[((int64_t)q * O + o) * RW + j];
-  dB[f] = __fmul_rn(c, s);
+  for (int q = 0; q < P.splitsB; ++q) s += P.partB[((int64_t)q * O + o) * RW + j];
+  P.dB[f] = P.splitsB ? __fmul_rn(c, s) : 0.0f;
 }
 
-// Bt[RW, O] = B[O, r]^T with rows r .. RW-1 zero; a workgroup moves 64 rows
-// of B (at most 64 x 64 elements, 16 per thread, all loads issued first)
-// through LDS so both sides are read and written contiguously.
-__global__ __launch_bounds__(256) void transpose_b_kernel(const uint16_t* __restrict__ B, int O, int r, int RW,
-                                                          uint16_t* __restrict__ Bt) {
+// Bt[RW, O] = B[O, r]^T with rows r .. RW-1 zero, for the experts of a launch
+// set (grid.y; an expert without tokens has no Bt and is skipped); a
+// workgroup moves 64 rows of B (at most 64 x 64 elements, 16 per thread, all
+// loads issued first) through LDS so both sides are read and written
+// contiguously.
+struct BtList {
+  const uint16_t* B[kLoraExperts];
+  uint16_t* Bt[kLoraExperts];
+};
+__global__ __launch_bounds__(256) void transpose_b_kernel(BtList bl, int O, int r, int RW) {
   __shared__ uint16_t t[64][65];
+  const uint16_t* __restrict__ B = bl.B[blockIdx.y];
+  uint16_t* __restrict__ Bt = bl.Bt[blockIdx.y];
+  if (Bt == nullptr) return;
   const int o0 = blockIdx.x * 64;
   const int rows = min(64, O - o0);
   const int n = rows * r;
@@ -491,19 +559,16 @@ __global__ __launch_bounds__(256) void transpose_b_kernel(const uint16_t* __rest
   }
 }
 
-__global__ void fill_zero_kernel(float* p, int64_t n) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e < n) p[e] = 0.0f;
-}
-
 namespace {
 int rank_width(int r) { return r <= 32 ? 32 : 64; }
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
-int64_t padded_tokens(int T) { return ((int64_t)T + kTmTok - 1) / kTmTok * kTmTok; }
+int64_t padded_tokens(int64_t T) { return (T + kTmTok - 1) / kTmTok * kTmTok; }
 
 // Token range per workgroup of the token contraction: about 256 workgroups
-// per product over its column tiles, in whole 64-token stages.
-int tokens_per_split(int T, int N) {
+// per product over its column tiles, in whole 64-token stages (chosen per
+// expert, as for a single call, so a batched expert computes exactly what
+// its own call computes).
+int tokens_per_split(int64_t T, int N) {
   const int64_t Tp = padded_tokens(T);
   const int64_t tiles = (N + kTmCols - 1) / kTmCols;
   int64_t want = 256 / tiles;
@@ -512,7 +577,7 @@ int tokens_per_split(int T, int N) {
   tps = (tps + kTmTok - 1) / kTmTok * kTmTok;
   return (int)(tps < kTmTok ? kTmTok : tps);
 }
-int64_t splits_of(int T, int N) {
+int64_t splits_of(int64_t T, int N) {
   const int tps = tokens_per_split(T, N);
   return (padded_tokens(T) + tps - 1) / tps;
 }
@@ -527,84 +592,149 @@ TmProblem tm_problem(const uint16_t* Lt, const uint16_t* R, int T, int N, float*
   p.tps = tokens_per_split(T, N);
   p.splits = (int)splits_of(T, N);
   p.trans = trans;
+  p.T = T;
+  p.Tp = (int)padded_tokens(T);
+  p.blk0 = 0;
   return p;
 }
-}  // namespace
 
-size_t lora_grads_workspace(int T, int O, int I, int r) {
-  if (T <= 0) return 0;
+// One expert's scratch: P and Q transposed as bf16 hi/lo [2][RW][Tp], B^T
+// [RW][O], the token-range partials of dA and dB and the K-chunk partials of
+// P and Q.  Nothing for an expert without tokens.
+struct ExpertScratch {
+  uint16_t *Pt, *Qt, *Bt;
+  float *partA, *partB, *partP, *partQ;
+};
+size_t expert_scratch(int64_t T, int O, int I, int r, char* base, ExpertScratch* out) {
+  if (T <= 0) {
+    if (out) *out = ExpertScratch{};
+    return 0;
+  }
   const size_t RW = rank_width(r);
   const size_t Tp = (size_t)padded_tokens(T);
   const size_t kcI = (I + kThinKChunk - 1) / kThinKChunk, kcO = (O + kThinKChunk - 1) / kThinKChunk;
-  return 2 * align256(2 * RW * Tp * 2) + align256(RW * O * 2) + align256((size_t)splits_of(T, I) * I * RW * 4) +
-         align256((size_t)splits_of(T, O) * O * RW * 4) + align256(kcI * Tp * RW * 4) + align256(kcO * Tp * RW * 4);
+  const size_t sz[7] = {align256(2 * RW * Tp * 2), align256(2 * RW * Tp * 2), align256(RW * O * 2),
+                        align256((size_t)splits_of(T, I) * I * RW * 4), align256((size_t)splits_of(T, O) * O * RW * 4),
+                        align256(kcI * Tp * RW * 4), align256(kcO * Tp * RW * 4)};
+  size_t at = 0;
+  char* ptr[7];
+  for (int k = 0; k < 7; ++k) {
+    ptr[k] = base ? base + at : nullptr;
+    at += sz[k];
+  }
+  if (out) {
+    out->Pt = reinterpret_cast<uint16_t*>(ptr[0]);
+    out->Qt = reinterpret_cast<uint16_t*>(ptr[1]);
+    out->Bt = reinterpret_cast<uint16_t*>(ptr[2]);
+    out->partA = reinterpret_cast<float*>(ptr[3]);
+    out->partB = reinterpret_cast<float*>(ptr[4]);
+    out->partP = reinterpret_cast<float*>(ptr[5]);
+    out->partQ = reinterpret_cast<float*>(ptr[6]);
+  }
+  return at;
+}
+}  // namespace
+
+size_t lora_grads_workspace(int T, int O, int I, int r) { return expert_scratch(T, O, I, r, nullptr, nullptr); }
+
+size_t lora_grads_batched_workspace(int E, const int64_t* T, int O, int I, int r) {
+  size_t total = 0;
+  for (int e = 0; e < E; ++e) total += expert_scratch(T[e], O, I, r, nullptr, nullptr);
+  return total;
+}
+
+// Experts e0 .. e0 + n - 1 (n <= kLoraExperts) in one launch set: B^T, P and
+// Q, their transposed hi/lo pairs, the token contractions and the reduction.
+// X and dY hold the experts' token rows one after another (tok0: the first
+// row of expert e0); B, A, dB, dA are stacked [E, O, r], [E, r, I].
+static int lora_set(int e0, int n, const int64_t* T, int64_t tok0, int O, int I, int r, const uint16_t* X,
+                    const uint16_t* dY, const uint16_t* B, const uint16_t* A, float c, float* dB, float* dA,
+                    char*& ws, hipStream_t s) {
+  const int RW = rank_width(r);
+  const int kcI = (I + kThinKChunk - 1) / kThinKChunk, kcO = (O + kThinKChunk - 1) / kThinKChunk;
+  BtList bl{};
+  ThinNList nl{};
+  TmList ml{};
+  RedList rl{};
+  int nblk = 0, fblk = 0, mblk = 0, rblk = 0;
+  int64_t tok = tok0;
+  const int red_per = (int)(((int64_t)r * (I + O) + 255) / 256);
+  for (int k = 0; k < n; ++k) {
+    const int e = e0 + k;
+    const int Te = (int)T[e];
+    ExpertScratch w;
+    ws += expert_scratch(Te, O, I, r, ws, &w);
+    const uint16_t* xe = X + tok * I;
+    const uint16_t* dye = dY + tok * O;
+    tok += Te;
+    bl.B[k] = B + (int64_t)e * O * r;
+    bl.Bt[k] = w.Bt;
+    RedProb rp{};
+    rp.dA = dA + (int64_t)e * r * I;
+    rp.dB = dB + (int64_t)e * O * r;
+    rp.blk0 = rblk;
+    rblk += red_per;
+    if (Te > 0) {
+      const int Tp = (int)padded_tokens(Te);
+      ThinNProb P{xe, A + (int64_t)e * r * I, w.partP, w.Pt, I, kcI, Te, Tp, nblk, fblk};
+      nblk += Tp / 32 * kcI;
+      fblk += Tp / 32;
+      ThinNProb Q{dye, w.Bt, w.partQ, w.Qt, O, kcO, Te, Tp, nblk, fblk};
+      nblk += Tp / 32 * kcO;
+      fblk += Tp / 32;
+      nl.p[nl.n++] = P;
+      nl.p[nl.n++] = Q;
+      TmProblem ma = tm_problem(w.Qt, xe, Te, I, w.partA, 0);   // dA = c Q^T X
+      ma.blk0 = mblk;
+      mblk += ma.tiles * ma.splits;
+      TmProblem mb = tm_problem(w.Pt, dye, Te, O, w.partB, 1);  // dB = c (P^T dY)^T
+      mb.blk0 = mblk;
+      mblk += mb.tiles * mb.splits;
+      ml.p[ml.n++] = ma;
+      ml.p[ml.n++] = mb;
+      rp.partA = w.partA;
+      rp.partB = w.partB;
+      rp.splitsA = ma.splits;
+      rp.splitsB = mb.splits;
+    }
+    rl.p[rl.n++] = rp;
+  }
+  if (nl.n > 0) {
+    hipLaunchKernelGGL(transpose_b_kernel, dim3((unsigned)((O + 63) / 64), (unsigned)n), dim3(256), 0, s, bl, O,
+                       r, RW);
+    if (RW == 32) {
+      hipLaunchKernelGGL(thin_n_kernel<1>, dim3((unsigned)nblk), dim3(512), 0, s, nl, r);
+      hipLaunchKernelGGL(thin_n_finish_kernel<32>, dim3((unsigned)fblk), dim3(256), 0, s, nl);
+      hipLaunchKernelGGL(thin_m_kernel<1>, dim3((unsigned)mblk), dim3(256), 0, s, ml);
+    } else {
+      hipLaunchKernelGGL(thin_n_kernel<2>, dim3((unsigned)nblk), dim3(512), 0, s, nl, r);
+      hipLaunchKernelGGL(thin_n_finish_kernel<64>, dim3((unsigned)fblk), dim3(256), 0, s, nl);
+      hipLaunchKernelGGL(thin_m_kernel<2>, dim3((unsigned)mblk), dim3(256), 0, s, ml);
+    }
+  }
+  hipLaunchKernelGGL(thin_m_reduce_kernel, dim3((unsigned)rblk), dim3(256), 0, s, rl, RW, r, I, O, c);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+int lora_grads_batched_launch(int E, const int64_t* T, int O, int I, int r, const void* X, const void* dY,
+                              const void* B, const void* A, float c, float* dB, float* dA, void* workspace,
+                              hipStream_t s) {
+  char* ws = static_cast<char*>(workspace);
+  int64_t tok = 0;
+  for (int e0 = 0; e0 < E; e0 += kLoraExperts) {
+    const int n = E - e0 < kLoraExperts ? E - e0 : kLoraExperts;
+    if (lora_set(e0, n, T, tok, O, I, r, static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(dY),
+                 static_cast<const uint16_t*>(B), static_cast<const uint16_t*>(A), c, dB, dA, ws, s) != 0)
+      return -1;
+    for (int k = 0; k < n; ++k) tok += T[e0 + k];
+  }
+  return 0;
 }
 
 int lora_grads_launch(int T, int O, int I, int r, const void* X, const void* dY, const void* B, const void* A,
                       float c, float* dB, float* dA, void* workspace, hipStream_t s) {
-  if (T == 0) {
-    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)(((int64_t)O * r + 255) / 256)), dim3(256), 0, s, dB,
-                       (int64_t)O * r);
-    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)(((int64_t)I * r + 255) / 256)), dim3(256), 0, s, dA,
-                       (int64_t)I * r);
-    return hipGetLastError() == hipSuccess ? 0 : -1;
-  }
-  const int RW = rank_width(r);
-  const int Tp = (int)padded_tokens(T);
-  char* w = static_cast<char*>(workspace);
-  uint16_t* Pt = reinterpret_cast<uint16_t*>(w);           // (X A^T)^T as hi/lo [2][RW][Tp]
-  w += align256((size_t)2 * RW * Tp * 2);
-  uint16_t* Qt = reinterpret_cast<uint16_t*>(w);           // (dY B)^T as hi/lo [2][RW][Tp]
-  w += align256((size_t)2 * RW * Tp * 2);
-  uint16_t* Bt = reinterpret_cast<uint16_t*>(w);
-  w += align256((size_t)RW * O * 2);
-  float* partA = reinterpret_cast<float*>(w);
-  w += align256((size_t)splits_of(T, I) * I * RW * 4);
-  float* partB = reinterpret_cast<float*>(w);
-  w += align256((size_t)splits_of(T, O) * O * RW * 4);
-  const int kcI = (I + kThinKChunk - 1) / kThinKChunk, kcO = (O + kThinKChunk - 1) / kThinKChunk;
-  float* partP = reinterpret_cast<float*>(w);
-  w += align256((size_t)kcI * Tp * RW * 4);
-  float* partQ = reinterpret_cast<float*>(w);
-  const uint16_t* x = static_cast<const uint16_t*>(X);
-  const uint16_t* dy = static_cast<const uint16_t*>(dY);
-  hipLaunchKernelGGL(transpose_b_kernel, dim3((unsigned)((O + 63) / 64)), dim3(256), 0, s,
-                     static_cast<const uint16_t*>(B), O, r, RW, Bt);
-  // P = X A^T and Q = dY B
-  ThinNPair np;
-  np.L[0] = x;
-  np.Rt[0] = static_cast<const uint16_t*>(A);
-  np.part[0] = partP;
-  np.Lt[0] = Pt;
-  np.K[0] = I;
-  np.chunks[0] = kcI;
-  np.L[1] = dy;
-  np.Rt[1] = Bt;
-  np.part[1] = partQ;
-  np.Lt[1] = Qt;
-  np.K[1] = O;
-  np.chunks[1] = kcO;
-  const dim3 ngrid((unsigned)(Tp / 32), (unsigned)(kcI + kcO));
-  const dim3 fgrid((unsigned)(Tp / 32), 2);
-  if (RW == 32) {
-    hipLaunchKernelGGL(thin_n_kernel<1>, ngrid, dim3(512), 0, s, np, T, r, Tp);
-    hipLaunchKernelGGL(thin_n_finish_kernel<32>, fgrid, dim3(256), 0, s, np, Tp);
-  } else {
-    hipLaunchKernelGGL(thin_n_kernel<2>, ngrid, dim3(512), 0, s, np, T, r, Tp);
-    hipLaunchKernelGGL(thin_n_finish_kernel<64>, fgrid, dim3(256), 0, s, np, Tp);
-  }
-  // dA = c Q^T X  and  dB = c (P^T dY)^T
-  TmPair mp;
-  mp.p[0] = tm_problem(Qt, x, T, I, partA, 0);
-  mp.p[1] = tm_problem(Pt, dy, T, O, partB, 1);
-  mp.blocks0 = mp.p[0].tiles * mp.p[0].splits;
-  const unsigned mblocks = (unsigned)(mp.blocks0 + mp.p[1].tiles * mp.p[1].splits);
-  if (RW == 32) hipLaunchKernelGGL(thin_m_kernel<1>, dim3(mblocks), dim3(256), 0, s, mp, T, Tp);
-  else hipLaunchKernelGGL(thin_m_kernel<2>, dim3(mblocks), dim3(256), 0, s, mp, T, Tp);
-  const int64_t outs = (int64_t)r * (I + O);
-  hipLaunchKernelGGL(thin_m_reduce_kernel, dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, s, partA,
-                     mp.p[0].splits, partB, mp.p[1].splits, RW, r, I, O, c, dA, dB);
-  return hipGetLastError() == hipSuccess ? 0 : -1;
+  const int64_t t = T;
+  return lora_grads_batched_launch(1, &t, O, I, r, X, dY, B, A, c, dB, dA, workspace, s);
 }
 
 }  // namespace sq

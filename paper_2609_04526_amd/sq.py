@@ -118,6 +118,11 @@ def load():
         "sq_qat_requant": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, ctypes.c_float,
                                           _c_p, _c_p, ctypes.c_float, _c_p, _c_p, _c_p]),
         "sq_lora_grads_workspace": (ctypes.c_size_t, [_c_i64, _c_i64, _c_i64, ctypes.c_int]),
+        "sq_qat_requant_batched": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p,
+                                                  _c_p, _c_p, _c_p, ctypes.c_float, _c_p, _c_p, _c_p]),
+        "sq_lora_grads_batched_workspace": (ctypes.c_size_t, [_c_i64, _c_p, _c_i64, _c_i64, ctypes.c_int]),
+        "sq_lora_grads_batched": (ctypes.c_int, [_c_i64, _c_p, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p, _c_p,
+                                                 ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
         "sq_lora_grads": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p, _c_p,
                                          ctypes.c_float, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
         "sq_qast_scales": (ctypes.c_int, [ctypes.c_int, _c_i64, _c_i64, ctypes.c_int, _c_p, _c_p, _c_p,
@@ -548,6 +553,83 @@ def sq_qat_requant(fmt, codes, scales, B, A, alpha_over_r, ws2=1.0, codes_out=No
                                                    _ptr(A), float(alpha_over_r), _ptr(codes_out),
                                                    _ptr(scales_out), _stream()))
     return codes_out, scales_out
+
+
+def sq_qat_requant_batched(fmt, codes, scales, B, A, alpha_over_r, ws2=None, codes_out=None, scales_out=None):
+    """sq_qat_requant for E stacked experts: codes uint8 [E, O, I/2], scales uint8 [E, O, G],
+    B bf16 [E, O, r], A bf16 [E, r, I]; ws2: E per-expert NVFP4 scalars."""
+    fmt = _fmt(fmt)
+    if not isinstance(codes, torch.Tensor) or codes.dim() != 3 or not isinstance(B, torch.Tensor) or B.dim() != 3:
+        raise ValueError("codes and B must be 3-D (stacked experts)")
+    E, O, I = codes.shape[0], codes.shape[1], codes.shape[2] * 2
+    r = B.shape[2]
+    G = _block(fmt, I)
+    _need(codes, "codes", torch.uint8)
+    _need(scales, "scales", torch.uint8, (E, O, G))
+    _need(B, "B", _BF16, (E, O, r))
+    _need(A, "A", _BF16, (E, r, I))
+    if codes_out is None:
+        codes_out = torch.empty_like(codes)
+    if scales_out is None:
+        scales_out = torch.empty_like(scales)
+    _need(codes_out, "codes_out", torch.uint8, (E, O, I // 2))
+    _need(scales_out, "scales_out", torch.uint8, (E, O, G))
+    w = None
+    if fmt == NVFP4:
+        if ws2 is None or len(ws2) != E:
+            raise ValueError("NVFP4 needs one ws2 per expert")
+        w = (ctypes.c_float * E)(*[float(v) for v in ws2])
+    _dev(codes, scales, B, A, codes_out, scales_out)
+    _check("sq_qat_requant_batched", load().sq_qat_requant_batched(
+        fmt, E, O, I, r, _ptr(codes), _ptr(scales), ctypes.cast(w, ctypes.c_void_p) if w is not None else None,
+        _ptr(B), _ptr(A), float(alpha_over_r), _ptr(codes_out), _ptr(scales_out), _stream()))
+    return codes_out, scales_out
+
+
+def _tokens(T):
+    arr = (ctypes.c_int64 * max(len(T), 1))(*[int(t) for t in T])
+    return arr
+
+
+def sq_lora_grads_batched_workspace(T, O, I, r):
+    return int(load().sq_lora_grads_batched_workspace(len(T), ctypes.cast(_tokens(T), ctypes.c_void_p), O, I, r))
+
+
+def sq_lora_grads_batched(T, X, dY, B, A, alpha_over_r, dB=None, dA=None, workspace=None):
+    """STE factor gradients of E experts: T the E token counts; X bf16 [sum T, I] and
+    dY bf16 [sum T, O] with the experts' token rows one after another; B bf16 [E, O, r],
+    A bf16 [E, r, I] -> dB fp32 [E, O, r], dA fp32 [E, r, I]."""
+    T = [int(t) for t in T]
+    E = len(T)
+    if not isinstance(B, torch.Tensor) or B.dim() != 3 or B.shape[0] != E:
+        raise ValueError("B must be [E, O, r] with one expert per token count")
+    _, O, r = B.shape
+    Ttot, I = _dims2(X, "X")
+    if Ttot != sum(T):
+        raise ValueError(f"X has {Ttot} rows, the token counts add to {sum(T)}")
+    _need(X, "X", _BF16)
+    _need(dY, "dY", _BF16, (Ttot, O))
+    _need(B, "B", _BF16)
+    _need(A, "A", _BF16, (E, r, I))
+    dev = B.device
+    if dB is None:
+        dB = torch.empty((E, O, r), dtype=torch.float32, device=dev)
+    if dA is None:
+        dA = torch.empty((E, r, I), dtype=torch.float32, device=dev)
+    _need(dB, "dB", _F32, (E, O, r))
+    _need(dA, "dA", _F32, (E, r, I))
+    tarr = _tokens(T)
+    need = int(load().sq_lora_grads_batched_workspace(E, ctypes.cast(tarr, ctypes.c_void_p), O, I, r))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if workspace is not None:
+        _need(workspace, "workspace", torch.uint8)
+    _dev(X, dY, B, A, dB, dA, workspace)
+    nbytes = workspace.numel() if workspace is not None else 0
+    _check("sq_lora_grads_batched", load().sq_lora_grads_batched(
+        E, ctypes.cast(tarr, ctypes.c_void_p), O, I, r, _ptr(X), _ptr(dY), _ptr(B), _ptr(A), float(alpha_over_r),
+        _ptr(dB), _ptr(dA), _ptr(workspace), nbytes, _stream()))
+    return dB, dA
 
 
 def sq_lora_grads_workspace(T, O, I, r):

@@ -158,3 +158,56 @@ def test_qat_step_forward_and_dx(sq, fmt):
     Wq = linear.dequant(fmt, rc, rs, ws2)
     assert normwise(Y.float().cpu().numpy(), linear.forward(X.float().numpy(), Wq)) <= GEMM_TOL
     assert normwise(dX.float().cpu().numpy(), linear.backward_dx(dY.float().numpy(), Wq)) <= GEMM_TOL
+
+
+# ---------------------------------------------------------------- MoE experts
+@pytest.mark.parametrize("fmt,E,O,I,r", [("mx", 5, 264, 1056, 32), ("nv", 3, 136, 784, 58), ("nv", 300, 8, 32, 1)])
+def test_requant_batched_equals_single_calls(sq, fmt, E, O, I, r):
+    """Stacked experts (300: two launches of the 256-entry ws2 table), each
+    with its own ws2 for NVFP4: every expert's codes and scales equal its own
+    sq_qat_requant call bit for bit, and the first equals the oracle."""
+    parts = [layer(fmt, O, I, r, seed=6600 + 7 * e) for e in range(E)]
+    codes = torch.from_numpy(np.stack([p[0] for p in parts])).cuda()
+    sb = torch.from_numpy(np.stack([p[1] for p in parts])).cuda()
+    ws2 = [float(np.float32(p[2] * (1 + 0.25 * (e % 3)))) for e, p in enumerate(parts)]
+    B = torch.stack([p[3] for p in parts]).cuda()
+    A = torch.stack([p[4] for p in parts]).cuda()
+    print(f"[qat requant batched] fmt={fmt} E={E} O={O} I={I} r={r}", flush=True)
+    c, s = sq.sq_qat_requant_batched(fmt, codes, sb, B, A, 2.0, ws2 if fmt == "nv" else None)
+    torch.cuda.synchronize()
+    for e in range(E):
+        ce, se = sq.sq_qat_requant(fmt, codes[e], sb[e], B[e], A[e], 2.0, ws2[e] if fmt == "nv" else 1.0)
+        torch.cuda.synchronize()
+        assert torch.equal(c[e], ce) and torch.equal(s[e], se), e
+    rc, rs = qat.requant(fmt, parts[0][0], parts[0][1], ws2[0] if fmt == "nv" else 1.0, parts[0][3], parts[0][4], 2.0)
+    assert np.array_equal(c[0].cpu().numpy(), rc) and np.array_equal(s[0].cpu().numpy(), rs)
+
+
+@pytest.mark.parametrize("Ts,O,I,r", [([300, 0, 1, 129, 77], 264, 1056, 32),
+                                      ([64] * 40 + [0, 513], 64, 512, 58),
+                                      ([0, 0], 16, 32, 4)])
+def test_lora_grads_batched_equals_single_calls(sq, Ts, O, I, r):
+    """Experts with ragged, single, zero and repeated token counts (42 experts:
+    two launch sets of 32): every expert's dB, dA equal its own sq_lora_grads
+    call bit for bit, and match the oracle; experts without tokens get zeros."""
+    E = len(Ts)
+    g = inputs.rng(6700 + E)
+    X = inputs.bf16_normal(6701 + E, (sum(Ts), I)).cuda()
+    dY = inputs.bf16_normal(6702 + E, (sum(Ts), O)).cuda()
+    B = torch.from_numpy(g.standard_normal((E, O, r)).astype(np.float32) * 0.05).to(torch.bfloat16).cuda()
+    A = torch.from_numpy(g.standard_normal((E, r, I)).astype(np.float32) * 0.05).to(torch.bfloat16).cuda()
+    print(f"[lora grads batched] E={E} T={Ts[:6]}... O={O} I={I} r={r}", flush=True)
+    dB, dA = sq.sq_lora_grads_batched(Ts, X, dY, B, A, 2.0)
+    torch.cuda.synchronize()
+    t0 = 0
+    for e, T in enumerate(Ts):
+        Xe, dYe = X[t0:t0 + T], dY[t0:t0 + T]
+        t0 += T
+        sB, sA = sq.sq_lora_grads(Xe, dYe, B[e], A[e], 2.0)
+        torch.cuda.synchronize()
+        assert torch.equal(dB[e], sB) and torch.equal(dA[e], sA), e
+        if T == 0:
+            assert torch.count_nonzero(dB[e]).item() == 0 and torch.count_nonzero(dA[e]).item() == 0
+        elif e < 4:
+            rB, rA = qat.lora_grads(Xe.cpu(), dYe.cpu(), B[e].cpu(), A[e].cpu(), 2.0)
+            assert normwise(dB[e].cpu().numpy(), rB) <= GRAD_TOL and normwise(dA[e].cpu().numpy(), rA) <= GRAD_TOL
