@@ -1035,16 +1035,22 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup 
 }
 
 // Tile configurations.  Each entry: BM, BN, waves along M, waves along N, stages,
-// K per stage.  The large tile is used when its grid still gives every CU a
+// K per stage.  The large tile's 8 waves take 128 x 64 each (2 along M, 4
+// along N) in the MXFP4 forward, dX and dS: every wave dequantises or reads
+// only its own 64 columns of the weight operand, so the register forward
+// converts each code tile in 2 waves instead of 4 (4096^3 forward 117 -> 106
+// us, the 8B MLP forwards -7%, dS -2%, dX -1%; the per-element summation
+// order, and so every result, is unchanged).  The NVFP4 forward timed the
+// same either way and keeps 64 x 128.  The large tile is used when its grid still gives every CU a
 // workgroup; smaller grids (the 1024-wide key/value projections, MoE experts
 // of a few hundred rows) take the 128 x 128 tile, with four times as many
 // workgroups.  That tile runs 8 waves of 64 x 32 (two workgroups fit a CU):
 // against 4 waves of 64 x 64, the key/value forward gained 16% and the MoE
 // stack 10%.
 #define SQ_CFG_FWD 256, 256, 4, 2, 2, 64
-#define SQ_CFG_DX 256, 256, 4, 2, 2, 64
-#define SQ_CFG_DS 256, 256, 4, 2, 2, 64
-#define SQ_CFG_FWDC 256, 256, 4, 2, 2, 64
+#define SQ_CFG_DX 256, 256, 2, 4, 2, 64
+#define SQ_CFG_DS 256, 256, 2, 4, 2, 64
+#define SQ_CFG_FWDC 256, 256, 2, 4, 2, 64
 #define SQ_CFG_SMALL 128, 128, 2, 4, 2, 64
 constexpr int kCUs = 256;   // MI355X compute units
 
