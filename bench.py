@@ -85,6 +85,8 @@ def parse():
     p.add_argument("--no-lifecycle", action="store_true")
     p.add_argument("--no-moe", action="store_true")
     p.add_argument("--no-mlp-nv", action="store_true")
+    p.add_argument("--no-cpu-plan", action="store_true",
+                   help="time only the main oracle sample, not the per-workload oracle plan")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="also run a plain device copy of this many MiB (the copy mode of "
                         "sq_merge_scales: reads N and writes N bytes) to calibrate HBM counters")
@@ -138,7 +140,7 @@ def model_merge(sq, steps):
                                generator=inputs.device_generator(6900))
     code_copy = code_plane.clone()
     for name, fmt, block, mode in (("mx_delta", "mx", 32, "delta"), ("nv_delta", "nv", 16, "delta"),
-                                   ("mx_swap", "mx", 32, "copy")):
+                                   ("mx_swap", "mx", 32, "copy"), ("nv_swap", "nv", 16, "copy")):
         shapes = [(o, i // block) for _ in range(inputs.LLAMA8B_LAYERS) for (_, o, i) in inputs.LLAMA8B_LAYER]
         sizes = [o * g for (o, g) in shapes]
         total = sum(sizes)
@@ -150,8 +152,11 @@ def model_merge(sq, steps):
                               for k, (o, g) in enumerate(shapes)])
         if mode == "delta":
             aux = inputs.device_task_delta(7500, effective_scales_torch(fmt, base, ws2), fmt).float()
-        else:
+        elif fmt == "mx":
             aux = torch.cat([inputs.device_e8m0_normal_exponents(7600 + k, o, g, -6.0, 1.5).reshape(-1)
+                             for k, (o, g) in enumerate(shapes)])
+        else:
+            aux = torch.cat([inputs.device_e4m3_abs_normal(7600 + k, o, g).reshape(-1)
                              for k, (o, g) in enumerate(shapes)])
         scales = base.clone()
         descs, off = [], 0
@@ -225,7 +230,10 @@ def model_lifecycle(sq, steps=3):
     the deploy-side rules (toward zero, stochastic, whole-tensor scale), each
     as one rtn_quantize_grouped call over all 224 linears (and nearest-even
     once more as one rtn_quantize call per linear).  Algorithmic
-    bytes 2 + 0.5 + 1/B per weight.  The diff census counts code nibbles that differ from the base
+    bytes 2 + 0.5 + 1/B per weight.  The re-quantising swap of a task into the
+    served model also runs as one fused pass per linear, base codes + scales +
+    the task's rank-16 adapter -> new codes + scales (sq_qat_requant, nearest
+    even), with no bf16 weight in between.  The diff census counts code nibbles that differ from the base
     plane (per tie rule) and between the tie rules, and changed scale bytes."""
     lut = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0],
                        device="cuda")
@@ -296,6 +304,32 @@ def model_lifecycle(sq, steps=3):
                 sb_moved = sum(int((it["sr"] != it["sb"]).sum().item()) for it in items)
                 res[label]["code_nibbles_vs_base_frac"] = round(nb_moved / weights, 5)
                 res[label]["scale_bytes_vs_base"] = sb_moved
+        # the re-quantising swap from the base planes and the task adapter
+        fused_items = []
+        for k, it in enumerate(items):
+            o, half = it["codes"].shape
+            g = inputs.device_generator(8700 + k)
+            fused_items.append((it, (torch.randn((o, 16), generator=g, device="cuda") * 0.02).to(torch.bfloat16),
+                                (torch.randn((16, 2 * half), generator=g, device="cuda") * 0.02).to(torch.bfloat16)))
+
+        def run_fused():
+            for it, Bq, Aq in fused_items:
+                sq.sq_qat_requant(fmt, it["codes"], it["sb"], Bq, Aq, 1.0, ws2 if fmt == "nv" else 1.0,
+                                  codes_out=it["cr"], scales_out=it["sr"])
+        run_fused()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            run_fused()
+        e1.record()
+        torch.cuda.synchronize()
+        fms = e0.elapsed_time(e1) / steps
+        fbytes = weights * (0.5 + 1.0 / block) * 2            # codes + scales read, written
+        res["requant_swap_fused"] = {"ms": round(fms, 3), "GB/s": round(fbytes / (fms * 1e-3) / 1e9, 1),
+                                     "what": "sq_qat_requant over all 224 linears: base codes + scales + "
+                                             "rank-16 task adapter -> re-quantised codes + scales"}
+        del fused_items
         # census (ties to even and ties away, both with the fixed ws2 for NVFP4)
         sq.rtn_quantize_grouped(fmt, "even", [dict(W=it["Wm"], codes=it["ce"], scales=it["se"], ws2_out=it["w2"],
                                                    ws2_in=ws2 if fmt == "nv" else 0.0) for it in items])
@@ -382,8 +416,8 @@ def model_step(sq, steps, warmup, comparator=True):
     the QAT-LoRA step runs the weight-space STE comparator on the native path
     (fused re-quantisation of W + B A, forward and dX on those codes, factor
     gradients through the rank).  A second, framework-style comparator repeats
-    the paper's own construction on layer 0's seven linears (rank 32), reported
-    x32 as an extrapolation: W' = deq(W) + B A, RTN fake-quantisation
+    the paper's own construction on all 224 linears (rank 32, each with its own
+    weight and factors): W' = deq(W) + B A, RTN fake-quantisation
     (rtn_quantize, then a torch dequant), the three dense bf16 GEMMs through
     torch (hipBLASLt) with dW materialised in fp32, then dB = dW A^T and
     dA = B^T dW."""
@@ -569,15 +603,23 @@ def model_moe(sq, steps=3, warmup=1):
     buffers are shared across layers (values do not change the timing).  The
     QAST variant adds the batched rank-32 scale step of all experts per linear
     (sq_qast_scales_batched before the forward, sq_qast_factor_grads_batched
-    after dS)."""
+    after dS).  The QAT-LoRA variant is the weight-space comparator on the
+    same experts: sq_qat_requant_batched (all experts' W + B A re-quantised)
+    before the grouped forward, then the grouped dX on those codes and
+    sq_lora_grads_batched (rank 32) instead of dS."""
     L, E, topk, Tm, r = 48, 128, 8, 4096, 32
     g = inputs.rng(8800)
     Ts = g.multinomial(Tm * topk, g.dirichlet(np.full(E, 2.0))).tolist()
     shapes = (("gate", 768, 2048), ("up", 768, 2048), ("down", 2048, 768))
     acts = {}
-    for (name, o, i) in shapes:
-        acts[name] = dict(X=[inputs.device_bf16_normal(8900 + e, (T, i)) for e, T in enumerate(Ts)],
-                          dY=[inputs.device_bf16_normal(9100 + e, (T, o)) for e, T in enumerate(Ts)],
+    offs = np.concatenate([[0], np.cumsum(Ts)]).tolist()
+    for k, (name, o, i) in enumerate(shapes):
+        # the routed rows of all experts, expert after expert (the grouped layout)
+        Xall = inputs.device_bf16_normal(8900 + k, (offs[-1], i))
+        dYall = inputs.device_bf16_normal(9100 + k, (offs[-1], o))
+        acts[name] = dict(Xall=Xall, dYall=dYall,
+                          X=[Xall[offs[e]:offs[e + 1]] for e in range(E)],
+                          dY=[dYall[offs[e]:offs[e + 1]] for e in range(E)],
                           Y=[torch.empty((T, o), dtype=torch.bfloat16, device="cuda") for T in Ts],
                           dX=[torch.empty((T, i), dtype=torch.bfloat16, device="cuda") for T in Ts],
                           dS=[torch.empty((o, i // 32), dtype=torch.float32, device="cuda") for _ in Ts])
@@ -664,6 +706,43 @@ def model_moe(sq, steps=3, warmup=1):
                                                 workspace=q["ws"])
 
     qast_ms = timed(run_qast)
+    del qtables
+
+    # QAT-LoRA on the same experts: per linear, stacked factors B [E, o, r],
+    # A [E, r, i] and the re-quantised planes (shared across layers)
+    qt = {}
+    for (name, o, i) in shapes:
+        gg = inputs.device_generator(9950 + o)
+        qt[name] = dict(B=(torch.randn((E, o, r), generator=gg, device="cuda") * 0.02).to(torch.bfloat16),
+                        A=(torch.randn((E, r, i), generator=gg, device="cuda") * 0.02).to(torch.bfloat16),
+                        c=torch.empty((E, o, i // 2), dtype=torch.uint8, device="cuda"),
+                        s=torch.empty((E, o, i // 32), dtype=torch.uint8, device="cuda"),
+                        dB=torch.empty((E, o, r), dtype=torch.float32, device="cuda"),
+                        dA=torch.empty((E, r, i), dtype=torch.float32, device="cuda"))
+        qt[name]["ws"] = torch.empty(max(1, sq.sq_lora_grads_batched_workspace(Ts, o, i, r)), dtype=torch.uint8,
+                                     device="cuda")
+    ttables = {}
+    for (name, _, _) in shapes:
+        a, q = acts[name], qt[name]
+        cl, sl = [q["c"][e] for e in range(E)], [q["s"][e] for e in range(E)]
+        ttables[name] = (sq.ExpertTable("fwd", "mx", a["X"], cl, sl, a["Y"]),
+                         sq.ExpertTable("dx", "mx", a["dY"], cl, sl, a["dX"]))
+
+    def run_qat():
+        for l in range(L):
+            for (name, _, _) in shapes:
+                q = qt[name]
+                sq.sq_qat_requant_batched("mx", layers[l][name]["codes"], layers[l][name]["scales"], q["B"], q["A"],
+                                          1.0, codes_out=q["c"], scales_out=q["s"])
+                ttables[name][0].run()
+        for l in reversed(range(L)):
+            for (name, _, _) in reversed(shapes):
+                q, a = qt[name], acts[name]
+                ttables[name][1].run()
+                sq.sq_lora_grads_batched(Ts, a["Xall"], a["dYall"], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"],
+                                         workspace=q["ws"])
+
+    qat_ms = timed(run_qat)
     out = {"workload": "MXFP4 30B-A3B-shaped MoE stack: 48 layers x 128 experts x {gate, up [768, 2048], "
                        "down [2048, 768]}, 4096 tokens top-8 (32768 routed rows per layer): grouped fwd + dX + dS",
            "expert_rows": {"min": int(min(Ts)), "max": int(max(Ts)), "mean": round(rows / E, 1)},
@@ -672,8 +751,15 @@ def model_moe(sq, steps=3, warmup=1):
            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
            "qast_step": {"ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
                          "note": "batched rank-32 QAST scale step of all experts per linear; the paper reports "
-                                 "QAST within noise of its no-STE baseline on its MoE (context only)"}}
-    del layers, acts, qa, tables, qtables
+                                 "QAST within noise of its no-STE baseline on its MoE (context only)"},
+           "qat_lora_step": {"what": "QAT-LoRA weight-space STE on the native path, rank 32: "
+                                     "sq_qat_requant_batched before each grouped forward, grouped dX on the "
+                                     "re-quantised codes, sq_lora_grads_batched instead of dS",
+                             "ms": round(qat_ms, 3), "ratio_to_scale_step": round(qat_ms / ms, 3),
+                             "ratio_to_qast_step": round(qat_ms / qast_ms, 3),
+                             "note": "the paper reports 8882 vs 3958 ms per step (2.2x) for QAT-LoRA against "
+                                     "Scale-QLoRA on its MoE, through framework ops (context only)"}}
+    del layers, acts, qa, qt, tables, ttables
     torch.cuda.empty_cache()
     return out
 
@@ -820,6 +906,131 @@ def cpu_baseline(X, dY, codes, sb, delta, src, Wm_host):
             "host_cpus": os.cpu_count()}
 
 
+def hbm_copy_ceiling(sq, mib=2048, reps=10):
+    """A measured streaming ceiling beside the 8 TB/s spec: a 2 GiB
+    device-to-device copy through torch (copy_) and through the copy mode of
+    sq_merge_scales (one plane, 2 GiB), bytes read + written per second."""
+    nb = mib << 20
+    a = torch.empty(nb, dtype=torch.uint8, device="cuda").fill_(7)
+    b = torch.empty_like(a)
+    res = {"bytes_each_way": nb}
+    for name, fn in (("torch_copy", lambda: b.copy_(a)), ("sq_merge_copy", lambda: sq.sq_merge_scales(FMT, b, src=a))):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res[name] = {"ms": round(ms, 3), "GB/s": round(2 * nb / (ms * 1e-3) / 1e9, 1),
+                     "frac_of_8TB/s": round(2 * nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    del a, b
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_plan():
+    """The oracle timed per workload on the host cores, with all BLAS threads
+    and with one (threadpoolctl): the tiny MXFP4 layer in full (forward, dX,
+    dS and the merge of its perturbed plane); the NVFP4 MLP projections at 8192
+    tokens in full with all threads, and on 256 of the 8192 tokens with one
+    (scaled by 32, labelled extrapolated); the 8B model step as layer 0's seven
+    linears at 4096 tokens, reported x32 (extrapolated); the lifecycle over
+    the model's first 8 linears (NVFP4 merge of their scale planes, MXFP4 RTN
+    of the first 256 rows of their bf16 weights), scaled to all 224 by bytes
+    (extrapolated)."""
+    from oracle import linear, merge, rtn
+    from threadpoolctl import threadpool_limits
+    ws2 = float(np.float32(1.0 / 448.0))
+
+    def gemms(fmt, X, dY, codes, sb, w2):
+        W = linear.dequant(fmt, codes, sb, w2)
+        linear.forward(X, W)
+        linear.backward_dx(dY, W)
+        linear.backward_dscale(fmt, X, dY, codes)
+
+    def timed(fn):
+        t0 = time.perf_counter()
+        fn()
+        return time.perf_counter() - t0
+
+    def layer(fmt, Tn, o, i, seed):
+        X = inputs.bf16_normal(seed, (Tn, i)).double().numpy()
+        dY = inputs.bf16_normal(seed + 1, (Tn, o)).double().numpy()
+        codes = inputs.codes_uniform(seed + 2, o, i)
+        sb = (inputs.e8m0_uniform_exponents(seed + 3, o, i // 32, -8, -3) if fmt == "mx"
+              else inputs.e4m3_abs_normal(seed + 3, o, i // 16))
+        return X, dY, codes, sb
+
+    out = {}
+    # tiny MXFP4 layer, whole
+    X, dY, codes, sb = layer("mx", 64, 256, 512, 1000)
+    dlt = inputs.e8m0_step_delta(1009, sb, 0.10)
+    fl = 6.0 * 64 * 256 * 512
+    for label, nthreads in (("all_threads", None), ("one_thread", 1)):
+        with threadpool_limits(limits=nthreads):
+            tiny = lambda: (gemms("mx", X, dY, codes, sb, 1.0), merge.merge_delta("mx", sb, dlt))  # noqa: E731
+            tiny()                                           # the thread pool starts up on the first call
+            t = min(timed(tiny) for _ in range(3))
+        out.setdefault("tiny_mxfp4_64x256x512", {})[label] = {"seconds": round(t, 4),
+                                                             "GFLOP/s": round(fl / t / 1e9, 2)}
+    # NVFP4 MLP at 8192 tokens
+    mlp = (("gate", 14336, 4096), ("up", 14336, 4096), ("down", 4096, 14336))
+    res = {}
+    t_all = 0.0
+    for k, (name, o, i) in enumerate(mlp):
+        X, dY, codes, sb = layer("nv", 8192, o, i, 9000 + 10 * k)
+        t_all += timed(lambda: gemms("nv", X, dY, codes, sb, ws2))
+        del X, dY
+    fl = 6.0 * 8192 * sum(o * i for (_, o, i) in mlp)
+    res["all_threads"] = {"seconds": round(t_all, 2), "TFLOP/s": round(fl / t_all / 1e12, 4), "measured": "full"}
+    t_one = 0.0
+    with threadpool_limits(limits=1):
+        for k, (name, o, i) in enumerate(mlp):
+            X, dY, codes, sb = layer("nv", 256, o, i, 9100 + 10 * k)
+            t_one += timed(lambda: gemms("nv", X, dY, codes, sb, ws2))
+    res["one_thread"] = {"seconds_extrapolated": round(t_one * 32, 1), "TFLOP/s": round(fl / (t_one * 32) / 1e12, 5),
+                         "measured": "256 of 8192 tokens, x32 (extrapolated)"}
+    out["mlp_nvfp4_t8192"] = res
+    # 8B step: layer 0 at 4096 tokens, x32
+    t_l0 = 0.0
+    for k, (name, o, i) in enumerate(inputs.LLAMA8B_LAYER):
+        X, dY, codes, sb = layer("mx", 4096, o, i, 9200 + 10 * k)
+        t_l0 += timed(lambda: gemms("mx", X, dY, codes, sb, 1.0))
+        del X, dY
+    fl = 6.0 * 4096 * sum(o * i for (_, o, i) in inputs.LLAMA8B_LAYER) * inputs.LLAMA8B_LAYERS
+    out["step_8b"] = {"seconds_extrapolated": round(t_l0 * inputs.LLAMA8B_LAYERS, 1),
+                      "TFLOP/s": round(fl / (t_l0 * inputs.LLAMA8B_LAYERS) / 1e12, 4),
+                      "measured": f"layer 0 (7 linears) in {t_l0:.1f} s with all threads, x32 (extrapolated)"}
+    # lifecycle: the first 8 linears' planes and weights, scaled by bytes to 224
+    first = inputs.LLAMA8B_LAYER + inputs.LLAMA8B_LAYER[:1]
+    t_merge = t_rtn = 0.0
+    mbytes = rbytes = 0
+    for k, (name, o, i) in enumerate(first):
+        sbn = inputs.e4m3_abs_normal(9300 + k, o, i // 16)
+        d = inputs.relative_jitter(9400 + k, sbn.astype(np.float64), 0.02)
+        t_merge += timed(lambda: merge.merge_delta("nv", sbn, d, ws2))
+        mbytes += 6 * sbn.size
+        Wm = inputs.bf16_normal(9500 + k, (256, i)).float().numpy() * np.float32(0.01)
+        t_rtn += timed(lambda: rtn.quantize("mx", Wm, rtn.TIE_EVEN))
+        rbytes += 256 * i * 2 + 256 * i // 2 + 256 * i // 32
+        del Wm
+    tot_m = 6 * sum(o * i // 16 for (_, o, i) in inputs.LLAMA8B_LAYER) * inputs.LLAMA8B_LAYERS
+    tot_r = sum(o * i * 2 + o * i // 2 + o * i // 32 for (_, o, i) in inputs.LLAMA8B_LAYER) * inputs.LLAMA8B_LAYERS
+    out["lifecycle_8b"] = {"nv_merge": {"seconds_extrapolated": round(t_merge * tot_m / mbytes, 1),
+                                        "GB/s": round(mbytes / t_merge / 1e9, 3)},
+                           "mx_rtn": {"seconds_extrapolated": round(t_rtn * tot_r / rbytes, 1),
+                                      "GB/s": round(rbytes / t_rtn / 1e9, 3)},
+                           "measured": "merge: the first 8 linears' scale planes; RTN: the first 256 rows of "
+                                       "each of the first 8 linears; both scaled to all 224 by bytes "
+                                       "(extrapolated)"}
+    out["cores"] = os.cpu_count()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -857,6 +1068,14 @@ def main():
         for n in names:
             calls[n]()
 
+    # The chip needs some tens of milliseconds of load before its clock
+    # settles: a fixed 300 ms of untimed steps comes before the warmup steps,
+    # whatever --warmup asks for.
+    t_pre = time.perf_counter()
+    while time.perf_counter() - t_pre < 0.3:
+        step()
+        torch.cuda.synchronize()
+    preheat_ms = (time.perf_counter() - t_pre) * 1e3
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -894,6 +1113,8 @@ def main():
     torch.cuda.synchronize()
     vendor_ms = e0.elapsed_time(e1) / args.steps
 
+    copy_ceiling = hbm_copy_ceiling(sq)
+
     gemm_flops = 2.0 * T * O * I
     tflops = 3 * gemm_flops / (ms_step * 1e-3) / 1e12
     kernels = {}
@@ -918,6 +1139,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "preheat_ms": round(preheat_ms, 1),
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -933,6 +1155,7 @@ def main():
         "vendor_bf16_gemm": {"what": "torch.mm bf16 X W^T, same 4096^3 shape (hipBLASLt)",
                              "ms": round(vendor_ms, 4),
                              "TFLOP/s": round(gemm_flops / (vendor_ms * 1e-3) / 1e12, 1)},
+        "hbm_copy_ceiling": copy_ceiling,
     }
     if args.calib_copy_mib:
         nb = args.calib_copy_mib << 20
@@ -955,8 +1178,26 @@ def main():
     if not args.no_lifecycle:
         out["lifecycle_8b"] = model_lifecycle(sq)
         torch.cuda.empty_cache()
+    if "merge_8b" in out and "lifecycle_8b" in out:
+        # a hot swap of the served task: the scale-only swap (NVFP4 planes
+        # copied) against re-quantising every linear's weights
+        sw = out["merge_8b"]["nv_swap"]["ms"]
+        rq = out["lifecycle_8b"]["nv"]
+        out["swap_nvfp4_8b"] = {
+            "scale_swap_ms": sw,
+            "requant_swap_rtn_ms": rq["even"]["ms"],
+            "requant_swap_fused_ms": rq["requant_swap_fused"]["ms"],
+            "ratio_rtn": round(rq["even"]["ms"] / sw, 1),
+            "ratio_fused": round(rq["requant_swap_fused"]["ms"] / sw, 1),
+            "what": "scale-only swap of all 224 NVFP4 scale planes (sq_merge_scales_grouped copy) against "
+                    "re-quantising all 224 linears: rtn_quantize_grouped of the resident bf16 W + B A, and the "
+                    "fused pass from base codes + scales + adapter (sq_qat_requant)",
+            "note": "the paper reports 0.059 s against 7.45 s (~125x) for Llama-8B NVFP4 on one H200, "
+                    "through its own loaders (context only)"}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(X, dY, codes, sb, delta, src, Wm.float().cpu().numpy())
+        if not args.no_cpu_plan:
+            out["cpu_baseline"]["plan"] = cpu_plan()
     print(json.dumps(out), flush=True)
 
 

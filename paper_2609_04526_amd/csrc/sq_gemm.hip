@@ -10,8 +10,10 @@
 //                                                M=I  N=O  K=T
 //
 // All three feed v_mfma_f32_32x32x16_bf16 (fp32 accumulation) from LDS, in
-// K stages of 64, on 256 x 256 tiles of 8 waves (each 64 x 128) with two LDS
-// stages; grids that would leave CUs idle use 128 x 128 tiles of 4 waves.
+// K stages of 64, on 256 x 256 tiles of 8 waves (128 x 64 each in the MXFP4
+// forward, dX and dS; 64 x 128 in the LDS-dequantised forward) with two LDS
+// stages; grids that would leave CUs idle use 128 x 128 tiles, and a grid
+// ending in a short partial wave runs that remainder as half tiles.
 // How each operand reaches the matrix cores:
 //   * bf16 activations are copied global -> LDS by buffer loads that write LDS
 //     directly (no registers), with reads past the operand's end returning
@@ -23,14 +25,19 @@
 //     transpose read ds_read_b64_tr_b16: within each 16-lane group, lane i
 //     receives column i of the 4x16 block whose rows the group's lanes supply,
 //     so two reads give a lane the 8 consecutive k of its MFMA operand;
-//   * W (FWD and DX) is loaded as packed codes and scale bytes into registers
-//     one or two stages ahead, dequantised exactly to bf16 (sq_device.h) and
-//     written to a double-buffered LDS tile once per workgroup.
-// Each stage: wait for its DMA, one s_barrier, issue the W loads, then four
-// 16-deep MFMA slices; the next stage's DMA is issued in quarters between the
-// operand reads and the MFMAs of the first slices, so the address unit is
-// not flooded at the barrier.  Waits are explicit vmcnt counts and the
-// barrier is the raw s_barrier, so later loads stay in flight across it.
+//   * W in the MXFP4 forward: the packed codes are copied to LDS as they are
+//     and each wave dequantises its own operand in registers (kFwdC);
+//   * W elsewhere (dX, the NVFP4 forward): packed codes and scale bytes are
+//     loaded into registers one or two stages ahead, dequantised exactly to
+//     bf16 (sq_device.h) and written to a double-buffered LDS tile once per
+//     workgroup.
+// Two schedules: the late-barrier one (MXFP4 forward, dX, dS; see `step2`)
+// reads each slice's operands one slice ahead and publishes the next stage
+// before the last slice's MFMAs; the LDS-dequantised forward waits for its
+// stage, passes one s_barrier, issues the W loads, then runs four 16-deep
+// MFMA slices with the next stage's DMA issued in quarters between them.
+// Waits are explicit vmcnt counts and the barrier is the raw s_barrier, so
+// later loads stay in flight across it.
 //
 // The DS epilogue multiplies each accumulator dW[o,j] by its E2M1 code and
 // sums over the block in registers (the 32x32 MFMA output puts 8 of a
@@ -569,9 +576,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
                                                               (uint32_t)k0 * (uint32_t)g.O * 2u, wave_u);
     }
   };
-  // The forward and dX (kFwdR, kDx) run the two-stage schedule of `step`;
-  // the MXFP4 register forward and dS run the late-barrier schedule of `step2`.
-  constexpr bool kLate = MODE == kFwdC || MODE == kDs;
+  // The LDS-dequantised forward (kFwdR) runs the two-stage schedule of
+  // `step`; the MXFP4 register forward, dX and dS run the late-barrier
+  // schedule of `step2`.
+  constexpr bool kLate = MODE == kFwdC || MODE == kDs || MODE == kDx;
   static_assert(kLate || STAGES == 2, "the early-barrier schedule keeps two stages");
 
   // ---- W through registers (DX: W^T tile [64 o][BN i]; FWDR: W tile
@@ -791,8 +799,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // drain at every barrier.  Right after the barrier the buffer of stage kt
   // is free: half of the DMA of stage kt + STAGES goes out there, the other
   // half in the first slice of stage kt + 1, so each stage's copy has
-  // STAGES - 1 stages to land.  A W tile (kFwdR, kDx) for stage kt + 1 is
-  // committed to LDS before the barrier of stage kt.
+  // STAGES - 1 stages to land.  dX's W tile for stage kt + 1 is loaded into
+  // registers in slice 0 of stage kt and committed to LDS before its barrier
+  // (against the two-stage early-barrier schedule: the 8B MLP dX products
+  // -2.5%, the 4096^3 one unchanged).
   struct Frag {
     bf16x8 a[TM];
     bf16x8 b[TN];
@@ -821,6 +831,14 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) f.cd[j] = cst[j][kk];
+    } else if constexpr (MODE == kDx) {
+      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+      const SQ_LDS uint16_t* b = wbuf(kt);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        f.a[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 2 * kk + h32));
+#pragma unroll
+      for (int j = 0; j < TN; ++j) f.b[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
     } else {
       const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
       const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
@@ -887,12 +905,19 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     // kt + STAGES - 1's DMA and the W loads go out here
     read(SC, kt, I1{}, F1);
     if (kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
+    if constexpr (kWReg) {            // dX: the W items of stage kt + 1
+      if (kt + 1 < nk) load_w(kt + 1, I0{});
+    }
     mma(F0);
     read(SC, kt, I2{}, F0);
     mma(F1);
     read(SC, kt, I3{}, F1);
     mma(F0);
-    // publish stage kt + 1: everyone's DMA
+    // publish stage kt + 1: its W tile (dX; the tile's previous contents,
+    // stage kt - 1, were read before the last barrier), then everyone's DMA
+    if constexpr (kWReg) {
+      if (kt + 1 < nk) commit_w(kt + 1, I0{});
+    }
     // stage kt + 1 has landed once at most kAhead (kAheadLow) loads are
     // outstanding, if the DMA of stages kt + 2 .. kt + STAGES - 1 all went out
     // after it; in the last stages fewer did, and everything is waited for
@@ -912,6 +937,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // prologue: stage 0 in LDS and its slice 0 read, then the DMA of stages
   // 1 .. STAGES - 2 and the first half of stage STAGES - 1
   if (nk > 0) {
+    if constexpr (kWReg) {
+      load_w(0, I0{});
+      commit_w(0, I0{});
+    }
     if constexpr (MODE == kFwdC) load_sc(0);
     issue_dma(I0{}, 0);
     wait_vm_lgkm0<0>();
