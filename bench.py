@@ -907,14 +907,18 @@ def cpu_baseline(X, dY, codes, sb, delta, src, Wm_host):
 
 
 def hbm_copy_ceiling(sq, mib=2048, reps=10):
-    """A measured streaming ceiling beside the 8 TB/s spec: a 2 GiB
+    """Measured streaming ceilings beside the 8 TB/s spec: a 2 GiB
     device-to-device copy through torch (copy_) and through the copy mode of
-    sq_merge_scales (one plane, 2 GiB), bytes read + written per second."""
+    sq_merge_scales (one plane; 1:1 reads and writes), and a read-only pass
+    over two 2 GiB buffers (the byte audit, sq_byte_diff), in bytes moved per
+    second."""
     nb = mib << 20
     a = torch.empty(nb, dtype=torch.uint8, device="cuda").fill_(7)
     b = torch.empty_like(a)
     res = {"bytes_each_way": nb}
-    for name, fn in (("torch_copy", lambda: b.copy_(a)), ("sq_merge_copy", lambda: sq.sq_merge_scales(FMT, b, src=a))):
+    counts = torch.zeros(2, dtype=torch.int64, device="cuda")
+    for name, fn in (("torch_copy", lambda: b.copy_(a)), ("sq_merge_copy", lambda: sq.sq_merge_scales(FMT, b, src=a)),
+                     ("read_only_sq_byte_diff", lambda: sq.sq_byte_diff(a, b, counts=counts))):
         for _ in range(2):
             fn()
         torch.cuda.synchronize()
@@ -927,6 +931,7 @@ def hbm_copy_ceiling(sq, mib=2048, reps=10):
         ms = e0.elapsed_time(e1) / reps
         res[name] = {"ms": round(ms, 3), "GB/s": round(2 * nb / (ms * 1e-3) / 1e9, 1),
                      "frac_of_8TB/s": round(2 * nb / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    del counts
     del a, b
     torch.cuda.empty_cache()
     return res
