@@ -319,10 +319,16 @@ constexpr int group_m() {
   return MODE == kDs ? 8 : 4;
 }
 
-template <int kGroupM>
-__device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
+// Position in the tile order of workgroup bid of nb: XCD x = bid % 8 takes
+// the x-th contiguous stretch of the order (stretches differ by at most one).
+__device__ __forceinline__ int xcd_stretch(int bid, int nb) {
   const int x = bid % kXcds, q = nb / kXcds, r = nb % kXcds;
-  const int idx = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + bid / kXcds;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + bid / kXcds;
+}
+
+// Tile (tm, tn) at position idx of the grouped column-by-column order.
+template <int kGroupM>
+__device__ __forceinline__ void tile_at(int idx, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int per_group = kGroupM * tiles_n;
   const int group = idx / per_group;
   const int first_m = group * kGroupM;
@@ -330,6 +336,11 @@ __device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_
   const int in = idx - group * per_group;
   tm = first_m + in % gm;
   tn = in / gm;
+}
+
+template <int kGroupM>
+__device__ __forceinline__ void tile_of(int bid, int nb, int tiles_m, int tiles_n, int& tm, int& tn) {
+  tile_at<kGroupM>(xcd_stretch(bid, nb), tiles_m, tiles_n, tm, tn);
 }
 
 template <int MODE, int BM, int BN, int STAGES, int BK, int NW>
@@ -434,20 +445,96 @@ __device__ __forceinline__ void epi_store_bf16(const f32x16 (&acc)[TM][TN], SQ_L
     }
 }
 
+// ------------------------------------------------------------------ dS epilogue
+// A dS tile's rows are input features j, its columns output features o.  In
+// 32x32 MFMA tile (i, j) lane l holds rows 8 q + 4 (l / 32) + 0..3 (q = 0..3)
+// of column l % 32, and each group of 4 rows takes its 4 codes from one
+// 16-bit pair of the packed plane.  The 16 bytes of codes of row o and the
+// tile's 32 features hold the pairs of both lane halves; cw[j TM + i] is that
+// chunk, zeros for a row outside the layer.  The chunk starts at byte
+// o I / 2 + jb / 2: 16-byte aligned for MXFP4 (I is a multiple of 32), 8-byte
+// aligned for NVFP4 (a multiple of 16), which loads it as two halves.
+template <int FMT, int TM, int TN>
+__device__ __forceinline__ void ds_codes(u32x4 (&cw)[TM * TN], const uint8_t* codes, int O, int I, int r0, int c0,
+                                         int lane) {
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(codes, (uint32_t)((size_t)O * (I >> 1)));
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int o = c0 + j * 32 + (lane & 31);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int jb = r0 + i * 32;
+      const uint32_t off = o < O && jb < I ? (uint32_t)o * (uint32_t)(I >> 1) + (uint32_t)(jb >> 1) : kOOB;
+      if constexpr (FMT == kMX) {
+        cw[j * TM + i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, 0, 0));
+      } else {
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, (int)off, 0, 0));
+        const u32x2 hi = __builtin_bit_cast(
+            u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, (int)(off == kOOB ? kOOB : off + 8u), 0, 0));
+        cw[j * TM + i] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      }
+    }
+  }
+}
+
+// Products with the codes, summed over each scale block (32 features for
+// MXFP4, 16 for NVFP4; the 32 rows of an MFMA tile are split over the two
+// lane halves) and stored to dS[o, block].
+template <int FMT, int TM, int TN>
+__device__ __forceinline__ void ds_store(const f32x16 (&acc)[TM][TN], const u32x4 (&cw)[TM * TN], float* dS, int O,
+                                         int I, int G, int r0, int c0, int lane) {
+  const int lrow = 4 * (lane >> 5);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int o = c0 + j * 32 + (lane & 31);
+    const bool o_ok = o < O;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int jb = r0 + i * 32;          // first feature of this 32-row tile
+      float prod[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // the pair of rows jb + 8 q + lrow .. + 3: bytes 4 q + lrow / 2 of the chunk
+        const uint32_t c = jb + 8 * q + lrow < I ? (cw[j * TM + i][q] >> (4 * lrow)) & 0xFFFFu : 0u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) prod[4 * q + e] = acc[i][j][4 * q + e] * e2m1_to_f32((c >> (4 * e)) & 15u);
+      }
+      if constexpr (FMT == kMX) {
+        float s = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += prod[r];
+        s += __shfl_xor(s, 32);
+        if (lane < 32 && o_ok && jb < I) dS[(size_t)o * G + jb / 32] = s;
+      } else {
+        float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) { s0 += prod[r]; s1 += prod[8 + r]; }
+        s0 += __shfl_xor(s0, 32);
+        s1 += __shfl_xor(s1, 32);
+        const int b = jb / 16 + (lane >> 5);
+        const float s = (lane < 32) ? s0 : s1;
+        if (o_ok && b * 16 < I) dS[(size_t)o * G + b] = s;
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ kernel
 // Block tile BM x BN, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN) built
 // from 32x32 MFMA tiles; STAGES LDS stages for the DMA operands.
 // One workgroup's tile: bid is its index among the nb workgroups of one
-// product (the XCD-aware order reads bid % 8 as the XCD, which holds when the
-// product's first workgroup sits at a multiple of 8 in the grid).
-template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
+// product, dealt to XCDs by bid % 8; with ORDERED, bid is already the tile's
+// position in the product's tile order (the grouped launch deals its XCD
+// stretches over all experts at once).
+template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK, bool ORDERED = false>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int B = ScaleOperand<FMT>::kBlock;
-  static_assert(MODE == kDs || BK == kBK, "K-contiguous tiles use 64-wide stages");
-  static_assert(BK == 32 || BK == 64, "stage depth");
+  // every schedule reads a stage as four 16-deep MFMA slices
+  static_assert(BK == kBK, "64-deep stages");
   using L = SmemLayout<MODE, BM, BN, STAGES, BK, WGM * WGN>;
   constexpr bool kWReg = L::kWReg;
   constexpr int kDma = dma_count<MODE, BM, BN, NT, BK>();   // DMA loads per thread per stage
@@ -484,8 +571,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   const int tiles = tiles_m * tiles_n;
   const int split = (MODE == kDs && g.ksplit > 1) ? bid / tiles : 0;
   int tm, tn;
-  tile_of<group_m<MODE>()>((MODE == kDs && g.ksplit > 1) ? bid - split * tiles : bid, (MODE == kDs && g.ksplit > 1) ? tiles : nb,
-          tiles_m, tiles_n, tm, tn);
+  if constexpr (ORDERED) tile_at<group_m<MODE>()>(bid, tiles_m, tiles_n, tm, tn);
+  else tile_of<group_m<MODE>()>((MODE == kDs && g.ksplit > 1) ? bid - split * tiles : bid, (MODE == kDs && g.ksplit > 1) ? tiles : nb,
+                                tiles_m, tiles_n, tm, tn);
   const int m0 = g.m_off + tm * BM, n0 = g.n_off + tn * BN;
 
   auto stage = [&](auto SC) -> SQ_LDS uint8_t* {
@@ -988,44 +1076,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     else
       epi_store_direct<true, FMT, TM, TN>(acc, g, m0 + wm0, n0 + wn0, lane);
   } else {
-    // rows are input features j, columns output features o
-    const int lrow = 4 * (lane >> 5), lcol = lane & 31;
     float* dS = reinterpret_cast<float*>(g.out) + (size_t)split * g.O * g.G;   // partial plane when split
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int o = n0 + wn0 + j * 32 + lcol;
-      const bool o_ok = o < g.O;
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int jb = m0 + wm0 + i * 32;          // first feature of this 32-row tile
-        float prod[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int j0 = jb + 8 * q + lrow;        // 4 consecutive features j0..j0+3
-          uint32_t cw = 0;
-          if (o_ok && j0 < g.I)
-            cw = *reinterpret_cast<const uint16_t*>(g.codes + (size_t)o * (g.I >> 1) + (j0 >> 1));
-#pragma unroll
-          for (int e = 0; e < 4; ++e) prod[4 * q + e] = acc[i][j][4 * q + e] * e2m1_to_f32((cw >> (4 * e)) & 15u);
-        }
-        if constexpr (FMT == kMX) {
-          float s = 0.0f;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s += prod[r];
-          s += __shfl_xor(s, 32);
-          if (lane < 32 && o_ok && jb < g.I) dS[(size_t)o * g.G + jb / 32] = s;
-        } else {
-          float s0 = 0.0f, s1 = 0.0f;
-#pragma unroll
-          for (int r = 0; r < 8; ++r) { s0 += prod[r]; s1 += prod[8 + r]; }
-          s0 += __shfl_xor(s0, 32);
-          s1 += __shfl_xor(s1, 32);
-          const int b = jb / 16 + (lane >> 5);
-          const float s = (lane < 32) ? s0 : s1;
-          if (o_ok && b * 16 < g.I) dS[(size_t)o * g.G + b] = s;
-        }
-      }
-    }
+    u32x4 cw[TM * TN];
+    ds_codes<FMT, TM, TN>(cw, g.codes, g.O, g.I, m0 + wm0, n0 + wn0, lane);
+    ds_store<FMT, TM, TN>(acc, cw, dS, g.O, g.I, g.G, m0 + wm0, n0 + wn0, lane);
   }
 }
 
@@ -1035,11 +1089,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmArgs g) {
 }
 
 // Grouped products (one per MoE expert, same O and I, own tokens and
-// weights): expert e owns workgroups [tile_begin[e], tile_begin[e] + tiles of
-// e), its range starting at a multiple of 8; the rest of the range exits.
+// weights): the experts' tiles form one order, expert by expert, expert e
+// holding positions [tile_begin[e], tile_begin[e + 1]).  Each XCD takes one
+// contiguous stretch of that order, so the workgroups of an expert share an
+// L2 and read its activation and weight panels from HBM about once; dealing
+// every expert's tiles over all 8 XCDs made each L2 fetch them again (the
+// 128-expert MoE layer moved 4 to 8 times its operand bytes).
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup gg) {
-  const int b = (int)blockIdx.x;
+  const int b = xcd_stretch((int)blockIdx.x, (int)gridDim.x);
   int lo = 0, hi = gg.count - 1;                 // last e with tile_begin[e] <= b
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -1060,7 +1118,210 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup 
   const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const int local = b - gg.tile_begin[e];
   if (local >= tiles) return;
-  gemm_tile<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>(g, local, tiles);
+  gemm_tile<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK, true>(g, local, tiles);
+}
+
+// Streamed grouped dS.  With a few hundred tokens per expert a dS tile holds
+// only a few 64-token stages, and a workgroup per tile spends most of its
+// life filling the pipeline (the first stage's round trip) and draining it
+// (the epilogue's code loads and stores): 128 experts of 768 x 2048 at 256
+// tokens ran at a third of the rate of the same tiles over 2048 tokens.
+// Here each workgroup stays resident and runs its share of the tiles as one
+// pipeline of stages: the DMA of the stage after a tile's last one (the next
+// tile's first) goes out while the last is multiplied, and the block sums are
+// stored while the next tile's stages are in flight.
+//
+// Every expert has the same tile grid (I x O in BM x BN tiles), so position p
+// of the order is tile p % tiles (column-by-column order) of expert p / tiles.
+// XCD x takes the x-th contiguous stretch of positions and its workgroups
+// deal it round robin, so the tiles in flight on one XCD are neighbours in
+// the order and share their experts' panels in L2.  Stages run the two-stage
+// late schedule of gemm_tile (every barrier waits for all loads), with a DMA
+// cursor and a compute cursor walking the same sequence of (tile, stage)
+// pairs; an expert without tokens runs one stage of zeros, so its dS is 0.
+// Each output element is summed in the same order as in gemm_tile.
+template <int FMT, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  using L = SmemLayout<kDs, BM, BN, 2, kBK, WGM * WGN>;
+  using DA = DmaNat<BM, NT, kBK>;
+  using DB = DmaNat<BN, NT, kBK>;
+  constexpr int na = DA::kInst, nb = DB::kInst;
+  __shared__ __attribute__((aligned(16))) uint8_t lds0[L::kStageAlloc];
+  __shared__ __attribute__((aligned(16))) uint8_t lds1[L::kStageAlloc];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+  const int O = gg.base.O, I = gg.base.I, G = gg.base.G;
+  const int tiles_m = (I + BM - 1) / BM, tiles_n = (O + BN - 1) / BN, per = tiles_m * tiles_n;
+  const int total = per * gg.count;
+
+  // positions first, first + step, ... below end
+  const int w = (int)blockIdx.x, nwg = (int)gridDim.x, x = w % kXcds;
+  const int step = nwg / kXcds + (x < nwg % kXcds ? 1 : 0);
+  const int tq = total / kXcds, tr = total % kXcds;
+  const int s0 = x < tr ? x * (tq + 1) : tr * (tq + 1) + (x - tr) * tq;
+  const int first = s0 + w / kXcds, end = s0 + (x < tr ? tq + 1 : tq);
+  if (first >= end) return;
+
+  struct Tile {
+    int e, m0, n0, nk;
+  };
+  auto locate = [&](int pos, Tile& t) {
+    t.e = pos / per;
+    int tm, tn;
+    tile_at<group_m<kDs>()>(pos - t.e * per, tiles_m, tiles_n, tm, tn);
+    t.m0 = tm * BM;
+    t.n0 = tn * BN;
+    const int T = gg.T[t.e];
+    t.nk = T > 0 ? (T + kBK - 1) / kBK : 1;
+  };
+
+  // DMA cursor: stage dkt of the tile at position dpos
+  Tile dt;
+  int dpos = first, dkt = 0;
+  bool dvalid = true;
+  DmaRsrc ra, rb;
+  DA dA;
+  DB dB;
+  auto dma_tile = [&]() {
+    locate(dpos, dt);
+    const int T = gg.T[dt.e];
+    ra = make_dma_rsrc(gg.a[dt.e], (uint32_t)((size_t)T * I * 2));
+    rb = make_dma_rsrc(gg.b[dt.e], (uint32_t)((size_t)T * O * 2));
+    dA.init(I, I, dt.m0, tid);
+    dB.init(O, O, dt.n0, tid);
+  };
+  dma_tile();
+  // quarters Q0 and Q0 + 1 of the cursor's stage into stage buffer st
+  auto dma_half = [&](SQ_LDS uint8_t* st, auto Q0) {
+    constexpr int q = decltype(Q0)::value;
+    const uint32_t k0 = (uint32_t)dkt * kBK;
+    dA.template issue_part<q * na / 4, (q + 1) * na / 4>(ra, (SQ_LDS uint16_t*)st, k0 * (uint32_t)I * 2u, wave_u);
+    dB.template issue_part<q * nb / 4, (q + 1) * nb / 4>(rb, (SQ_LDS uint16_t*)(st + L::kA), k0 * (uint32_t)O * 2u,
+                                                        wave_u);
+    dA.template issue_part<(q + 1) * na / 4, (q + 2) * na / 4>(ra, (SQ_LDS uint16_t*)st, k0 * (uint32_t)I * 2u,
+                                                              wave_u);
+    dB.template issue_part<(q + 1) * nb / 4, (q + 2) * nb / 4>(rb, (SQ_LDS uint16_t*)(st + L::kA),
+                                                              k0 * (uint32_t)O * 2u, wave_u);
+  };
+  auto dma_advance = [&]() {
+    if (++dkt == dt.nk) {
+      dkt = 0;
+      dpos += step;
+      dvalid = dpos < end;
+      if (dvalid) dma_tile();
+    }
+  };
+
+  // compute cursor: stage ckt of the tile at position cpos
+  Tile ct;
+  int cpos = first, ckt = 0;
+  locate(cpos, ct);
+  u32x4 cw[TM * TN];
+  auto tile_codes = [&]() {
+    ds_codes<FMT, TM, TN>(cw, gg.codes[ct.e], O, I, ct.m0 + wm0, ct.n0 + wn0, lane);
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  struct Frag {
+    bf16x8 a[TM];
+    bf16x8 b[TN];
+  };
+  Frag F0, F1;
+  auto read = [&](SQ_LDS uint8_t* st, auto KK, Frag& f) {
+    constexpr int kk = decltype(KK)::value;
+    const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
+    const SQ_LDS uint16_t* b = (const SQ_LDS uint16_t*)(st + L::kA);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) f.a[i] = nat_frag<BM>(a, kk, wm0 + i * 32, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) f.b[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
+  };
+  auto mma = [&](Frag& f) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+
+  // One stage in buffer cur (its slice 0 already in F0): the second half of
+  // the next stage's DMA goes out after slice 1 is read, every load is waited
+  // for at the barrier, then the next stage's slice 0 is read and the first
+  // half of the stage after it is issued into cur.  Returns false after the
+  // workgroup's last stage.
+  auto stage_step = [&](SQ_LDS uint8_t* cur, SQ_LDS uint8_t* nxt) -> bool {
+    read(cur, I1{}, F1);
+    if (dvalid) {
+      dma_half(nxt, I2{});
+      dma_advance();
+    }
+    mma(F0);
+    read(cur, I2{}, F0);
+    mma(F1);
+    read(cur, I3{}, F1);
+    mma(F0);
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    const bool last = ckt + 1 == ct.nk;
+    const bool more = !last || cpos + step < end;
+    if (more) read(nxt, I0{}, F0);
+    if (dvalid) dma_half(cur, I0{});
+    mma(F1);
+    if (!last) {
+      ++ckt;
+      return true;
+    }
+    ds_store<FMT, TM, TN>(acc, cw, reinterpret_cast<float*>(gg.out[ct.e]), O, I, G, ct.m0 + wm0, ct.n0 + wn0, lane);
+    if (!more) return false;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    cpos += step;
+    ckt = 0;
+    locate(cpos, ct);
+    tile_codes();
+    return true;
+  };
+
+  // prologue: the first stage whole, the first tile's codes, then the first
+  // half of the second stage
+  dma_half((SQ_LDS uint8_t*)lds0, I0{});
+  dma_half((SQ_LDS uint8_t*)lds0, I2{});
+  dma_advance();
+  tile_codes();
+  wait_vm_lgkm0<0>();
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  read((SQ_LDS uint8_t*)lds0, I0{}, F0);
+  if (dvalid) dma_half((SQ_LDS uint8_t*)lds1, I0{});
+  SQ_LDS uint8_t* cur = (SQ_LDS uint8_t*)lds0;
+  SQ_LDS uint8_t* nxt = (SQ_LDS uint8_t*)lds1;
+  while (stage_step(cur, nxt)) {
+    SQ_LDS uint8_t* t = cur;
+    cur = nxt;
+    nxt = t;
+  }
 }
 
 // Tile configurations.  Each entry: BM, BN, waves along M, waves along N, stages,
@@ -1197,8 +1458,7 @@ int gemm_dx(int fmt, int T, int O, int I, const void* dY, const uint8_t* codes,
 }
 
 // ------------------------------------------------------------------ grouped
-// One launch per kGroupMax experts.  Workgroups of expert e start at a
-// multiple of 8 so the XCD-aware order inside each expert still holds.
+// One launch per kGroupMax experts, one workgroup per tile.
 template <int MODE, int FMT, int BM, int BN, int WGM, int WGN, int STAGES, int BK>
 static int launch_grouped(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
   using L = SmemLayout<MODE, BM, BN, STAGES, BK, WGM * WGN>;
@@ -1216,11 +1476,37 @@ static int launch_grouped(GemmGroup& gg, const ExpertProblem* p, int n, hipStrea
     gg.T[e] = p[e].T;
     gg.ws2[e] = FMT == kNV ? p[e].ws2 : 1.0f;
     gg.tile_begin[e] = blocks;
-    blocks += (tiles + 7) / 8 * 8;
+    blocks += tiles;
   }
   if (blocks == 0) return 0;
   hipLaunchKernelGGL((gemm_grouped_kernel<MODE, FMT, BM, BN, WGM, WGN, STAGES, BK>), dim3(blocks),
                      dim3(64 * WGM * WGN), 0, s, gg);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// The streamed dS: two resident workgroups per CU (the grid never exceeds the
+// tile count, so every XCD's stretch of positions has a workgroup), each
+// running about total / 512 tiles.
+#define SQ_CFG_DS_STREAM 128, 128, 2, 4
+template <int FMT, int BM, int BN, int WGM, int WGN>
+static int launch_ds_stream(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
+  using L = SmemLayout<kDs, BM, BN, 2, kBK, WGM * WGN>;
+  static_assert(2 * L::kBytes <= 160 * 1024, "two workgroups per CU");
+  gg.count = n;
+  for (int e = 0; e < n; ++e) {
+    gg.a[e] = static_cast<const uint16_t*>(p[e].a);
+    gg.b[e] = static_cast<const uint16_t*>(p[e].b);
+    gg.codes[e] = p[e].codes;
+    gg.scales[e] = nullptr;
+    gg.out[e] = p[e].out;
+    gg.T[e] = p[e].T;
+    gg.ws2[e] = 1.0f;
+    gg.tile_begin[e] = 0;
+  }
+  const int64_t total = (int64_t)((gg.base.M + BM - 1) / BM) * ((gg.base.N + BN - 1) / BN) * n;
+  if (total == 0) return 0;
+  const int blocks = (int)(total < 2 * kCUs ? total : 2 * kCUs);
+  hipLaunchKernelGGL((ds_stream_kernel<FMT, BM, BN, WGM, WGN>), dim3(blocks), dim3(64 * WGM * WGN), 0, s, gg);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -1239,6 +1525,7 @@ static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream
   const bool large = big >= kCUs && tokens >= (int64_t)512 * n;
   if (large) return launch_grouped<MODE, FMT, BM, BN, REST...>(gg, p, n, s);
   if constexpr (MODE == kFwdC) return launch_grouped<MODE, FMT, SQ_CFG_SMALL_FWDC>(gg, p, n, s);
+  else if constexpr (MODE == kDs) return launch_ds_stream<FMT, SQ_CFG_DS_STREAM>(gg, p, n, s);
   else return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
 }
 

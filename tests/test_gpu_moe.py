@@ -1,18 +1,21 @@
 """GPU parity of the grouped MoE expert products (sq_fwd_grouped,
 sq_bwd_dx_grouped, sq_bwd_dscale_grouped) against the oracle, per expert.
 
-The grouped forward and dX accumulate every output element in the same order
-as the single-product kernels, so they are also compared with sq_fwd /
-sq_bwd_dx bit for bit; dS is compared with the oracle (normwise 2e-3, the
-bar of the single products), and an expert with no tokens gets dS = 0."""
+The grouped products accumulate every output element in the same order as
+the single-product kernels, so they are also compared with sq_fwd /
+sq_bwd_dx / sq_bwd_dscale bit for bit (dS where the single call does not
+split its token sum, i.e. needs no workspace); against the oracle every
+element is held to the summation bound of tests/parity_check.py besides the
+normwise 2e-3 bar.  An expert with no tokens gets dS = 0."""
 
 import numpy as np
 import pytest
 import torch
 
 from conftest import ensure_library, gpu_ready
-from oracle import linear
+from oracle import codec, linear
 from paper_2609_04526_amd import inputs
+from parity_check import assert_elements
 
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not gpu_ready(), reason="needs a GPU")]
 
@@ -49,6 +52,36 @@ def cuda(arrs):
     return [torch.from_numpy(a).cuda() for a in arrs]
 
 
+def check_elements(fmt, X, dY, codes, W, Y=None, dX=None, dS=None, what=""):
+    """Every element of the given fp32 outputs within the summation bound of
+    its K terms (Y: I terms, dX: O terms, dS: T terms, then the code
+    multiply and the block sum)."""
+    Xd, dYd = np.asarray(X, np.float64), np.asarray(dY, np.float64)
+    T, I = Xd.shape
+    O = W.shape[0]
+    if Y is not None:
+        assert_elements(Y, linear.forward(Xd, W), np.abs(Xd) @ np.abs(W).T, I + 2, what + " Y")
+    if dX is not None:
+        assert_elements(dX, linear.backward_dx(dYd, W), np.abs(dYd) @ np.abs(W), O + 2, what + " dX")
+    if dS is not None:
+        B = codec.BLOCK[fmt]
+        aS = (np.abs(linear.code_values(codes)) * (np.abs(dYd).T @ np.abs(Xd))).reshape(O, I // B, B).sum(axis=2)
+        assert_elements(dS, linear.backward_dscale(fmt, Xd, dYd, codes), aS, T + B + 2, what + " dS")
+
+
+def single_dscale_equal(sq, fmt, X, dY, codes, dS):
+    """dS of one expert equals the single call's bit for bit (when that call
+    keeps the token sum whole); returns whether it was compared."""
+    T, I = X.shape
+    O = dY.shape[1]
+    if sq.sq_bwd_dscale_workspace(fmt, T, O, I) != 0:
+        return False
+    one = sq.sq_bwd_dscale(fmt, X, dY, codes)
+    torch.cuda.synchronize()
+    assert torch.equal(one, dS)
+    return True
+
+
 @pytest.mark.parametrize("fmt", ["mx", "nv"])
 def test_grouped_products_match_oracle_and_single(sq, fmt):
     """Eight experts with ragged token counts, including none and one."""
@@ -74,10 +107,13 @@ def test_grouped_products_match_oracle_and_single(sq, fmt):
         assert normwise(Ys[e].cpu().numpy(), linear.forward(Xs[e].float().numpy(), W)) <= TOL
         assert normwise(dXs[e].cpu().numpy(), linear.backward_dx(dYs[e].float().numpy(), W)) <= TOL
         assert normwise(dSs[e].cpu().numpy(), dS_ref) <= TOL
+        check_elements(fmt, Xs[e].float().numpy(), dYs[e].float().numpy(), codes[e], W,
+                       Ys[e].cpu().numpy(), dXs[e].cpu().numpy(), dSs[e].cpu().numpy(), f"expert {e}")
         y1 = sq.sq_fwd(fmt, Xd[e], cd[e], sd[e], ws2[e])
         dx1 = sq.sq_bwd_dx(fmt, dYd[e], cd[e], sd[e], ws2[e])
         torch.cuda.synchronize()
         assert torch.equal(y1, Ys[e]) and torch.equal(dx1, dXs[e])
+        single_dscale_equal(sq, fmt, Xd[e], dYd[e], cd[e], dSs[e])
 
 
 def test_more_experts_than_one_launch_holds(sq):
@@ -127,3 +163,45 @@ def test_moe_layer_shapes_sampled(sq):
             assert normwise(Ys[e].cpu().numpy(), linear.forward(X, W)) <= TOL
             assert normwise(dXs[e].cpu().numpy(), linear.backward_dx(dY, W)) <= TOL
             assert normwise(dSs[e].cpu().numpy(), linear.backward_dscale("mx", X, dY, codes[e])) <= TOL
+            check_elements("mx", X, dY, codes[e], W, Ys[e].cpu().numpy(), dXs[e].cpu().numpy(),
+                           dSs[e].cpu().numpy(), f"O={O} I={I} expert {e} T={Ts[e]}")
+        # every expert's dS equals its single product where that keeps the
+        # token sum whole (here: fewer than 8 token stages, T <= 448)
+        compared = sum(single_dscale_equal(sq, "mx", Xd[e], dYd[e], cd[e], dSs[e]) for e in range(E))
+        assert compared >= sum(T <= 448 for T in Ts)
+
+
+# Grouped dS of short token sums runs each workgroup's share of the tiles as
+# one pipeline (tiles of 1 to 5 token stages back to back, empty experts
+# in between, fewer tiles than XCDs, workgroups with one tile and with many).
+STREAM_CASES = [
+    ("mx", 128, 128, [5, 0, 64, 65, 1, 0, 200]),          # 1 tile per expert, 7 tiles
+    ("nv", 128, 144, [3, 130, 0, 66]),                   # 2 tiles per expert, ragged feature tile
+    ("mx", 256, 384, [(37 * e) % 150 for e in range(64)]),
+    ("nv", 768, 2048, [(97 * e + 13) % 300 for e in range(40)]),
+]
+
+
+@pytest.mark.parametrize("fmt,O,I,Ts", STREAM_CASES, ids=lambda x: str(x)[:40])
+def test_streamed_dscale_tile_sequences(sq, fmt, O, I, Ts):
+    codes, scales, ws2 = experts(fmt, len(Ts), O, I, 8100 + O + I)
+    cd = cuda(codes)
+    Xd = [inputs.device_bf16_normal(8200 + e, (T, I)) for e, T in enumerate(Ts)]
+    dYd = [inputs.device_bf16_normal(8300 + e, (T, O)) for e, T in enumerate(Ts)]
+    print(f"[moe stream ds] fmt={fmt} O={O} I={I} experts={len(Ts)} T={Ts[:8]}...", flush=True)
+    dSs = sq.sq_bwd_dscale_grouped(fmt, Xd, dYd, cd)
+    torch.cuda.synchronize()
+    compared = 0
+    for e, T in enumerate(Ts):
+        if T == 0:
+            assert torch.count_nonzero(dSs[e]).item() == 0
+            continue
+        compared += single_dscale_equal(sq, fmt, Xd[e], dYd[e], cd[e], dSs[e])
+    assert compared >= len([T for T in Ts if T]) // 2
+    g = inputs.rng(8400 + O)
+    for e in sorted(set(g.choice(len(Ts), 4, replace=False).tolist())):
+        if Ts[e] == 0:
+            continue
+        X, dY = Xd[e].float().cpu().numpy(), dYd[e].float().cpu().numpy()
+        W = linear.dequant(fmt, codes[e], scales[e], ws2[e])
+        check_elements(fmt, X, dY, codes[e], W, dS=dSs[e].cpu().numpy(), what=f"expert {e} T={Ts[e]}")

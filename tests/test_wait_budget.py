@@ -277,3 +277,94 @@ def test_model_follows_the_kernel_source():
     assert "constexpr int kDmaLow = kCodesSplit ? kDma - DC::kInst : kDma;" in s
     assert "if ((kt & 7) == 7 && kt + 1 < nk) load_sc((kt + 1) >> 3);" in s
     assert "if constexpr (MODE == kFwdC && P == 0) dC.template issue_part<0, DC::kInst>" in s
+
+
+# ---------------------------------------------------------------- streamed dS
+# ds_stream_kernel runs a workgroup's tiles back to back as one pipeline of
+# two stage buffers: a DMA cursor and a compute cursor walk the same list of
+# (tile, stage) pairs, every barrier is preceded by a wait for all loads.
+
+def stream_replay(nks):
+    """Replay one wave of the streamed dS over tiles with nks[t] stages each;
+    returns the (tile, stage) sequences the two cursors walked."""
+    seq = [(t, k) for t, nk in enumerate(nks) for k in range(nk)]
+    w = Wave()
+    holder = {}
+    reads = {}                 # global stage -> barrier count of its last read
+    dma_walk, mma_walk = [], []
+    cur = {"d": 0}             # DMA cursor: index into seq
+
+    def dma_half(buf, first):
+        g = cur["d"]
+        prev = holder.get(buf)
+        if first and prev is not None and prev != g:
+            assert reads.get(prev, -1) < w.barriers, ("buffer reused before its reads were fenced", nks, g, prev)
+        holder[buf] = g
+        w.issue(("dma", g), 2)
+        if not first:
+            dma_walk.append(seq[g])
+            cur["d"] += 1
+
+    def read(g):
+        assert not w.pending(("dma", g)), ("read before landing", nks, g)
+        assert holder[g % 2] == g
+        reads[g] = w.barriers
+
+    # prologue
+    dma_half(0, True)
+    dma_half(0, False)
+    w.wait(0)
+    w.barriers += 1
+    read(0)
+    if cur["d"] < len(seq):
+        dma_half(1, True)
+    g = 0
+    while True:
+        read(g)                                   # slice 1
+        if cur["d"] < len(seq):
+            dma_half((g + 1) % 2, False)
+        read(g)                                   # slices 2, 3
+        read(g)
+        mma_walk.append(seq[g])
+        w.wait(0)
+        w.barriers += 1
+        more = g + 1 < len(seq)
+        if more:
+            read(g + 1)                           # slice 0 of the next stage
+        if cur["d"] < len(seq):
+            dma_half(g % 2, True)
+        if not more:
+            break
+        g += 1
+    w.wait(0)
+    assert all(l[1] for l in w.loads)
+    return dma_walk, mma_walk, seq
+
+
+def test_stream_cursors_cover_every_stage():
+    import random
+    rnd = random.Random(5)
+    cases = [[1], [1, 1], [1, 1, 1, 1], [4], [2, 1, 3], [1, 5, 1, 1, 2]]
+    cases += [[rnd.randint(1, 6) for _ in range(rnd.randint(1, 14))] for _ in range(300)]
+    for nks in cases:
+        dma_walk, mma_walk, seq = stream_replay(nks)
+        assert dma_walk == seq and mma_walk == seq, nks
+
+
+def test_stream_model_follows_the_kernel_source():
+    """The calls of ds_stream_kernel's stage_step and prologue in the order
+    stream_replay models."""
+    s = source()
+    i = s.index("auto stage_step = [&](SQ_LDS uint8_t* cur, SQ_LDS uint8_t* nxt) -> bool {")
+    j = s.index("// prologue: the first stage whole", i)
+    pat = r"\b(read|dma_half|dma_advance|mma|wait_vm_lgkm0<\w+>|__builtin_amdgcn_s_barrier|ds_store<FMT, TM, TN>|tile_codes|locate)\s*\("
+    body = [m.group(1) for m in re.finditer(pat, s[i:j])]
+    assert body == ["read", "dma_half", "dma_advance", "mma", "read", "mma", "read", "mma", "wait_vm_lgkm0<0>",
+                    "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma", "ds_store<FMT, TM, TN>", "locate", "tile_codes"], body
+    k = s.index("while (stage_step(cur, nxt))", j)
+    pro = [m.group(1) for m in re.finditer(pat, s[j:k])]
+    assert pro == ["dma_half", "dma_half", "dma_advance", "tile_codes", "wait_vm_lgkm0<0>",
+                   "__builtin_amdgcn_s_barrier", "read", "dma_half"], pro
+    # the halves: quarters 2-3 of the next stage mid-step, 0-1 of the one after at the end
+    assert "dma_half(nxt, I2{});" in s[i:j] and "if (dvalid) dma_half(cur, I0{});" in s[i:j]
+    assert "const bool more = !last || cpos + step < end;" in s[i:j]
