@@ -989,23 +989,18 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     using SN = std::integral_constant<int, (S + 1) % STAGES>;            // stage kt + 1
     using SP = std::integral_constant<int, (S + STAGES - 1) % STAGES>;   // stage kt + STAGES - 1
     take_scales(kt);
-    // slice 0 (operands in F0): read slice 1; the second half of stage
-    // kt + STAGES - 1's DMA and the W loads go out here
+    // slice 0 (operands in F0): the W loads (dX), then read slice 1 and
+    // issue the second half of stage kt + STAGES - 1's DMA
+    if constexpr (kWReg) {            // dX: the W items of stage kt + 2
+      if (kt + 2 < nk) load_w(kt + 2, I0{});
+    }
     read(SC, kt, I1{}, F1);
     if (kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
-    if constexpr (kWReg) {            // dX: the W items of stage kt + 1
-      if (kt + 1 < nk) load_w(kt + 1, I0{});
-    }
     mma(F0);
     read(SC, kt, I2{}, F0);
     mma(F1);
     read(SC, kt, I3{}, F1);
     mma(F0);
-    // publish stage kt + 1: its W tile (dX; the tile's previous contents,
-    // stage kt - 1, were read before the last barrier), then everyone's DMA
-    if constexpr (kWReg) {
-      if (kt + 1 < nk) commit_w(kt + 1, I0{});
-    }
     // stage kt + 1 has landed once at most kAhead (kAheadLow) loads are
     // outstanding, if the DMA of stages kt + 2 .. kt + STAGES - 1 all went out
     // after it; in the last stages fewer did, and everything is waited for
@@ -1020,14 +1015,27 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     if (kt + 1 < nk) read(SN{}, kt + 1, I0{}, F0);
     if (kt + STAGES < nk) dma_half(SC, kt + STAGES, I0{});
     mma(F1);
+    // dX: stage kt + 2's W tile into the buffer stage kt used (every read of
+    // it came before the barrier).  Its items were loaded before the wait at
+    // the barrier, so converting them waits for nothing; loading them a
+    // stage ahead of their conversion keeps the round trip of the W items
+    // off the step's critical path (converting a stage's items in the step
+    // that loaded them cost dX 12-14%).  The next barrier publishes the tile.
+    if constexpr (kWReg) {
+      if (kt + 2 < nk) commit_w(kt + 2, I0{});
+    }
   };
 
   // prologue: stage 0 in LDS and its slice 0 read, then the DMA of stages
   // 1 .. STAGES - 2 and the first half of stage STAGES - 1
   if (nk > 0) {
-    if constexpr (kWReg) {
+    if constexpr (kWReg) {            // dX: the W tiles of stages 0 and 1
       load_w(0, I0{});
       commit_w(0, I0{});
+      if (1 < nk) {
+        load_w(1, I0{});
+        commit_w(1, I0{});
+      }
     }
     if constexpr (MODE == kFwdC) load_sc(0);
     issue_dma(I0{}, 0);

@@ -17,7 +17,9 @@ the barriers, for every stage count from 1 to 40, and checks:
   (b) a copy into a stage buffer is issued only after a barrier that follows
       every read of the stage the buffer held before;
   (c) dX's W tile of stage s is written only after a barrier that follows
-      every read of stage s - 2's tile (two W buffers).
+      every read of stage s - 2's tile (two W buffers), and converted from
+      items that a wait has already completed (the step that loads stage
+      s's items converts them right after its barrier).
 
 The replay mirrors the body of `step2` and the prologue in
 csrc/sq_gemm.hip; `test_model_follows_the_kernel_source` compares the
@@ -161,12 +163,15 @@ def replay(mode, cfg, nk, wave):
         if mode == "dx":
             w.w_last_read[stage] = w.barriers
 
-    def commit_w(stage):
+    def commit_w(stage, in_loop):
         prev = stage - 2
         if prev >= 0:
             assert w.w_last_read.get(prev, -1) < w.barriers, (mode, cfg, nk, wave, stage, "W tile reuse")
-        # the compiler waits for the W registers before the dequantisation;
-        # loads complete in order, so everything older completes with them
+        if in_loop:
+            # converted after the barrier whose wait completed the items
+            assert not w.pending(("w", stage)), (mode, cfg, nk, wave, stage, "W items still in flight")
+        # (the prologue's compiler wait completes the items and, loads
+        # completing in order, everything older)
         ws = [i for i, l in enumerate(w.loads) if l[0] == ("w", stage)]
         for l in w.loads[:ws[-1] + 1]:
             l[1] = True
@@ -178,7 +183,10 @@ def replay(mode, cfg, nk, wave):
     if nk > 0:
         if mode == "dx":
             w.issue(("w", 0), 2 * w_items)
-            commit_w(0)
+            commit_w(0, False)
+            if 1 < nk:
+                w.issue(("w", 1), 2 * w_items)
+                commit_w(1, False)
         if mode == "fwdc":
             load_sc(0)
         dma_half(0, True)
@@ -195,15 +203,13 @@ def replay(mode, cfg, nk, wave):
     for kt in range(nk):
         if mode == "fwdc" and kt % 8 == 7 and kt + 1 < nk:
             load_sc((kt + 1) // 8)
+        if mode == "dx" and kt + 2 < nk:
+            w.issue(("w", kt + 2), 2 * w_items)
         read(kt)                                               # slice 1
         if kt + STAGES - 1 < nk:
             dma_half(kt + STAGES - 1, False)
-        if mode == "dx" and kt + 1 < nk:
-            w.issue(("w", kt + 1), 2 * w_items)
         read(kt)                                               # slices 2, 3
         read(kt)
-        if mode == "dx" and kt + 1 < nk:
-            commit_w(kt + 1)
         if kt + STAGES - 1 < nk:
             w.wait(ahead if codes_wave else ahead_low)
         else:
@@ -213,6 +219,8 @@ def replay(mode, cfg, nk, wave):
             read(kt + 1)                                       # slice 0 of the next stage (a)
         if kt + STAGES < nk:
             dma_half(kt + STAGES, True)
+        if mode == "dx" and kt + 2 < nk:
+            commit_w(kt + 2, True)
     w.wait(0)
     assert all(l[1] for l in w.loads)
     return w
@@ -266,12 +274,16 @@ def test_model_follows_the_kernel_source():
     i = s.index("auto step2 = [&](auto SC, int kt) {")
     j = s.index("// prologue: stage 0 in LDS", i)
     step2 = _calls(s[i:j])
-    assert step2 == ["take_scales", "read", "dma_half", "load_w", "mma", "read", "mma", "read", "mma", "commit_w",
+    assert step2 == ["take_scales", "load_w", "read", "dma_half", "mma", "read", "mma", "read", "mma",
                      "wait_vm_lgkm0<kAhead>", "wait_vm_lgkm0<kAheadLow>", "wait_vm_lgkm0<0>",
-                     "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma"], step2
+                     "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma", "commit_w"], step2
     k = s.index("for (int kt0 = 0; kt0 < nk; kt0 += STAGES)", j)
     pro = _calls(s[j:k])
-    assert pro == ["load_w", "commit_w", "wait_vm_lgkm0<0>", "__builtin_amdgcn_s_barrier", "read", "dma_half"], pro
+    assert pro == ["load_w", "commit_w", "load_w", "commit_w", "wait_vm_lgkm0<0>", "__builtin_amdgcn_s_barrier",
+                   "read", "dma_half"], pro
+    # the W items of stage kt + 2 are loaded before the barrier's wait and
+    # converted after it
+    assert "if (kt + 2 < nk) load_w(kt + 2, I0{});" in s and "if (kt + 2 < nk) commit_w(kt + 2, I0{});" in s
     # the budgets and the code-slice split as the replay derives them
     assert "constexpr int kAhead = (STAGES - 2) * kDma < 63 ? (STAGES - 2) * kDma : 63;" in s
     assert "constexpr int kDmaLow = kCodesSplit ? kDma - DC::kInst : kDma;" in s
