@@ -1518,6 +1518,15 @@ static int launch_ds_stream(GemmGroup& gg, const ExpertProblem* p, int n, hipStr
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// Grouped products below the large tile: experts of a few hundred tokens or
+// fewer pad their last token tile, so the MXFP4 register forward takes 64 x
+// 256 tiles (64-token granularity, 8 waves of 64 x 32; the same flops per
+// tile as 128 x 128): 128 experts of 64 tokens 167 -> 128 us, of 256 tokens
+// 61 -> 59 us.  dX takes them only when experts average at most 96 tokens
+// (at 64 tokens 184 -> 117 us; at 256, 72 -> 82 us, where 128 x 128 wins).
+#define SQ_CFG_GROUPED_FWDC 64, 256, 1, 8, 4, 64
+#define SQ_CFG_GROUPED_THIN 64, 256, 1, 8, 2, 64
+
 // The large tile when the experts' tiles fill the chip and an expert averages
 // at least 512 tokens (rows of the forward and dX, the contraction of dS:
 // shorter token sums leave a 256 x 256 dS tile a few stages between its
@@ -1532,9 +1541,12 @@ static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream
   }
   const bool large = big >= kCUs && tokens >= (int64_t)512 * n;
   if (large) return launch_grouped<MODE, FMT, BM, BN, REST...>(gg, p, n, s);
-  if constexpr (MODE == kFwdC) return launch_grouped<MODE, FMT, SQ_CFG_SMALL_FWDC>(gg, p, n, s);
+  if constexpr (MODE == kFwdC) return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_FWDC>(gg, p, n, s);
   else if constexpr (MODE == kDs) return launch_ds_stream<FMT, SQ_CFG_DS_STREAM>(gg, p, n, s);
-  else return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+  else if constexpr (MODE == kDx) {
+    if (tokens <= (int64_t)96 * n) return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_THIN>(gg, p, n, s);
+    return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+  } else return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
 }
 
 template <int MODE>

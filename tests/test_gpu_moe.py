@@ -117,7 +117,8 @@ def test_grouped_products_match_oracle_and_single(sq, fmt):
 
 
 def test_more_experts_than_one_launch_holds(sq):
-    """70 experts (two launches of at most 64), bf16 outputs."""
+    """70 experts (two launches of at most 64), bf16 outputs; under 96 tokens
+    per expert on average, so dX takes the 64-token tiles."""
     O, I = 64, 128
     Ts = [(13 * e) % 97 for e in range(70)]
     codes, scales, ws2 = experts("mx", len(Ts), O, I, 7300)
@@ -126,6 +127,7 @@ def test_more_experts_than_one_launch_holds(sq):
     cd, sd = cuda(codes), cuda(scales)
     Xd, dYd = [x.cuda() for x in Xs], [d.cuda() for d in dYs]
     Ys = sq.sq_fwd_grouped("mx", Xd, cd, sd, out_dtype=torch.bfloat16)
+    dXs = sq.sq_bwd_dx_grouped("mx", dYd, cd, sd)
     dSs = sq.sq_bwd_dscale_grouped("mx", Xd, dYd, cd)
     torch.cuda.synchronize()
     for e, T in enumerate(Ts):
@@ -136,6 +138,39 @@ def test_more_experts_than_one_launch_holds(sq):
         assert normwise(Ys[e].float().cpu().numpy(), linear.forward(Xs[e].float().numpy(), W)) <= TOL
         dS_ref = linear.backward_dscale("mx", Xs[e].float().numpy(), dYs[e].float().numpy(), codes[e])
         assert normwise(dSs[e].cpu().numpy(), dS_ref) <= TOL
+        check_elements("mx", Xs[e].float().numpy(), dYs[e].float().numpy(), codes[e], W,
+                       dX=dXs[e].cpu().numpy(), what=f"expert {e}")
+        dx1 = sq.sq_bwd_dx("mx", dYd[e], cd[e], sd[e])
+        torch.cuda.synchronize()
+        assert torch.equal(dx1, dXs[e])
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+def test_thin_experts_64_token_tiles(sq, fmt):
+    """Experts of 1 to 140 tokens (64-token tiles for the MXFP4 register
+    forward and, at under 96 tokens per expert, for dX): every expert equals
+    its single products bit for bit, sampled ones the oracle per element."""
+    O, I = 768, 2048
+    Ts = [1, 63, 64, 65, 0, 127, 128, 129, 140, 7, 33, 96]
+    codes, scales, ws2 = experts(fmt, len(Ts), O, I, 7350)
+    cd, sd = cuda(codes), cuda(scales)
+    Xd = [inputs.device_bf16_normal(7360 + e, (T, I)) for e, T in enumerate(Ts)]
+    dYd = [inputs.device_bf16_normal(7380 + e, (T, O)) for e, T in enumerate(Ts)]
+    print(f"[moe thin] fmt={fmt} T={Ts}", flush=True)
+    Ys = sq.sq_fwd_grouped(fmt, Xd, cd, sd, ws2)
+    dXs = sq.sq_bwd_dx_grouped(fmt, dYd, cd, sd, ws2)
+    torch.cuda.synchronize()
+    for e, T in enumerate(Ts):
+        if T == 0:
+            continue
+        y1 = sq.sq_fwd(fmt, Xd[e], cd[e], sd[e], ws2[e])
+        dx1 = sq.sq_bwd_dx(fmt, dYd[e], cd[e], sd[e], ws2[e])
+        torch.cuda.synchronize()
+        assert torch.equal(y1, Ys[e]) and torch.equal(dx1, dXs[e]), e
+    for e in (0, 3, 8):
+        W = linear.dequant(fmt, codes[e], scales[e], ws2[e])
+        check_elements(fmt, Xd[e].float().cpu().numpy(), dYd[e].float().cpu().numpy(), codes[e], W,
+                       Ys[e].cpu().numpy(), dXs[e].cpu().numpy(), what=f"expert {e} T={Ts[e]}")
 
 
 def test_moe_layer_shapes_sampled(sq):
