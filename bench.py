@@ -410,7 +410,9 @@ def model_step(sq, steps, warmup, comparator=True):
     dX and dS (171.5 TFLOP).  Inputs are drawn on the device (one X shared by
     q/k/v, one by gate/up, one each for o and down; one dY per linear); dS is
     kept per linear, Y and dX go to per-shape buffers.  The step runs every
-    forward in layer order, then every backward in reverse order.
+    forward in layer order, then every backward in reverse order; k and v,
+    which share their input and shape, run each product as one grouped launch
+    of both (`per_linear_one_layer` times them apart too, as k_* and v_*).
 
     The QAST step reruns it with every linear's scales from a rank-32 adapter;
     the QAT-LoRA step runs the weight-space STE comparator on the native path
@@ -439,17 +441,49 @@ def model_step(sq, steps, warmup, comparator=True):
             dss.append(torch.empty((o, i // 32), dtype=torch.float32, device="cuda"))
     ybuf = {(o, i): torch.empty((Tm, o), dtype=torch.bfloat16, device="cuda") for (_, o, i) in shapes}
     dxbuf = {(o, i): torch.empty((Tm, i), dtype=torch.bfloat16, device="cuda") for (_, o, i) in shapes}
+    # k and v share their input and shape: each of their products runs as one
+    # grouped launch of both (512 tiles instead of two launches of 256 that
+    # leave half of every CU's workgroup slots empty)
+    KV = (1, 2)
+    assert [shapes[k][0] for k in KV] == ["k", "v"]
+    kv_y = [torch.empty((Tm, 1024), dtype=torch.bfloat16, device="cuda") for _ in KV]
+    kv_dx = [torch.empty((Tm, 4096), dtype=torch.bfloat16, device="cuda") for _ in KV]
+
+    def kv_tables(code_of, scale_of, with_ds=True):
+        """Per layer, the grouped k+v tables over the given per-linear codes
+        and scales (linear index n -> tensor)."""
+        out = []
+        for l in range(L):
+            ns = [l * len(shapes) + k for k in KV]
+            x = xs[l]["k"]
+            c, sc = [code_of(n) for n in ns], [scale_of(n) for n in ns]
+            t = dict(fwd=sq.ExpertTable("fwd", "mx", [x, x], c, sc, kv_y),
+                     dx=sq.ExpertTable("dx", "mx", [dys[n] for n in ns], c, sc, kv_dx))
+            if with_ds:
+                t["ds"] = sq.ExpertTable("ds", "mx", [x, x], c, None, [dss[n] for n in ns],
+                                         acts2=[dys[n] for n in ns])
+            out.append(t)
+        return out
+
+    kv = kv_tables(lambda n: codes[n], lambda n: scales[n])
 
     def run(events=None):
         for l in range(L):
             for k, (name, o, i) in enumerate(shapes):
                 n = l * len(shapes) + k
-                sq.sq_fwd("mx", xs[l][name], codes[n], scales[n], 1.0, Y=ybuf[(o, i)])
+                if k == KV[0]:
+                    kv[l]["fwd"].run()
+                elif k not in KV:
+                    sq.sq_fwd("mx", xs[l][name], codes[n], scales[n], 1.0, Y=ybuf[(o, i)])
         for l in reversed(range(L)):
             for k, (name, o, i) in reversed(list(enumerate(shapes))):
                 n = l * len(shapes) + k
-                sq.sq_bwd_dx("mx", dys[n], codes[n], scales[n], 1.0, dX=dxbuf[(o, i)])
-                sq.sq_bwd_dscale("mx", xs[l][name], dys[n], codes[n], dS=dss[n])
+                if k == KV[1]:
+                    kv[l]["dx"].run()
+                    kv[l]["ds"].run()
+                elif k not in KV:
+                    sq.sq_bwd_dx("mx", dys[n], codes[n], scales[n], 1.0, dX=dxbuf[(o, i)])
+                    sq.sq_bwd_dscale("mx", xs[l][name], dys[n], codes[n], dS=dss[n])
 
     for _ in range(warmup):
         run()
@@ -483,6 +517,18 @@ def model_step(sq, steps, warmup, comparator=True):
             torch.cuda.synchronize()
             t = a.elapsed_time(b) / L
             per[f"{name}_{prod}"] = {"ms": round(t, 4), "TFLOP/s": round(2.0 * Tm * o * i / (t * 1e-3) / 1e12, 1)}
+    # k and v as the step runs them: one grouped launch of both per product
+    for prod in ("fwd", "dx", "ds"):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for l in range(L):
+            kv[l][prod].run()
+        b.record()
+        torch.cuda.synchronize()
+        t = a.elapsed_time(b) / L
+        per[f"kv_grouped_{prod}"] = {"ms": round(t, 4),
+                                     "TFLOP/s": round(2 * 2.0 * Tm * 1024 * 4096 / (t * 1e-3) / 1e12, 1)}
+    del kv
     fused = model_step_fused(sq, codes, scales, dys, xs, Tm, L, steps, warmup, flops)
     # The QAST step: every linear's scales come from its rank-32 adapter
     # (on-grid bytes + clamp mask), the products run on those bytes, and dS
@@ -501,19 +547,28 @@ def model_step(sq, steps, warmup, comparator=True):
     qws = torch.empty(max(sq.sq_qast_factor_grads_workspace(o, i // 32, r) for (_, o, i) in shapes),
                       dtype=torch.uint8, device="cuda")
 
+    kv_qast = kv_tables(lambda n: codes[n], lambda n: qa[n]["sc"])
+
     def run_qast():
         for l in range(L):
             for k, (name, o, i) in enumerate(shapes):
                 n = l * len(shapes) + k
                 q = qa[n]
                 sq.sq_qast_scales("mx", scales[n], q["B"], q["A"], 1.0, scales_out=q["sc"], mask_out=q["m"])
-                sq.sq_fwd("mx", xs[l][name], codes[n], q["sc"], 1.0, Y=ybuf[(o, i)])
+                if k == KV[1]:
+                    kv_qast[l]["fwd"].run()
+                elif k not in KV:
+                    sq.sq_fwd("mx", xs[l][name], codes[n], q["sc"], 1.0, Y=ybuf[(o, i)])
         for l in reversed(range(L)):
             for k, (name, o, i) in reversed(list(enumerate(shapes))):
                 n = l * len(shapes) + k
                 q = qa[n]
-                sq.sq_bwd_dx("mx", dys[n], codes[n], q["sc"], 1.0, dX=dxbuf[(o, i)])
-                sq.sq_bwd_dscale("mx", xs[l][name], dys[n], codes[n], dS=dss[n])
+                if k == KV[1]:
+                    kv_qast[l]["dx"].run()
+                    kv_qast[l]["ds"].run()
+                elif k not in KV:
+                    sq.sq_bwd_dx("mx", dys[n], codes[n], q["sc"], 1.0, dX=dxbuf[(o, i)])
+                    sq.sq_bwd_dscale("mx", xs[l][name], dys[n], codes[n], dS=dss[n])
                 sq.sq_qast_factor_grads(dss[n], q["m"], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"], workspace=qws)
 
     for _ in range(warmup):
@@ -525,6 +580,7 @@ def model_step(sq, steps, warmup, comparator=True):
     e1.record()
     torch.cuda.synchronize()
     qast_ms = e0.elapsed_time(e1) / steps
+    del kv_qast
 
     # The QAT-LoRA comparator on the native path: every linear's weight
     # W = deq(W) + B A (rank 32) is re-quantised by the fused kernel before its
@@ -542,18 +598,26 @@ def model_step(sq, steps, warmup, comparator=True):
     lws = torch.empty(max(sq.sq_lora_grads_workspace(Tm, o, i, r) for (_, o, i) in shapes),
                       dtype=torch.uint8, device="cuda")
 
+    kv_qat = kv_tables(lambda n: qt[n]["c"], lambda n: qt[n]["s"], with_ds=False)
+
     def run_qat():
         for l in range(L):
             for k, (name, o, i) in enumerate(shapes):
                 n = l * len(shapes) + k
                 q = qt[n]
                 sq.sq_qat_requant("mx", codes[n], scales[n], q["B"], q["A"], 1.0, codes_out=q["c"], scales_out=q["s"])
-                sq.sq_fwd("mx", xs[l][name], q["c"], q["s"], 1.0, Y=ybuf[(o, i)])
+                if k == KV[1]:
+                    kv_qat[l]["fwd"].run()
+                elif k not in KV:
+                    sq.sq_fwd("mx", xs[l][name], q["c"], q["s"], 1.0, Y=ybuf[(o, i)])
         for l in reversed(range(L)):
             for k, (name, o, i) in reversed(list(enumerate(shapes))):
                 n = l * len(shapes) + k
                 q = qt[n]
-                sq.sq_bwd_dx("mx", dys[n], q["c"], q["s"], 1.0, dX=dxbuf[(o, i)])
+                if k == KV[1]:
+                    kv_qat[l]["dx"].run()
+                elif k not in KV:
+                    sq.sq_bwd_dx("mx", dys[n], q["c"], q["s"], 1.0, dX=dxbuf[(o, i)])
                 sq.sq_lora_grads(xs[l][name], dys[n], q["B"], q["A"], 1.0, dB=q["dB"], dA=q["dA"], workspace=lws)
 
     for _ in range(warmup):
@@ -565,7 +629,7 @@ def model_step(sq, steps, warmup, comparator=True):
     e1.record()
     torch.cuda.synchronize()
     qat_ms = e0.elapsed_time(e1) / steps
-    del qt, lws
+    del qt, lws, kv_qat
 
     out = {"workload": "MXFP4 8B-shaped model, 32 layers x 7 linears, 4096 tokens: fwd + dX + dS of every linear",
            "ms": round(ms, 3), "TFLOP": round(flops / 1e12, 2),
