@@ -213,6 +213,16 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
   constexpr bool kHoist = FMT == kNV && RULE != kRuleWholeTensor;
   RcpDivisor wd;
   if (kHoist) wd = make_rcp_divisor(ws2_ptr ? *ws2_ptr : ws2_val);
+  // a ws2 in [2^-55, 2^55] (one test per weight, workgroup-uniform) lets
+  // every quotient of the weight skip div_exact's range check
+  if (kHoist && wd.d >= 0x1p-55f && wd.d <= 0x1p55f) {
+#pragma unroll
+    for (int u = 0; u < kRtnChunks; ++u) {
+      const int64_t c = c0 + 256 * u;
+      rtn_chunk<FMT, RULE, 1>(v[u], c, c < n_chunks, ws2_ptr, ws2_val, amax_t, seed, codes, scales, pack, &wd);
+    }
+    return;
+  }
 #pragma unroll
   for (int u = 0; u < kRtnChunks; ++u) {
     const int64_t c = c0 + 256 * u;

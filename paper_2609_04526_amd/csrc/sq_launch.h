@@ -99,11 +99,14 @@ struct RtnItem {
 // each.
 constexpr int kRtnPerLaunch = 56;
 // Chunks of 8 weights per lane: MXFP4 nearest-even (the lightest per-chunk
-// work) streams best with two, every other format and rule with four (more
-// loads in flight behind the longer arithmetic): 3.6-3.7 -> 3.9-4.0 TB/s for
-// NVFP4 nearest-even over the 8B model, while MXFP4 nearest-even went
-// 5.7 -> 5.5 with four.
-constexpr int rtn_chunks(int fmt, int rule) { return (fmt == 0 && rule == 0) ? 2 : 4; }
+// work) streams best with two; NVFP4 nearest, away and toward zero, whose
+// per-weight quotient makes the arithmetic longest, with eight (more loads in
+// flight behind it: nearest-even over 28 linears of the 8B shapes 0.545 ->
+// 0.505 ms against four; sixteen halves the occupancy and is slower); the
+// others with four.
+constexpr int rtn_chunks(int fmt, int rule) {
+  return (fmt == 0 && rule == 0) ? 2 : (fmt == 1 && rule < 3) ? 8 : 4;
+}
 constexpr int rtn_span(int fmt, int rule) { return 256 * rtn_chunks(fmt, rule); }
 struct RtnBatch {
   const uint16_t* w[kRtnPerLaunch];

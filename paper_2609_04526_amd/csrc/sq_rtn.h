@@ -82,8 +82,12 @@ enum : int { kRuleEven = 0, kRuleAway = 1, kRuleRtz = 2, kRuleStochastic = 3, kR
 // groups of four blocks, written as one 4-byte store by the group's first
 // lane (the wave's lanes must all take part: the bytes cross lanes).
 // ws2d: the NVFP4 ws2 with its reciprocal, taken once per thread by the
-// caller (null: derived here from ws2_ptr / ws2_val).
-template <int FMT, int RULE>
+// caller (null: derived here from ws2_ptr / ws2_val).  NVFAST = 1: the caller
+// has checked that ws2 lies in [2^-55, 2^55], so ws2 and every block scale
+// e4m3 * ws2 (E4M3 values lie in [2^-9, 448]) are divisors div_exact takes
+// through their reciprocal: the quotients skip the per-element range check
+// (same results).
+template <int FMT, int RULE, int NVFAST = -1>
 __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, const float* ws2_ptr, float ws2_val,
                                           const float* amax_t, uint64_t seed,
                                           uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
@@ -145,7 +149,7 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
     }
     // fp32(sixth / ws2): div_exact is correctly rounded for quotients at or
     // above 2^-26, and the E4M3 encoder turns every smaller one into 0
-    sbyte = e4m3_encode_rne_sat(div_exact(sixth, wd));
+    sbyte = e4m3_encode_rne_sat(div_exact<NVFAST>(sixth, wd));
     eff = __fmul_rn(e4m3_to_f32(sbyte), ws2);
   }
 
@@ -157,11 +161,28 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
   float q[8];
   RcpDivisor ed;                                            // NVFP4: q = w / eff, exactly (div_exact)
   if (FMT == kNV) ed = make_rcp_divisor(eff);
+  auto weight = [&](int k) { return __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16); };
+  // NVFAST: a block whose scale is nonzero and whose quotients stay below
+  // 2^100 (|w| <= amax <= 2^100 eff) takes div_exact's refinement without
+  // its zero and overflow cases: the refined quotient is exact, and of the
+  // signs only that of a zero w can be lost, which copysign restores.  Zero
+  // scales, NaN blocks and overflowing quotients take the general path.
+  if (FMT == kNV && NVFAST == 1 && eff != 0.0f && amax <= __fmul_rn(eff, 0x1p100f)) {
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const float w = __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16);
-    if (FMT == kMX) q[k] = __fmul_rn(w, eff);               // w / 2^k, one rounding
-    else q[k] = (eff == 0.0f) ? 0.0f : div_exact(w, ed);
+    for (int k = 0; k < 8; ++k) {
+      const float w = weight(k);
+      const float q0 = __fmul_rn(w, ed.r);
+      const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, ed.d, w), ed.r, q0);
+      const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, ed.d, w), ed.r, q1);
+      q[k] = __builtin_copysignf(q2, w);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float w = weight(k);
+      if (FMT == kMX) q[k] = __fmul_rn(w, eff);             // w / 2^k, one rounding
+      else q[k] = (eff == 0.0f) ? 0.0f : div_exact<NVFAST>(w, ed);
+    }
   }
   uint32_t packed = 0;
 #pragma unroll

@@ -70,3 +70,59 @@ def test_ws2_quotients_near_e4m3_midpoints():
                 q = np.float32(t * (1 + k * 2.0 ** -23))
                 x = np.float32(np.float64(q) * np.float64(ws2))
                 assert div_seq(x, ws2) == np.float32(x / ws2), (ws2, x)
+
+
+def e4m3_values():
+    """Every positive finite E4M3 ("fn") value."""
+    vals = [m / 8 * 2.0 ** -6 for m in range(1, 8)]
+    vals += [(1 + m / 8) * 2.0 ** e for e in range(-6, 9) for m in range(8)]
+    return np.array([v for v in vals if v <= 448.0])
+
+
+def bf16(x):
+    """Round fp32 values to bf16 (nearest even), as float32."""
+    u = np.asarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    u = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32)
+
+
+def element_quotient(w, d):
+    """The NVFP4 re-quantiser's per-weight quotient for a block whose scale d
+    is nonzero and whose |w| / d stays below 2^100: the two corrected
+    products of div_seq, with the sign of w copied onto the result."""
+    return np.float32(np.copysign(div_seq(w, d), np.float32(w)))
+
+
+def test_rtn_element_quotient_is_the_rounded_quotient():
+    """fp32(w / eff) for bf16 weights w (zeros, subnormal and normal bf16,
+    values next to every E2M1 decision point) and block scales
+    eff = fp32(e4m3 * ws2): equal bit for bit, signed zeros included, where
+    the quotient is at or above 2^-26; below, both are smaller than 0.25 with
+    the sign of w, so the E2M1 code (a signed zero) is the same."""
+    g = np.random.default_rng(11)
+    e4 = e4m3_values()
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0])
+    vals = np.concatenate([mids, [0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]])
+    checked = 0
+    for ws2 in (np.float32(1 / 448), np.float32(3.0517578e-05), np.float32(0.0123), np.float32(2.0 ** -55),
+                np.float32(2.0 ** 55)):
+        for s in g.choice(e4, 24, replace=False):
+            eff = np.float32(np.float32(s) * ws2)
+            ws = [np.float32(0.0), np.float32(-0.0), np.float32(2.0 ** -133), -np.float32(2.0 ** -130)]
+            for v in g.choice(vals, 6, replace=False):
+                for k in range(-3, 4):
+                    ws.append(bf16(np.float32(v * float(eff) * (1 + k * 2.0 ** -8))))
+                    ws.append(-bf16(np.float32(v * float(eff) * (1 + k * 2.0 ** -9))))
+            for w in ws:
+                w = np.float32(w)
+                if not np.isfinite(w) or abs(float(w)) > 2.0 ** 100 * float(eff):
+                    continue
+                got = element_quotient(w, eff)
+                ref = rn32(Fraction(float(w)) / Fraction(float(eff)))
+                ref = np.float32(np.copysign(ref, w)) if ref == 0 else np.float32(ref)
+                if abs(float(ref)) >= 2.0 ** -26:
+                    assert got.view(np.uint32) == ref.view(np.uint32), (ws2, eff, w, got, ref)
+                else:
+                    assert abs(float(got)) < 0.25 and np.signbit(got) == np.signbit(w), (eff, w, got)
+                checked += 1
+    assert checked > 3000
