@@ -481,31 +481,39 @@ __device__ __forceinline__ void ds_codes(u32x4 (&cw)[TM * TN], const uint8_t* co
 // Products with the codes, summed over each scale block (32 features for
 // MXFP4, 16 for NVFP4; the 32 rows of an MFMA tile are split over the two
 // lane halves) and stored to dS[o, block].
-template <int FMT, int TM, int TN>
+// INTERIOR: the tile lies inside the layer (every row below I, every column
+// below O), so no element needs a range check.
+template <int FMT, int TM, int TN, bool INTERIOR>
 __device__ __forceinline__ void ds_store(const f32x16 (&acc)[TM][TN], const u32x4 (&cw)[TM * TN], float* dS, int O,
                                          int I, int G, int r0, int c0, int lane) {
   const int lrow = 4 * (lane >> 5);
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int o = c0 + j * 32 + (lane & 31);
-    const bool o_ok = o < O;
+    const bool o_ok = INTERIOR || o < O;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int jb = r0 + i * 32;          // first feature of this 32-row tile
       float prod[16];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        // the pair of rows jb + 8 q + lrow .. + 3: bytes 4 q + lrow / 2 of the chunk
-        const uint32_t c = jb + 8 * q + lrow < I ? (cw[j * TM + i][q] >> (4 * lrow)) & 0xFFFFu : 0u;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) prod[4 * q + e] = acc[i][j][4 * q + e] * e2m1_to_f32((c >> (4 * e)) & 15u);
+        // the pair of rows jb + 8 q + lrow .. + 3: bytes 4 q + lrow / 2 of the
+        // chunk, decoded two codes per convert (E2M1 values are exact in fp32)
+        const uint32_t c = INTERIOR || jb + 8 * q + lrow < I ? cw[j * TM + i][q] >> (4 * lrow) : 0u;
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const f32x2 v01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, 1.0f, 0);
+        const f32x2 v23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, 1.0f, 1);
+        prod[4 * q + 0] = acc[i][j][4 * q + 0] * v01[0];
+        prod[4 * q + 1] = acc[i][j][4 * q + 1] * v01[1];
+        prod[4 * q + 2] = acc[i][j][4 * q + 2] * v23[0];
+        prod[4 * q + 3] = acc[i][j][4 * q + 3] * v23[1];
       }
       if constexpr (FMT == kMX) {
         float s = 0.0f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) s += prod[r];
         s += __shfl_xor(s, 32);
-        if (lane < 32 && o_ok && jb < I) dS[(size_t)o * G + jb / 32] = s;
+        if (lane < 32 && o_ok && (INTERIOR || jb < I)) dS[(size_t)o * G + jb / 32] = s;
       } else {
         float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
@@ -514,7 +522,7 @@ __device__ __forceinline__ void ds_store(const f32x16 (&acc)[TM][TN], const u32x
         s1 += __shfl_xor(s1, 32);
         const int b = jb / 16 + (lane >> 5);
         const float s = (lane < 32) ? s0 : s1;
-        if (o_ok && b * 16 < I) dS[(size_t)o * G + b] = s;
+        if (o_ok && (INTERIOR || b * 16 < I)) dS[(size_t)o * G + b] = s;
       }
     }
   }
@@ -1087,7 +1095,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     float* dS = reinterpret_cast<float*>(g.out) + (size_t)split * g.O * g.G;   // partial plane when split
     u32x4 cw[TM * TN];
     ds_codes<FMT, TM, TN>(cw, g.codes, g.O, g.I, m0 + wm0, n0 + wn0, lane);
-    ds_store<FMT, TM, TN>(acc, cw, dS, g.O, g.I, g.G, m0 + wm0, n0 + wn0, lane);
+    if (m0 + BM <= g.I && n0 + BN <= g.O)
+      ds_store<FMT, TM, TN, true>(acc, cw, dS, g.O, g.I, g.G, m0 + wm0, n0 + wn0, lane);
+    else
+      ds_store<FMT, TM, TN, false>(acc, cw, dS, g.O, g.I, g.G, m0 + wm0, n0 + wn0, lane);
   }
 }
 
@@ -1297,7 +1308,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
       ++ckt;
       return true;
     }
-    ds_store<FMT, TM, TN>(acc, cw, reinterpret_cast<float*>(gg.out[ct.e]), O, I, G, ct.m0 + wm0, ct.n0 + wn0, lane);
+    float* const dS = reinterpret_cast<float*>(gg.out[ct.e]);
+    if (ct.m0 + BM <= I && ct.n0 + BN <= O)
+      ds_store<FMT, TM, TN, true>(acc, cw, dS, O, I, G, ct.m0 + wm0, ct.n0 + wn0, lane);
+    else
+      ds_store<FMT, TM, TN, false>(acc, cw, dS, O, I, G, ct.m0 + wm0, ct.n0 + wn0, lane);
     if (!more) return false;
 #pragma unroll
     for (int i = 0; i < TM; ++i)

@@ -369,10 +369,11 @@ def test_stream_model_follows_the_kernel_source():
     s = source()
     i = s.index("auto stage_step = [&](SQ_LDS uint8_t* cur, SQ_LDS uint8_t* nxt) -> bool {")
     j = s.index("// prologue: the first stage whole", i)
-    pat = r"\b(read|dma_half|dma_advance|mma|wait_vm_lgkm0<\w+>|__builtin_amdgcn_s_barrier|ds_store<FMT, TM, TN>|tile_codes|locate)\s*\("
+    pat = r"\b(read|dma_half|dma_advance|mma|wait_vm_lgkm0<\w+>|__builtin_amdgcn_s_barrier|ds_store<FMT, TM, TN, (?:true|false)>|tile_codes|locate)\s*\("
     body = [m.group(1) for m in re.finditer(pat, s[i:j])]
     assert body == ["read", "dma_half", "dma_advance", "mma", "read", "mma", "read", "mma", "wait_vm_lgkm0<0>",
-                    "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma", "ds_store<FMT, TM, TN>", "locate", "tile_codes"], body
+                    "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma", "ds_store<FMT, TM, TN, true>",
+                    "ds_store<FMT, TM, TN, false>", "locate", "tile_codes"], body
     k = s.index("while (stage_step(cur, nxt))", j)
     pro = [m.group(1) for m in re.finditer(pat, s[j:k])]
     assert pro == ["dma_half", "dma_half", "dma_advance", "tile_codes", "wait_vm_lgkm0<0>",
