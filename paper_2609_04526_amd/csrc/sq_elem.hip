@@ -187,6 +187,45 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
   uint8_t* codes = b.codes[p];
   uint8_t* scales = b.scales[p];
   constexpr int kRtnChunks = rtn_chunks(FMT, RULE);
+  // NVFP4 nearest and toward zero: a lane takes whole 16-weight blocks (its
+  // chunks 2 b and 2 b + 1 for blocks b = b0 + 256 u), so each block's scale
+  // arithmetic runs once (rtn_block16_nv)
+  constexpr bool kBlocks = FMT == kNV && (RULE == kRuleEven || RULE == kRuleAway || RULE == kRuleRtz);
+  if constexpr (kBlocks) {
+    static_assert(kRtnChunks % 2 == 0, "whole blocks per lane");
+    const int64_t b0 = (int64_t)(wg - b.span_begin[p]) * (rtn_span(FMT, RULE) / 2) + threadIdx.x;
+    uint4 v[kRtnChunks];
+#pragma unroll
+    for (int u = 0; u < kRtnChunks / 2; ++u) {
+      const int64_t c = 2 * (b0 + 256 * u);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (c + h < n_chunks) {
+          const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(W + 8 * (c + h)));
+          v[2 * u + h] = make_uint4(t[0], t[1], t[2], t[3]);
+        } else {
+          v[2 * u + h] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    }
+    const int64_t n_blocks = n_chunks / 2;
+    const int64_t pack = (reinterpret_cast<uintptr_t>(scales) & 3) == 0 ? n_blocks / 4 * 4 : 0;
+    const RcpDivisor wd = make_rcp_divisor(b.ws2_ptr[p] ? *b.ws2_ptr[p] : b.ws2_val[p]);
+    if (wd.d >= 0x1p-55f && wd.d <= 0x1p55f) {
+#pragma unroll
+      for (int u = 0; u < kRtnChunks / 2; ++u) {
+        const int64_t blk = b0 + 256 * u;
+        rtn_block16_nv<RULE, 1>(v[2 * u], v[2 * u + 1], blk, blk < n_blocks, wd, codes, scales, pack);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kRtnChunks / 2; ++u) {
+        const int64_t blk = b0 + 256 * u;
+        rtn_block16_nv<RULE, -1>(v[2 * u], v[2 * u + 1], blk, blk < n_blocks, wd, codes, scales, pack);
+      }
+    }
+    return;
+  }
   const int64_t c0 = (int64_t)(wg - b.span_begin[p]) * rtn_span(FMT, RULE) + threadIdx.x;
   uint4 v[kRtnChunks];
 #pragma unroll

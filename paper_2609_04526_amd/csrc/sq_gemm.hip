@@ -28,8 +28,8 @@
 //   * W in the MXFP4 forward: the packed codes are copied to LDS as they are
 //     and each wave dequantises its own operand in registers (kFwdC);
 //   * W elsewhere (dX, the NVFP4 forward): packed codes and scale bytes are
-//     loaded into registers one or two stages ahead, dequantised exactly to
-//     bf16 (sq_device.h) and written to a double-buffered LDS tile once per
+//     loaded into registers two stages ahead, dequantised exactly to bf16
+//     (sq_device.h) and written to a double-buffered LDS tile once per
 //     workgroup.
 // Two schedules: the late-barrier one (MXFP4 forward, dX, dS; see `step2`)
 // reads each slice's operands one slice ahead and publishes the next stage
@@ -43,6 +43,11 @@
 // sums over the block in registers (the 32x32 MFMA output puts 8 of a
 // 16-row block's rows in one lane and the other 8 in the lane 32 away), so
 // dW never leaves the chip and dS is written once, without atomics.
+//
+// MoE experts (grouped calls) run the same tile code over one tile order of
+// all experts, dealt to XCDs in contiguous stretches; grouped dS over short
+// token sums runs as resident workgroups that stream their tiles' stages
+// back to back (ds_stream_kernel).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -795,20 +800,19 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     }
   };
 
-  // ---- one K stage: wait for its data, refill the oldest stage, multiply
+  // ---- one K stage of the early-barrier schedule (kFwdR): wait for its
+  // data, refill the oldest stage, multiply
+  static_assert(kLate || MODE == kFwdR, "the early-barrier schedule serves the LDS-dequantised forward");
   auto step = [&](auto SC, int kt) {
     constexpr int S = decltype(SC)::value;
     constexpr int SNEXT = (S + STAGES - 1) % STAGES;          // stage that receives kt + STAGES - 1
     // stage kt is complete once every load this thread issued has landed:
     // the last DMA quarter went out at the end of the previous step, and the
-    // W registers of stage kt + 1 (kt + 2 for kFwdR) are loaded after this wait
+    // W registers of stage kt + 2 are loaded after this wait
     wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (kWAhead == 2) load_w(kt + 2, std::integral_constant<int, S % 2>{});
-    else if constexpr (kWReg) {
-      if (kt + 1 < nk) load_w(kt + 1, std::integral_constant<int, 0>{});
-    }
     __builtin_amdgcn_sched_barrier(0);
 
     // quarters 2 s and 2 s + 1 of the next stage's DMA are issued between the
@@ -845,26 +849,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
       }
-      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
-    } else if constexpr (MODE == kDx) {
-      const SQ_LDS uint16_t* a = (const SQ_LDS uint16_t*)st;
-      const SQ_LDS uint16_t* b = wbuf(kt);
-#pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        bf16x8 fa[TM], fb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          fa[i] = *(const SQ_LDS bf16x8*)(a + kc_off(wm0 + i * 32 + (lane & 31), 2 * kk + (lane >> 5)));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) fb[j] = nat_frag<BN>(b, kk, wn0 + j * 32, lane);
-        before_mfma(kk);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-      }
-      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, kWAhead == 2 ? (S + 1) % 2 : 0>{});
+      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, (S + 1) % 2>{});
     }
   };
 
@@ -895,10 +880,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // drain at every barrier.  Right after the barrier the buffer of stage kt
   // is free: half of the DMA of stage kt + STAGES goes out there, the other
   // half in the first slice of stage kt + 1, so each stage's copy has
-  // STAGES - 1 stages to land.  dX's W tile for stage kt + 1 is loaded into
-  // registers in slice 0 of stage kt and committed to LDS before its barrier
-  // (against the two-stage early-barrier schedule: the 8B MLP dX products
-  // -2.5%, the 4096^3 one unchanged).
+  // STAGES - 1 stages to land.  dX's W items for stage kt + 2 are loaded at
+  // the start of step kt and converted to its LDS tile right after that
+  // step's barrier (see the end of step2).
   struct Frag {
     bf16x8 a[TM];
     bf16x8 b[TN];

@@ -100,10 +100,11 @@ struct RtnItem {
 constexpr int kRtnPerLaunch = 56;
 // Chunks of 8 weights per lane: MXFP4 nearest-even (the lightest per-chunk
 // work) streams best with two; NVFP4 nearest, away and toward zero, whose
-// per-weight quotient makes the arithmetic longest, with eight (more loads in
-// flight behind it: nearest-even over 28 linears of the 8B shapes 0.545 ->
-// 0.505 ms against four; sixteen halves the occupancy and is slower); the
-// others with four.
+// per-weight quotient makes the arithmetic longest, with eight, four whole
+// 16-weight blocks (more loads in flight behind it: nearest-even over 28
+// linears of the 8B shapes 0.545 -> 0.505 ms against four chunks when a block
+// spanned two lanes; sixteen halve the occupancy and are slower; with whole
+// blocks per lane two and four blocks time alike); the others with four.
 constexpr int rtn_chunks(int fmt, int rule) {
   return (fmt == 0 && rule == 0) ? 2 : (fmt == 1 && rule < 3) ? 8 : 4;
 }

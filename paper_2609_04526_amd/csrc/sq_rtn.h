@@ -254,4 +254,96 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
   }
 }
 
+// NVFP4 nearest (RULE even or away) and round-toward-zero re-quantisation
+// of one whole 16-weight block per lane (its two chunks of 8, already
+// loaded), the same arithmetic as rtn_chunk: the block's amax, scale byte,
+// block scale and its reciprocal are taken once per block instead of once in
+// each of the block's two lanes, and the amax needs no shuffle.  NVFAST as in
+// rtn_chunk.  blk is the block index within the weight (codes at byte 8 blk,
+// the scale at byte blk).  pack_below > 0: the lanes hold consecutive blocks
+// from a multiple of 64 on and the scale plane is 4-byte aligned; blocks
+// below pack_below are whole groups of four, whose scale bytes leave as one
+// 4-byte store from the group's first lane (every lane of the wave must take
+// part: the bytes cross lanes).
+template <int RULE, int NVFAST>
+__device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, int64_t blk, bool valid,
+                                               const RcpDivisor& wd, uint8_t* __restrict__ codes,
+                                               uint8_t* __restrict__ scales, int64_t pack_below) {
+  static_assert(RULE == kRuleEven || RULE == kRuleAway || RULE == kRuleRtz, "nearest and toward-zero rules");
+  const uint32_t h[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+  uint32_t am = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) am = max(am, max(h[k] & 0x7FFFu, (h[k] >> 16) & 0x7FFFu));
+  const float amax = __uint_as_float(am << 16);
+  const float sixth = amax >= 0x1p-120f ? div_exact<1>(amax, RcpDivisor{6.0f, 0x1.555556p-3f, true})
+                                        : __fdiv_rn(amax, 6.0f);
+  const uint32_t sbyte = e4m3_encode_rne_sat(div_exact<NVFAST>(sixth, wd));
+  const float eff = __fmul_rn(e4m3_to_f32(sbyte), wd.d);
+  const RcpDivisor ed = make_rcp_divisor(eff);
+  auto weight = [&](int k) { return __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16); };
+  float q[16];
+  if (NVFAST == 1 && eff != 0.0f && amax <= __fmul_rn(eff, 0x1p100f)) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float w = weight(k);
+      const float q0 = __fmul_rn(w, ed.r);
+      const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, ed.d, w), ed.r, q0);
+      const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, ed.d, w), ed.r, q1);
+      q[k] = __builtin_copysignf(q2, w);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) q[k] = (eff == 0.0f) ? 0.0f : div_exact<NVFAST>(weight(k), ed);
+  }
+  uint32_t packed[2] = {0u, 0u};
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+    packed[p >> 2] |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, q[2 * p], q[2 * p + 1], 1.0f, 0) & 0xFFu)
+                      << (8 * (p & 3));
+  if (RULE == kRuleAway) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float a = fabsf(q[k]);
+      packed[k >> 3] += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * (k & 7))) : 0u;
+    }
+  }
+  if (RULE == kRuleRtz) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float a = fminf(fabsf(q[k]), 6.0f);
+      const uint32_t m = (packed[k >> 3] >> (4 * (k & 7))) & 7u;
+      packed[k >> 3] -= (e2m1_mag(m) > a) ? (1u << (4 * (k & 7))) : 0u;
+    }
+  }
+  if (am > 0x7F80u || eff == 0.0f) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const uint32_t hb = (h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+      const uint32_t mag = (q[k] != q[k]) ? 0u : ((packed[k >> 3] >> (4 * (k & 7))) & 7u);
+      packed[k >> 3] = (packed[k >> 3] & ~(15u << (4 * (k & 7)))) | ((mag | ((hb >> 12) & 8u)) << (4 * (k & 7)));
+    }
+  }
+  uint32_t* c32 = reinterpret_cast<uint32_t*>(codes);
+  if (pack_below > 0) {
+    const uint32_t b1 = (uint32_t)__shfl_down((int)sbyte, 1);
+    const uint32_t b2 = (uint32_t)__shfl_down((int)sbyte, 2);
+    const uint32_t b3 = (uint32_t)__shfl_down((int)sbyte, 3);
+    if (valid) {
+      __builtin_nontemporal_store(packed[0], c32 + 2 * blk);
+      __builtin_nontemporal_store(packed[1], c32 + 2 * blk + 1);
+      if (blk < pack_below) {
+        if ((blk & 3) == 0) reinterpret_cast<uint32_t*>(scales)[blk >> 2] = sbyte | (b1 << 8) | (b2 << 16) | (b3 << 24);
+      } else {
+        scales[blk] = (uint8_t)sbyte;
+      }
+    }
+    return;
+  }
+  if (valid) {
+    c32[2 * blk] = packed[0];
+    c32[2 * blk + 1] = packed[1];
+    scales[blk] = (uint8_t)sbyte;
+  }
+}
+
 }  // namespace sq
