@@ -211,17 +211,27 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
     const int64_t n_blocks = n_chunks / 2;
     const int64_t pack = (reinterpret_cast<uintptr_t>(scales) & 3) == 0 ? n_blocks / 4 * 4 : 0;
     const RcpDivisor wd = make_rcp_divisor(b.ws2_ptr[p] ? *b.ws2_ptr[p] : b.ws2_val[p]);
+    // the block scale fp32(e4m3 * ws2) and its reciprocal for each of the 128
+    // scale bytes, once per workgroup instead of once per block
+    __shared__ float tab[256];
+    if (threadIdx.x < 128) {
+      const float e = __fmul_rn(e4m3_to_f32(threadIdx.x), wd.d);
+      tab[2 * threadIdx.x] = e;
+      tab[2 * threadIdx.x + 1] = __fdiv_rn(1.0f, e);
+    }
+    __syncthreads();
+    const __attribute__((address_space(3))) float* tl = (const __attribute__((address_space(3))) float*)tab;
     if (wd.d >= 0x1p-55f && wd.d <= 0x1p55f) {
 #pragma unroll
       for (int u = 0; u < kRtnChunks / 2; ++u) {
         const int64_t blk = b0 + 256 * u;
-        rtn_block16_nv<RULE, 1>(v[2 * u], v[2 * u + 1], blk, blk < n_blocks, wd, codes, scales, pack);
+        rtn_block16_nv<RULE, 1>(v[2 * u], v[2 * u + 1], blk, blk < n_blocks, wd, tl, codes, scales, pack);
       }
     } else {
 #pragma unroll
       for (int u = 0; u < kRtnChunks / 2; ++u) {
         const int64_t blk = b0 + 256 * u;
-        rtn_block16_nv<RULE, -1>(v[2 * u], v[2 * u + 1], blk, blk < n_blocks, wd, codes, scales, pack);
+        rtn_block16_nv<RULE, -1>(v[2 * u], v[2 * u + 1], blk, blk < n_blocks, wd, tl, codes, scales, pack);
       }
     }
     return;

@@ -184,10 +184,13 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
       else q[k] = (eff == 0.0f) ? 0.0f : div_exact<NVFAST>(w, ed);
     }
   }
+  // the convert writes its two codes into byte p of its first operand and
+  // keeps the other bytes, so four of them build the word
   uint32_t packed = 0;
-#pragma unroll
-  for (int p = 0; p < 4; ++p)
-    packed |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, q[2 * p], q[2 * p + 1], 1.0f, 0) & 0xFFu) << (8 * p);
+  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[0], q[1], 1.0f, 0);
+  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[2], q[3], 1.0f, 1);
+  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[4], q[5], 1.0f, 2);
+  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[6], q[7], 1.0f, 3);
   if (RULE == kRuleAway) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {                           // a tie magnitude is below 6: no carry
@@ -265,21 +268,32 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
 // below pack_below are whole groups of four, whose scale bytes leave as one
 // 4-byte store from the group's first lane (every lane of the wave must take
 // part: the bytes cross lanes).
+// tab[2 b], tab[2 b + 1] hold fp32(e4m3(b) * ws2) and its correctly rounded
+// reciprocal for every non-negative scale byte b (the caller's per-workgroup
+// table).
 template <int RULE, int NVFAST>
 __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, int64_t blk, bool valid,
-                                               const RcpDivisor& wd, uint8_t* __restrict__ codes,
-                                               uint8_t* __restrict__ scales, int64_t pack_below) {
+                                               const RcpDivisor& wd, const __attribute__((address_space(3))) float* tab,
+                                               uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                               int64_t pack_below) {
   static_assert(RULE == kRuleEven || RULE == kRuleAway || RULE == kRuleRtz, "nearest and toward-zero rules");
   const uint32_t h[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-  uint32_t am = 0;
+  // the amax on bit patterns, two bf16 magnitudes per packed 16-bit max
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  u16x2 m2 = {0, 0};
 #pragma unroll
-  for (int k = 0; k < 8; ++k) am = max(am, max(h[k] & 0x7FFFu, (h[k] >> 16) & 0x7FFFu));
+  for (int k = 0; k < 8; ++k) m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(u16x2, h[k] & 0x7FFF7FFFu));
+  const uint32_t am = max((uint32_t)m2[0], (uint32_t)m2[1]);
   const float amax = __uint_as_float(am << 16);
   const float sixth = amax >= 0x1p-120f ? div_exact<1>(amax, RcpDivisor{6.0f, 0x1.555556p-3f, true})
                                         : __fdiv_rn(amax, 6.0f);
   const uint32_t sbyte = e4m3_encode_rne_sat(div_exact<NVFAST>(sixth, wd));
-  const float eff = __fmul_rn(e4m3_to_f32(sbyte), wd.d);
-  const RcpDivisor ed = make_rcp_divisor(eff);
+  const uint32_t ti = 2u * (sbyte & 127u);          // sbyte <= 0x7F: sixth / ws2 is never negative
+  const float eff = tab[ti];
+  RcpDivisor ed;
+  ed.d = eff;
+  ed.r = tab[ti + 1];
+  ed.fast = eff >= 0x1p-64f && eff <= 0x1p64f;
   auto weight = [&](int k) { return __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16); };
   float q[16];
   if (NVFAST == 1 && eff != 0.0f && amax <= __fmul_rn(eff, 0x1p100f)) {
@@ -295,11 +309,16 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
 #pragma unroll
     for (int k = 0; k < 16; ++k) q[k] = (eff == 0.0f) ? 0.0f : div_exact<NVFAST>(weight(k), ed);
   }
-  uint32_t packed[2] = {0u, 0u};
+  uint32_t packed[2];
 #pragma unroll
-  for (int p = 0; p < 8; ++p)
-    packed[p >> 2] |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, q[2 * p], q[2 * p + 1], 1.0f, 0) & 0xFFu)
-                      << (8 * (p & 3));
+  for (int hf = 0; hf < 2; ++hf) {                // byte-selected converts, as in rtn_chunk
+    uint32_t w = 0;
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 0], q[8 * hf + 1], 1.0f, 0);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 2], q[8 * hf + 3], 1.0f, 1);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 4], q[8 * hf + 5], 1.0f, 2);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 6], q[8 * hf + 7], 1.0f, 3);
+    packed[hf] = w;
+  }
   if (RULE == kRuleAway) {
 #pragma unroll
     for (int k = 0; k < 16; ++k) {

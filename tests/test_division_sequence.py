@@ -126,3 +126,38 @@ def test_rtn_element_quotient_is_the_rounded_quotient():
                     assert abs(float(got)) < 0.25 and np.signbit(got) == np.signbit(w), (eff, w, got)
                 checked += 1
     assert checked > 3000
+
+
+def hard_quotients(n, seed, within=2.0 ** -21):
+    """bf16 weights w and fp32 block scales d whose quotient w / d lies within
+    `within` ulp of a midpoint between two fp32 values (where a quotient off
+    by a fraction of an ulp rounds the wrong way), found among n random
+    pairs in float64 (53 bits resolve the distance to 2^-29 ulp)."""
+    g = np.random.default_rng(seed)
+    out = []
+    for _ in range(n // 4_000_000):
+        m = 4_000_000
+        w = (128 + g.integers(0, 128, m)).astype(np.float64) * 2.0 ** (g.integers(-8, 8, m) - 7)
+        d = g.uniform(1.0, 2.0, m).astype(np.float32).astype(np.float64) * 2.0 ** g.integers(-10, 10, m)
+        x = w / d
+        e = np.floor(np.log2(x))
+        t = x / 2.0 ** (e - 23)
+        dist = np.abs(t - np.floor(t) - 0.5)
+        for i in np.nonzero(dist < within)[0]:
+            out.append((np.float32(w[i]) * (1 if g.integers(0, 2) else -1), np.float32(d[i])))
+    return out
+
+
+def test_rtn_element_quotient_hard_cases():
+    """Quotients within 2^-21 ulp of an fp32 rounding midpoint, the cases a
+    quotient that is merely faithful can round the wrong way: the element
+    form still gives fp32(w / d) bit for bit."""
+    cases = hard_quotients(16_000_000, 13)
+    assert len(cases) >= 6
+    naive_wrong = 0
+    for w, d in cases:
+        ref = np.float32(rn32(Fraction(float(w)) / Fraction(float(d))))
+        assert element_quotient(w, d).view(np.uint32) == ref.view(np.uint32), (w, d)
+        naive_wrong += np.float32(np.float32(w) * np.float32(np.float32(1.0) / d)) != ref
+    # the cases are hard: the plain product with the reciprocal misrounds some
+    assert naive_wrong >= 2
