@@ -330,8 +330,10 @@ def test_rtn_ties_and_specials(sq):
 def test_rtn_tiny_blocks_and_extreme_ws2(sq, ws2):
     """Block amax values on both sides of 2^-120 (where amax / 6 leaves the
     reciprocal path for a full division), bf16 subnormals, zeros, and a
-    per-tensor ws2 inside and outside [2^-64, 2^64] (0: recomputed), in both
-    formats against the oracle."""
+    per-tensor ws2 inside and outside [2^-55, 2^55] (the range the NVFP4 kernels'
+    shortened division assumes; 0: recomputed), in both
+    formats against the oracle, for the two nearest rules and round toward
+    zero."""
     O, I = 16, 512
     g = inputs.rng(4300)
     W = (g.standard_normal((O, I)) * 0.02).astype(np.float32)
@@ -357,6 +359,15 @@ def test_rtn_tiny_blocks_and_extreme_ws2(sq, ws2):
             if fmt == "nv":
                 got = w2.cpu().numpy()[0]
                 assert got == rw or (np.isnan(got) and np.isnan(rw))
+        # round toward zero takes the same block path for NVFP4
+        ref_ws2 = ws2_in if (fmt == "nv" and ws2_in > 0) else None
+        c, s, w2 = sq.rtn_quantize_rule(fmt, Wb.cuda(), "rtz", ws2_in, 0)
+        torch.cuda.synchronize()
+        rc, rs, rw = rtn.quantize_rule(fmt, Wf, "rtz", ref_ws2, 0)
+        assert np.array_equal(s.cpu().numpy(), rs) and np.array_equal(c.cpu().numpy(), rc)
+        if w2 is not None:
+            got = w2.cpu().numpy()[0]
+            assert got == rw or (np.isnan(got) and np.isnan(rw))
 
 
 def test_rtn_delta_zero_fixed_point(sq):
