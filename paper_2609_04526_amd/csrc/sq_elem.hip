@@ -182,6 +182,8 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
     else hi = mid - 1;
   }
   const int p = lo;
+  // a given ws2 is also the weight's ws2 output (one store, no launch of its own)
+  if (b.ws2_out[p] != nullptr && wg == b.span_begin[p] && threadIdx.x == 0) *b.ws2_out[p] = b.ws2_val[p];
   const int64_t n_chunks = b.n_chunks[p];
   const uint16_t* __restrict__ W = b.w[p];
   uint8_t* codes = b.codes[p];
@@ -366,8 +368,6 @@ int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream
     } else if (nv && !(it.ws2_in > 0.0f)) {
       tensor_amax(w, n_chunks, it.ws2_out, s);
       hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, it.ws2_out);
-    } else if (nv && it.ws2_out) {
-      hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, it.ws2_out, it.ws2_in);
     }
   }
   RtnBatch batch{};
@@ -382,7 +382,12 @@ int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream
   for (int k = 0; k < n; ++k) {
     const RtnItem& it = items[k];
     const int64_t n_chunks = it.O * it.I / 8;
-    if (n_chunks == 0) continue;
+    if (n_chunks == 0) {
+      // no workgroup of its own: a given ws2 reaches its slot by a launch
+      if (nv && rule != kRuleWholeTensor && it.ws2_in > 0.0f && it.ws2_out)
+        hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, it.ws2_out, it.ws2_in);
+      continue;
+    }
     const int64_t span = rtn_span(fmt, rule);
     const int64_t c = (n_chunks + span - 1) / span;
     if (batch.count == kRtnPerLaunch || spans + c > INT32_MAX)
@@ -400,6 +405,7 @@ int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream
     } else if (nv) {
       batch.ws2_ptr[p] = it.ws2_in > 0.0f ? nullptr : it.ws2_out;
       batch.ws2_val[p] = it.ws2_in;
+      batch.ws2_out[p] = it.ws2_in > 0.0f ? it.ws2_out : nullptr;
     } else {
       batch.ws2_val[p] = 1.0f;
     }

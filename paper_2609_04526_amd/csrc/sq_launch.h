@@ -99,14 +99,12 @@ struct RtnItem {
 // each.
 constexpr int kRtnPerLaunch = 56;
 // Chunks of 8 weights per lane: MXFP4 nearest-even (the lightest per-chunk
-// work) streams best with two; NVFP4 nearest, away and toward zero, whose
-// per-weight quotient makes the arithmetic longest, with eight, four whole
-// 16-weight blocks (more loads in flight behind it: nearest-even over 28
-// linears of the 8B shapes 0.545 -> 0.505 ms against four chunks when a block
-// spanned two lanes; sixteen halve the occupancy and are slower; with whole
-// blocks per lane two and four blocks time alike); the others with four.
+// work) streams best with two; NVFP4 nearest, away and toward zero take two
+// whole 16-weight blocks per lane (nearest-even over 28 linears of the 8B
+// shapes: 0.389 ms, against 0.44 ms with one block and with four, whose
+// longer-lived waves leave fewer loads in flight); the others four.
 constexpr int rtn_chunks(int fmt, int rule) {
-  return (fmt == 0 && rule == 0) ? 2 : (fmt == 1 && rule < 3) ? 8 : 4;
+  return (fmt == 0 && rule == 0) ? 2 : 4;
 }
 constexpr int rtn_span(int fmt, int rule) { return 256 * rtn_chunks(fmt, rule); }
 struct RtnBatch {
@@ -119,9 +117,11 @@ struct RtnBatch {
   uint64_t seed[kRtnPerLaunch];
   int32_t span_begin[kRtnPerLaunch];
   float ws2_val[kRtnPerLaunch];
+  float* ws2_out[kRtnPerLaunch];          // slot that receives ws2_val (the weight's first workgroup), or null
   int32_t count;
   int32_t spans;
 };
+static_assert(sizeof(RtnBatch) <= 4096, "kernel arguments are limited to 4 KiB");
 // Re-quantises n weights under one rule (as rtn_rule_launch on each, in
 // launches of up to kRtnPerLaunch weights); every weight that needs an amax
 // slot has its own ws2_out.

@@ -296,14 +296,49 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
   ed.fast = eff >= 0x1p-64f && eff <= 0x1p64f;
   auto weight = [&](int k) { return __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16); };
   float q[16];
+  // near: some code of the block may depend on more than the product w r
+  // (always true off the fast path, where q holds the exact quotients)
+  bool near = true;
   if (NVFAST == 1 && eff != 0.0f && amax <= __fmul_rn(eff, 0x1p100f)) {
+    // q0 = RN(w r) with r = RN(1 / eff) is w / eff (1 + e1)(1 + e2), |e1|, |e2|
+    // <= 2^-24, so q0 and RN(w / eff) lie within 3 float steps of each other
+    // (2^-23 |w / eff| is at most 2 steps of the binade, 4 just below a power
+    // of two, where the steps halve, and the exact quotient adds half a
+    // step).  Every value at which an E2M1 code changes under the three rules
+    // (rounding boundaries 0.25, 0.75, ..., 5 and grid points 0.5, 1, ..., 6)
+    // has a significand with at most two fraction bits: its bit pattern is a
+    // multiple of 2^21.  When q0 lies more than 3 steps from every such
+    // pattern, no such value lies between q0 and the exact quotient, and the
+    // code taken from q0 is the exact quotient's under each rule (the sign
+    // too: r > 0).  A block scale that is a power of two has an exact
+    // reciprocal, and q0 is then the exact quotient.  Otherwise each weight
+    // whose q0 falls in the window is corrected, in a branch the wave takes
+    // only when one of its lanes needs it (with ws2 = fp32(1 / 448), weights
+    // and scales that share an odd factor put about 1 quotient in 150 on a
+    // tie).  Ties away from zero still need the window there: an exact
+    // quotient can sit on a midpoint, and only the window's branch marks the
+    // block for the midpoint test below.
+    const bool pow2 = (__float_as_uint(eff) & 0x7FFFFFu) == 0u;
+    uint32_t lim = RULE != kRuleAway && pow2 ? 0u : (7u << 11);
+    asm("" : "+v"(lim));   // one register compare per weight, not a scale test and a constant compare
+    near = false;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) q[k] = __fmul_rn(weight(k), ed.r);
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-      const float w = weight(k);
-      const float q0 = __fmul_rn(w, ed.r);
-      const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, ed.d, w), ed.r, q0);
-      const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, ed.d, w), ed.r, q1);
-      q[k] = __builtin_copysignf(q2, w);
+      // ((bits + 3) mod 2^21) << 11 in one instruction with inline operands
+      uint32_t dk;
+      asm("v_add_lshl_u32 %0, %1, 3, 11" : "=v"(dk) : "v"(__float_as_uint(q[k])));
+      if (__builtin_amdgcn_ballot_w64(dk < lim) != 0) {
+        asm volatile("" ::: "memory");   // keeps the branch (no speculation of its body)
+        // Markstein's correction, twice: q1 is faithful, q2 = RN(w / eff)
+        const float w = weight(k);
+        const float q0 = q[k];
+        const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, ed.d, w), ed.r, q0);
+        const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, ed.d, w), ed.r, q1);
+        q[k] = dk < lim ? __builtin_copysignf(q2, w) : q0;
+        near = true;
+      }
     }
   } else {
 #pragma unroll
@@ -319,7 +354,8 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
     w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 6], q[8 * hf + 7], 1.0f, 3);
     packed[hf] = w;
   }
-  if (RULE == kRuleAway) {
+  // ties (away from zero): only an exact quotient can sit on a midpoint
+  if (RULE == kRuleAway && near) {
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       const float a = fabsf(q[k]);
@@ -344,9 +380,10 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
   }
   uint32_t* c32 = reinterpret_cast<uint32_t*>(codes);
   if (pack_below > 0) {
-    const uint32_t b1 = (uint32_t)__shfl_down((int)sbyte, 1);
-    const uint32_t b2 = (uint32_t)__shfl_down((int)sbyte, 2);
-    const uint32_t b3 = (uint32_t)__shfl_down((int)sbyte, 3);
+    // lanes 1, 2, 3 of each quad to its lane 0 (DPP quad permutations)
+    const uint32_t b1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)sbyte, 0x55, 0xF, 0xF, false);
+    const uint32_t b2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)sbyte, 0xAA, 0xF, 0xF, false);
+    const uint32_t b3 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)sbyte, 0xFF, 0xF, 0xF, false);
     if (valid) {
       __builtin_nontemporal_store(packed[0], c32 + 2 * blk);
       __builtin_nontemporal_store(packed[1], c32 + 2 * blk + 1);

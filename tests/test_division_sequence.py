@@ -161,3 +161,57 @@ def test_rtn_element_quotient_hard_cases():
         naive_wrong += np.float32(np.float32(w) * np.float32(np.float32(1.0) / d)) != ref
     # the cases are hard: the plain product with the reciprocal misrounds some
     assert naive_wrong >= 2
+
+
+def product_window_flag(q0):
+    """The NVFP4 re-quantiser's test on a block's product quotients: a bit
+    pattern within 3 of a multiple of 2^21 (a value whose significand has at
+    most two fraction bits)."""
+    b = np.asarray(q0, np.float32).view(np.uint32).astype(np.uint64)
+    return ((b + 3) % (1 << 21)) < 7
+
+
+def test_rtn_product_quotient_window():
+    """Where the product quotient q0 = fp32(w fp32(1/d)) lies more than 3 float
+    steps from every value whose significand has at most two fraction bits,
+    its E2M1 code under each rule (nearest even, nearest away, toward zero)
+    is that of fp32(w / d).  Quotients are aimed at every rounding boundary
+    and grid point of E2M1 (0.25 .. 6) from both sides, with bf16 weights of
+    both signs and fp32 divisors over a wide exponent range; the window is
+    needed (some codes of q0 differ from the exact quotient's) and catches
+    every such case."""
+    from oracle import rtn
+    g = np.random.default_rng(29)
+    targets = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    n = 2_000_000
+    w = bf16((g.uniform(1.0, 2.0, n) * 2.0 ** g.integers(-30, 30, n)).astype(np.float32))
+    w = np.where(g.integers(0, 2, n) == 1, -w, w).astype(np.float32)
+    v = g.choice(targets, n) * (1.0 + g.integers(-12, 13, n) * 2.0 ** -24)
+    d = (np.abs(w).astype(np.float64) / v).astype(np.float32)
+    r = (np.float32(1.0) / d).astype(np.float32)
+    q0 = (w * r).astype(np.float32)
+    qx = (w / d).astype(np.float32)
+    flag = product_window_flag(q0)
+    differ = np.zeros(n, bool)
+    for rule in ("even", "away", "rtz"):
+        if rule == "rtz":
+            c0, cx = rtn.e2m1_round_rule(q0, rule), rtn.e2m1_round_rule(qx, rule)
+        else:
+            c0, cx = rtn.e2m1_round_magnitude(q0, rule), rtn.e2m1_round_magnitude(qx, rule)
+        differ |= c0 != cx
+    assert np.array_equal(np.signbit(q0), np.signbit(qx))
+    # the bound the window rests on: q0 within 3 float steps of fp32(w / d),
+    # here and over unaimed pairs (any divisor significand, quotients across
+    # many binades)
+    steps = np.abs(q0.view(np.uint32).astype(np.int64) - qx.view(np.uint32).astype(np.int64))
+    assert steps.max() <= 3
+    w2 = bf16((g.uniform(1.0, 2.0, n) * 2.0 ** g.integers(-20, 20, n)).astype(np.float32))
+    d2 = (g.uniform(1.0, 2.0, n) * 2.0 ** g.integers(-20, 20, n)).astype(np.float32)
+    q2 = (w2 * (np.float32(1.0) / d2).astype(np.float32)).astype(np.float32)
+    x2 = (w2 / d2).astype(np.float32)
+    assert np.abs(q2.view(np.uint32).astype(np.int64) - x2.view(np.uint32).astype(np.int64)).max() <= 3
+    assert differ.sum() > 100
+    assert not np.any(differ & ~flag), np.nonzero(differ & ~flag)[0][:5]
+    # on quotients spread evenly the window is rare
+    u = (g.uniform(0.0, 8.0, n)).astype(np.float32)
+    assert product_window_flag(u).mean() < 1e-5

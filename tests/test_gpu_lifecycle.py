@@ -370,6 +370,58 @@ def test_rtn_tiny_blocks_and_extreme_ws2(sq, ws2):
             assert got == rw or (np.isnan(got) and np.isnan(rw))
 
 
+@pytest.mark.parametrize("ws2", [float(np.float32(1 / 448)), 2.0 ** -9, 0.0123])
+def test_rtn_nv_quotients_on_change_points(sq, ws2):
+    """NVFP4 blocks whose quotients w / eff fall on, or within a few fp32 steps
+    of, the values where an E2M1 code changes (midpoints 0.25 .. 5, grid points
+    0.5 .. 6), both signs: blocks whose scale is a power of two (scale bytes
+    of mantissa 1.75 with ws2 = fp32(1/448), every byte of mantissa 1 with
+    ws2 = 2^-9), where the product with the reciprocal is exact and lands on
+    the midpoints themselves, and blocks of every other scale byte, where
+    bf16 weights next to V eff give quotients a few steps from V.  Codes and
+    scales under nearest even, nearest away and toward zero equal the
+    oracle's byte for byte."""
+    w2 = np.float32(ws2)
+    change = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    g = inputs.rng(4400)
+    O, I = 96, 512
+    G = I // 16
+    W = np.zeros((O, G, 16), np.float32)
+    pos = np.array([b for b in range(0x08, 0x7F) if 1e-30 < codec.E4M3_TABLE[b] * float(w2)])
+    for o in range(O):
+        for gb in range(G):
+            s = codec.E4M3_TABLE[g.choice(pos)]
+            eff = np.float32(s * float(w2))
+            # the block amax, 6 eff rounded to bf16, picks back s (or a neighbour)
+            blk = [bf16_round(6.0 * float(eff))]
+            for k in range(15):
+                v = change[g.integers(0, change.size)] * float(eff)
+                v *= 1.0 + g.integers(-4, 5) * 2.0 ** -9 if g.integers(0, 3) == 0 else 1.0
+                blk.append(bf16_round(v) * (1 if g.integers(0, 2) else -1))
+            W[o, gb] = np.array(blk, np.float32)[g.permutation(16)]
+    W = W.reshape(O, I)
+    Wb = torch.from_numpy(W).to(torch.bfloat16)
+    Wf = Wb.float().numpy()
+    ws2_in = float(w2)
+    print(f"[rtn change points] ws2={ws2_in}", flush=True)
+    for tie, tc in (("even", sq.TIE_EVEN), ("away", sq.TIE_AWAY)):
+        c, s_, _ = sq.rtn_quantize("nv", Wb.cuda(), tc, ws2_in)
+        torch.cuda.synchronize()
+        rc, rs, _ = rtn.quantize("nv", Wf, tie, ws2_in)
+        assert np.array_equal(s_.cpu().numpy(), rs)
+        bad = np.argwhere(c.cpu().numpy() != rc)
+        assert bad.size == 0, (tie, bad[:5])
+    c, s_, _ = sq.rtn_quantize_rule("nv", Wb.cuda(), "rtz", ws2_in, 0)
+    torch.cuda.synchronize()
+    rc, rs, _ = rtn.quantize_rule("nv", Wf, "rtz", ws2_in, 0)
+    assert np.array_equal(s_.cpu().numpy(), rs) and np.array_equal(c.cpu().numpy(), rc)
+
+
+def bf16_round(x):
+    """x rounded to bf16 (nearest even), as a float."""
+    return float(torch.tensor([x], dtype=torch.float32).to(torch.bfloat16).float()[0])
+
+
 def test_rtn_delta_zero_fixed_point(sq):
     O, I = 64, 256
     codes = inputs.codes_uniform(4100, O, I)
