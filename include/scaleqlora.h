@@ -95,8 +95,9 @@ typedef enum {
  * chip and the contraction accumulates in fp32 on the bf16 matrix cores; for
  * NVFP4 ws2 is applied once to the fp32 accumulator.  Results are
  * deterministic.  The order in which the fp32 sums of one 64-deep K stage are
- * taken depends on the path: MXFP4 with codes and scales 16-byte aligned and
- * I % 512 == 0 dequantises in registers (a lane takes 32 consecutive k), other
+ * taken depends on the path: MXFP4 with codes 16-byte and scales 8-byte
+ * aligned and I % 256 == 0 dequantises in registers (a lane takes 32
+ * consecutive k), other
  * calls dequantise through LDS, so the two can differ in the last bits.
  */
 int sq_fwd(int fmt, int64_t T, int64_t O, int64_t I,
@@ -214,8 +215,8 @@ int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream
  * exactly what the single-product entry point computes for it (sq_fwd,
  * sq_bwd_dx, sq_bwd_dscale), with the same accumulation order per output
  * element (the MXFP4 forward dequantises in registers when every expert's
- * codes and scales are 16-byte aligned and I % 512 == 0, as sq_fwd does for
- * one); the whole list runs in one launch per 64 experts.
+ * codes are 16-byte and scales 8-byte aligned and I % 256 == 0, as sq_fwd
+ * does for one); the whole list runs in one launch per 64 experts.
  *
  *   act     sq_fwd_grouped, sq_bwd_dscale_grouped: X_e bf16 [T_e, I];
  *           sq_bwd_dx_grouped: dY_e bf16 [T_e, O]  (16-byte aligned)

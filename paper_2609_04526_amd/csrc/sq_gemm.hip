@@ -771,13 +771,14 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
 
   // ---- kFwdC: the E8M0 scale bytes of the wave's code rows.  Lane (n, h) of
   // 32-row slice j uses row n0 + wn0 + 32 j + n, block 2 kt + h (the 32 codes
-  // of that block are the lane's half of stage kt).  One 16-byte load per
-  // slice brings the row's 16 blocks of 8 stages; the next 16 bytes are
+  // of that block are the lane's half of stage kt).  Two 8-byte loads per
+  // slice bring the row's 16 blocks of 8 stages; the next 16 bytes are
   // loaded during the last of those stages, into the same registers, once
   // that stage's scale operands have been taken.  The launcher takes this
-  // path only when G is a multiple of 16 (I % 512 == 0), so chunks never run
-  // past a row and the stage count is a multiple of 8.  A row outside the
-  // layer reads at an offset past the plane: zeros.
+  // path only when G is a multiple of 8 (I % 256 == 0), so every stage is
+  // whole and each 8-byte half starts 8-byte aligned; the last chunk of a row
+  // may run into the next row (bytes no stage uses).  A row outside the
+  // layer, and a half past the plane, read zeros.
   constexpr int kSc = MODE == kFwdC ? TN : 1;
   u32x4 scw[kSc];
   uint32_t sc0[kSc];
@@ -794,9 +795,13 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   auto load_sc = [&](int chunk) {
     if constexpr (MODE == kFwdC) {
 #pragma unroll
-      for (int j = 0; j < kSc; ++j)
-        scw[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                               rs_sc, (int)(sc0[j] + 16u * (uint32_t)chunk), 0, 0));
+      for (int j = 0; j < kSc; ++j) {
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const uint32_t off = sc0[j] + 16u * (uint32_t)chunk;
+        const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs_sc, (int)off, 0, 0));
+        const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs_sc, (int)(off + 8u), 0, 0));
+        scw[j] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      }
     }
   };
 
@@ -1423,13 +1428,15 @@ static int launch_sized(const GemmArgs& g, hipStream_t s) {
 }
 
 // The MXFP4 forward dequantises in registers (kFwdC) when every row's scales
-// split into 16-byte runs and the code and scale planes are 16-byte aligned;
+// split into 8-byte runs (G % 8 == 0), the code planes are 16-byte aligned
+// and the scale planes 8-byte aligned;
 // the grouped forward makes the same choice as the single one, so an
 // expert's output equals the single product's bit for bit.
 static bool regs_dequant_ok(int G, const ExpertProblem* p, int n) {
-  if (G % 16 != 0) return false;
+  if (G % 8 != 0) return false;
   for (int e = 0; e < n; ++e)
-    if (((reinterpret_cast<uintptr_t>(p[e].codes) | reinterpret_cast<uintptr_t>(p[e].scales)) & 15) != 0) return false;
+    if ((reinterpret_cast<uintptr_t>(p[e].codes) & 15) != 0 || (reinterpret_cast<uintptr_t>(p[e].scales) & 7) != 0)
+      return false;
   return true;
 }
 

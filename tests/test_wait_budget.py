@@ -177,7 +177,7 @@ def replay(mode, cfg, nk, wave):
             l[1] = True
 
     def load_sc(chunk):
-        w.issue(("sc", chunk), TN)
+        w.issue(("sc", chunk), 2 * TN)          # two 8-byte halves per row slice
 
     # prologue
     if nk > 0:
