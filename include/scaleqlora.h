@@ -216,7 +216,8 @@ int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream
  * sq_bwd_dx, sq_bwd_dscale), with the same accumulation order per output
  * element (the MXFP4 forward dequantises in registers when every expert's
  * codes are 16-byte and scales 8-byte aligned and I % 256 == 0, as sq_fwd
- * does for one); the whole list runs in one launch per 64 experts.
+ * does for one); the whole list runs in one launch per 128 experts (fewer
+ * when one kind of pointer of those experts spans 4 GiB or more).
  *
  *   act     sq_fwd_grouped, sq_bwd_dscale_grouped: X_e bf16 [T_e, I];
  *           sq_bwd_dx_grouped: dY_e bf16 [T_e, O]  (16-byte aligned)

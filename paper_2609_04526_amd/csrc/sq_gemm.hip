@@ -54,6 +54,7 @@
 #include <atomic>
 #include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "sq_device.h"
 #include "sq_launch.h"
@@ -95,20 +96,61 @@ struct GemmArgs {
 };
 
 // Up to kGroupMax experts per grouped launch, passed by value (kernel
-// arguments stay under 4 KiB).
+// arguments stay under 4 KiB): each kind of pointer is a base and a 32-bit
+// byte offset per expert, so the run of experts a launch takes is cut short
+// where the pointers of one kind would span 4 GiB or more.  The second
+// operand is dS's dY, or the forward's and dX's scale plane.  An operand an
+// expert does not have (null, read with a size of zero) gets offset 0.
 struct GemmGroup {
   GemmArgs base;                  // shared: O, I, G, N (fwd/dx) or M, N (ds), out_bf16
-  const uint16_t* a[kGroupMax];
-  const uint16_t* b[kGroupMax];
-  const uint8_t* codes[kGroupMax];
-  const uint8_t* scales[kGroupMax];
-  void* out[kGroupMax];
+  const uint8_t* a0;
+  const uint8_t* p0;
+  const uint8_t* codes0;
+  uint8_t* out0;
+  uint32_t a[kGroupMax];
+  uint32_t p[kGroupMax];
+  uint32_t codes[kGroupMax];
+  uint32_t out[kGroupMax];
   int T[kGroupMax];
   float ws2[kGroupMax];
   int tile_begin[kGroupMax];
   int count;
+  __device__ const uint16_t* act(int e) const { return reinterpret_cast<const uint16_t*>(a0 + a[e]); }
+  __device__ const uint8_t* second(int e) const { return p0 + p[e]; }
+  __device__ const uint8_t* code_plane(int e) const { return codes0 + codes[e]; }
+  __device__ void* output(int e) const { return out0 + out[e]; }
 };
 static_assert(sizeof(GemmGroup) <= 4096, "kernel argument budget");
+
+// Bases and offsets of experts p[0, n) (dS: the second operand is b, else
+// the scale plane); false when one kind's pointers span 4 GiB or more.
+static bool set_experts(GemmGroup& gg, const ExpertProblem* p, int n, bool ds) {
+  auto pack = [&](auto get, const uint8_t*& base, uint32_t* off) {
+    uintptr_t lo = UINTPTR_MAX, hi = 0;
+    for (int e = 0; e < n; ++e) {
+      const uintptr_t v = reinterpret_cast<uintptr_t>(get(p[e]));
+      if (v == 0) continue;
+      lo = v < lo ? v : lo;
+      hi = v > hi ? v : hi;
+    }
+    if (lo == UINTPTR_MAX) lo = hi = 0;
+    if (hi - lo > 0xFFFFFFFFu) return false;
+    base = reinterpret_cast<const uint8_t*>(lo);
+    for (int e = 0; e < n; ++e) {
+      const uintptr_t v = reinterpret_cast<uintptr_t>(get(p[e]));
+      off[e] = v == 0 ? 0u : (uint32_t)(v - lo);
+    }
+    return true;
+  };
+  const uint8_t* out0 = nullptr;
+  const bool ok = pack([](const ExpertProblem& x) { return x.a; }, gg.a0, gg.a) &&
+                  pack([ds](const ExpertProblem& x) { return ds ? x.b : static_cast<const void*>(x.scales); },
+                       gg.p0, gg.p) &&
+                  pack([](const ExpertProblem& x) { return x.codes; }, gg.codes0, gg.codes) &&
+                  pack([](const ExpertProblem& x) { return x.out; }, out0, gg.out);
+  gg.out0 = const_cast<uint8_t*>(out0);
+  return ok;
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -1114,11 +1156,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_grouped_kernel(GemmGroup 
   }
   const int e = lo;
   GemmArgs g = gg.base;
-  g.a = gg.a[e];
-  g.b = gg.b[e];
-  g.codes = gg.codes[e];
-  g.scales = gg.scales[e];
-  g.out = gg.out[e];
+  g.a = gg.act(e);
+  g.b = MODE == kDs ? reinterpret_cast<const uint16_t*>(gg.second(e)) : nullptr;
+  g.codes = gg.code_plane(e);
+  g.scales = MODE == kDs ? nullptr : gg.second(e);
+  g.out = gg.output(e);
   g.T = gg.T[e];
   g.ws2 = gg.ws2[e];
   if (MODE == kDs) g.K = g.T;
@@ -1199,8 +1241,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
   auto dma_tile = [&]() {
     locate(dpos, dt);
     const int T = gg.T[dt.e];
-    ra = make_dma_rsrc(gg.a[dt.e], (uint32_t)((size_t)T * I * 2));
-    rb = make_dma_rsrc(gg.b[dt.e], (uint32_t)((size_t)T * O * 2));
+    ra = make_dma_rsrc(gg.act(dt.e), (uint32_t)((size_t)T * I * 2));
+    rb = make_dma_rsrc(gg.second(dt.e), (uint32_t)((size_t)T * O * 2));
     dA.init(I, I, dt.m0, tid);
     dB.init(O, O, dt.n0, tid);
   };
@@ -1232,7 +1274,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
   locate(cpos, ct);
   u32x4 cw[TM * TN];
   auto tile_codes = [&]() {
-    ds_codes<FMT, TM, TN>(cw, gg.codes[ct.e], O, I, ct.m0 + wm0, ct.n0 + wn0, lane);
+    ds_codes<FMT, TM, TN>(cw, gg.code_plane(ct.e), O, I, ct.m0 + wm0, ct.n0 + wn0, lane);
   };
 
   f32x16 acc[TM][TN];
@@ -1297,7 +1339,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
       ++ckt;
       return true;
     }
-    float* const dS = reinterpret_cast<float*>(gg.out[ct.e]);
+    float* const dS = reinterpret_cast<float*>(gg.output(ct.e));
     if (ct.m0 + BM <= I && ct.n0 + BN <= O)
       ds_store<FMT, TM, TN, true>(acc, cw, dS, O, I, G, ct.m0 + wm0, ct.n0 + wn0, lane);
     else
@@ -1482,11 +1524,6 @@ static int launch_grouped(GemmGroup& gg, const ExpertProblem* p, int n, hipStrea
   for (int e = 0; e < n; ++e) {
     const int M = MODE == kDs ? gg.base.M : p[e].T;
     const int tiles = ((M + BM - 1) / BM) * ((gg.base.N + BN - 1) / BN);
-    gg.a[e] = static_cast<const uint16_t*>(p[e].a);
-    gg.b[e] = static_cast<const uint16_t*>(p[e].b);
-    gg.codes[e] = p[e].codes;
-    gg.scales[e] = p[e].scales;
-    gg.out[e] = p[e].out;
     gg.T[e] = p[e].T;
     gg.ws2[e] = FMT == kNV ? p[e].ws2 : 1.0f;
     gg.tile_begin[e] = blocks;
@@ -1508,11 +1545,6 @@ static int launch_ds_stream(GemmGroup& gg, const ExpertProblem* p, int n, hipStr
   static_assert(2 * L::kBytes <= 160 * 1024, "two workgroups per CU");
   gg.count = n;
   for (int e = 0; e < n; ++e) {
-    gg.a[e] = static_cast<const uint16_t*>(p[e].a);
-    gg.b[e] = static_cast<const uint16_t*>(p[e].b);
-    gg.codes[e] = p[e].codes;
-    gg.scales[e] = nullptr;
-    gg.out[e] = p[e].out;
     gg.T[e] = p[e].T;
     gg.ws2[e] = 1.0f;
     gg.tile_begin[e] = 0;
@@ -1566,20 +1598,48 @@ static int run_grouped(int fmt, int O, int I, int n, const ExpertProblem* p, int
   if (MODE == kFwdR) { gg.base.N = O; gg.base.K = I; }
   else if (MODE == kDx) { gg.base.N = I; gg.base.K = O; }
   else { gg.base.M = I; gg.base.N = O; }
-  for (int e0 = 0; e0 < n; e0 += kGroupMax) {
-    const int m = n - e0 < kGroupMax ? n - e0 : kGroupMax;
+  // Launch sets: from the first expert not yet launched, every later one
+  // whose pointers keep each kind's span under 4 GiB, up to kGroupMax (the
+  // experts of a stacked tensor, or of one allocator pool, share a set; an
+  // expert's results do not depend on the set it runs in).
+  const bool regs = MODE == kFwdR && fmt == kMX && regs_dequant_ok(gg.base.G, p, n);
+  std::vector<uint8_t> done((size_t)n, 0);
+  ExpertProblem set[kGroupMax];
+  for (int first = 0; first < n;) {
+    uintptr_t lo[4], hi[4];
+    for (int k = 0; k < 4; ++k) { lo[k] = UINTPTR_MAX; hi[k] = 0; }
+    int m = 0;
+    for (int e = first; e < n && m < kGroupMax; ++e) {
+      if (done[(size_t)e]) continue;
+      const void* ptr[4] = {p[e].a, MODE == kDs ? p[e].b : static_cast<const void*>(p[e].scales), p[e].codes,
+                            p[e].out};
+      uintptr_t nlo[4], nhi[4];
+      bool fits = true;
+      for (int k = 0; k < 4; ++k) {
+        const uintptr_t v = reinterpret_cast<uintptr_t>(ptr[k]);
+        nlo[k] = v != 0 && v < lo[k] ? v : lo[k];
+        nhi[k] = v != 0 && v > hi[k] ? v : hi[k];
+        fits = fits && (nlo[k] == UINTPTR_MAX || nhi[k] - nlo[k] <= 0xFFFFFFFFu);
+      }
+      if (!fits) continue;
+      for (int k = 0; k < 4; ++k) { lo[k] = nlo[k]; hi[k] = nhi[k]; }
+      set[m++] = p[e];
+      done[(size_t)e] = 1;
+    }
+    while (first < n && done[(size_t)first]) ++first;
+    if (!set_experts(gg, set, m, MODE == kDs)) return -1;     // cannot happen: the set was chosen to fit
     int rc;
-    if (MODE == kFwdR && fmt == kMX && regs_dequant_ok(gg.base.G, p + e0, m))
-      rc = grouped_sized<kFwdC, kMX, SQ_CFG_FWDC>(gg, p + e0, m, s);
+    if (regs)
+      rc = grouped_sized<kFwdC, kMX, SQ_CFG_FWDC>(gg, set, m, s);
     else if (MODE == kFwdR)
-      rc = fmt == kMX ? grouped_sized<kFwdR, kMX, SQ_CFG_FWD>(gg, p + e0, m, s)
-                      : grouped_sized<kFwdR, kNV, SQ_CFG_FWD>(gg, p + e0, m, s);
+      rc = fmt == kMX ? grouped_sized<kFwdR, kMX, SQ_CFG_FWD>(gg, set, m, s)
+                      : grouped_sized<kFwdR, kNV, SQ_CFG_FWD>(gg, set, m, s);
     else if (MODE == kDx)
-      rc = fmt == kMX ? grouped_sized<kDx, kMX, SQ_CFG_DX>(gg, p + e0, m, s)
-                      : grouped_sized<kDx, kNV, SQ_CFG_DX>(gg, p + e0, m, s);
+      rc = fmt == kMX ? grouped_sized<kDx, kMX, SQ_CFG_DX>(gg, set, m, s)
+                      : grouped_sized<kDx, kNV, SQ_CFG_DX>(gg, set, m, s);
     else
-      rc = fmt == kMX ? grouped_sized<kDs, kMX, SQ_CFG_DS>(gg, p + e0, m, s)
-                      : grouped_sized<kDs, kNV, SQ_CFG_DS>(gg, p + e0, m, s);
+      rc = fmt == kMX ? grouped_sized<kDs, kMX, SQ_CFG_DS>(gg, set, m, s)
+                      : grouped_sized<kDs, kNV, SQ_CFG_DS>(gg, set, m, s);
     if (rc != 0) return rc;
   }
   return 0;

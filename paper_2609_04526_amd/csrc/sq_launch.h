@@ -69,7 +69,7 @@ int merge_launch(const MergeBatch& b, hipStream_t s);
 // Grouped products over MoE experts that share O and I: each expert has its
 // own tokens (T >= 0), activations, weights and output.  Up to kGroupMax
 // experts per launch; the caller splits longer lists.
-constexpr int kGroupMax = 64;
+constexpr int kGroupMax = 128;
 struct ExpertProblem {
   const void* a;            // fwd, ds: X [T, I]; dx: dY [T, O]
   const void* b;            // ds: dY [T, O]

@@ -117,10 +117,10 @@ def test_grouped_products_match_oracle_and_single(sq, fmt):
 
 
 def test_more_experts_than_one_launch_holds(sq):
-    """70 experts (two launches of at most 64), bf16 outputs; under 96 tokens
-    per expert on average, so dX takes the 64-token tiles."""
+    """150 experts (two launches of at most 128), bf16 outputs; under 96
+    tokens per expert on average, so dX takes the 64-token tiles."""
     O, I = 64, 128
-    Ts = [(13 * e) % 97 for e in range(70)]
+    Ts = [(13 * e) % 97 for e in range(150)]
     codes, scales, ws2 = experts("mx", len(Ts), O, I, 7300)
     Xs = [inputs.bf16_normal(7400 + e, (T, I)) for e, T in enumerate(Ts)]
     dYs = [inputs.bf16_normal(7500 + e, (T, O)) for e, T in enumerate(Ts)]
@@ -143,6 +143,45 @@ def test_more_experts_than_one_launch_holds(sq):
         dx1 = sq.sq_bwd_dx("mx", dYd[e], cd[e], sd[e])
         torch.cuda.synchronize()
         assert torch.equal(dx1, dXs[e])
+
+
+def test_experts_spread_over_more_than_4_gib(sq):
+    """Expert activations and output gradients placed 4.5 GiB apart in one
+    buffer: a launch's 32-bit offsets from one base cannot reach both, so the
+    launch takes fewer experts.  Grouped products equal the single ones bit
+    for bit and the oracle within the bar."""
+    O, I, Ts = 64, 512, [40, 72, 16]
+    codes, scales, _ = experts("mx", 3, O, I, 7700)
+    cd, sd = cuda(codes), cuda(scales)
+    far = 9 << 29                                            # 4.5 GiB in bytes
+    places = [0, far, 1 << 25]                               # X_e at these byte offsets, dY_e 16 MiB after
+    big = torch.empty((far + (1 << 26)) // 2, dtype=torch.bfloat16, device="cuda")
+    Xs = [inputs.bf16_normal(7710 + e, (T, I)) for e, T in enumerate(Ts)]
+    dYs = [inputs.bf16_normal(7720 + e, (T, O)) for e, T in enumerate(Ts)]
+    Xd, dYd = [], []
+    for e, T in enumerate(Ts):
+        x0, d0 = places[e] // 2, (places[e] + (1 << 24)) // 2
+        Xd.append(big[x0:x0 + T * I].view(T, I))
+        dYd.append(big[d0:d0 + T * O].view(T, O))
+        Xd[e].copy_(Xs[e].cuda())
+        dYd[e].copy_(dYs[e].cuda())
+    print("[moe spread] experts 4.5 GiB apart", flush=True)
+    Ys = sq.sq_fwd_grouped("mx", Xd, cd, sd)
+    dXs = sq.sq_bwd_dx_grouped("mx", dYd, cd, sd)
+    dSs = sq.sq_bwd_dscale_grouped("mx", Xd, dYd, cd)
+    torch.cuda.synchronize()
+    for e in range(3):
+        y1 = sq.sq_fwd("mx", Xd[e], cd[e], sd[e])
+        dx1 = sq.sq_bwd_dx("mx", dYd[e], cd[e], sd[e])
+        torch.cuda.synchronize()
+        assert torch.equal(y1, Ys[e]) and torch.equal(dx1, dXs[e])
+        assert single_dscale_equal(sq, "mx", Xd[e], dYd[e], cd[e], dSs[e])
+        W = linear.dequant("mx", codes[e], scales[e])
+        assert normwise(Ys[e].float().cpu().numpy(), linear.forward(Xs[e].float().numpy(), W)) <= TOL
+        dS_ref = linear.backward_dscale("mx", Xs[e].float().numpy(), dYs[e].float().numpy(), codes[e])
+        assert normwise(dSs[e].cpu().numpy(), dS_ref) <= TOL
+    del big, Xd, dYd
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("fmt", ["mx", "nv"])
