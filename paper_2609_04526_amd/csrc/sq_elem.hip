@@ -282,16 +282,43 @@ __global__ __launch_bounds__(256) void rtn_kernel(RtnBatch batch_arg) {
   }
 }
 
-__global__ void rtn_amax_init(float* slot) { *reinterpret_cast<uint32_t*>(slot) = 0u; }
+// Tensor amax passes of up to kRtnPerLaunch weights per launch: the slots
+// are zeroed, every weight's workgroups fold their maxima into its slot, and
+// the slots are finished (ws2 from the amax, or a given value stored).
+struct AmaxBatch {
+  const uint16_t* w[kRtnPerLaunch];
+  float* slot[kRtnPerLaunch];
+  int64_t n_chunks[kRtnPerLaunch];
+  int32_t wg_begin[kRtnPerLaunch + 1];   // workgroups [wg_begin[p], wg_begin[p + 1]) take weight p
+  float val[kRtnPerLaunch];              // finishing: 0 = ws2 from the amax, else the value stored
+  int32_t count;
+};
+static_assert(sizeof(AmaxBatch) <= 4096, "kernel arguments are limited to 4 KiB");
 
-// Tensor amax (as bf16 bits) for the recomputed ws2: 4 loads in flight per
-// lane, one integer atomicMax per workgroup (a max of bit patterns is
-// order-independent, so the result is deterministic).
-__global__ __launch_bounds__(256) void rtn_amax(const uint16_t* __restrict__ W, int64_t n_chunks, float* slot) {
+__global__ __launch_bounds__(64) void rtn_slots_zero(AmaxBatch b) {
+  if ((int)threadIdx.x < b.count) *reinterpret_cast<uint32_t*>(b.slot[threadIdx.x]) = 0u;
+}
+
+// Tensor amax (as bf16 bits, in an fp32 slot) of each weight: 4 loads in
+// flight per lane, one integer atomicMax per workgroup (a max of bit patterns
+// is order-independent, so the result is deterministic).
+__global__ __launch_bounds__(256) void rtn_amax(AmaxBatch batch_arg) {
+  (void)batch_arg;
+  const __attribute__((address_space(4))) AmaxBatch& b =
+      *(const __attribute__((address_space(4))) AmaxBatch*)__builtin_amdgcn_kernarg_segment_ptr();
+  const int wg = (int)blockIdx.x;
+  int lo = 0, hi = b.count - 1;                 // the weight whose workgroups hold wg
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (b.wg_begin[mid] <= wg) lo = mid;
+    else hi = mid - 1;
+  }
+  const uint16_t* __restrict__ W = b.w[lo];
+  const int64_t n_chunks = b.n_chunks[lo];
   __shared__ uint32_t red[4];
   uint32_t am = 0;
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t stride = (int64_t)(b.wg_begin[lo + 1] - b.wg_begin[lo]) * 256;
+  int64_t c = (int64_t)(wg - b.wg_begin[lo]) * 256 + threadIdx.x;
   for (; c + 3 * stride < n_chunks; c += 4 * stride) {
     uint4 v[4];
 #pragma unroll
@@ -314,17 +341,25 @@ __global__ __launch_bounds__(256) void rtn_amax(const uint16_t* __restrict__ W, 
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = am;
   __syncthreads();
   if (threadIdx.x == 0)
-    atomicMax(reinterpret_cast<unsigned int*>(slot), max(max(red[0], red[1]), max(red[2], red[3])) << 16);
+    atomicMax(reinterpret_cast<unsigned int*>(b.slot[lo]), max(max(red[0], red[1]), max(red[2], red[3])) << 16);
 }
 
-__global__ void rtn_ws2_store(float* slot, float v) { *slot = v; }
-
-__global__ void rtn_ws2_finalize(float* slot) {
-  const float amax = *slot;
-  float ws2 = __fdiv_rn(__fdiv_rn(amax, 6.0f), 448.0f);
+// ws2 = amax / 6 / 448 (1 for an all-zero weight) in place of the amax, or
+// the given value
+__global__ __launch_bounds__(64) void rtn_slots_finish(AmaxBatch b) {
+  const int k = (int)threadIdx.x;
+  if (k >= b.count) return;
+  float* slot = b.slot[k];
+  if (b.val[k] != 0.0f) {
+    *slot = b.val[k];
+    return;
+  }
+  float ws2 = __fdiv_rn(__fdiv_rn(*slot, 6.0f), 448.0f);
   if (ws2 == 0.0f) ws2 = 1.0f;
   *slot = ws2;
 }
+
+__global__ void rtn_ws2_store(float* slot, float v) { *slot = v; }
 
 namespace {
 template <int FMT, int RULE>
@@ -346,29 +381,77 @@ int rtn_batch_rule(int rule, const RtnBatch& b, hipStream_t s) {
   }
 }
 
-// The tensor amax (as the bits of an fp32 holding a bf16 value) into *slot.
-void tensor_amax(const uint16_t* w, int64_t n_chunks, float* slot, hipStream_t s) {
-  hipLaunchKernelGGL(rtn_amax_init, dim3(1), dim3(1), 0, s, slot);
-  const int64_t want = (n_chunks + 1023) / 1024;
-  const unsigned grid = (unsigned)(want < 1024 ? (want > 0 ? want : 1) : 1024);
-  hipLaunchKernelGGL(rtn_amax, dim3(grid), dim3(256), 0, s, w, n_chunks, slot);
-}
+// Amax passes over the weights that need one, kRtnPerLaunch per launch set:
+// zero the slots, fold each weight's amax into its slot, then (finish) turn
+// the slots into ws2 or store the given values.
+class AmaxPasses {
+ public:
+  AmaxPasses(bool finish, hipStream_t s) : finish_(finish), s_(s) {}
+  int add(const uint16_t* w, int64_t n_chunks, float* slot, float val) {
+    const int p = b_.count++;
+    b_.w[p] = w;
+    b_.slot[p] = slot;
+    b_.n_chunks[p] = n_chunks;
+    b_.val[p] = val;
+    b_.wg_begin[p] = wgs_;
+    const int64_t want = (n_chunks + 1023) / 1024;
+    wgs_ += (int32_t)(want < 1024 ? (want > 0 ? want : 1) : 1024);
+    b_.wg_begin[p + 1] = wgs_;
+    return b_.count == kRtnPerLaunch ? flush() : 0;
+  }
+  int flush() {
+    if (b_.count == 0) return 0;
+    hipLaunchKernelGGL(rtn_slots_zero, dim3(1), dim3(64), 0, s_, b_);
+    hipLaunchKernelGGL(rtn_amax, dim3((unsigned)wgs_), dim3(256), 0, s_, b_);
+    if (finish_) hipLaunchKernelGGL(rtn_slots_finish, dim3(1), dim3(64), 0, s_, b_);
+    b_ = AmaxBatch{};
+    wgs_ = 0;
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+  }
+
+ private:
+  AmaxBatch b_{};
+  int32_t wgs_ = 0;
+  bool finish_;
+  hipStream_t s_;
+};
+
+// Slots finished after the codes are written (whole-tensor rule), kRtnPerLaunch per launch.
+class SlotFinish {
+ public:
+  explicit SlotFinish(hipStream_t s) : s_(s) {}
+  int add(float* slot, float val) {
+    const int p = b_.count++;
+    b_.slot[p] = slot;
+    b_.val[p] = val;
+    return b_.count == kRtnPerLaunch ? flush() : 0;
+  }
+  int flush() {
+    if (b_.count == 0) return 0;
+    hipLaunchKernelGGL(rtn_slots_finish, dim3(1), dim3(64), 0, s_, b_);
+    b_ = AmaxBatch{};
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+  }
+
+ private:
+  AmaxBatch b_{};
+  hipStream_t s_;
+};
 }  // namespace
 
 int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream_t s) {
   const bool nv = fmt == kNV;
   // pre-passes: the tensor amax of every weight that needs one (whole-tensor
-  // rule, or a recomputed NVFP4 ws2), each into its own ws2_out slot
-  for (int k = 0; k < n; ++k) {
-    const RtnItem& it = items[k];
-    const int64_t n_chunks = it.O * it.I / 8;
-    const uint16_t* w = static_cast<const uint16_t*>(it.W);
-    if (rule == kRuleWholeTensor) {
-      tensor_amax(w, n_chunks, it.ws2_out, s);            // ws2_out holds the amax while the codes are written
-    } else if (nv && !(it.ws2_in > 0.0f)) {
-      tensor_amax(w, n_chunks, it.ws2_out, s);
-      hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, it.ws2_out);
+  // rule: ws2_out holds the amax while the codes are written; a recomputed
+  // NVFP4 ws2: ws2_out receives the ws2), each into its own ws2_out slot
+  {
+    AmaxPasses pre(rule != kRuleWholeTensor, s);
+    for (int k = 0; k < n; ++k) {
+      const RtnItem& it = items[k];
+      if (rule == kRuleWholeTensor || (nv && !(it.ws2_in > 0.0f)))
+        if (pre.add(static_cast<const uint16_t*>(it.W), it.O * it.I / 8, it.ws2_out, 0.0f) != 0) return -1;
     }
+    if (pre.flush() != 0) return -1;
   }
   RtnBatch batch{};
   int64_t spans = 0;
@@ -415,11 +498,12 @@ int rtn_grouped_launch(int fmt, int rule, int n, const RtnItem* items, hipStream
   if (rule == kRuleWholeTensor) {
     // then the ws2 used: recomputed from the amax (NVFP4 without ws2_in), else
     // ws2_in (NVFP4) or 1 (MXFP4)
+    SlotFinish post(s);
     for (int k = 0; k < n; ++k) {
       const RtnItem& it = items[k];
-      if (nv && !(it.ws2_in > 0.0f)) hipLaunchKernelGGL(rtn_ws2_finalize, dim3(1), dim3(1), 0, s, it.ws2_out);
-      else hipLaunchKernelGGL(rtn_ws2_store, dim3(1), dim3(1), 0, s, it.ws2_out, nv ? it.ws2_in : 1.0f);
+      if (post.add(it.ws2_out, nv && !(it.ws2_in > 0.0f) ? 0.0f : (nv ? it.ws2_in : 1.0f)) != 0) return -1;
     }
+    if (post.flush() != 0) return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
