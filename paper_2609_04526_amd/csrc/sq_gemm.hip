@@ -1564,6 +1564,11 @@ static int launch_ds_stream(GemmGroup& gg, const ExpertProblem* p, int n, hipStr
 // (at 64 tokens 184 -> 117 us; at 256, 72 -> 82 us, where 128 x 128 wins).
 #define SQ_CFG_GROUPED_FWDC 64, 256, 1, 8, 4, 64
 #define SQ_CFG_GROUPED_THIN 64, 256, 1, 8, 2, 64
+// Experts of at least 2048 tokens whose 256 x 256 tiles would not fill the
+// chip (the 8B step's k and v projections, 1024 x 4096 at 4096 tokens, as
+// one grouped forward) take 128 x 256 tiles, 8 waves of 64 x 64, four stages:
+// 77.3 -> 75.9 us for the pair.
+#define SQ_CFG_GROUPED_FWDC_LONG 128, 256, 2, 4, 4, 64
 
 // The large tile when the experts' tiles fill the chip and an expert averages
 // at least 512 tokens (rows of the forward and dX, the contraction of dS:
@@ -1579,7 +1584,10 @@ static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream
   }
   const bool large = big >= kCUs && tokens >= (int64_t)512 * n;
   if (large) return launch_grouped<MODE, FMT, BM, BN, REST...>(gg, p, n, s);
-  if constexpr (MODE == kFwdC) return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_FWDC>(gg, p, n, s);
+  if constexpr (MODE == kFwdC) {
+    if (tokens >= (int64_t)2048 * n) return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_FWDC_LONG>(gg, p, n, s);
+    return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_FWDC>(gg, p, n, s);
+  }
   else if constexpr (MODE == kDs) return launch_ds_stream<FMT, SQ_CFG_DS_STREAM>(gg, p, n, s);
   else if constexpr (MODE == kDx) {
     if (tokens <= (int64_t)96 * n) return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_THIN>(gg, p, n, s);

@@ -145,6 +145,33 @@ def test_more_experts_than_one_launch_holds(sq):
         assert torch.equal(dx1, dXs[e])
 
 
+@pytest.mark.parametrize("Ts", [[4096, 4096], [2048, 3000, 2500]])
+def test_long_experts_grouped_forward(sq, Ts):
+    """Experts of 2048 tokens and more whose 256 x 256 tiles would not fill
+    the chip (the 8B step's k and v projections, 1024 x 4096, as one grouped
+    forward; and a ragged set): the grouped forward takes 128 x 256 tiles and
+    equals each single forward bit for bit; sampled rows against the oracle
+    within the element bound."""
+    O, I = 1024, 4096
+    codes, scales, _ = experts("mx", len(Ts), O, I, 7800)
+    cd, sd = cuda(codes), cuda(scales)
+    Xs = [inputs.bf16_normal(7810 + e, (T, I)) for e, T in enumerate(Ts)]
+    Xd = [x.cuda() for x in Xs]
+    print(f"[moe long] Ts={Ts}", flush=True)
+    Ys = sq.sq_fwd_grouped("mx", Xd, cd, sd)
+    torch.cuda.synchronize()
+    g = inputs.rng(7820)
+    for e, T in enumerate(Ts):
+        y1 = sq.sq_fwd("mx", Xd[e], cd[e], sd[e])
+        torch.cuda.synchronize()
+        assert torch.equal(y1, Ys[e])
+        rows = np.sort(np.concatenate([g.choice(T, 7, replace=False), [T - 1]]))
+        W = linear.dequant("mx", codes[e], scales[e])
+        Xr = Xs[e].float().numpy()[rows]
+        check_elements("mx", Xr, np.zeros((rows.size, O), np.float32), codes[e], W,
+                       Y=Ys[e].float().cpu().numpy()[rows], what=f"expert {e}")
+
+
 def test_experts_spread_over_more_than_4_gib(sq):
     """Expert activations and output gradients placed 4.5 GiB apart in one
     buffer: a launch's 32-bit offsets from one base cannot reach both, so the

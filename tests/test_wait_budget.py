@@ -60,7 +60,8 @@ def configs():
 # Tile configurations each late-schedule product can run with (single and
 # grouped launches, the small tile, the two half tiles of a split grid).
 LATE = {
-    "fwdc": ["SQ_CFG_FWDC", "SQ_CFG_SMALL_FWDC", "SQ_CFG_HALF_N_FWDC", "SQ_CFG_HALF_M", "SQ_CFG_GROUPED_FWDC"],
+    "fwdc": ["SQ_CFG_FWDC", "SQ_CFG_SMALL_FWDC", "SQ_CFG_HALF_N_FWDC", "SQ_CFG_HALF_M", "SQ_CFG_GROUPED_FWDC",
+             "SQ_CFG_GROUPED_FWDC_LONG"],
     "dx": ["SQ_CFG_DX", "SQ_CFG_SMALL", "SQ_CFG_HALF_N", "SQ_CFG_HALF_M", "SQ_CFG_GROUPED_THIN"],
     "ds": ["SQ_CFG_DS", "SQ_CFG_SMALL", "SQ_CFG_HALF_N_DS", "SQ_CFG_HALF_M_DS"],
 }
