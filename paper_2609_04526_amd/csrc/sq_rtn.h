@@ -66,6 +66,20 @@ __device__ __forceinline__ float e2m1_mag(uint32_t m) {
   return (float)((0xC8643210u >> (4u * m)) & 0xFu) * 0.5f;
 }
 
+// E2M1 code of q rounded toward zero (magnitude index of the largest grid
+// value at or below min(|q|, 6), and the sign bit of q), from q's bits: bits
+// 22..30 hold the exponent and the first fraction bit, b = 254 + 2e + f1 for
+// |q| = (1.f1...) 2^e, so |q| in [1, 8) has index b - 252 (1 -> 2, 1.5 -> 3,
+// 2 -> 4, 3 -> 5, 4 -> 6, 6 -> 7); larger magnitudes, infinity included, stop
+// at 7, [0.5, 1) (b = 252 or 253) has index 1 and smaller magnitudes 0.  A
+// NaN q gives 7 and is fixed up by the caller.
+__device__ __forceinline__ uint32_t e2m1_rtz_code(float q) {
+  const uint32_t u = __float_as_uint(q);
+  const int b = (int)((u >> 22) & 0x1FFu);
+  const int m = min(max(b - 252, 0), 7) | (b == 252 ? 1 : 0);
+  return (uint32_t)m | ((u >> 28) & 8u);
+}
+
 // Rounding rules of the re-quantiser.  The nearest rules and round-toward-zero
 // and stochastic rounding keep the per-block scale; the whole-tensor rule
 // takes one scale from the tensor amax (the deploy-side quantisers of the
@@ -187,10 +201,15 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
   // the convert writes its two codes into byte p of its first operand and
   // keeps the other bytes, so four of them build the word
   uint32_t packed = 0;
-  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[0], q[1], 1.0f, 0);
-  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[2], q[3], 1.0f, 1);
-  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[4], q[5], 1.0f, 2);
-  packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[6], q[7], 1.0f, 3);
+  if (RULE == kRuleRtz) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) packed |= e2m1_rtz_code(q[k]) << (4 * k);
+  } else {
+    packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[0], q[1], 1.0f, 0);
+    packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[2], q[3], 1.0f, 1);
+    packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[4], q[5], 1.0f, 2);
+    packed = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(packed, q[6], q[7], 1.0f, 3);
+  }
   if (RULE == kRuleAway) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {                           // a tie magnitude is below 6: no carry
@@ -198,7 +217,7 @@ __device__ __forceinline__ void rtn_chunk(const uint4 v, int64_t c, bool valid, 
       packed += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * k)) : 0u;
     }
   }
-  if (RULE == kRuleRtz || RULE == kRuleStochastic) {
+  if (RULE == kRuleStochastic) {
     // The nearest magnitude is the truncated one or the one above it: step
     // down where it lies above min(|q|, 6).  Stochastic rounding then goes up
     // from the truncated magnitude lo iff u * gap < a - m(lo), which is
@@ -296,9 +315,10 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
   ed.fast = eff >= 0x1p-64f && eff <= 0x1p64f;
   auto weight = [&](int k) { return __uint_as_float(((h[k >> 1] >> (16 * (k & 1))) & 0xFFFFu) << 16); };
   float q[16];
-  // near: some code of the block may depend on more than the product w r
-  // (always true off the fast path, where q holds the exact quotients)
-  bool near = true;
+  // fast: codes from the products (below); tie: ties away from zero found
+  // there, one per code nibble
+  bool fast = false;
+  uint32_t tie[2] = {0u, 0u};
   if (NVFAST == 1 && eff != 0.0f && amax <= __fmul_rn(eff, 0x1p100f)) {
     // q0 = RN(w r) with r = RN(1 / eff) is w / eff (1 + e1)(1 + e2), |e1|, |e2|
     // <= 2^-24, so q0 and RN(w / eff) lie within 3 float steps of each other
@@ -315,13 +335,13 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
     // whose q0 falls in the window is corrected, in a branch the wave takes
     // only when one of its lanes needs it (with ws2 = fp32(1 / 448), weights
     // and scales that share an odd factor put about 1 quotient in 150 on a
-    // tie).  Ties away from zero still need the window there: an exact
-    // quotient can sit on a midpoint, and only the window's branch marks the
-    // block for the midpoint test below.
+    // tie).  Ties away from zero keep the window there too: an exact quotient
+    // can sit on a midpoint, and a midpoint lies in the window, so the
+    // midpoint test runs in the window's branch only.
     const bool pow2 = (__float_as_uint(eff) & 0x7FFFFFu) == 0u;
     uint32_t lim = RULE != kRuleAway && pow2 ? 0u : (7u << 11);
     asm("" : "+v"(lim));   // one register compare per weight, not a scale test and a constant compare
-    near = false;
+    fast = true;
 #pragma unroll
     for (int k = 0; k < 16; ++k) q[k] = __fmul_rn(weight(k), ed.r);
 #pragma unroll
@@ -337,7 +357,10 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
         const float q1 = __builtin_fmaf(__builtin_fmaf(-q0, ed.d, w), ed.r, q0);
         const float q2 = __builtin_fmaf(__builtin_fmaf(-q1, ed.d, w), ed.r, q1);
         q[k] = dk < lim ? __builtin_copysignf(q2, w) : q0;
-        near = true;
+        if (RULE == kRuleAway) {
+          const float a = fabsf(q[k]);
+          tie[k >> 3] |= (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * (k & 7))) : 0u;
+        }
       }
     }
   } else {
@@ -348,26 +371,29 @@ __device__ __forceinline__ void rtn_block16_nv(const uint4 lo, const uint4 hi, i
 #pragma unroll
   for (int hf = 0; hf < 2; ++hf) {                // byte-selected converts, as in rtn_chunk
     uint32_t w = 0;
-    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 0], q[8 * hf + 1], 1.0f, 0);
-    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 2], q[8 * hf + 3], 1.0f, 1);
-    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 4], q[8 * hf + 5], 1.0f, 2);
-    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 6], q[8 * hf + 7], 1.0f, 3);
+    if (RULE == kRuleRtz) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) w |= e2m1_rtz_code(q[8 * hf + k]) << (4 * k);
+    } else {
+      w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 0], q[8 * hf + 1], 1.0f, 0);
+      w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 2], q[8 * hf + 3], 1.0f, 1);
+      w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 4], q[8 * hf + 5], 1.0f, 2);
+      w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, q[8 * hf + 6], q[8 * hf + 7], 1.0f, 3);
+    }
     packed[hf] = w;
   }
-  // ties (away from zero): only an exact quotient can sit on a midpoint
-  if (RULE == kRuleAway && near) {
+  // ties away from zero take the next magnitude (a tie magnitude is below 6:
+  // no carry out of the nibble)
+  if (RULE == kRuleAway) {
+    if (fast) {
+      packed[0] += tie[0];
+      packed[1] += tie[1];
+    } else {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const float a = fabsf(q[k]);
-      packed[k >> 3] += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * (k & 7))) : 0u;
-    }
-  }
-  if (RULE == kRuleRtz) {
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const float a = fminf(fabsf(q[k]), 6.0f);
-      const uint32_t m = (packed[k >> 3] >> (4 * (k & 7))) & 7u;
-      packed[k >> 3] -= (e2m1_mag(m) > a) ? (1u << (4 * (k & 7))) : 0u;
+      for (int k = 0; k < 16; ++k) {
+        const float a = fabsf(q[k]);
+        packed[k >> 3] += (a == 0.25f || a == 1.25f || a == 2.5f || a == 5.0f) ? (1u << (4 * (k & 7))) : 0u;
+      }
     }
   }
   if (am > 0x7F80u || eff == 0.0f) {
