@@ -665,6 +665,8 @@ def model_moe(sq, steps=3, warmup=1):
     one grouped dX and one grouped dS, all 128 experts in each launch.  Every
     layer has its own expert weights; the routed activations and output
     buffers are shared across layers (values do not change the timing).  The
+    fused variant stacks gate and up into one weight per expert (6 grouped
+    products per layer, the pair's dX summed in one contraction).  The
     QAST variant adds the batched rank-32 scale step of all experts per linear
     (sq_qast_scales_batched before the forward, sq_qast_factor_grads_batched
     after dS).  The QAT-LoRA variant is the weight-space comparator on the
@@ -729,6 +731,37 @@ def model_moe(sq, steps=3, warmup=1):
     ms = timed(run)
     rows = sum(Ts)
     flops = 6.0 * rows * L * sum(o * i for (_, o, i) in shapes)
+
+    # the same stack with gate and up stacked into one [1536, 2048] weight per
+    # expert (the fused-projection layout): one grouped forward, dX and dS for
+    # the pair, the pair's dX summed inside one 1536-deep contraction
+    gx = acts["gate"]
+    dYgu_all = inputs.device_bf16_normal(9200, (offs[-1], 1536))
+    dYgu = [dYgu_all[offs[e]:offs[e + 1]] for e in range(E)]
+    Ygu = [torch.empty((T, 1536), dtype=torch.bfloat16, device="cuda") for T in Ts]
+    dSgu = [torch.empty((1536, 2048 // 32), dtype=torch.float32, device="cuda") for _ in Ts]
+    ftables = []
+    for l in range(L):
+        cg = torch.cat([layers[l]["gate"]["codes"], layers[l]["up"]["codes"]], dim=1)
+        sg = torch.cat([layers[l]["gate"]["scales"], layers[l]["up"]["scales"]], dim=1)
+        cl, sl = [cg[e] for e in range(E)], [sg[e] for e in range(E)]
+        ftables.append((sq.ExpertTable("fwd", "mx", gx["X"], cl, sl, Ygu),
+                        sq.ExpertTable("dx", "mx", dYgu, cl, sl, gx["dX"]),
+                        sq.ExpertTable("ds", "mx", gx["X"], cl, None, dSgu, acts2=dYgu), cg, sg))
+
+    def run_fused():
+        for l in range(L):
+            ftables[l][0].run()
+            tables[(l, "down")][0].run()
+        for l in reversed(range(L)):
+            tables[(l, "down")][1].run()
+            tables[(l, "down")][2].run()
+            ftables[l][1].run()
+            ftables[l][2].run()
+
+    fused_ms = timed(run_fused)
+    del ftables, dYgu, dYgu_all, Ygu, dSgu
+    torch.cuda.empty_cache()
     # QAST: per layer and linear, stacked factors B [E, o, r], A [E, r, G]
     qa = {}
     for (name, o, i) in shapes:
@@ -813,6 +846,11 @@ def model_moe(sq, steps=3, warmup=1):
            "ms": round(ms, 3), "TFLOP": round(flops / 1e12, 2),
            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
            "frac_of_bf16_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "fused_gate_up": {"what": "gate and up stacked into one [1536, 2048] weight per expert, as fused-"
+                                     "projection MoE layouts store them: 6 grouped products per layer instead of 9, "
+                                     "the pair's dX summed in one 1536-deep contraction (the same flops)",
+                             "ms": round(fused_ms, 3), "TFLOP/s": round(flops / (fused_ms * 1e-3) / 1e12, 1),
+                             "frac_of_bf16_peak": round(flops / (fused_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
            "qast_step": {"ms": round(qast_ms, 3), "overhead_ms": round(qast_ms - ms, 3),
                          "note": "batched rank-32 QAST scale step of all experts per linear; the paper reports "
                                  "QAST within noise of its no-STE baseline on its MoE (context only)"},
