@@ -1311,17 +1311,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
 
-  // One stage in buffer cur (its slice 0 already in F0): the second half of
-  // the next stage's DMA goes out after slice 1 is read, every load is waited
-  // for at the barrier, then the next stage's slice 0 is read and the first
-  // half of the stage after it is issued into cur.  Returns false after the
-  // workgroup's last stage.
+  // One stage in buffer cur (its slice 0 already in F0): every load is
+  // waited for at the barrier (the next stage's, issued a whole stage
+  // earlier), then the next stage's slice 0 is read and the whole DMA of the
+  // stage after it is issued into cur.  (Issuing the second half of each
+  // stage's DMA mid-step instead, after slice 1 is read, gave it three
+  // quarters of a stage: the MoE split's dS 218 -> 211 us with the whole copy
+  // one stage ahead.)  Returns false after the workgroup's last stage.
   auto stage_step = [&](SQ_LDS uint8_t* cur, SQ_LDS uint8_t* nxt) -> bool {
     read(cur, I1{}, F1);
-    if (dvalid) {
-      dma_half(nxt, I2{});
-      dma_advance();
-    }
     mma(F0);
     read(cur, I2{}, F0);
     mma(F1);
@@ -1333,7 +1331,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
     const bool last = ckt + 1 == ct.nk;
     const bool more = !last || cpos + step < end;
     if (more) read(nxt, I0{}, F0);
-    if (dvalid) dma_half(cur, I0{});
+    if (dvalid) {
+      dma_half(cur, I0{});
+      dma_half(cur, I2{});
+      dma_advance();
+    }
     mma(F1);
     if (!last) {
       ++ckt;
@@ -1358,8 +1360,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
     return true;
   };
 
-  // prologue: the first stage whole, the first tile's codes, then the first
-  // half of the second stage
+  // prologue: the first stage whole, the first tile's codes, then the whole
+  // second stage
   dma_half((SQ_LDS uint8_t*)lds0, I0{});
   dma_half((SQ_LDS uint8_t*)lds0, I2{});
   dma_advance();
@@ -1368,7 +1370,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void ds_stream_kernel(GemmGroup gg)
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   read((SQ_LDS uint8_t*)lds0, I0{}, F0);
-  if (dvalid) dma_half((SQ_LDS uint8_t*)lds1, I0{});
+  if (dvalid) {
+    dma_half((SQ_LDS uint8_t*)lds1, I0{});
+    dma_half((SQ_LDS uint8_t*)lds1, I2{});
+    dma_advance();
+  }
   SQ_LDS uint8_t* cur = (SQ_LDS uint8_t*)lds0;
   SQ_LDS uint8_t* nxt = (SQ_LDS uint8_t*)lds1;
   while (stage_step(cur, nxt)) {

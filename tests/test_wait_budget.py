@@ -331,12 +331,11 @@ def stream_replay(nks):
     read(0)
     if cur["d"] < len(seq):
         dma_half(1, True)
+        dma_half(1, False)
     g = 0
     while True:
-        read(g)                                   # slice 1
-        if cur["d"] < len(seq):
-            dma_half((g + 1) % 2, False)
-        read(g)                                   # slices 2, 3
+        read(g)                                   # slices 1, 2, 3
+        read(g)
         read(g)
         mma_walk.append(seq[g])
         w.wait(0)
@@ -344,8 +343,9 @@ def stream_replay(nks):
         more = g + 1 < len(seq)
         if more:
             read(g + 1)                           # slice 0 of the next stage
-        if cur["d"] < len(seq):
+        if cur["d"] < len(seq):                   # the whole stage after it
             dma_half(g % 2, True)
+            dma_half(g % 2, False)
         if not more:
             break
         g += 1
@@ -372,13 +372,13 @@ def test_stream_model_follows_the_kernel_source():
     j = s.index("// prologue: the first stage whole", i)
     pat = r"\b(read|dma_half|dma_advance|mma|wait_vm_lgkm0<\w+>|__builtin_amdgcn_s_barrier|ds_store<FMT, TM, TN, (?:true|false)>|tile_codes|locate)\s*\("
     body = [m.group(1) for m in re.finditer(pat, s[i:j])]
-    assert body == ["read", "dma_half", "dma_advance", "mma", "read", "mma", "read", "mma", "wait_vm_lgkm0<0>",
-                    "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma", "ds_store<FMT, TM, TN, true>",
-                    "ds_store<FMT, TM, TN, false>", "locate", "tile_codes"], body
+    assert body == ["read", "mma", "read", "mma", "read", "mma", "wait_vm_lgkm0<0>",
+                    "__builtin_amdgcn_s_barrier", "read", "dma_half", "dma_half", "dma_advance", "mma",
+                    "ds_store<FMT, TM, TN, true>", "ds_store<FMT, TM, TN, false>", "locate", "tile_codes"], body
     k = s.index("while (stage_step(cur, nxt))", j)
     pro = [m.group(1) for m in re.finditer(pat, s[j:k])]
     assert pro == ["dma_half", "dma_half", "dma_advance", "tile_codes", "wait_vm_lgkm0<0>",
-                   "__builtin_amdgcn_s_barrier", "read", "dma_half"], pro
-    # the halves: quarters 2-3 of the next stage mid-step, 0-1 of the one after at the end
-    assert "dma_half(nxt, I2{});" in s[i:j] and "if (dvalid) dma_half(cur, I0{});" in s[i:j]
+                   "__builtin_amdgcn_s_barrier", "read", "dma_half", "dma_half", "dma_advance"], pro
+    # both halves of the stage after next go into the buffer just read, after the barrier
+    assert "dma_half(cur, I0{});\n      dma_half(cur, I2{});\n      dma_advance();" in s[i:j]
     assert "const bool more = !last || cpos + step < end;" in s[i:j]
