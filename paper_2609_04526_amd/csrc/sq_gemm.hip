@@ -1023,18 +1023,24 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   constexpr int kAheadLow = (STAGES - 2) * kDmaLow < 63 ? (STAGES - 2) * kDmaLow : 63;
   const bool codes_wave = !kCodesSplit || wave_u < DC::kWaveInst;
 
+  // The register forward issues each stage's whole DMA right after the
+  // barrier that frees its buffer (the 14336 x 4096 forward 394 -> 386 us,
+  // the MoE gate forward -3%); dX and dS keep the second half for the next
+  // step's first slice (issued whole they ran 1% and 3% slower).
+  constexpr bool kWhole = MODE == kFwdC;
   auto step2 = [&](auto SC, int kt) {
     constexpr int S = decltype(SC)::value;
     using SN = std::integral_constant<int, (S + 1) % STAGES>;            // stage kt + 1
     using SP = std::integral_constant<int, (S + STAGES - 1) % STAGES>;   // stage kt + STAGES - 1
     take_scales(kt);
     // slice 0 (operands in F0): the W loads (dX), then read slice 1 and
-    // issue the second half of stage kt + STAGES - 1's DMA
+    // (but for the forward) issue the second half of stage kt + STAGES - 1's
+    // DMA
     if constexpr (kWReg) {            // dX: the W items of stage kt + 2
       if (kt + 2 < nk) load_w(kt + 2, I0{});
     }
     read(SC, kt, I1{}, F1);
-    if (kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
+    if (!kWhole && kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
     mma(F0);
     read(SC, kt, I2{}, F0);
     mma(F1);
@@ -1052,7 +1058,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if (kt + 1 < nk) read(SN{}, kt + 1, I0{}, F0);
-    if (kt + STAGES < nk) dma_half(SC, kt + STAGES, I0{});
+    if (kt + STAGES < nk) {
+      dma_half(SC, kt + STAGES, I0{});
+      if (kWhole) dma_half(SC, kt + STAGES, I2{});
+    }
     mma(F1);
     // dX: stage kt + 2's W tile into the buffer stage kt used (every read of
     // it came before the barrier).  Its items were loaded before the wait at
@@ -1066,7 +1075,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   };
 
   // prologue: stage 0 in LDS and its slice 0 read, then the DMA of stages
-  // 1 .. STAGES - 2 and the first half of stage STAGES - 1
+  // 1 .. STAGES - 2 and the first half of stage STAGES - 1 (the forward: all
+  // of it)
   if (nk > 0) {
     if constexpr (kWReg) {            // dX: the W tiles of stages 0 and 1
       load_w(0, I0{});
@@ -1088,7 +1098,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     if constexpr (STAGES > 3) {
       if (2 < nk) issue_dma(I2{}, 2);
     }
-    if (STAGES - 1 < nk) dma_half(std::integral_constant<int, STAGES - 1>{}, STAGES - 1, I0{});
+    if (STAGES - 1 < nk) {
+      dma_half(std::integral_constant<int, STAGES - 1>{}, STAGES - 1, I0{});
+      if (kWhole) dma_half(std::integral_constant<int, STAGES - 1>{}, STAGES - 1, I2{});
+    }
   }
   for (int kt0 = 0; kt0 < nk; kt0 += STAGES) {
     step2(I0{}, kt0);

@@ -180,6 +180,7 @@ def replay(mode, cfg, nk, wave):
     def load_sc(chunk):
         w.issue(("sc", chunk), 2 * TN)          # two 8-byte halves per row slice
 
+    whole = mode == "fwdc"             # the forward issues each stage's DMA whole, after the barrier
     # prologue
     if nk > 0:
         if mode == "dx":
@@ -201,13 +202,15 @@ def replay(mode, cfg, nk, wave):
                 dma_half(s, False)
         if STAGES - 1 < nk:
             dma_half(STAGES - 1, True)
+            if whole:
+                dma_half(STAGES - 1, False)
     for kt in range(nk):
         if mode == "fwdc" and kt % 8 == 7 and kt + 1 < nk:
             load_sc((kt + 1) // 8)
         if mode == "dx" and kt + 2 < nk:
             w.issue(("w", kt + 2), 2 * w_items)
         read(kt)                                               # slice 1
-        if kt + STAGES - 1 < nk:
+        if not whole and kt + STAGES - 1 < nk:
             dma_half(kt + STAGES - 1, False)
         read(kt)                                               # slices 2, 3
         read(kt)
@@ -220,6 +223,8 @@ def replay(mode, cfg, nk, wave):
             read(kt + 1)                                       # slice 0 of the next stage (a)
         if kt + STAGES < nk:
             dma_half(kt + STAGES, True)
+            if whole:
+                dma_half(kt + STAGES, False)
         if mode == "dx" and kt + 2 < nk:
             commit_w(kt + 2, True)
     w.wait(0)
@@ -262,6 +267,21 @@ def test_a_shorter_wait_budget_is_caught(monkeypatch):
             replay("ds", cfg, nk, 0)
 
 
+def test_a_larger_forward_budget_is_caught(monkeypatch):
+    """The same for the forward's four-stage grouped tile, whose stages go
+    out whole after the barrier: one load more in flight at the wait fails."""
+    import sys
+    cfg = configs()["SQ_CFG_GROUPED_FWDC"]
+    assert cfg[4] == 4
+    k_dma, ahead, ahead_low, split, cw = kernel_constants("fwdc", *cfg)
+    monkeypatch.setattr(sys.modules[__name__], "kernel_constants",
+                        lambda *a: (k_dma, ahead + 1, ahead_low + 1, split, cw))
+    with pytest.raises(AssertionError):
+        for nk in range(1, 12):
+            for wave in range(cfg[2] * cfg[3]):
+                replay("fwdc", cfg, nk, wave)
+
+
 def _calls(body):
     pat = (r"\b(take_scales|read|dma_half|load_w|commit_w|mma|wait_vm_lgkm0<\w+>|"
            r"__builtin_amdgcn_s_barrier)\s*\(")
@@ -277,11 +297,17 @@ def test_model_follows_the_kernel_source():
     step2 = _calls(s[i:j])
     assert step2 == ["take_scales", "load_w", "read", "dma_half", "mma", "read", "mma", "read", "mma",
                      "wait_vm_lgkm0<kAhead>", "wait_vm_lgkm0<kAheadLow>", "wait_vm_lgkm0<0>",
-                     "__builtin_amdgcn_s_barrier", "read", "dma_half", "mma", "commit_w"], step2
+                     "__builtin_amdgcn_s_barrier", "read", "dma_half", "dma_half", "mma", "commit_w"], step2
     k = s.index("for (int kt0 = 0; kt0 < nk; kt0 += STAGES)", j)
     pro = _calls(s[j:k])
     assert pro == ["load_w", "commit_w", "load_w", "commit_w", "wait_vm_lgkm0<0>", "__builtin_amdgcn_s_barrier",
-                   "read", "dma_half"], pro
+                   "read", "dma_half", "dma_half"], pro
+    # the forward issues a stage's second half with its first (after the
+    # barrier, and in the prologue), the others one step later
+    assert "constexpr bool kWhole = MODE == kFwdC;" in s
+    assert "if (!kWhole && kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});" in s[i:j]
+    assert "if (kWhole) dma_half(SC, kt + STAGES, I2{});" in s[i:j]
+    assert "if (kWhole) dma_half(std::integral_constant<int, STAGES - 1>{}, STAGES - 1, I2{});" in s[j:k]
     # the W items of stage kt + 2 are loaded before the barrier's wait and
     # converted after it
     assert "if (kt + 2 < nk) load_w(kt + 2, I0{});" in s and "if (kt + 2 < nk) commit_w(kt + 2, I0{});" in s
