@@ -733,7 +733,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // The forward fetches W two stages ahead through branch-free buffer loads
   // (an item outside the layer reads at an offset past the operand: zeros),
   // so the wait before a dequantisation leaves the newer loads in flight.
-  constexpr int kWAhead = MODE == kFwdR ? 2 : 1;
+  // dX tiles below 256 x 256 convert a stage's W items in the middle of the
+  // step before it (see step2), which takes a second register set; the
+  // 256 x 256 tile has no registers to spare and converts them right after
+  // the barrier that frees their buffer
+  constexpr bool kWMid = MODE == kDx && BM * BN < 256 * 256;
+  constexpr int kWAhead = (MODE == kFwdR || kWMid) ? 2 : 1;   // register sets of W items
   uint32_t w_reg[kWAhead][kWPer], w_sb[kWAhead][kWPer];
   // Forward W items: row o = n0 + idx/8 is fixed, the 8 columns start at
   // kt*64 + (idx%8)*8, so each item keeps byte offsets at kt = 0 (past the
@@ -1036,12 +1041,23 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
     // slice 0 (operands in F0): the W loads (dX), then read slice 1 and
     // (but for the forward) issue the second half of stage kt + STAGES - 1's
     // DMA
-    if constexpr (kWReg) {            // dX: the W items of stage kt + 2
+    if constexpr (kWMid) {            // dX: the W items of stage kt + 2, in the set of its parity
+      if (kt + 2 < nk) load_w(kt + 2, std::integral_constant<int, S % 2>{});
+    } else if constexpr (kWReg) {     // dX: the W items of stage kt + 2
       if (kt + 2 < nk) load_w(kt + 2, I0{});
     }
     read(SC, kt, I1{}, F1);
     if (!kWhole && kt + STAGES - 1 < nk) dma_half(SP{}, kt + STAGES - 1, I2{});
     mma(F0);
+    // dX below 256 x 256: stage kt + 1's W tile, from the items loaded a
+    // step ago (the last barrier's wait completed them), into the buffer of
+    // stage kt - 1 (read before that barrier); the next barrier publishes
+    // it.  Written here, in the middle of the step, the tile's LDS writes do
+    // not meet the burst of stage copies and operand reads that follows each
+    // barrier.
+    if constexpr (kWMid) {
+      if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, (S + 1) % 2>{});
+    }
     read(SC, kt, I2{}, F0);
     mma(F1);
     read(SC, kt, I3{}, F1);
@@ -1063,13 +1079,14 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
       if (kWhole) dma_half(SC, kt + STAGES, I2{});
     }
     mma(F1);
-    // dX: stage kt + 2's W tile into the buffer stage kt used (every read of
-    // it came before the barrier).  Its items were loaded before the wait at
-    // the barrier, so converting them waits for nothing; loading them a
-    // stage ahead of their conversion keeps the round trip of the W items
-    // off the step's critical path (converting a stage's items in the step
-    // that loaded them cost dX 12-14%).  The next barrier publishes the tile.
-    if constexpr (kWReg) {
+    // dX 256 x 256: stage kt + 2's W tile into the buffer stage kt used
+    // (every read of it came before the barrier).  Its items were loaded
+    // before the wait at the barrier, so converting them waits for nothing;
+    // loading them a stage ahead of their conversion keeps the round trip of
+    // the W items off the step's critical path (converting a stage's items
+    // in the step that loaded them cost dX 12-14%).  The next barrier
+    // publishes the tile.
+    if constexpr (kWReg && !kWMid) {
       if (kt + 2 < nk) commit_w(kt + 2, I0{});
     }
   };
@@ -1078,7 +1095,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int bid, int nb) {
   // 1 .. STAGES - 2 and the first half of stage STAGES - 1 (the forward: all
   // of it)
   if (nk > 0) {
-    if constexpr (kWReg) {            // dX: the W tiles of stages 0 and 1
+    if constexpr (kWMid) {            // dX below 256 x 256: stage 0's W tile and stage 1's items
+      load_w(0, I0{});
+      commit_w(0, I0{});
+      if (1 < nk) load_w(1, I1{});
+    } else if constexpr (kWReg) {     // dX: the W tiles of stages 0 and 1
       load_w(0, I0{});
       commit_w(0, I0{});
       if (1 < nk) {

@@ -17,9 +17,12 @@ the barriers, for every stage count from 1 to 40, and checks:
   (b) a copy into a stage buffer is issued only after a barrier that follows
       every read of the stage the buffer held before;
   (c) dX's W tile of stage s is written only after a barrier that follows
-      every read of stage s - 2's tile (two W buffers), and converted from
-      items that a wait has already completed (the step that loads stage
-      s's items converts them right after its barrier).
+      every read of stage s - 2's tile (two W buffers), converted from items
+      that a wait has already completed, and published by a barrier before
+      the first read of stage s.  The step that loads stage s's items (step
+      s - 2) converts them right after its barrier in the 256 x 256 tile;
+      smaller tiles convert them in the middle of step s - 1, after its first
+      slice's MFMAs.
 
 The replay mirrors the body of `step2` and the prologue in
 csrc/sq_gemm.hip; `test_model_follows_the_kernel_source` compares the
@@ -143,8 +146,10 @@ def replay(mode, cfg, nk, wave):
     q = dma_plan(mode, *cfg, wave)
     NT = 64 * WGM * WGN
     w_items = 64 * (BN // 8) // NT if mode == "dx" else 0       # kWPer
+    mid = mode == "dx" and BM * BN < 256 * 256                 # kWMid
     w = Wave()
     holder = {}                                                # buffer -> stage it holds
+    w_published = {}                                           # W tile stage -> barrier count at its write
 
     def dma_half(stage, first):
         buf = stage % STAGES
@@ -162,6 +167,8 @@ def replay(mode, cfg, nk, wave):
         assert not w.pending(("dma", stage)), (mode, cfg, nk, wave, stage, "read before landing")
         w.last_read_barrier[stage] = w.barriers
         if mode == "dx":
+            # (c) the stage's W tile was written before a barrier already passed
+            assert w_published.get(stage, w.barriers) < w.barriers, (mode, cfg, nk, wave, stage, "W tile unpublished")
             w.w_last_read[stage] = w.barriers
 
     def commit_w(stage, in_loop):
@@ -176,6 +183,7 @@ def replay(mode, cfg, nk, wave):
         ws = [i for i, l in enumerate(w.loads) if l[0] == ("w", stage)]
         for l in w.loads[:ws[-1] + 1]:
             l[1] = True
+        w_published[stage] = w.barriers
 
     def load_sc(chunk):
         w.issue(("sc", chunk), 2 * TN)          # two 8-byte halves per row slice
@@ -188,7 +196,8 @@ def replay(mode, cfg, nk, wave):
             commit_w(0, False)
             if 1 < nk:
                 w.issue(("w", 1), 2 * w_items)
-                commit_w(1, False)
+                if not mid:
+                    commit_w(1, False)
         if mode == "fwdc":
             load_sc(0)
         dma_half(0, True)
@@ -212,6 +221,8 @@ def replay(mode, cfg, nk, wave):
         read(kt)                                               # slice 1
         if not whole and kt + STAGES - 1 < nk:
             dma_half(kt + STAGES - 1, False)
+        if mid and kt + 1 < nk:
+            commit_w(kt + 1, True)                             # after slice 0's MFMAs
         read(kt)                                               # slices 2, 3
         read(kt)
         if kt + STAGES - 1 < nk:
@@ -225,7 +236,7 @@ def replay(mode, cfg, nk, wave):
             dma_half(kt + STAGES, True)
             if whole:
                 dma_half(kt + STAGES, False)
-        if mode == "dx" and kt + 2 < nk:
+        if mode == "dx" and not mid and kt + 2 < nk:
             commit_w(kt + 2, True)
     w.wait(0)
     assert all(l[1] for l in w.loads)
@@ -295,13 +306,19 @@ def test_model_follows_the_kernel_source():
     i = s.index("auto step2 = [&](auto SC, int kt) {")
     j = s.index("// prologue: stage 0 in LDS", i)
     step2 = _calls(s[i:j])
-    assert step2 == ["take_scales", "load_w", "read", "dma_half", "mma", "read", "mma", "read", "mma",
-                     "wait_vm_lgkm0<kAhead>", "wait_vm_lgkm0<kAheadLow>", "wait_vm_lgkm0<0>",
+    # (dX below 256 x 256 loads into the set of the stage's parity and
+    # converts after slice 0's MFMAs; the 256 x 256 tile after the barrier)
+    assert step2 == ["take_scales", "load_w", "load_w", "read", "dma_half", "mma", "commit_w", "read", "mma",
+                     "read", "mma", "wait_vm_lgkm0<kAhead>", "wait_vm_lgkm0<kAheadLow>", "wait_vm_lgkm0<0>",
                      "__builtin_amdgcn_s_barrier", "read", "dma_half", "dma_half", "mma", "commit_w"], step2
     k = s.index("for (int kt0 = 0; kt0 < nk; kt0 += STAGES)", j)
     pro = _calls(s[j:k])
-    assert pro == ["load_w", "commit_w", "load_w", "commit_w", "wait_vm_lgkm0<0>", "__builtin_amdgcn_s_barrier",
-                   "read", "dma_half", "dma_half"], pro
+    assert pro == ["load_w", "commit_w", "load_w", "load_w", "commit_w", "load_w", "commit_w", "wait_vm_lgkm0<0>",
+                   "__builtin_amdgcn_s_barrier", "read", "dma_half", "dma_half"], pro
+    assert "constexpr bool kWMid = MODE == kDx && BM * BN < 256 * 256;" in s
+    assert "if (kt + 2 < nk) load_w(kt + 2, std::integral_constant<int, S % 2>{});" in s[i:j]
+    assert "if (kt + 1 < nk) commit_w(kt + 1, std::integral_constant<int, (S + 1) % 2>{});" in s[i:j]
+    assert "if (1 < nk) load_w(1, I1{});" in s[j:k]
     # the forward issues a stage's second half with its first (after the
     # barrier, and in the prologue), the others one step later
     assert "constexpr bool kWhole = MODE == kFwdC;" in s
