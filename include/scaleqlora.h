@@ -217,7 +217,9 @@ int sq_merge_scales_grouped(int n_desc, const sq_merge_desc* descs, void* stream
  * element (the MXFP4 forward dequantises in registers when every expert's
  * codes are 16-byte and scales 8-byte aligned and I % 256 == 0, as sq_fwd
  * does for one); the whole list runs in one launch per 128 experts (fewer
- * when one kind of pointer of those experts spans 4 GiB or more).
+ * when one kind of pointer of those experts spans 4 GiB or more), and
+ * sq_bwd_dx_grouped may run the rows of experts' short last token tiles in a
+ * second launch of its own.
  *
  *   act     sq_fwd_grouped, sq_bwd_dscale_grouped: X_e bf16 [T_e, I];
  *           sq_bwd_dx_grouped: dY_e bf16 [T_e, O]  (16-byte aligned)

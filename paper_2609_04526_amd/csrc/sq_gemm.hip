@@ -1610,6 +1610,63 @@ static int launch_ds_stream(GemmGroup& gg, const ExpertProblem* p, int n, hipStr
 // 77.3 -> 75.9 us for the pair.
 #define SQ_CFG_GROUPED_FWDC_LONG 128, 256, 2, 4, 4, 64
 
+// Grouped dX on 128 x 128 tiles: an expert whose last 128-token tile would
+// hold 64 rows or fewer can send those rows to a second launch of 64 x 256
+// tiles (the same per-element sums: every output row is computed alone), so
+// that tile is not half padding.  Over the MoE layer's routed split (128
+// experts, 256 rows on average) half the experts end that way: for the gate
+// and up dX (I = 2048) 5120 tiles become 4096 and 512 of 64 x 256, and the
+// product ran 214 -> 203 us.  The second launch is worth it only when it
+// saves more than it costs: counted in rounds of two workgroups per CU, the
+// 64 x 256 launch takes whole rounds (a partial round still lasts a tile) at
+// about 1.15 times a 128 x 128 tile (the down dX, I = 768, would go from
+// 1920 tiles to 1536 and 192: 175 -> 180 us, so it stays whole).  If the
+// moved pointers do not fit the launch's 32-bit offsets, the experts run
+// unsplit.
+template <int FMT>
+static int dx_split_tails(GemmGroup& gg, const ExpertProblem* p, int n, hipStream_t s) {
+  const int64_t cols = (gg.base.I + 127) / 128, cols_thin = (gg.base.I + 255) / 256;
+  int64_t all = 0, kept = 0, moved = 0;
+  for (int e = 0; e < n; ++e) {
+    const int t = p[e].T % 128;
+    all += (int64_t)((p[e].T + 127) / 128) * cols;
+    if (t > 0 && t <= 64) {
+      kept += (int64_t)(p[e].T / 128) * cols;
+      moved += cols_thin;
+    } else {
+      kept += (int64_t)((p[e].T + 127) / 128) * cols;
+    }
+  }
+  const double slots = 2.0 * kCUs;
+  if (moved == 0 || (double)kept / slots + 1.15 * (double)((moved + 2 * kCUs - 1) / (2 * kCUs)) >= (double)all / slots)
+    return launch_grouped<kDx, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+  ExpertProblem whole[kGroupMax], tail[kGroupMax];
+  int nw = 0, nt = 0;
+  const size_t a_row = (size_t)gg.base.O * 2, out_row = (size_t)gg.base.I * (gg.base.out_bf16 ? 2 : 4);
+  for (int e = 0; e < n; ++e) {
+    const int t = p[e].T % 128;
+    if (t == 0 || t > 64) {
+      whole[nw++] = p[e];
+      continue;
+    }
+    const int head = p[e].T - t;
+    if (head > 0) {
+      whole[nw] = p[e];
+      whole[nw++].T = head;
+    }
+    tail[nt] = p[e];
+    tail[nt].a = static_cast<const uint8_t*>(p[e].a) + (size_t)head * a_row;
+    tail[nt].out = static_cast<uint8_t*>(p[e].out) + (size_t)head * out_row;
+    tail[nt++].T = t;
+  }
+  GemmGroup gw = gg, gt = gg;
+  if (nt == 0 || !set_experts(gw, whole, nw, false) || !set_experts(gt, tail, nt, false))
+    return launch_grouped<kDx, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+  const int rc = nw > 0 ? launch_grouped<kDx, FMT, SQ_CFG_SMALL>(gw, whole, nw, s) : 0;
+  if (rc != 0) return rc;
+  return launch_grouped<kDx, FMT, SQ_CFG_GROUPED_THIN>(gt, tail, nt, s);
+}
+
 // The large tile when the experts' tiles fill the chip and an expert averages
 // at least 512 tokens (rows of the forward and dX, the contraction of dS:
 // shorter token sums leave a 256 x 256 dS tile a few stages between its
@@ -1631,7 +1688,7 @@ static int grouped_sized(GemmGroup& gg, const ExpertProblem* p, int n, hipStream
   else if constexpr (MODE == kDs) return launch_ds_stream<FMT, SQ_CFG_DS_STREAM>(gg, p, n, s);
   else if constexpr (MODE == kDx) {
     if (tokens <= (int64_t)96 * n) return launch_grouped<MODE, FMT, SQ_CFG_GROUPED_THIN>(gg, p, n, s);
-    return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
+    return dx_split_tails<FMT>(gg, p, n, s);
   } else return launch_grouped<MODE, FMT, SQ_CFG_SMALL>(gg, p, n, s);
 }
 

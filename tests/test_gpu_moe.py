@@ -270,6 +270,27 @@ def test_moe_layer_shapes_sampled(sq):
         # token sum whole (here: fewer than 8 token stages, T <= 448)
         compared = sum(single_dscale_equal(sq, "mx", Xd[e], dYd[e], cd[e], dSs[e]) for e in range(E))
         assert compared >= sum(T <= 448 for T in Ts)
+        # every expert's dX equals its single product bit for bit; for the
+        # gate shape the experts whose last 128-token tile would hold 64 rows
+        # or fewer run those rows in a second launch of 64 x 256 tiles
+        if I == 2048:
+            assert dx_tail_split_taken(Ts, I)
+        for e in range(E):
+            one = sq.sq_bwd_dx("mx", dYd[e], cd[e], sd[e])
+            assert torch.equal(one, dXs[e]), (O, I, e, Ts[e])
+
+
+def dx_tail_split_taken(Ts, I, cus=256):
+    """Whether grouped dX (128 x 128 tiles) moves the short last token tiles
+    of its experts to a 64 x 256 launch: when the moved tiles' rounds (two
+    workgroups per CU, whole rounds, 1.15 times a 128 x 128 tile) and the
+    kept tiles' take less than all tiles kept whole."""
+    cols, cols_thin = (I + 127) // 128, (I + 255) // 256
+    whole = sum((T + 127) // 128 for T in Ts) * cols
+    kept = sum((T // 128 if 0 < T % 128 <= 64 else (T + 127) // 128) for T in Ts) * cols
+    moved = sum(cols_thin for T in Ts if 0 < T % 128 <= 64)
+    slots = 2 * cus
+    return moved > 0 and kept / slots + 1.15 * ((moved + slots - 1) // slots) < whole / slots
 
 
 # Grouped dS of short token sums runs each workgroup's share of the tiles as
