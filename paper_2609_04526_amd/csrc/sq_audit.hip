@@ -37,10 +37,7 @@ __device__ __forceinline__ uint32_t field_encode(float v) {
 // spans w, w + grid, ...  Outputs are written with streaming stores, and the
 // scale planes of NVFP4 (the larger ones) are read with streaming loads, as
 // in the merge.
-#ifndef SQ_AUDIT_STEPS
-#define SQ_AUDIT_STEPS 8
-#endif
-constexpr int kAuditSteps = SQ_AUDIT_STEPS;
+constexpr int kAuditSteps = 8;
 constexpr int64_t kAuditSpan = 1024 * kAuditSteps;
 
 template <int FMT>
@@ -159,12 +156,10 @@ static unsigned stream_grid(int64_t n, int64_t per_wg) {
   return (unsigned)(want < 4096 ? (want > 0 ? want : 1) : 4096);
 }
 
-#ifndef SQ_AUDIT_GRID
-#define SQ_AUDIT_GRID 16384
-#endif
+constexpr int64_t kAuditGrid = 16384;
 static unsigned span_grid(int64_t n) {
   const int64_t want = (n + kAuditSpan - 1) / kAuditSpan;
-  return (unsigned)(want < SQ_AUDIT_GRID ? want : SQ_AUDIT_GRID);
+  return (unsigned)(want < kAuditGrid ? want : kAuditGrid);
 }
 
 int applied_launch(int fmt, int64_t n, const uint8_t* before, const uint8_t* after, float* applied, hipStream_t s) {
@@ -188,11 +183,9 @@ int byte_diff_launch(int64_t n, const uint8_t* a, const uint8_t* b, uint64_t* co
   // One workgroup per CU streams best: on the 8B model's planes the audit ran
   // at 3.5 / 4.7 TB/s (MXFP4 / NVFP4) from 4096 workgroups and 5.8-6.0 /
   // 6.7 TB/s from 256, each lane keeping its four 16-byte pairs in flight.
-#ifndef SQ_DIFF_GRID
-#define SQ_DIFF_GRID 256
-#endif
+  constexpr int64_t kDiffGrid = 256;
   const int64_t want = (n + 16383) / 16384;
-  const unsigned grid = (unsigned)(want < SQ_DIFF_GRID ? (want > 0 ? want : 1) : SQ_DIFF_GRID);
+  const unsigned grid = (unsigned)(want < kDiffGrid ? (want > 0 ? want : 1) : kDiffGrid);
   hipLaunchKernelGGL(byte_diff_kernel, dim3(grid), dim3(256), 0, s, a, b, n,
                      reinterpret_cast<unsigned long long*>(counts));
   return hipGetLastError() == hipSuccess ? 0 : -1;

@@ -129,13 +129,8 @@ int merge_launch(const MergeBatch& b, hipStream_t s) {
   // Measured on the 8B model's planes (medians of interleaved runs): copies
   // stream best from 2048 workgroups, MXFP4 deltas from 4096, and NVFP4
   // deltas (16-step spans, a longer grid step per scale) from 16384.
-#ifndef SQ_MERGE_NV_GRID
-#define SQ_MERGE_NV_GRID 16384
-#endif
-#ifndef SQ_MERGE_MX_GRID
-#define SQ_MERGE_MX_GRID 4096
-#endif
-  const int64_t cap = b.kinds == kMergeCopy ? 2048 : ((b.kinds & kMergeNvDelta) ? SQ_MERGE_NV_GRID : SQ_MERGE_MX_GRID);
+  constexpr int64_t kNvGrid = 16384, kMxGrid = 4096;
+  const int64_t cap = b.kinds == kMergeCopy ? 2048 : ((b.kinds & kMergeNvDelta) ? kNvGrid : kMxGrid);
   const dim3 grid((unsigned)(b.spans < cap ? b.spans : cap));
   if (b.small) {
     // few scales in all: one-step spans, one workgroup each

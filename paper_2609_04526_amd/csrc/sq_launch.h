@@ -27,28 +27,17 @@ int gemm_dscale_static(int fmt, int T, int O, int I, const void* X, const void* 
 // mode) and owns the spans [span_begin[p], span_begin[p+1]).
 constexpr int kMergePlanesPerLaunch = 112;
 enum MergeKind { kMergeCopy = 1, kMergeMxDelta = 2, kMergeNvDelta = 4 };
-#ifndef SQ_MERGE_DELTA_STEPS_MX
-#define SQ_MERGE_DELTA_STEPS_MX 8
-#endif
-#ifndef SQ_MERGE_DELTA_STEPS_NV
-#define SQ_MERGE_DELTA_STEPS_NV 16
-#endif
-#ifndef SQ_MERGE_COPY_STEPS
-#define SQ_MERGE_COPY_STEPS 8
-#endif
+constexpr int kMergeDeltaStepsMx = 8, kMergeDeltaStepsNv = 16, kMergeCopySteps = 8;
 // Steps of 4 scales (and a 16-byte fp32 delta) per lane in one delta span;
 // NVFP4's longer grid step hides better behind more loads in flight.  A
 // launch over few scales (below kMergeSmallScales in all) takes one-step
 // spans instead, so that it still spreads over the CUs.
-#ifndef SQ_MERGE_SMALL_SCALES
-#define SQ_MERGE_SMALL_SCALES (int64_t(1) << 24)
-#endif
-constexpr int64_t kMergeSmallScales = SQ_MERGE_SMALL_SCALES;
+constexpr int64_t kMergeSmallScales = int64_t(1) << 24;
 constexpr int delta_steps(int fmt, bool small = false) {
-  return small ? 1 : (fmt == 1 ? SQ_MERGE_DELTA_STEPS_NV : SQ_MERGE_DELTA_STEPS_MX);
+  return small ? 1 : (fmt == 1 ? kMergeDeltaStepsNv : kMergeDeltaStepsMx);
 }
 constexpr int delta_span(int fmt, bool small = false) { return 1024 * delta_steps(fmt, small); }   // 256 lanes x 4 scales per step
-constexpr int copy_steps(bool small = false) { return small ? 1 : SQ_MERGE_COPY_STEPS; }
+constexpr int copy_steps(bool small = false) { return small ? 1 : kMergeCopySteps; }
 constexpr int copy_span(bool small = false) { return 4096 * copy_steps(small); }    // 256 lanes x 16 bytes per step
 struct MergeBatch {
   uint8_t* scales[kMergePlanesPerLaunch];
