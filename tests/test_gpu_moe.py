@@ -280,6 +280,25 @@ def test_moe_layer_shapes_sampled(sq):
             assert torch.equal(one, dXs[e]), (O, I, e, Ts[e])
 
 
+def test_grouped_dx_tail_split_nvfp4_bf16(sq):
+    """Grouped NVFP4 dX with bf16 outputs over the routed split of a MoE
+    layer (gate shape), where the short last token tiles run in a second
+    launch: every expert's dX equals its single product bit for bit."""
+    E, O, I = 128, 768, 2048
+    g = inputs.rng(7650)
+    Ts = g.multinomial(4096 * 8, g.dirichlet(np.full(E, 2.0))).tolist()
+    assert dx_tail_split_taken(Ts, I)
+    codes, scales, ws2 = experts("nv", E, O, I, 7660)
+    cd, sd = cuda(codes), cuda(scales)
+    dYd = [inputs.device_bf16_normal(7670 + e, (T, O)) for e, T in enumerate(Ts)]
+    print(f"[moe dx split] nv bf16 O={O} I={I} experts={E} tokens={sum(Ts)}", flush=True)
+    dXs = sq.sq_bwd_dx_grouped("nv", dYd, cd, sd, ws2, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    for e in range(E):
+        one = sq.sq_bwd_dx("nv", dYd[e], cd[e], sd[e], ws2[e], out_dtype=torch.bfloat16)
+        assert torch.equal(one, dXs[e]), (e, Ts[e])
+
+
 def dx_tail_split_taken(Ts, I, cus=256):
     """Whether grouped dX (128 x 128 tiles) moves the short last token tiles
     of its experts to a 64 x 256 launch: when the moved tiles' rounds (two
