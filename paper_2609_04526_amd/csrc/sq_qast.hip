@@ -32,22 +32,27 @@ namespace sq {
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 // ------------------------------------------------------------------ scales
-// A workgroup per tile of 32 rows x 32 blocks of one expert (blockIdx.y): the
-// tile's A columns [RMAX][32] and B rows [32][RMAX] are staged in LDS as fp32
-// (every load issued together; ranks past r are 0 and add exact zeros), and
-// thread (g, row group) adds the r terms of its four rows in increasing k.
+// A workgroup per tile of 128 rows x 32 blocks of one expert (blockIdx.y):
+// the tile's A columns [RMAX][32] and B rows, transposed to [RMAX][128], are
+// staged in LDS as fp32 (every load issued together; ranks past r are 0 and
+// add exact zeros), and thread (row group, block group) adds the r terms of
+// its 4 x 4 outputs in increasing k, two 16-byte LDS reads per 16 fused
+// multiply-adds.  Where G % 4 == 0 and the byte planes are 4-byte aligned
+// (vec), a thread's four blocks of a row are one 4-byte load and store.
 // Experts are stacked: rows e*O .. e*O + O - 1 of base, B, out and mask
 // belong to expert e, whose A is A + e*r*G and whose ws2 is ws2[e].
-constexpr int kScRows = 32;
+constexpr int kScRows = 128;
 constexpr int kScCols = 32;
 
 template <int FMT, int RMAX>
 __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restrict__ base,
                                                           const uint16_t* __restrict__ B,
                                                           const uint16_t* __restrict__ A, int O, int G, int r,
-                                                          float c, Ws2Table ws2, uint8_t* out, uint8_t* mask) {
-  __shared__ float at[RMAX][kScCols + 1];
-  __shared__ float bt[kScRows][RMAX + 1];
+                                                          float c, Ws2Table ws2, uint8_t* out, uint8_t* mask,
+                                                          int vec) {
+  constexpr int kAPad = kScCols + 4, kBPad = kScRows + 4;    // rows stay 16-byte aligned
+  __shared__ __attribute__((aligned(16))) float at[RMAX][kAPad];
+  __shared__ __attribute__((aligned(16))) float bt[RMAX][kBPad];
   const int e = blockIdx.y;
   const size_t rows0 = (size_t)e * O;
   const uint16_t* ae = A + (size_t)e * r * G;
@@ -61,18 +66,26 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
 #pragma unroll
   for (int u = 0; u < kScRows * RMAX / 256; ++u) {
     const int i = threadIdx.x + 256 * u, ro = i / RMAX, k = i % RMAX;
-    bt[ro][k] = (k < r && o0 + ro < O) ? bf16_bits_to_f32(B[(rows0 + o0 + ro) * r + k]) : 0.0f;
+    bt[k][ro] = (k < r && o0 + ro < O) ? bf16_bits_to_f32(B[(rows0 + o0 + ro) * r + k]) : 0.0f;
   }
   __syncthreads();
-  const int gi = threadIdx.x % kScCols, rq = (threadIdx.x / kScCols) * 4;
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  const int gq = (threadIdx.x % (kScCols / 4)) * 4, rq = (threadIdx.x / (kScCols / 4)) * 4;
+  float acc[4][4];
 #pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[q][j] = 0.0f;
+#pragma unroll 4
   for (int k = 0; k < RMAX; ++k) {
-    const float a = at[k][gi];
+    const float4 a = *reinterpret_cast<const float4*>(&at[k][gq]);
+    const float4 b = *reinterpret_cast<const float4*>(&bt[k][rq]);
+    const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[q] = __builtin_fmaf(bt[rq + q][k], a, acc[q]);
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[q][j] = __builtin_fmaf(bv[q], av[j], acc[q][j]);
   }
-  const int g = g0 + gi;
+  const int g = g0 + gq;
   if (g >= G) return;
   const Ws2Div wd = make_ws2_div(ws2.v[e]);
 #pragma unroll
@@ -80,10 +93,26 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
     const int o = o0 + rq + q;
     if (o >= O) break;
     const size_t idx = (rows0 + o) * G + g;
-    bool clamped;
-    const uint32_t nb = grid_update<FMT>(base[idx], __fmul_rn(acc[q], c), wd, clamped);
-    out[idx] = (uint8_t)nb;
-    if (mask) mask[idx] = clamped ? 0 : 1;
+    if (vec) {                                  // blocks g .. g + 3, one word each way
+      const uint32_t in = *reinterpret_cast<const uint32_t*>(base + idx);
+      uint32_t nw = 0, mw = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        bool clamped;
+        nw |= grid_update<FMT>((in >> (8 * j)) & 0xFFu, __fmul_rn(acc[q][j], c), wd, clamped) << (8 * j);
+        mw |= (clamped ? 0u : 1u) << (8 * j);
+      }
+      *reinterpret_cast<uint32_t*>(out + idx) = nw;
+      if (mask) *reinterpret_cast<uint32_t*>(mask + idx) = mw;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (g + j >= G) break;
+        bool clamped;
+        out[idx + j] = (uint8_t)grid_update<FMT>(base[idx + j], __fmul_rn(acc[q][j], c), wd, clamped);
+        if (mask) mask[idx + j] = clamped ? 0 : 1;
+      }
+    }
   }
 }
 
@@ -256,8 +285,10 @@ int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base,
     const uint16_t* Ap = a + (size_t)e0 * r * G;
     uint8_t* op = out + rows0 * G;
     uint8_t* mp = mask ? mask + rows0 * G : nullptr;
+    const auto al4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
+    const int vec = G % 4 == 0 && al4(bp) && al4(op) && (mp == nullptr || al4(mp)) ? 1 : 0;
 #define SQ_QAST_SCALES(F, R) \
-    hipLaunchKernelGGL((qast_scales_kernel<F, R>), grid, dim3(256), 0, s, bp, Bp, Ap, O, G, r, c, t, op, mp)
+    hipLaunchKernelGGL((qast_scales_kernel<F, R>), grid, dim3(256), 0, s, bp, Bp, Ap, O, G, r, c, t, op, mp, vec)
     if (fmt == kMX) {
       if (r <= 8) SQ_QAST_SCALES(kMX, 8);
       else if (r <= 16) SQ_QAST_SCALES(kMX, 16);
