@@ -18,8 +18,8 @@
 // for bit.  The factor gradients accumulate in fp32 in a fixed order (dB: over
 // the blocks in order; dA: rows in order within 32-row chunks, then the chunk
 // partials through a fixed per-lane order and butterfly): deterministic.  The
-// backward kernels stage 32-row x 64-block tiles of dS * m in LDS with all of
-// a tile's loads in flight together.
+// backward kernels stage tiles of dS * m in LDS with all of a tile's loads in
+// flight together.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -117,117 +117,156 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
 }
 
 // ------------------------------------------------------------------ dB, dA
-// Both backward products stage tiles of v = dS * m (32 rows x 64 blocks, fp32)
-// in LDS with every load of the tile issued together, plus the matching
-// factor tile.  blockIdx.y is the expert (its rows, its A).
-constexpr int kQRows = 32;          // rows per tile
-constexpr int kQCols = 64;          // blocks per tile
-constexpr int kDaRows = kQRows;
-
-__device__ __forceinline__ void stage_v(float (&vt)[kQRows][kQCols + 1], const float* __restrict__ dS,
-                                        const uint8_t* __restrict__ mask, int O, int G, int o0, int g0) {
-#pragma unroll
-  for (int u = 0; u < kQRows * kQCols / 256; ++u) {
-    const int i = threadIdx.x + 256 * u, ro = i / kQCols, gi = i % kQCols;
-    const int o = o0 + ro, g = g0 + gi;
-    float v = 0.0f;
-    if (o < O && g < G) {
-      const size_t at = (size_t)o * G + g;
-      v = dS[at];
-      if (mask) v *= (float)mask[at];
-    }
-    vt[ro][gi] = v;
-  }
-}
+// Both backward products stage tiles of v = dS * m (fp32) in LDS with every
+// load of the tile issued together, plus the matching factor tile, and give
+// each thread a 4 x 4 (dA: 4 x TG) block of outputs.  blockIdx.y is the
+// expert (its rows, its A).  dA is summed over 32-row chunks (partials in the
+// workspace, then a fixed-order reduction).
+constexpr int kDaRows = 32;         // rows per dA chunk
 
 // dB[o, k] = c sum over g in increasing order of v[o, g] A[k, g]: a workgroup
-// owns 32 rows and walks the blocks in tiles of 64; thread (k, row group)
-// accumulates 32 / (256 / RMAX) rows of one rank.
+// owns 4096 / RMAX rows and walks the blocks in tiles of 32, staging v and A
+// transposed ([g][row], [g][k]) so that thread (row group, rank group) reads
+// its four rows and four ranks of a block with two 16-byte LDS reads and adds
+// 16 products.
+constexpr int kDbCols = 32;
+template <int RMAX>
+constexpr int db_rows() { return 4 * (256 / (RMAX / 4)); }
+
 template <int RMAX>
 __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ dS, const uint8_t* __restrict__ mask,
                                                       const uint16_t* __restrict__ A, int O, int G, int r, float c,
                                                       float* __restrict__ dB) {
-  constexpr int kGroups = 256 / RMAX, kRowsPer = kQRows / kGroups;
-  __shared__ float vt[kQRows][kQCols + 1];
-  __shared__ float at[RMAX][kQCols + 1];
+  constexpr int KQ = RMAX / 4, ROWS = db_rows<RMAX>();
+  __shared__ __attribute__((aligned(16))) float vt[kDbCols][ROWS + 4];
+  __shared__ __attribute__((aligned(16))) float at[kDbCols][RMAX + 4];
   const int e = blockIdx.y;
   dS += (size_t)e * O * G;
   if (mask) mask += (size_t)e * O * G;
   A += (size_t)e * r * G;
   dB += (size_t)e * O * r;
-  const int o0 = blockIdx.x * kQRows;
-  const int k = threadIdx.x % RMAX, grp = threadIdx.x / RMAX;
-  float acc[kRowsPer];
+  const int o0 = blockIdx.x * ROWS;
+  const int kq = (threadIdx.x % KQ) * 4, rq = (threadIdx.x / KQ) * 4;
+  float acc[4][4];
 #pragma unroll
-  for (int q = 0; q < kRowsPer; ++q) acc[q] = 0.0f;
-  for (int g0 = 0; g0 < G; g0 += kQCols) {
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[q][j] = 0.0f;
+  for (int g0 = 0; g0 < G; g0 += kDbCols) {
     __syncthreads();                                     // the previous tiles are consumed
-    stage_v(vt, dS, mask, O, G, o0, g0);
+#pragma unroll 4
+    for (int u = 0; u < ROWS * kDbCols / 256; ++u) {
+      const int i = threadIdx.x + 256 * u, ro = i / kDbCols, gi = i % kDbCols;
+      const int o = o0 + ro, g = g0 + gi;
+      float v = 0.0f;
+      if (o < O && g < G) {
+        const size_t at_ = (size_t)o * G + g;
+        v = dS[at_];
+        if (mask) v *= (float)mask[at_];
+      }
+      vt[gi][ro] = v;
+    }
 #pragma unroll
-    for (int u = 0; u < RMAX * kQCols / 256; ++u) {
-      const int i = threadIdx.x + 256 * u, kk = i / kQCols, gi = i % kQCols;
-      at[kk][gi] = (kk < r && g0 + gi < G) ? bf16_bits_to_f32(A[(size_t)kk * G + g0 + gi]) : 0.0f;
+    for (int u = 0; u < RMAX * kDbCols / 256; ++u) {
+      const int i = threadIdx.x + 256 * u, kk = i / kDbCols, gi = i % kDbCols;
+      at[gi][kk] = (kk < r && g0 + gi < G) ? bf16_bits_to_f32(A[(size_t)kk * G + g0 + gi]) : 0.0f;
     }
     __syncthreads();
-    const int gn = min(kQCols, G - g0);
+    const int gn = min(kDbCols, G - g0);
     for (int gi = 0; gi < gn; ++gi) {
-      const float a = at[k][gi];
+      const float4 a = *reinterpret_cast<const float4*>(&at[gi][kq]);
+      const float4 v = *reinterpret_cast<const float4*>(&vt[gi][rq]);
+      const float av[4] = {a.x, a.y, a.z, a.w}, vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int q = 0; q < kRowsPer; ++q) acc[q] = __builtin_fmaf(vt[grp * kRowsPer + q][gi], a, acc[q]);
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) acc[q][jj] = __builtin_fmaf(vv[q], av[jj], acc[q][jj]);
     }
   }
-  if (k >= r) return;
 #pragma unroll
-  for (int q = 0; q < kRowsPer; ++q) {
-    const int o = o0 + grp * kRowsPer + q;
-    if (o < O) dB[(size_t)o * r + k] = __fmul_rn(acc[q], c);
+  for (int q = 0; q < 4; ++q) {
+    const int o = o0 + rq + q;
+    if (o >= O) break;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      if (kq + jj < r) dB[(size_t)o * r + kq + jj] = __fmul_rn(acc[q][jj], c);
   }
 }
 
-// Partial dA over one 32-row chunk and 64 blocks: part[chunk][k][g] = sum
-// over the chunk's rows in increasing order of B[o, k] v[o, g]; thread
-// (g, rank group) accumulates RMAX / 4 ranks of one block.
+// Partial dA over one 32-row chunk: part[chunk][k][g] = sum over the chunk's
+// rows in increasing order of B[o, k] v[o, g].  A workgroup takes the chunk's
+// rows for 1024 TG / RMAX blocks; thread (rank group, block group) holds four
+// ranks and TG blocks (TG = RMAX / 16, at least 1) and per row reads them
+// with one 16-byte and one TG-wide LDS read.
+template <int RMAX>
+constexpr int da_tg() { return RMAX >= 16 ? RMAX / 16 : 1; }
+template <int RMAX>
+constexpr int da_cols() { return 1024 * da_tg<RMAX>() / RMAX; }
+
 template <int RMAX>
 __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __restrict__ dS,
                                                               const uint8_t* __restrict__ mask,
                                                               const uint16_t* __restrict__ B, int O, int G, int r,
                                                               float* __restrict__ part) {
-  constexpr int KW = RMAX / 4;
-  __shared__ float vt[kQRows][kQCols + 1];
-  __shared__ float bt[kQRows][RMAX + 1];
+  constexpr int TG = da_tg<RMAX>(), GT = da_cols<RMAX>(), KQ = RMAX / 4;
+  static_assert(KQ * (GT / TG) == 256, "a thread per rank group and block group");
+  __shared__ __attribute__((aligned(16))) float vt[kDaRows][GT + 4];
+  __shared__ __attribute__((aligned(16))) float bt[kDaRows][RMAX + 4];
   const int e = blockIdx.y;
-  const int chunks = (O + kQRows - 1) / kQRows;
+  const int chunks = (O + kDaRows - 1) / kDaRows;
   dS += (size_t)e * O * G;
   if (mask) mask += (size_t)e * O * G;
   B += (size_t)e * O * r;
   part += (size_t)e * chunks * r * G;
-  const int gtiles = (G + kQCols - 1) / kQCols;
-  const int chunk = (int)blockIdx.x / gtiles, g0 = ((int)blockIdx.x % gtiles) * kQCols;
-  const int o0 = chunk * kQRows;
-  stage_v(vt, dS, mask, O, G, o0, g0);
+  const int gtiles = (G + GT - 1) / GT;
+  const int chunk = (int)blockIdx.x / gtiles, g0 = ((int)blockIdx.x % gtiles) * GT;
+  const int o0 = chunk * kDaRows;
+#pragma unroll 4
+  for (int u = 0; u < kDaRows * GT / 256; ++u) {
+    const int i = threadIdx.x + 256 * u, ro = i / GT, gi = i % GT;
+    const int o = o0 + ro, g = g0 + gi;
+    float v = 0.0f;
+    if (o < O && g < G) {
+      const size_t at_ = (size_t)o * G + g;
+      v = dS[at_];
+      if (mask) v *= (float)mask[at_];
+    }
+    vt[ro][gi] = v;
+  }
 #pragma unroll
-  for (int u = 0; u < (kQRows * RMAX + 255) / 256; ++u) {
+  for (int u = 0; u < (kDaRows * RMAX + 255) / 256; ++u) {
     const int i = threadIdx.x + 256 * u;
-    if (i < kQRows * RMAX) {
+    if (i < kDaRows * RMAX) {
       const int ro = i / RMAX, kk = i % RMAX;
       bt[ro][kk] = (kk < r && o0 + ro < O) ? bf16_bits_to_f32(B[(size_t)(o0 + ro) * r + kk]) : 0.0f;
     }
   }
   __syncthreads();
-  const int gi = threadIdx.x % kQCols, k0 = (threadIdx.x / kQCols) * KW;
-  float acc[KW];
+  const int kq = (threadIdx.x % KQ) * 4, gq = (threadIdx.x / KQ) * TG;
+  float acc[4][TG];
 #pragma unroll
-  for (int j = 0; j < KW; ++j) acc[j] = 0.0f;
-  const int on = min(kQRows, O - o0);
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int t = 0; t < TG; ++t) acc[j][t] = 0.0f;
+  const int on = min(kDaRows, O - o0);
   for (int ro = 0; ro < on; ++ro) {
-    const float v = vt[ro][gi];
+    const float4 b = *reinterpret_cast<const float4*>(&bt[ro][kq]);
+    const float bv[4] = {b.x, b.y, b.z, b.w};
+    float vv[TG];
 #pragma unroll
-    for (int j = 0; j < KW; ++j) acc[j] = __builtin_fmaf(bt[ro][k0 + j], v, acc[j]);
+    for (int t = 0; t < TG; ++t) vv[t] = vt[ro][gq + t];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int t = 0; t < TG; ++t) acc[j][t] = __builtin_fmaf(bv[j], vv[t], acc[j][t]);
   }
-  if (g0 + gi >= G) return;
 #pragma unroll
-  for (int j = 0; j < KW; ++j)
-    if (k0 + j < r) part[((size_t)chunk * r + k0 + j) * G + g0 + gi] = acc[j];
+  for (int j = 0; j < 4; ++j) {
+    if (kq + j >= r) break;
+#pragma unroll
+    for (int t = 0; t < TG; ++t)
+      if (g0 + gq + t < G) part[((size_t)chunk * r + kq + j) * G + g0 + gq + t] = acc[j][t];
+  }
 }
 
 // dA[i] = c sum over the chunk partials.  Up to 64 chunks: a thread per
@@ -312,12 +351,12 @@ size_t qast_grads_workspace(int E, int O, int G, int r) {
 template <int RMAX>
 static int qast_grads_r(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
                         const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
-  const int chunks = (O + kQRows - 1) / kQRows;
-  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)chunks, (unsigned)E), dim3(256), 0, s, dS, mask, A, O, G, r,
-                     c, dB);
+  const int chunks = (O + kDaRows - 1) / kDaRows;
+  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + db_rows<RMAX>() - 1) / db_rows<RMAX>()), (unsigned)E),
+                     dim3(256), 0, s, dS, mask, A, O, G, r, c, dB);
   hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>,
-                     dim3((unsigned)(((G + kQCols - 1) / kQCols) * (int64_t)chunks), (unsigned)E), dim3(256), 0, s,
-                     dS, mask, B, O, G, r, part);
+                     dim3((unsigned)(((G + da_cols<RMAX>() - 1) / da_cols<RMAX>()) * (int64_t)chunks), (unsigned)E),
+                     dim3(256), 0, s, dS, mask, B, O, G, r, part);
   const int64_t n = (int64_t)E * r * G;
   const int64_t rblocks = chunks <= kDaFewChunks ? (n + 255) / 256 : (n + 3) / 4;
   hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, part, chunks, r, G, E, c, dA);
