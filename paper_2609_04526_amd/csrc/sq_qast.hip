@@ -32,58 +32,70 @@ namespace sq {
 __device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 // ------------------------------------------------------------------ scales
-// A workgroup per tile of 128 rows x 32 blocks of one expert (blockIdx.y):
-// the tile's A columns [RMAX][32] and B rows, transposed to [RMAX][128], are
+// A workgroup per tile of 32 TB rows x 32 blocks of one expert (blockIdx.y):
+// the tile's A columns [RMAX][32] and B rows, transposed to [RMAX][32 TB], are
 // staged in LDS as fp32 (every load issued together; ranks past r are 0 and
 // add exact zeros), and thread (row group, block group) adds the r terms of
-// its 4 x 4 outputs in increasing k, two 16-byte LDS reads per 16 fused
-// multiply-adds.  Where G % 4 == 0 and the byte planes are 4-byte aligned
-// (vec), a thread's four blocks of a row are one 4-byte load and store.
-// Experts are stacked: rows e*O .. e*O + O - 1 of base, B, out and mask
-// belong to expert e, whose A is A + e*r*G and whose ws2 is ws2[e].
-constexpr int kScRows = 128;
+// its 4 rows x TB blocks in increasing k, with a 16-byte LDS read of B and a
+// TB-wide one of A per 4 TB fused multiply-adds.  TB = 4 where the tiles
+// still give every CU two workgroups (the stacked experts of an MoE layer),
+// else TB = 1 (one linear: four times the workgroups).  With TB = 4, where
+// G % 4 == 0 and the byte planes are 4-byte aligned (vec), a thread's four
+// blocks of a row are one 4-byte load and store.  Experts are stacked: rows
+// e*O .. e*O + O - 1 of base, B, out and mask belong to expert e, whose A is
+// A + e*r*G and whose ws2 is ws2[e].
 constexpr int kScCols = 32;
+template <int TB>
+constexpr int sc_rows() { return 32 * TB; }
 
-template <int FMT, int RMAX>
+template <int FMT, int RMAX, int TB>
 __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restrict__ base,
                                                           const uint16_t* __restrict__ B,
                                                           const uint16_t* __restrict__ A, int O, int G, int r,
                                                           float c, Ws2Table ws2, uint8_t* out, uint8_t* mask,
                                                           int vec) {
-  constexpr int kAPad = kScCols + 4, kBPad = kScRows + 4;    // rows stay 16-byte aligned
+  constexpr int ROWS = sc_rows<TB>();
+  constexpr int kAPad = kScCols + 4, kBPad = ROWS + 4;      // rows stay 16-byte aligned
   __shared__ __attribute__((aligned(16))) float at[RMAX][kAPad];
   __shared__ __attribute__((aligned(16))) float bt[RMAX][kBPad];
   const int e = blockIdx.y;
   const size_t rows0 = (size_t)e * O;
   const uint16_t* ae = A + (size_t)e * r * G;
   const int gtiles = (G + kScCols - 1) / kScCols;
-  const int o0 = ((int)blockIdx.x / gtiles) * kScRows, g0 = ((int)blockIdx.x % gtiles) * kScCols;
+  const int o0 = ((int)blockIdx.x / gtiles) * ROWS, g0 = ((int)blockIdx.x % gtiles) * kScCols;
 #pragma unroll
   for (int u = 0; u < RMAX * kScCols / 256; ++u) {
     const int i = threadIdx.x + 256 * u, k = i / kScCols, gi = i % kScCols;
     at[k][gi] = (k < r && g0 + gi < G) ? bf16_bits_to_f32(ae[(size_t)k * G + g0 + gi]) : 0.0f;
   }
 #pragma unroll
-  for (int u = 0; u < kScRows * RMAX / 256; ++u) {
+  for (int u = 0; u < ROWS * RMAX / 256; ++u) {
     const int i = threadIdx.x + 256 * u, ro = i / RMAX, k = i % RMAX;
     bt[k][ro] = (k < r && o0 + ro < O) ? bf16_bits_to_f32(B[(rows0 + o0 + ro) * r + k]) : 0.0f;
   }
   __syncthreads();
-  const int gq = (threadIdx.x % (kScCols / 4)) * 4, rq = (threadIdx.x / (kScCols / 4)) * 4;
-  float acc[4][4];
+  const int gq = (threadIdx.x % (kScCols / TB)) * TB, rq = (threadIdx.x / (kScCols / TB)) * 4;
+  float acc[4][TB];
 #pragma unroll
   for (int q = 0; q < 4; ++q)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[q][j] = 0.0f;
+    for (int j = 0; j < TB; ++j) acc[q][j] = 0.0f;
 #pragma unroll 4
   for (int k = 0; k < RMAX; ++k) {
-    const float4 a = *reinterpret_cast<const float4*>(&at[k][gq]);
+    float av[TB];
+    if constexpr (TB == 4) {
+      const float4 a = *reinterpret_cast<const float4*>(&at[k][gq]);
+      av[0] = a.x; av[1] = a.y; av[2] = a.z; av[3] = a.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < TB; ++j) av[j] = at[k][gq + j];
+    }
     const float4 b = *reinterpret_cast<const float4*>(&bt[k][rq]);
-    const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+    const float bv[4] = {b.x, b.y, b.z, b.w};
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[q][j] = __builtin_fmaf(bv[q], av[j], acc[q][j]);
+      for (int j = 0; j < TB; ++j) acc[q][j] = __builtin_fmaf(bv[q], av[j], acc[q][j]);
   }
   const int g = g0 + gq;
   if (g >= G) return;
@@ -93,11 +105,11 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
     const int o = o0 + rq + q;
     if (o >= O) break;
     const size_t idx = (rows0 + o) * G + g;
-    if (vec) {                                  // blocks g .. g + 3, one word each way
+    if (TB == 4 && vec) {                       // blocks g .. g + 3, one word each way
       const uint32_t in = *reinterpret_cast<const uint32_t*>(base + idx);
       uint32_t nw = 0, mw = 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < TB; ++j) {
         bool clamped;
         nw |= grid_update<FMT>((in >> (8 * j)) & 0xFFu, __fmul_rn(acc[q][j], c), wd, clamped) << (8 * j);
         mw |= (clamped ? 0u : 1u) << (8 * j);
@@ -106,7 +118,7 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
       if (mask) *reinterpret_cast<uint32_t*>(mask + idx) = mw;
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < TB; ++j) {
         if (g + j >= G) break;
         bool clamped;
         out[idx + j] = (uint8_t)grid_update<FMT>(base[idx + j], __fmul_rn(acc[q][j], c), wd, clamped);
@@ -125,19 +137,20 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
 constexpr int kDaRows = 32;         // rows per dA chunk
 
 // dB[o, k] = c sum over g in increasing order of v[o, g] A[k, g]: a workgroup
-// owns 4096 / RMAX rows and walks the blocks in tiles of 32, staging v and A
-// transposed ([g][row], [g][k]) so that thread (row group, rank group) reads
-// its four rows and four ranks of a block with two 16-byte LDS reads and adds
-// 16 products.
+// owns 1024 RT / RMAX rows and walks the blocks in tiles of 32, staging v and
+// A transposed ([g][row], [g][k]) so that thread (row group, rank group)
+// reads its RT rows and four ranks of a block with two LDS reads and adds
+// 4 RT products.  RT = 4 where that still gives every CU two workgroups,
+// else RT = 1.
 constexpr int kDbCols = 32;
-template <int RMAX>
-constexpr int db_rows() { return 4 * (256 / (RMAX / 4)); }
+template <int RMAX, int RT>
+constexpr int db_rows() { return RT * (256 / (RMAX / 4)); }
 
-template <int RMAX>
+template <int RMAX, int RT>
 __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ dS, const uint8_t* __restrict__ mask,
                                                       const uint16_t* __restrict__ A, int O, int G, int r, float c,
                                                       float* __restrict__ dB) {
-  constexpr int KQ = RMAX / 4, ROWS = db_rows<RMAX>();
+  constexpr int KQ = RMAX / 4, ROWS = db_rows<RMAX, RT>();
   __shared__ __attribute__((aligned(16))) float vt[kDbCols][ROWS + 4];
   __shared__ __attribute__((aligned(16))) float at[kDbCols][RMAX + 4];
   const int e = blockIdx.y;
@@ -146,10 +159,10 @@ __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ 
   A += (size_t)e * r * G;
   dB += (size_t)e * O * r;
   const int o0 = blockIdx.x * ROWS;
-  const int kq = (threadIdx.x % KQ) * 4, rq = (threadIdx.x / KQ) * 4;
-  float acc[4][4];
+  const int kq = (threadIdx.x % KQ) * 4, rq = (threadIdx.x / KQ) * RT;
+  float acc[RT][4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
+  for (int q = 0; q < RT; ++q)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[q][j] = 0.0f;
   for (int g0 = 0; g0 < G; g0 += kDbCols) {
@@ -175,16 +188,23 @@ __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ 
     const int gn = min(kDbCols, G - g0);
     for (int gi = 0; gi < gn; ++gi) {
       const float4 a = *reinterpret_cast<const float4*>(&at[gi][kq]);
-      const float4 v = *reinterpret_cast<const float4*>(&vt[gi][rq]);
-      const float av[4] = {a.x, a.y, a.z, a.w}, vv[4] = {v.x, v.y, v.z, v.w};
+      const float av[4] = {a.x, a.y, a.z, a.w};
+      float vv[RT];
+      if constexpr (RT == 4) {
+        const float4 v = *reinterpret_cast<const float4*>(&vt[gi][rq]);
+        vv[0] = v.x; vv[1] = v.y; vv[2] = v.z; vv[3] = v.w;
+      } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+        for (int q = 0; q < RT; ++q) vv[q] = vt[gi][rq + q];
+      }
+#pragma unroll
+      for (int q = 0; q < RT; ++q)
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) acc[q][jj] = __builtin_fmaf(vv[q], av[jj], acc[q][jj]);
     }
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < RT; ++q) {
     const int o = o0 + rq + q;
     if (o >= O) break;
 #pragma unroll
@@ -308,6 +328,16 @@ __global__ __launch_bounds__(256) void qast_da_reduce_kernel(const float* __rest
 }
 
 // ------------------------------------------------------------------ launch
+constexpr int kQastCUs = 256;        // MI355X compute units
+
+template <int F, int R>
+static void scales_tb(bool tb4, dim3 grid, hipStream_t s, const uint8_t* bp, const uint16_t* Bp, const uint16_t* Ap,
+                      int O, int G, int r, float c, const Ws2Table& t, uint8_t* op, uint8_t* mp, int vec) {
+  if (tb4)
+    hipLaunchKernelGGL((qast_scales_kernel<F, R, 4>), grid, dim3(256), 0, s, bp, Bp, Ap, O, G, r, c, t, op, mp, vec);
+  else
+    hipLaunchKernelGGL((qast_scales_kernel<F, R, 1>), grid, dim3(256), 0, s, bp, Bp, Ap, O, G, r, c, t, op, mp, 0);
+}
 int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base, const void* B, const void* A,
                        float c, const float* ws2, uint8_t* out, uint8_t* mask, hipStream_t s) {
   const uint16_t* b = static_cast<const uint16_t*>(B);
@@ -317,8 +347,11 @@ int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base,
     Ws2Table t;
     for (int e = 0; e < m; ++e) t.v[e] = fmt == kNV ? ws2[e0 + e] : 1.0f;
     const size_t rows0 = (size_t)e0 * O;
-    const dim3 grid((unsigned)(((O + kScRows - 1) / kScRows) * (int64_t)((G + kScCols - 1) / kScCols)),
-                    (unsigned)m);
+    const int64_t gtiles = (G + kScCols - 1) / kScCols;
+    const int64_t wide = ((O + sc_rows<4>() - 1) / sc_rows<4>()) * gtiles * m;   // workgroups with TB = 4
+    const bool tb4 = wide >= 2 * kQastCUs;
+    const int rows = tb4 ? sc_rows<4>() : sc_rows<1>();
+    const dim3 grid((unsigned)(((O + rows - 1) / rows) * gtiles), (unsigned)m);
     const uint8_t* bp = base + rows0 * G;
     const uint16_t* Bp = b + rows0 * r;
     const uint16_t* Ap = a + (size_t)e0 * r * G;
@@ -326,8 +359,7 @@ int qast_scales_launch(int fmt, int E, int O, int G, int r, const uint8_t* base,
     uint8_t* mp = mask ? mask + rows0 * G : nullptr;
     const auto al4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
     const int vec = G % 4 == 0 && al4(bp) && al4(op) && (mp == nullptr || al4(mp)) ? 1 : 0;
-#define SQ_QAST_SCALES(F, R) \
-    hipLaunchKernelGGL((qast_scales_kernel<F, R>), grid, dim3(256), 0, s, bp, Bp, Ap, O, G, r, c, t, op, mp, vec)
+#define SQ_QAST_SCALES(F, R) scales_tb<F, R>(tb4, grid, s, bp, Bp, Ap, O, G, r, c, t, op, mp, vec)
     if (fmt == kMX) {
       if (r <= 8) SQ_QAST_SCALES(kMX, 8);
       else if (r <= 16) SQ_QAST_SCALES(kMX, 16);
@@ -352,8 +384,13 @@ template <int RMAX>
 static int qast_grads_r(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
                         const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
   const int chunks = (O + kDaRows - 1) / kDaRows;
-  hipLaunchKernelGGL(qast_db_kernel<RMAX>, dim3((unsigned)((O + db_rows<RMAX>() - 1) / db_rows<RMAX>()), (unsigned)E),
-                     dim3(256), 0, s, dS, mask, A, O, G, r, c, dB);
+  constexpr int kWide = db_rows<RMAX, 4>(), kNarrow = db_rows<RMAX, 1>();
+  if ((int64_t)((O + kWide - 1) / kWide) * E >= 2 * kQastCUs)
+    hipLaunchKernelGGL((qast_db_kernel<RMAX, 4>), dim3((unsigned)((O + kWide - 1) / kWide), (unsigned)E), dim3(256), 0,
+                       s, dS, mask, A, O, G, r, c, dB);
+  else
+    hipLaunchKernelGGL((qast_db_kernel<RMAX, 1>), dim3((unsigned)((O + kNarrow - 1) / kNarrow), (unsigned)E), dim3(256),
+                       0, s, dS, mask, A, O, G, r, c, dB);
   hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>,
                      dim3((unsigned)(((G + da_cols<RMAX>() - 1) / da_cols<RMAX>()) * (int64_t)chunks), (unsigned)E),
                      dim3(256), 0, s, dS, mask, B, O, G, r, part);
