@@ -136,6 +136,25 @@ __global__ __launch_bounds__(256) void qast_scales_kernel(const uint8_t* __restr
 // workspace, then a fixed-order reduction).
 constexpr int kDaRows = 32;         // rows per dA chunk
 
+// v = dS * m at blocks g .. g + 3 of row o (G % 4 == 0, dS 16-byte and mask
+// 4-byte aligned: one 16-byte and one 4-byte load); zeros past the plane.
+__device__ __forceinline__ float4 load_v4(const float* __restrict__ dS, const uint8_t* __restrict__ mask, int O,
+                                          int G, int o, int g) {
+  float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  if (o < O && g < G) {
+    const size_t at_ = (size_t)o * G + g;
+    v = *reinterpret_cast<const float4*>(dS + at_);
+    if (mask) {
+      const uint32_t m = *reinterpret_cast<const uint32_t*>(mask + at_);
+      v.x *= (float)(m & 0xFFu);
+      v.y *= (float)((m >> 8) & 0xFFu);
+      v.z *= (float)((m >> 16) & 0xFFu);
+      v.w *= (float)(m >> 24);
+    }
+  }
+  return v;
+}
+
 // dB[o, k] = c sum over g in increasing order of v[o, g] A[k, g]: a workgroup
 // owns 1024 RT / RMAX rows and walks the blocks in tiles of 32, staging v and
 // A transposed ([g][row], [g][k]) so that thread (row group, rank group)
@@ -149,7 +168,7 @@ constexpr int db_rows() { return RT * (256 / (RMAX / 4)); }
 template <int RMAX, int RT>
 __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ dS, const uint8_t* __restrict__ mask,
                                                       const uint16_t* __restrict__ A, int O, int G, int r, float c,
-                                                      float* __restrict__ dB) {
+                                                      float* __restrict__ dB, int vec) {
   constexpr int KQ = RMAX / 4, ROWS = db_rows<RMAX, RT>();
   __shared__ __attribute__((aligned(16))) float vt[kDbCols][ROWS + 4];
   __shared__ __attribute__((aligned(16))) float at[kDbCols][RMAX + 4];
@@ -167,17 +186,30 @@ __global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ 
     for (int j = 0; j < 4; ++j) acc[q][j] = 0.0f;
   for (int g0 = 0; g0 < G; g0 += kDbCols) {
     __syncthreads();                                     // the previous tiles are consumed
-#pragma unroll 4
-    for (int u = 0; u < ROWS * kDbCols / 256; ++u) {
-      const int i = threadIdx.x + 256 * u, ro = i / kDbCols, gi = i % kDbCols;
-      const int o = o0 + ro, g = g0 + gi;
-      float v = 0.0f;
-      if (o < O && g < G) {
-        const size_t at_ = (size_t)o * G + g;
-        v = dS[at_];
-        if (mask) v *= (float)mask[at_];
+    if (vec) {
+#pragma unroll
+      for (int u = 0; u < (ROWS * kDbCols / 4 + 255) / 256; ++u) {
+        const int i = threadIdx.x + 256 * u, ro = i / (kDbCols / 4), gq = (i % (kDbCols / 4)) * 4;
+        if (ROWS * kDbCols / 4 % 256 != 0 && i >= ROWS * kDbCols / 4) break;
+        const float4 v = load_v4(dS, mask, O, G, o0 + ro, g0 + gq);
+        vt[gq][ro] = v.x;
+        vt[gq + 1][ro] = v.y;
+        vt[gq + 2][ro] = v.z;
+        vt[gq + 3][ro] = v.w;
       }
-      vt[gi][ro] = v;
+    } else {
+#pragma unroll 4
+      for (int u = 0; u < ROWS * kDbCols / 256; ++u) {
+        const int i = threadIdx.x + 256 * u, ro = i / kDbCols, gi = i % kDbCols;
+        const int o = o0 + ro, g = g0 + gi;
+        float v = 0.0f;
+        if (o < O && g < G) {
+          const size_t at_ = (size_t)o * G + g;
+          v = dS[at_];
+          if (mask) v *= (float)mask[at_];
+        }
+        vt[gi][ro] = v;
+      }
     }
 #pragma unroll
     for (int u = 0; u < RMAX * kDbCols / 256; ++u) {
@@ -227,7 +259,7 @@ template <int RMAX>
 __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __restrict__ dS,
                                                               const uint8_t* __restrict__ mask,
                                                               const uint16_t* __restrict__ B, int O, int G, int r,
-                                                              float* __restrict__ part) {
+                                                              float* __restrict__ part, int vec) {
   constexpr int TG = da_tg<RMAX>(), GT = da_cols<RMAX>(), KQ = RMAX / 4;
   static_assert(KQ * (GT / TG) == 256, "a thread per rank group and block group");
   __shared__ __attribute__((aligned(16))) float vt[kDaRows][GT + 4];
@@ -241,17 +273,26 @@ __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __res
   const int gtiles = (G + GT - 1) / GT;
   const int chunk = (int)blockIdx.x / gtiles, g0 = ((int)blockIdx.x % gtiles) * GT;
   const int o0 = chunk * kDaRows;
-#pragma unroll 4
-  for (int u = 0; u < kDaRows * GT / 256; ++u) {
-    const int i = threadIdx.x + 256 * u, ro = i / GT, gi = i % GT;
-    const int o = o0 + ro, g = g0 + gi;
-    float v = 0.0f;
-    if (o < O && g < G) {
-      const size_t at_ = (size_t)o * G + g;
-      v = dS[at_];
-      if (mask) v *= (float)mask[at_];
+  static_assert(kDaRows * GT % 1024 == 0, "whole 16-byte loads per thread");
+  if (vec) {
+#pragma unroll
+    for (int u = 0; u < kDaRows * GT / 1024; ++u) {
+      const int i = threadIdx.x + 256 * u, ro = i / (GT / 4), gq = (i % (GT / 4)) * 4;
+      *reinterpret_cast<float4*>(&vt[ro][gq]) = load_v4(dS, mask, O, G, o0 + ro, g0 + gq);
     }
-    vt[ro][gi] = v;
+  } else {
+#pragma unroll 4
+    for (int u = 0; u < kDaRows * GT / 256; ++u) {
+      const int i = threadIdx.x + 256 * u, ro = i / GT, gi = i % GT;
+      const int o = o0 + ro, g = g0 + gi;
+      float v = 0.0f;
+      if (o < O && g < G) {
+        const size_t at_ = (size_t)o * G + g;
+        v = dS[at_];
+        if (mask) v *= (float)mask[at_];
+      }
+      vt[ro][gi] = v;
+    }
   }
 #pragma unroll
   for (int u = 0; u < (kDaRows * RMAX + 255) / 256; ++u) {
@@ -384,16 +425,18 @@ template <int RMAX>
 static int qast_grads_r(int E, int O, int G, int r, const float* dS, const uint8_t* mask, const uint16_t* B,
                         const uint16_t* A, float c, float* dB, float* dA, float* part, hipStream_t s) {
   const int chunks = (O + kDaRows - 1) / kDaRows;
+  const int vec = G % 4 == 0 && (reinterpret_cast<uintptr_t>(dS) & 15) == 0 &&
+                  (mask == nullptr || (reinterpret_cast<uintptr_t>(mask) & 3) == 0) ? 1 : 0;
   constexpr int kWide = db_rows<RMAX, 4>(), kNarrow = db_rows<RMAX, 1>();
   if ((int64_t)((O + kWide - 1) / kWide) * E >= 2 * kQastCUs)
     hipLaunchKernelGGL((qast_db_kernel<RMAX, 4>), dim3((unsigned)((O + kWide - 1) / kWide), (unsigned)E), dim3(256), 0,
-                       s, dS, mask, A, O, G, r, c, dB);
+                       s, dS, mask, A, O, G, r, c, dB, vec);
   else
     hipLaunchKernelGGL((qast_db_kernel<RMAX, 1>), dim3((unsigned)((O + kNarrow - 1) / kNarrow), (unsigned)E), dim3(256),
-                       0, s, dS, mask, A, O, G, r, c, dB);
+                       0, s, dS, mask, A, O, G, r, c, dB, vec);
   hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>,
                      dim3((unsigned)(((G + da_cols<RMAX>() - 1) / da_cols<RMAX>()) * (int64_t)chunks), (unsigned)E),
-                     dim3(256), 0, s, dS, mask, B, O, G, r, part);
+                     dim3(256), 0, s, dS, mask, B, O, G, r, part, vec);
   const int64_t n = (int64_t)E * r * G;
   const int64_t rblocks = chunks <= kDaFewChunks ? (n + 255) / 256 : (n + 3) / 4;
   hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, part, chunks, r, G, E, c, dA);
