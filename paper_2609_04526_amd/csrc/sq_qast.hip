@@ -166,18 +166,20 @@ template <int RMAX, int RT>
 constexpr int db_rows() { return RT * (256 / (RMAX / 4)); }
 
 template <int RMAX, int RT>
-__global__ __launch_bounds__(256) void qast_db_kernel(const float* __restrict__ dS, const uint8_t* __restrict__ mask,
-                                                      const uint16_t* __restrict__ A, int O, int G, int r, float c,
-                                                      float* __restrict__ dB, int vec) {
+constexpr int db_lds_floats() { return kDbCols * (db_rows<RMAX, RT>() + 4) + kDbCols * (RMAX + 4); }
+
+template <int RMAX, int RT>
+__device__ __forceinline__ void db_tile(int bx, int e, float* lds, const float* __restrict__ dS,
+                                        const uint8_t* __restrict__ mask, const uint16_t* __restrict__ A, int O,
+                                        int G, int r, float c, float* __restrict__ dB, int vec) {
   constexpr int KQ = RMAX / 4, ROWS = db_rows<RMAX, RT>();
-  __shared__ __attribute__((aligned(16))) float vt[kDbCols][ROWS + 4];
-  __shared__ __attribute__((aligned(16))) float at[kDbCols][RMAX + 4];
-  const int e = blockIdx.y;
+  float (*vt)[ROWS + 4] = reinterpret_cast<float (*)[ROWS + 4]>(lds);
+  float (*at)[RMAX + 4] = reinterpret_cast<float (*)[RMAX + 4]>(lds + kDbCols * (ROWS + 4));
   dS += (size_t)e * O * G;
   if (mask) mask += (size_t)e * O * G;
   A += (size_t)e * r * G;
   dB += (size_t)e * O * r;
-  const int o0 = blockIdx.x * ROWS;
+  const int o0 = bx * ROWS;
   const int kq = (threadIdx.x % KQ) * 4, rq = (threadIdx.x / KQ) * RT;
   float acc[RT][4];
 #pragma unroll
@@ -256,22 +258,23 @@ template <int RMAX>
 constexpr int da_cols() { return 1024 * da_tg<RMAX>() / RMAX; }
 
 template <int RMAX>
-__global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __restrict__ dS,
-                                                              const uint8_t* __restrict__ mask,
-                                                              const uint16_t* __restrict__ B, int O, int G, int r,
-                                                              float* __restrict__ part, int vec) {
+constexpr int da_lds_floats() { return kDaRows * (da_cols<RMAX>() + 4) + kDaRows * (RMAX + 4); }
+
+template <int RMAX>
+__device__ __forceinline__ void da_tile(int bx, int e, float* lds, const float* __restrict__ dS,
+                                        const uint8_t* __restrict__ mask, const uint16_t* __restrict__ B, int O,
+                                        int G, int r, float* __restrict__ part, int vec) {
   constexpr int TG = da_tg<RMAX>(), GT = da_cols<RMAX>(), KQ = RMAX / 4;
   static_assert(KQ * (GT / TG) == 256, "a thread per rank group and block group");
-  __shared__ __attribute__((aligned(16))) float vt[kDaRows][GT + 4];
-  __shared__ __attribute__((aligned(16))) float bt[kDaRows][RMAX + 4];
-  const int e = blockIdx.y;
+  float (*vt)[GT + 4] = reinterpret_cast<float (*)[GT + 4]>(lds);
+  float (*bt)[RMAX + 4] = reinterpret_cast<float (*)[RMAX + 4]>(lds + kDaRows * (GT + 4));
   const int chunks = (O + kDaRows - 1) / kDaRows;
   dS += (size_t)e * O * G;
   if (mask) mask += (size_t)e * O * G;
   B += (size_t)e * O * r;
   part += (size_t)e * chunks * r * G;
   const int gtiles = (G + GT - 1) / GT;
-  const int chunk = (int)blockIdx.x / gtiles, g0 = ((int)blockIdx.x % gtiles) * GT;
+  const int chunk = bx / gtiles, g0 = (bx % gtiles) * GT;
   const int o0 = chunk * kDaRows;
   static_assert(kDaRows * GT % 1024 == 0, "whole 16-byte loads per thread");
   if (vec) {
@@ -328,6 +331,25 @@ __global__ __launch_bounds__(256) void qast_da_partial_kernel(const float* __res
     for (int t = 0; t < TG; ++t)
       if (g0 + gq + t < G) part[((size_t)chunk * r + kq + j) * G + g0 + gq + t] = acc[j][t];
   }
+}
+
+// dB and the dA partials read the same v but are independent: one launch runs
+// both, workgroups below ndb taking dB rows and the rest dA chunks, so the
+// two short passes overlap instead of running one after the other.
+template <int RMAX, int RT>
+__global__ __launch_bounds__(256) void qast_grads_kernel(const float* __restrict__ dS,
+                                                         const uint8_t* __restrict__ mask,
+                                                         const uint16_t* __restrict__ A,
+                                                         const uint16_t* __restrict__ B, int O, int G, int r,
+                                                         float c, float* __restrict__ dB, float* __restrict__ part,
+                                                         int ndb, int vec) {
+  constexpr int kDb = db_lds_floats<RMAX, RT>(), kDa = da_lds_floats<RMAX>();
+  __shared__ __attribute__((aligned(16))) float lds[kDb > kDa ? kDb : kDa];
+  const int bx = (int)blockIdx.x, e = (int)blockIdx.y;
+  if (bx < ndb)
+    db_tile<RMAX, RT>(bx, e, lds, dS, mask, A, O, G, r, c, dB, vec);
+  else
+    da_tile<RMAX>(bx - ndb, e, lds, dS, mask, B, O, G, r, part, vec);
 }
 
 // dA[i] = c sum over the chunk partials.  Up to 64 chunks: a thread per
@@ -428,15 +450,16 @@ static int qast_grads_r(int E, int O, int G, int r, const float* dS, const uint8
   const int vec = G % 4 == 0 && (reinterpret_cast<uintptr_t>(dS) & 15) == 0 &&
                   (mask == nullptr || (reinterpret_cast<uintptr_t>(mask) & 3) == 0) ? 1 : 0;
   constexpr int kWide = db_rows<RMAX, 4>(), kNarrow = db_rows<RMAX, 1>();
-  if ((int64_t)((O + kWide - 1) / kWide) * E >= 2 * kQastCUs)
-    hipLaunchKernelGGL((qast_db_kernel<RMAX, 4>), dim3((unsigned)((O + kWide - 1) / kWide), (unsigned)E), dim3(256), 0,
-                       s, dS, mask, A, O, G, r, c, dB, vec);
-  else
-    hipLaunchKernelGGL((qast_db_kernel<RMAX, 1>), dim3((unsigned)((O + kNarrow - 1) / kNarrow), (unsigned)E), dim3(256),
-                       0, s, dS, mask, A, O, G, r, c, dB, vec);
-  hipLaunchKernelGGL(qast_da_partial_kernel<RMAX>,
-                     dim3((unsigned)(((G + da_cols<RMAX>() - 1) / da_cols<RMAX>()) * (int64_t)chunks), (unsigned)E),
-                     dim3(256), 0, s, dS, mask, B, O, G, r, part, vec);
+  const int nda = ((G + da_cols<RMAX>() - 1) / da_cols<RMAX>()) * chunks;
+  if ((int64_t)((O + kWide - 1) / kWide) * E >= 2 * kQastCUs) {
+    const int ndb = (O + kWide - 1) / kWide;
+    hipLaunchKernelGGL((qast_grads_kernel<RMAX, 4>), dim3((unsigned)(ndb + nda), (unsigned)E), dim3(256), 0, s, dS,
+                       mask, A, B, O, G, r, c, dB, part, ndb, vec);
+  } else {
+    const int ndb = (O + kNarrow - 1) / kNarrow;
+    hipLaunchKernelGGL((qast_grads_kernel<RMAX, 1>), dim3((unsigned)(ndb + nda), (unsigned)E), dim3(256), 0, s, dS,
+                       mask, A, B, O, G, r, c, dB, part, ndb, vec);
+  }
   const int64_t n = (int64_t)E * r * G;
   const int64_t rblocks = chunks <= kDaFewChunks ? (n + 255) / 256 : (n + 3) / 4;
   hipLaunchKernelGGL(qast_da_reduce_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, part, chunks, r, G, E, c, dA);
