@@ -218,3 +218,57 @@ def test_batched_experts_match_per_expert(sq, fmt, E, O, G, r):
         assert torch.equal(dB1, dB[e]) and torch.equal(dA1, dA[e])
         wB, wA = qast.factor_grads(dS[e], gm[e], Bs[e], As[e], 0.25)
         assert normwise(dB[e].cpu().numpy(), wB) <= TOL and normwise(dA[e].cpu().numpy(), wA) <= TOL
+
+
+def _rmax(r):
+    return 8 if r <= 8 else 16 if r <= 16 else 32 if r <= 32 else 64
+
+
+def wide_tiles_taken(E, O, G, r, cus=256):
+    """Whether a batched call of this shape runs the wide tiles: the scale step's
+    128-row x 32-block tiles and the dB pass's 4 rows per thread, each chosen
+    when it still gives every CU two workgroups."""
+    scales = E * -(-O // 128) * -(-G // 32) >= 2 * cus
+    db_rows = 4 * (256 // (_rmax(r) // 4))
+    return scales and E * -(-O // db_rows) >= 2 * cus
+
+
+@pytest.mark.parametrize("fmt,E,O,G,r", [("mx", 130, 520, 40, 32), ("nv", 130, 520, 37, 33)])
+def test_batched_wide_tiles(sq, fmt, E, O, G, r):
+    """Stacked experts at MoE-like sizes, where the batched calls take the wide
+    tiles (G % 4 == 0: word-wide byte planes and 16-byte dS loads; G = 37:
+    byte-wide, ragged last block tile; rank 33: the 64-rank kernels).  Every
+    expert's bytes, mask and gradients equal the single-plane calls' (narrow
+    tiles) bit for bit, and sampled experts equal the oracle."""
+    print(f"[qast wide] fmt={fmt} E={E} O={O} G={G} r={r}", flush=True)
+    assert wide_tiles_taken(E, O, G, r) and not wide_tiles_taken(1, O, G, r)
+    bases, ws2s, Bs, As = [], [], [], []
+    for e in range(E):
+        base, ws2 = plane(fmt, O, G, 8100 + e)
+        if fmt == "nv":
+            ws2 = float(np.float32(ws2 * (1 + e % 3)))
+        B, A = factors(fmt, base, ws2, r, 8300 + e, push=2.0)
+        if fmt == "nv":
+            A[0, :4] = 6000.0 * ws2                # past the ceiling where B[o, 0] is large
+        bases.append(base), ws2s.append(ws2), Bs.append(B), As.append(A)
+    base_d = torch.from_numpy(np.stack(bases)).cuda()
+    B_d, A_d = torch.stack(Bs).cuda(), torch.stack(As).cuda()
+    got, got_m = sq.sq_qast_scales_batched(fmt, base_d, B_d, A_d, 0.5, ws2s if fmt == "nv" else None)
+    dS = (inputs.rng(8500).standard_normal((E, O, G)) * 1e-2).astype(np.float32)
+    dS_d = torch.from_numpy(dS).cuda()
+    dB, dA = sq.sq_qast_factor_grads_batched(dS_d, got_m, B_d, A_d, 0.25)
+    torch.cuda.synchronize()
+    for e in range(E):
+        one, one_m = sq.sq_qast_scales(fmt, base_d[e], B_d[e], A_d[e], 0.5, ws2s[e])
+        dB1, dA1 = sq.sq_qast_factor_grads(dS_d[e], got_m[e], B_d[e], A_d[e], 0.25)
+        torch.cuda.synchronize()
+        assert torch.equal(one, got[e]) and torch.equal(one_m, got_m[e]), e
+        assert torch.equal(dB1, dB[e]) and torch.equal(dA1, dA[e]), e
+    gs, gm = got.cpu().numpy(), got_m.cpu().numpy()
+    if fmt == "nv":
+        assert 0 < int((gm == 0).sum()) < gm.size          # the ceiling binds somewhere
+    for e in (0, 1, 64, E - 1):
+        want, want_m = qast.qast_scales(fmt, bases[e], Bs[e], As[e], 0.5, ws2s[e])
+        assert np.array_equal(gs[e], want) and np.array_equal(gm[e], want_m)
+        wB, wA = qast.factor_grads(dS[e], gm[e], Bs[e], As[e], 0.25)
+        assert normwise(dB[e].cpu().numpy(), wB) <= TOL and normwise(dA[e].cpu().numpy(), wA) <= TOL
